@@ -1,0 +1,426 @@
+"""Pins of the float64 oracle against facts fixed outside the oracle itself.
+
+Each pin takes the oracle module ``O`` and raises AssertionError when the
+oracle disagrees with a closed form, an invariant, a special case that reduces
+to a library routine, brute force on a tiny input, or a value the paper
+prints.  ``test_oracle_pins`` runs them on the real oracle;
+``test_oracle_mutations`` runs them on copies of the oracle with a planted
+mistake and requires that some pin fails for every such copy.
+"""
+from __future__ import annotations
+
+import json
+import os
+
+import numpy as np
+import scipy.signal
+import scipy.special
+
+from paper_2609_24197_amd import inputs as I
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+rng0 = np.random.default_rng
+
+
+def _tiny_cfg(**kw):
+    base = dict(name="pin", B=2, k=4, d_model=32, H=4, P=8, N=4, G=1, chunk=2, Hq=4, Hkv=2, D=16,
+                lengths="list:37,5", dtype="f32", page_size=4)
+    base.update(kw)
+    return I.StepConfig(**base)
+
+
+def _paged_from_dense(K, V, ps, rng, extra=3):
+    """Scatter dense per-request K/V [L_b, Hkv, D] into a shuffled paged pool by page rows."""
+    B = len(K)
+    Hkv, D = K[0].shape[1], K[0].shape[2]
+    npg = [(k.shape[0] + ps - 1) // ps for k in K]
+    num = sum(npg) + extra
+    perm = rng.permutation(num)
+    maxp = max(1, max(npg))
+    table = np.full((B, maxp), -1, dtype=np.int32)
+    kc = np.full((num, ps, Hkv, D), np.nan)
+    vc = np.full((num, ps, Hkv, D), np.nan)
+    off = 0
+    for b in range(B):
+        for p in range(npg[b]):
+            phys = perm[off + p]
+            table[b, p] = phys
+            rows = slice(p * ps, min((p + 1) * ps, K[b].shape[0]))
+            n = rows.stop - rows.start
+            kc[phys, :n] = K[b][rows]
+            vc[phys, :n] = V[b][rows]
+        off += npg[b]
+    return kc, vc, table
+
+
+# --------------------------------------------------------------------------- attention
+
+def pin_single_key_returns_v(O):
+    """P1: one visible key -> the output is exactly that key's value."""
+    r = rng0(1)
+    q = r.standard_normal((1, 1, 2, 8))
+    kb = r.standard_normal((1, 1, 1, 8))
+    vb = r.standard_normal((1, 1, 1, 8))
+    kc = np.full((1, 4, 1, 8), np.nan)
+    o = O.paged_attention(q, kb, vb, kc, kc, np.array([[0]], np.int32), [0], page_size=4)
+    assert np.array_equal(o[0, 0, 0], vb[0, 0, 0]) and np.array_equal(o[0, 0, 1], vb[0, 0, 0])
+
+
+def pin_identical_keys_give_mean(O):
+    """P2: all keys equal -> uniform weights -> mean of V over exactly the visible keys."""
+    r = rng0(2)
+    L, T, Hkv, D, ps = 37, 3, 1, 8, 16
+    key = r.standard_normal(D)
+    Kd = [np.broadcast_to(key, (L, Hkv, D)).copy()]
+    Vd = [r.standard_normal((L, Hkv, D))]
+    kc, vc, table = _paged_from_dense(Kd, Vd, ps, r)
+    kb = np.broadcast_to(key, (1, T, Hkv, D)).copy()
+    vb = r.standard_normal((1, T, Hkv, D))
+    q = r.standard_normal((1, T, 2, D))
+    for window, causal in [(0, False), (0, True), (20, False), (8, True)]:
+        o = O.paged_attention(q, kb, vb, kc, vc, table, [L], page_size=ps, window=window,
+                              block_causal=causal)
+        for j in range(T):
+            lo = max(0, L + j - window + 1) if window else 0
+            nb = j + 1 if causal else T
+            vis = np.concatenate([Vd[0][lo:L, 0], vb[0, :nb, 0]])
+            assert np.allclose(o[0, j, 0], vis.mean(0), rtol=0, atol=1e-13), (window, causal, j)
+
+
+def pin_textbook_attention(O):
+    """P10 + P14: equals softmax(QK^T/sqrt(D))V on dense K/V with KV heads repeated g times."""
+    r = rng0(3)
+    Ls, T, Hq, Hkv, D, ps = [19, 0, 33], 5, 6, 2, 16, 8
+    g = Hq // Hkv
+    Kd = [r.standard_normal((L, Hkv, D)) for L in Ls]
+    Vd = [r.standard_normal((L, Hkv, D)) for L in Ls]
+    kc, vc, table = _paged_from_dense(Kd, Vd, ps, r)
+    q = r.standard_normal((3, T, Hq, D))
+    kb = r.standard_normal((3, T, Hkv, D))
+    vb = r.standard_normal((3, T, Hkv, D))
+    o = O.paged_attention(q, kb, vb, kc, vc, table, Ls, page_size=ps)
+    for b, L in enumerate(Ls):
+        K = np.repeat(np.concatenate([Kd[b], kb[b]], 0), g, axis=1)   # [n, Hq, D]
+        V = np.repeat(np.concatenate([Vd[b], vb[b]], 0), g, axis=1)
+        for hq in range(Hq):
+            w = scipy.special.softmax(q[b, :, hq] @ K[:, hq].T / np.sqrt(D), axis=-1)
+            assert np.allclose(o[b, :, hq], w @ V[:, hq], rtol=1e-12, atol=1e-12)
+
+
+def pin_block_order_invariance(O):
+    """P8: permuting block K/V rows leaves bidirectional outputs unchanged, but not causal ones."""
+    r = rng0(4)
+    T, D = 6, 8
+    q = r.standard_normal((1, T, 2, D))
+    kb = r.standard_normal((1, T, 1, D))
+    vb = r.standard_normal((1, T, 1, D))
+    kc = r.standard_normal((2, 4, 1, D))
+    table = np.array([[1, 0]], np.int32)
+    perm = r.permutation(T)
+    kw = dict(page_size=4)
+    a = O.paged_attention(q, kb, vb, kc, kc, table, [7], **kw)
+    b = O.paged_attention(q, kb[:, perm], vb[:, perm], kc, kc, table, [7], **kw)
+    assert np.allclose(a, b, rtol=1e-12, atol=1e-13)
+    c = O.paged_attention(q, kb, vb, kc, kc, table, [7], block_causal=True, **kw)
+    d = O.paged_attention(q, kb[:, perm], vb[:, perm], kc, kc, table, [7], block_causal=True, **kw)
+    assert not np.allclose(c, d)
+
+
+def pin_page_permutation_invariance(O):
+    """P5: relocating the physical pages and rewriting the table changes nothing (exactly)."""
+    r = rng0(5)
+    cfg = _tiny_cfg()
+    x = I.make_attn_inputs(cfg, seed=3, extra_pages=2)
+    kw = dict(page_size=cfg.page_size)
+    a = O.paged_attention(x["q"], x["k_blk"], x["v_blk"], x["k_cache"], x["v_cache"],
+                          x["page_table"], x["ctx_lens"], **kw)
+    perm = r.permutation(x["num_pages"])
+    kc = np.empty_like(x["k_cache"]); kc[perm] = x["k_cache"]
+    vc = np.empty_like(x["v_cache"]); vc[perm] = x["v_cache"]
+    t = np.where(x["page_table"] >= 0, perm[np.maximum(x["page_table"], 0)], -1).astype(np.int32)
+    b = O.paged_attention(x["q"], x["k_blk"], x["v_blk"], kc, vc, t, x["ctx_lens"], **kw)
+    assert np.array_equal(a, b)
+
+
+def pin_gather_slots(O):
+    """P6: slots recover the logical order of a pool filled page by page; -1 past the length."""
+    r = rng0(6)
+    Ls, ps = [1, 16, 17, 50, 0], 16
+    tok = [np.arange(L, dtype=float)[:, None, None] + 1000 * b for b, L in enumerate(Ls)]
+    kc, _, table = _paged_from_dense(tok, tok, ps, r)
+    flat = kc.reshape(-1)
+    sl = O.gather_slots(table, Ls, ps, 60)
+    assert sl.dtype == np.int32 and sl.shape == (5, 60)
+    for b, L in enumerate(Ls):
+        assert np.array_equal(flat[sl[b, :L]], tok[b][:, 0, 0])
+        assert np.all(sl[b, L:] == -1)
+
+
+def pin_rope(O):
+    """P12: identity at 0, norm preserving, relative positions only; complex-rotation form."""
+    r = rng0(7)
+    D = 16
+    x = r.standard_normal((1, 3, 2, D))
+    assert np.array_equal(O.rope(x, np.zeros((1, 3)), 1e6), x)
+    pos = np.array([[5, 17, 40000]])
+    y = O.rope(x, pos, 1e4)
+    assert np.allclose(np.linalg.norm(y, axis=-1), np.linalg.norm(x, axis=-1), rtol=1e-13)
+    # rotate-half pairing (i, i + D/2) is multiplication by exp(i * phi) of x_i + i x_{i+D/2}
+    zc = (x[..., :D // 2] + 1j * x[..., D // 2:]) * np.exp(
+        1j * pos[..., None, None] * 1e4 ** (-np.arange(D // 2) * 2.0 / D))
+    assert np.allclose(y, np.concatenate([zc.real, zc.imag], -1), rtol=1e-12, atol=1e-12)
+    qa, ka = O.rope(x[:, :1], [[7]], 1e6), O.rope(x[:, 1:2], [[3]], 1e6)
+    qb, kb = O.rope(x[:, :1], [[1007]], 1e6), O.rope(x[:, 1:2], [[1003]], 1e6)
+    assert np.allclose((qa * ka).sum(-1), (qb * kb).sum(-1), rtol=1e-9, atol=1e-12)
+
+
+def pin_gqa_groups(O):
+    """P14: query heads of one group that are equal give equal outputs; g = 1 is per-head MHA."""
+    r = rng0(8)
+    T, D = 3, 8
+    q = r.standard_normal((1, T, 4, D))
+    q[:, :, 1] = q[:, :, 0]
+    kb = r.standard_normal((1, T, 2, D))
+    vb = r.standard_normal((1, T, 2, D))
+    kc = r.standard_normal((1, 4, 2, D))
+    t = np.array([[0]], np.int32)
+    o = O.paged_attention(q, kb, vb, kc, kc, t, [3], page_size=4)
+    assert np.array_equal(o[:, :, 0], o[:, :, 1])
+    assert not np.allclose(o[:, :, 0], o[:, :, 2])
+    # head 2 reads KV head 1: same as a single-head problem on that KV head
+    o2 = O.paged_attention(q[:, :, 2:3], kb[:, :, 1:2], vb[:, :, 1:2], kc[:, :, 1:2, :].copy(),
+                           kc[:, :, 1:2, :].copy(), t, [3], page_size=4)
+    assert np.allclose(o[:, :, 2:3], o2, rtol=1e-14, atol=1e-14)
+
+
+# ------------------------------------------------------------------------------ Mamba
+
+def pin_scan_chunked_equals_sequential(O):
+    """P3: the SSD chunk algebra and the sequential recurrence agree for all chunk sizes."""
+    for T in (4, 7, 16, 32):
+        s = I.make_scan_inputs(2, T, 4, 8, 6, 2, seed=T, dtype="f32")
+        y0, S0 = O.ssd_sequential(s["x"], s["dt"], s["A"], s["Bm"], s["Cm"], s["Dskip"], s["S0"])
+        for Q in (1, 2, 4, 8, 16):
+            y1, S1 = O.ssd_chunked(s["x"], s["dt"], s["A"], s["Bm"], s["Cm"], s["Dskip"], s["S0"], chunk=Q)
+            assert np.linalg.norm(y1 - y0) <= 1e-12 * np.linalg.norm(y0), (T, Q)
+            assert np.linalg.norm(S1 - S0) <= 1e-12 * np.linalg.norm(S0), (T, Q)
+
+
+def pin_scan_scalar_is_first_order_filter(O):
+    """P7: P = N = 1, B = C = 1: y = first-order IIR of dt*x from state S0, plus D x (lfilter)."""
+    r = rng0(9)
+    T = 12
+    a_log = -0.3
+    dt = np.full((1, T, 1), 0.7)
+    A = np.array([a_log / 0.7])                       # exp(dt A) = exp(a_log) for every t
+    x = r.standard_normal((1, T, 1, 1))
+    one = np.ones((1, T, 1, 1))
+    S0 = np.array([[[[1.7]]]])
+    Dk = np.array([0.25])
+    y, S = O.ssd_sequential(x, dt, A, one, one, Dk, S0)
+    a = np.exp(a_log)
+    ref, _ = scipy.signal.lfilter([1.0], [1.0, -a], 0.7 * x[0, :, 0, 0], zi=[a * 1.7])
+    assert np.allclose(y[0, :, 0, 0], ref + 0.25 * x[0, :, 0, 0], rtol=1e-13, atol=1e-13)
+    assert np.isclose(S[0, 0, 0, 0], ref[-1], rtol=1e-13)
+
+
+def pin_scan_special_cases(O):
+    """P4 + P7: zero input/state -> 0; dt = 0 -> S0 C + D x; strong decay; one token."""
+    s = I.make_scan_inputs(2, 5, 4, 8, 6, 2, seed=11, dtype="f32")
+    x, dt, A, Bm, Cm, Dk, S0 = (s[k] for k in ("x", "dt", "A", "Bm", "Cm", "Dskip", "S0"))
+    x64, S064 = O.f64(x), O.f64(S0)
+    grp = np.arange(4) // 2
+    # zero input and zero state: exactly zero output and state, for any dt, B, C
+    y, S = O.ssd_sequential(np.zeros_like(x), dt, A, Bm, Cm, Dk, None)
+    assert not np.any(y) and not np.any(S)
+    # zero state and B = 0: only the skip term
+    y, _ = O.ssd_sequential(x, dt, A, np.zeros_like(Bm), Cm, Dk, None)
+    assert np.array_equal(y, Dk[None, None, :, None].astype(float) * x64)
+    # dt = 0: the state stays S0
+    y, S = O.ssd_sequential(x, np.zeros_like(dt), A, Bm, Cm, Dk, S0)
+    ref = np.einsum("bhpn,bthn->bthp", S064, O.f64(Cm)[:, :, grp]) + Dk[None, None, :, None] * x64
+    assert np.allclose(y, ref, rtol=1e-13, atol=1e-13) and np.array_equal(S, S064)
+    # strong decay: exp(dt A) = 0, y_t = dt_t (B_t . C_t) x_t + D x_t
+    y, _ = O.ssd_sequential(x, np.ones_like(dt), np.full(4, -1e4), Bm, Cm, Dk, S0)
+    bc = np.einsum("bthn,bthn->bth", O.f64(Bm)[:, :, grp], O.f64(Cm)[:, :, grp])
+    assert np.allclose(y, bc[..., None] * x64 + Dk[None, None, :, None] * x64, rtol=1e-13, atol=1e-13)
+    # one token: y0 = (e^{dt A} S0 + dt x (outer) B) C + D x
+    y, _ = O.ssd_sequential(x[:, :1], dt[:, :1], A, Bm[:, :1], Cm[:, :1], Dk, S0)
+    dt64, A64 = O.f64(dt), O.f64(A)
+    a = np.exp(dt64[:, 0] * A64)
+    St = a[:, :, None, None] * S064 + dt64[:, 0, :, None, None] * x64[:, 0, :, :, None] * O.f64(Bm)[:, 0, grp][:, :, None, :]
+    y0 = np.einsum("bhpn,bhn->bhp", St, O.f64(Cm)[:, 0, grp]) + Dk[None, :, None] * x64[:, 0]
+    assert np.allclose(y[:, 0], y0, rtol=1e-13, atol=1e-13)
+
+
+def pin_conv_is_convolution(O):
+    """Causal depthwise conv equals numpy's full convolution truncated to the first T samples."""
+    r = rng0(12)
+    x = r.standard_normal((2, 7, 5))
+    w = r.standard_normal((5, 4))
+    b = r.standard_normal(5)
+    y = O.causal_conv1d(x, w, b)
+    for bb in range(2):
+        for c in range(5):
+            ref = np.convolve(x[bb, :, c], w[c, ::-1])[:7] + b[c]
+            assert np.allclose(y[bb, :, c], ref, rtol=1e-13, atol=1e-13)
+
+
+def pin_pointwise(O):
+    """softplus, SiLU, RMSNorm and grouped gated RMSNorm at points with closed forms."""
+    assert np.isclose(O.softplus(np.array(0.0)), np.log(2.0), rtol=1e-15)
+    assert O.softplus(np.array(800.0)) == 800.0 and O.softplus(np.array(-800.0)) >= 0
+    assert np.isclose(O.silu(np.array(1.0)), 1.0 / (1.0 + np.exp(-1.0)))
+    w = np.array([1.0, 2.0, -3.0])
+    assert np.allclose(O.rmsnorm(np.full(3, -2.0), w, 0.0), -w)
+    assert np.allclose(O.rmsnorm(np.full(3, 2.0), w, 5.0), 2.0 / 3.0 * w)
+    r = rng0(13)
+    y, z = r.standard_normal((2, 12)), r.standard_normal((2, 12))
+    out = O.gated_rmsnorm(y, z, np.ones(12), 3, 0.0).reshape(2, 3, 4)
+    assert np.allclose(np.mean(out ** 2, -1), 1.0)
+    gz = (y * z / (1 + np.exp(-z))).reshape(2, 3, 4)
+    assert np.allclose(out / gz, (out / gz)[..., :1])      # each group is a scalar rescale
+
+
+def pin_state_init_layout(O):
+    """Fusion/projection: F = W_r h; S0[b, h, p, n] = (W_dS F)[(h P + p) N + n] (row-major reshape)."""
+    r = rng0(14)
+    B, dh, H, P, N = 2, 6, 2, 3, 4
+    h = r.standard_normal((B, dh))
+    Wr = r.standard_normal((dh, dh))
+    sel = r.integers(0, dh, size=H * P * N)
+    WdS = np.eye(dh)[sel]                               # row i picks F[sel[i]]
+    S0, F = O.state_init(h, Wr, WdS, H, P, N, block_rows=5)
+    assert np.allclose(F, h @ Wr.T, rtol=1e-14)
+    for b in range(B):
+        for hh in range(H):
+            for p in range(P):
+                for n in range(N):
+                    assert S0[b, hh, p, n] == F[b, sel[(hh * P + p) * N + n]]
+
+
+def pin_mixer_zero_and_causal(O):
+    """Mixer: u = 0 and S0 = 0 give exactly 0 (the gate SiLU(0) = 0); outputs are causal in t."""
+    cfg = _tiny_cfg(k=6)
+    W = I.make_weights(cfg, seed=1)
+    u = np.zeros((cfg.B, cfg.k, cfg.d_model))
+    out = O.mamba_mixer(u, np.zeros((cfg.B, cfg.H, cfg.P, cfg.N)), W, cfg)
+    assert not np.any(out)
+    r = rng0(15)
+    u = r.standard_normal((cfg.B, cfg.k, cfg.d_model))
+    S0 = r.standard_normal((cfg.B, cfg.H, cfg.P, cfg.N))
+    a = O.mamba_mixer(u, S0, W, cfg)
+    u2 = u.copy()
+    u2[:, 3:] = r.standard_normal(u2[:, 3:].shape)
+    b = O.mamba_mixer(u2, S0, W, cfg)
+    assert np.allclose(a[:, :3], b[:, :3], rtol=1e-12, atol=1e-12)
+    assert not np.allclose(a[:, 3:], b[:, 3:])
+    # the injected state reaches the first position
+    c = O.mamba_mixer(u, S0 * 2.0, W, cfg)
+    assert not np.allclose(a[:, 0], c[:, 0])
+
+
+def pin_draft_step_zero_input(O):
+    """Step with e = 0, h_last = 0: x1 = 0 so q = k = v_blk = 0; out = W_o mean(V over cache and block)."""
+    cfg = _tiny_cfg()
+    W = I.make_weights(cfg, seed=2)
+    x = I.make_inputs(cfg, seed=2)
+    x["h_last"] = np.zeros_like(x["h_last"])
+    x["block_emb"] = np.zeros_like(x["block_emb"])
+    out = O.draft_step(W, x, cfg)
+    sl = O.gather_slots(x["page_table"], x["ctx_lens"], cfg.page_size, int(max(x["ctx_lens"])))
+    vc = O.f64(x["v_cache"]).reshape(-1, cfg.Hkv, cfg.D)
+    g = cfg.Hq // cfg.Hkv
+    for b in range(cfg.B):
+        L = int(x["ctx_lens"][b])
+        mean_v = vc[sl[b, :L]].sum(0) / (L + cfg.k)           # block values are 0
+        o = np.repeat(mean_v, g, axis=0).reshape(-1)
+        ref = O.f64(W["W_o"]) @ o
+        assert np.allclose(out[b], ref[None, :], rtol=1e-12, atol=1e-13)
+
+
+def pin_table1_kv_bytes(O):
+    """Table 1: per-token target KV of the 8B targets from (KV heads, head dim, layers, bf16)."""
+    from paper_2609_24197_amd import roofline
+    with open(os.path.join(GOLDEN, "table1_kv_per_token.json")) as f:
+        t1 = json.load(f)
+    for row in t1["rows"]:
+        got = roofline.kv_bytes_per_token(row["kv_heads"], row["head_dim"], 2) * row["layers"]
+        assert got == row["target_kv_kib"] * 1024, row
+
+
+def pin_mixer_decay_rate(O):
+    """Mixer wiring of dt and A: with x = 0 and constant B, C, z the state term decays by
+    a = exp(-softplus(dt_bias) exp(A_log)) per position, and a tiny state keeps the gated
+    RMSNorm in its linear regime, so consecutive outputs differ by exactly that factor."""
+    cfg = _tiny_cfg(B=1, k=5, H=2, P=4, N=4, G=1, d_model=8)
+    r = rng0(16)
+    W = I.make_weights(cfg, seed=4)
+    W["dt_bias"] = np.full(cfg.H, 0.3, np.float32)
+    W["A_log"] = np.full(cfg.H, -0.5, np.float32)
+    Win = W["W_in"].copy()
+    Win[cfg.d_inner:] = 0.0                       # x, B, C and dt_raw rows -> 0
+    W["W_in"] = Win
+    cb = W["conv_b"].copy()
+    cb[:cfg.d_inner] = 0.0                        # x = SiLU(0) = 0; B, C = SiLU(bias)
+    W["conv_b"] = cb
+    u = np.broadcast_to(r.standard_normal(cfg.d_model), (1, cfg.k, cfg.d_model)).copy()
+    S0 = 1e-5 * r.standard_normal((1, cfg.H, cfg.P, cfg.N))
+    out = O.mamba_mixer(u, S0, W, cfg)
+    a = np.exp(-np.log1p(np.exp(0.3)) * np.exp(-0.5))
+    for t in range(1, cfg.k):
+        assert np.allclose(out[0, t], a ** t * out[0, 0], rtol=2e-3, atol=0), t
+
+
+def pin_draft_step_residuals(O):
+    """With both output projections zeroed the step is the identity on the block embeddings."""
+    cfg = _tiny_cfg()
+    W = I.make_weights(cfg, seed=5)
+    W["W_out"] = np.zeros_like(W["W_out"])
+    W["W_o"] = np.zeros_like(W["W_o"])
+    x = I.make_inputs(cfg, seed=5)
+    out = O.draft_step(W, x, cfg)
+    assert np.array_equal(out, O.f64(x["block_emb"]))
+
+
+def pin_attention_layer_dense(O):
+    """Attention layer against a dense sequence: the target stores K at positions 0..L-1 after
+    RoPE, the block sits at L..L+k-1; attention is textbook softmax (scipy) over the prefix and
+    the whole block, RoPE written as complex rotation, KV heads repeated g times."""
+    cfg = _tiny_cfg(B=2, k=3, Hq=4, Hkv=2, D=8, d_model=16, lengths="list:9,0", page_size=4)
+    r = rng0(17)
+    W = I.make_weights(cfg, seed=6)
+    W = {k: O.f64(v) for k, v in W.items()}
+    v = r.standard_normal((cfg.B, cfg.k, cfg.d_model))
+    Ls = [9, 0]
+    th = cfg.rope_theta
+    D, g = cfg.D, cfg.g
+
+    def rot(x, pos):                                  # x [..., D] at integer position
+        zc = (x[..., :D // 2] + 1j * x[..., D // 2:]) * np.exp(1j * pos * th ** (-np.arange(D // 2) * 2.0 / D))
+        return np.concatenate([zc.real, zc.imag], -1)
+
+    def nrm(x, w):
+        return x / np.sqrt(np.mean(x * x, -1, keepdims=True) + cfg.eps) * w
+
+    Kraw = [r.standard_normal((L, cfg.Hkv, D)) for L in Ls]
+    Kd = [np.stack([rot(Kraw[b][i], i) for i in range(L)]) if L else np.zeros((0, cfg.Hkv, D))
+          for b, L in enumerate(Ls)]
+    Vd = [r.standard_normal((L, cfg.Hkv, D)) for L in Ls]
+    kc, vc, table = _paged_from_dense(Kd, Vd, cfg.page_size, r)
+    cache = dict(k_cache=kc, v_cache=vc, page_table=table, ctx_lens=np.array(Ls))
+    out = O.attention_layer(v, W, cache, cfg)
+    for b, L in enumerate(Ls):
+        q = nrm((v[b] @ W["W_q"].T).reshape(cfg.k, cfg.Hq, D), W["q_norm_w"])
+        kb = nrm((v[b] @ W["W_k"].T).reshape(cfg.k, cfg.Hkv, D), W["k_norm_w"])
+        vb = (v[b] @ W["W_v"].T).reshape(cfg.k, cfg.Hkv, D)
+        q = np.stack([rot(q[j], L + j) for j in range(cfg.k)])
+        kb = np.stack([rot(kb[j], L + j) for j in range(cfg.k)])
+        K = np.repeat(np.concatenate([Kd[b], kb]), g, axis=1)
+        V = np.repeat(np.concatenate([Vd[b], vb]), g, axis=1)
+        o = np.stack([scipy.special.softmax(q[:, h] @ K[:, h].T / np.sqrt(D), -1) @ V[:, h]
+                      for h in range(cfg.Hq)], 1)
+        assert np.allclose(out[b], o.reshape(cfg.k, -1) @ W["W_o"].T, rtol=1e-11, atol=1e-12)
+
+
+PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

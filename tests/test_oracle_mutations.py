@@ -1,0 +1,69 @@
+"""Plant plausible mistakes in a copy of the oracle (on the CPU) and require a pin to catch each.
+
+Every mutation is an exact source substitution; the test first checks that the
+snippet exists so a mutation can never silently become a no-op.
+"""
+import os
+import sys
+import types
+
+import pytest
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+import oracle.hspec_oracle as O  # noqa: E402
+from oracle_pins import PINS  # noqa: E402
+
+SRC = open(O.__file__).read()
+
+MUTATIONS = {
+    "drop_skip_term": ("+ Dskip[None, :, None] * x[:, t]", ""),
+    "A_sign": ('A = -np.exp(f64(W["A_log"]))', 'A = np.exp(f64(W["A_log"]))'),
+    "dt_not_softplus": ('dt = softplus(dt_raw + f64(W["dt_bias"]))', 'dt = np.exp(dt_raw + f64(W["dt_bias"]))'),
+    "no_dt_bias": ('dt = softplus(dt_raw + f64(W["dt_bias"]))', 'dt = softplus(dt_raw)'),
+    "swap_B_C": ("Bt = Bm[:, t, grp, :]", "Bt = Cm[:, t, grp, :]"),
+    "no_dt_on_input": ("(dt[:, t, :, None] * x[:, t])", "(x[:, t])"),
+    "decay_before_not_after": ("a = np.exp(dt[:, t, :] * A[None, :])", "a = np.exp(A[None, :] + 0 * dt[:, t, :])"),
+    "conv_off_by_one": ("tau = t - (K - 1) + j", "tau = t - K + j"),
+    "conv_flipped_taps": ("out[..., t, :] += w[:, j] * x[..., tau, :]", "out[..., t, :] += w[:, K - 1 - j] * x[..., tau, :]"),
+    "gate_without_silu": ("g = y * silu(z)", "g = y * z"),
+    "gnorm_no_groups": ("gg = g.reshape(*shp[:-1], G, shp[-1] // G)", "gg = g.reshape(*shp[:-1], 1, shp[-1])"),
+    "rmsnorm_sum_not_mean": ("np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps)", "np.sqrt(np.sum(x * x, axis=-1, keepdims=True) + eps)"),
+    "rmsnorm_no_eps": ("np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps)", "np.sqrt(np.mean(x * x, axis=-1, keepdims=True))"),
+    "state_reshape_order": ("return S.reshape(h.shape[0], H, P, N), F",
+                            "return S.reshape(h.shape[0], H, N, P).transpose(0, 1, 3, 2), F"),
+    "state_proj_transposed_Wr": ("F = h @ f64(W_r).T", "F = h @ f64(W_r)"),
+    "slot_wrong_offset": ("out[b, i] = int(pt[b, i // page_size]) * page_size + i % page_size",
+                          "out[b, i] = int(pt[b, i // page_size]) * page_size + i // page_size"),
+    "rope_interleaved": ("x1, x2 = x[..., :half], x[..., half:]", "x1, x2 = x[..., 0::2], x[..., 1::2]"),
+    "rope_sign": ("x1 * c - x2 * s, x2 * c + x1 * s", "x1 * c + x2 * s, x2 * c - x1 * s"),
+    "rope_positions_from_zero": ("pos = L[:, None] + np.arange(T)[None, :]", "pos = 0 * L[:, None] + np.arange(T)[None, :]"),
+    "qk_norm_missing": ('q = rmsnorm(q, f64(W["q_norm_w"]), cfg.eps)', "q = q"),
+    "gqa_modulo": ("h = hq // g", "h = hq % Hkv"),
+    "scale_by_D": ("scale = D ** -0.5 if scale is None else scale", "scale = 1.0 / D if scale is None else scale"),
+    "window_off_by_one": ("lo = max(0, pos - window + 1) if window > 0 else 0", "lo = max(0, pos - window) if window > 0 else 0"),
+    "causal_flipped": ("nb = j + 1 if block_causal else T", "nb = T if block_causal else j + 1"),
+    "block_keys_dropped": ("K = np.concatenate([Kc[lo:L], kb[b, :nb]], axis=0)", "K = np.concatenate([Kc[lo:L], kb[b, :0]], axis=0)"),
+    "missing_mamba_residual": ("x1 = e + m_out", "x1 = m_out"),
+    "missing_attn_residual": ("out_sub = x1 + a_out", "out_sub = a_out"),
+    "chunk_decay_sign": ("decay = np.exp(lt[:, :, :, None] - lt[:, :, None, :])", "decay = np.exp(lt[:, :, None, :] - lt[:, :, :, None])"),
+}
+
+
+def _mutant(old, new):
+    assert SRC.count(old) >= 1, old
+    mod = types.ModuleType("oracle_mutant")
+    mod.__file__ = O.__file__
+    exec(compile(SRC.replace(old, new, 1), "oracle_mutant", "exec"), mod.__dict__)
+    return mod
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_some_pin_catches(name):
+    mod = _mutant(*MUTATIONS[name])
+    caught = []
+    for pin in PINS:
+        try:
+            pin(mod)
+        except Exception:  # AssertionError or a crash both count as caught
+            caught.append(pin.__name__)
+    assert caught, f"mutation {name} passes every pin"
