@@ -1,0 +1,230 @@
+/*
+ * hspec.h - C ABI of the MI355X (gfx950) block-drafting step of H-Spec
+ * ("Parallel Speculative Decoding Without a Drafter-Side KV Cache").
+ *
+ * One drafting step of the hybrid drafter has two layers:
+ *   (a) a Mamba-2 mixer run over the k-token draft block with a chunked parallel scan, its
+ *       per-head state initialised from a projection of the target model's last-position
+ *       hidden state (Sec. 3.3.1, the cross-layer fusion equation and "Parallel-drafting
+ *       compatibility");
+ *   (b) an attention layer whose k block queries attend, in place, over one target layer's
+ *       paged GQA K/V cache plus the block's own K/V, with RoPE positions continuing the
+ *       prefix (Sec. 3.3.2: "KV dimension", "Attention mask", "Positional alignment").
+ *
+ * Conventions shared by every entry point
+ *   - Memory: every tensor pointer is device memory owned by the caller; the library never
+ *     allocates, frees, or keeps a pointer after returning.  Tensors are dense row-major.
+ *   - Storage dtype (hspec_dtype): block/hidden inputs, weight matrices, conv weights and the
+ *     K/V cache use the configuration's dtype (bf16 or fp32).  Per-head and norm parameters
+ *     (dt_bias, A_log, D, norm gains) are always fp32.  Every output is fp32.
+ *   - Asynchrony: work is enqueued on `stream` (a hipStream_t, NULL = default stream) and the
+ *     call returns without synchronising.  Calls on different streams with disjoint
+ *     workspaces may run concurrently.
+ *   - Workspace: caller-provided device scratch of at least the size returned by the matching
+ *     *_workspace() query; 256-byte aligned.  Its first 4 bytes are a device status word that
+ *     the call resets and the kernels OR bits into (HSPEC_DEV_*); read it after the stream
+ *     completes with hspec_read_status().
+ *   - Errors: host-checkable problems (NULL pointers, non-positive or inconsistent sizes,
+ *     unsupported dimensions, a too-small workspace) return an error before anything is
+ *     enqueued.  A failed launch returns HSPEC_ERR_LAUNCH.  hspec_last_error() gives a
+ *     thread-local message for the last failing call.
+ *   - Device-resident page tables and context lengths are validated on the device: a page id
+ *     outside [0, num_pages) is read as zeros and sets HSPEC_DEV_BAD_PAGE; a context length
+ *     below 0 or above min(max_ctx_len, max_pages * page_size) is clamped and sets
+ *     HSPEC_DEV_BAD_CTX_LEN.  No out-of-bounds access happens in either case.
+ */
+#ifndef HSPEC_H
+#define HSPEC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  HSPEC_OK = 0,
+  HSPEC_ERR_NULL = 1,        /* a required pointer is NULL */
+  HSPEC_ERR_SHAPE = 2,       /* a size is non-positive or sizes disagree */
+  HSPEC_ERR_DTYPE = 3,       /* unknown storage dtype, or dtypes of two configs differ */
+  HSPEC_ERR_UNSUPPORTED = 4, /* a dimension this build has no kernel for */
+  HSPEC_ERR_WORKSPACE = 5,   /* workspace NULL, misaligned or smaller than required */
+  HSPEC_ERR_LAUNCH = 6       /* the HIP runtime rejected a launch */
+} hspec_status;
+
+typedef enum { HSPEC_BF16 = 0, HSPEC_F32 = 1 } hspec_dtype;
+
+/* hspec_attn_cfg.flags */
+enum {
+  HSPEC_BLOCK_CAUSAL = 1u << 0 /* block keys s visible to block query j only if s <= j
+                                  (default: the whole block is visible to every query) */
+};
+
+/* Device status bits (first int32 of the workspace). */
+enum { HSPEC_DEV_BAD_PAGE = 1, HSPEC_DEV_BAD_CTX_LEN = 2 };
+
+/*
+ * Mamba layer configuration (Sec. 3.3.1; sizes of App. B.1 "Mamba").
+ *   B requests, k draft positions, d_model hidden size, d_h = |M| * target hidden size
+ *   (the concatenated last-position hidden states), r fusion rank, H heads of P channels
+ *   (P must be 64), N = d_state (16, 32, 64 or 128), G groups of B/C (H % G == 0),
+ *   chunk = SSD chunk length (1..16), conv_w = causal conv width (1..8), eps of every RMSNorm.
+ *   d_inner = H*P, d_S = H*P*N.  d_h, r, d_model must be multiples of 8.
+ */
+typedef struct {
+  int B, k, d_model, d_h, r, H, P, N, G, chunk, conv_w;
+  hspec_dtype dtype;
+  float eps;
+} hspec_mamba_cfg;
+
+/*
+ * Mamba weights.  Matrices are [out, in] row-major in the storage dtype:
+ *   W_r [r, d_h] (Proj_r), W_dS [d_S, r] (Proj_dS; row (h*P + p)*N + n is state element
+ *   [h, p, n]), W_in [2*d_inner + 2*G*N + H, d_model] with output order (z, x, B, C, dt),
+ *   conv_w [d_inner + 2*G*N, conv_w] and conv_b [d_inner + 2*G*N] (storage dtype),
+ *   W_out [d_model, d_inner].  fp32: dt_bias [H], A_log [H] (A = -exp(A_log)), D [H],
+ *   gnorm_w [d_inner] (gain of the gated RMSNorm, normalised within each of the G groups).
+ */
+typedef struct {
+  const void *W_r, *W_dS, *W_in, *conv_w, *conv_b;
+  const float *dt_bias, *A_log, *D, *gnorm_w;
+  const void *W_out;
+} hspec_mamba_w;
+
+/*
+ * Attention layer configuration (Sec. 3.3.2; App. B.2 "Unified attention implementation").
+ *   Hq query heads, Hkv KV heads (Hq % Hkv == 0, query head q reads KV head q / (Hq/Hkv)),
+ *   D head dim (64 or 128), k * Hq/Hkv <= 128.  The target cache is two pools
+ *   [num_pages, page_size, Hkv, D] (K stored after RoPE), addressed through page_table
+ *   [B, max_pages] int32 and ctx_lens [B] int32: cache position i of request b lives in
+ *   slot page_table[b, i / page_size] * page_size + i % page_size.  Block position j sits at
+ *   RoPE position ctx_lens[b] + j.  window > 0 hides cache position p from the query at
+ *   position pos when pos - p >= window (sliding window; requires k <= window).
+ *   split_tokens: context length per split of the KV sweep (multiple of 64), 0 = automatic.
+ *   scale: softmax scale, 0 = 1/sqrt(D).  rope_theta: RoPE base (rotate-half pairing).
+ */
+typedef struct {
+  int B, k, d_model, Hq, Hkv, D, page_size, max_pages, num_pages, window, split_tokens;
+  unsigned flags;
+  hspec_dtype dtype;
+  float eps, scale;
+  double rope_theta;
+} hspec_attn_cfg;
+
+/*
+ * Attention weights: W_q [Hq*D, d_model], W_k and W_v [Hkv*D, d_model], W_o [d_model, Hq*D]
+ * (storage dtype); q_norm_w, k_norm_w [D] fp32 gains of the per-head RMSNorm of q and k.
+ */
+typedef struct {
+  const void *W_q, *W_k, *W_v, *W_o;
+  const float *q_norm_w, *k_norm_w;
+} hspec_attn_w;
+
+/* ------------------------------------------------------------------ layer-level calls */
+
+/*
+ * Mamba layer from the injected state (Sec. 3.3.1).
+ *   S0 = reshape(W_dS (W_r h_last), [H, P, N]) per request;
+ *   [z | xBC | dt_raw] = u W_in^T;  x, B, C = SiLU(causal_conv(xBC)) (zero left state);
+ *   dt = softplus(dt_raw + dt_bias);  y = selective scan of (x, dt, A, B, C, D) from S0;
+ *   out = W_out (RMSNorm_G(y * SiLU(z)) * gnorm_w).   No residual, no pre-norm.
+ * h_last [B, d_h], block_hidden u [B, k, d_model] (storage dtype); out [B, k, d_model] fp32;
+ * S_final [B, H, P, N] fp32 or NULL (the state after the last draft position).
+ */
+hspec_status hspec_mamba_block_scan(const hspec_mamba_cfg* cfg, const hspec_mamba_w* w,
+                                    const void* h_last, const void* block_hidden, float* out,
+                                    float* S_final, void* workspace, size_t ws_bytes, void* stream);
+size_t hspec_mamba_block_scan_workspace(const hspec_mamba_cfg* cfg);
+
+/*
+ * Attention layer over the target's paged K/V, in place (Sec. 3.3.2).
+ *   q = RMSNorm_D(x W_q^T) q_norm_w, k_b = RMSNorm_D(x W_k^T) k_norm_w, v_b = x W_v^T;
+ *   q, k_b rotated at positions ctx_len + j;  o = softmax over (visible cache keys, block keys);
+ *   out = o W_o^T.   No residual, no pre-norm.
+ * x [B, k, d_model] (storage dtype); k_cache, v_cache [num_pages, page_size, Hkv, D];
+ * page_table [B, max_pages], ctx_lens [B] (device int32); max_ctx_len: host upper bound of
+ * ctx_lens (sizes the launch; larger lengths are clamped and flagged); out [B, k, d_model] fp32.
+ */
+hspec_status hspec_target_kv_block_attn(const hspec_attn_cfg* cfg, const hspec_attn_w* w, const void* x,
+                                        const void* k_cache, const void* v_cache,
+                                        const int32_t* page_table, const int32_t* ctx_lens,
+                                        int max_ctx_len, float* out, void* workspace, size_t ws_bytes,
+                                        void* stream);
+size_t hspec_target_kv_block_attn_workspace(const hspec_attn_cfg* cfg, int max_ctx_len);
+
+/*
+ * One drafting step (Sec. 3.3 architecture: Mamba then attention):
+ *   x1 = e + Mamba(RMSNorm(e) norm1_w; S0(h_last));   out = x1 + Attn(RMSNorm(x1) norm2_w).
+ * The two configs must agree on B, k, d_model and dtype.  block_emb e [B, k, d_model]
+ * (storage dtype); norm1_w, norm2_w [d_model] fp32; other arguments as in the layer calls.
+ */
+hspec_status hspec_draft_step(const hspec_mamba_cfg* mcfg, const hspec_mamba_w* mw, const float* norm1_w,
+                              const hspec_attn_cfg* acfg, const hspec_attn_w* aw, const float* norm2_w,
+                              const void* h_last, const void* block_emb, const void* k_cache,
+                              const void* v_cache, const int32_t* page_table, const int32_t* ctx_lens,
+                              int max_ctx_len, float* out, void* workspace, size_t ws_bytes, void* stream);
+size_t hspec_draft_step_workspace(const hspec_mamba_cfg* mcfg, const hspec_attn_cfg* acfg, int max_ctx_len);
+
+/* --------------------------------------------------- primitives (same kernels as above) */
+
+/*
+ * Fusion + state projection only (Sec. 3.3.1 equation): S0 [B, H, P, N] fp32 =
+ * reshape(W_dS (W_r h_last)).  Uses cfg B, d_h, r, H, P, N, dtype.
+ */
+hspec_status hspec_state_init(const hspec_mamba_cfg* cfg, const hspec_mamba_w* w, const void* h_last,
+                              float* S0, void* workspace, size_t ws_bytes, void* stream);
+size_t hspec_state_init_workspace(const hspec_mamba_cfg* cfg);
+
+/*
+ * Selective scan (Sec. 3.3.1 recurrence), chunked: per head h of group g = h / (H/G),
+ *   S_t = exp(dt_t A_h) S_{t-1} + dt_t x_t (outer) B_t,   y_t = S_t C_t + D_h x_t,
+ * from S_{-1} = S0.  x [B, T, H, P], Bm, Cm [B, T, G, N], S0 [B, H, P, N] or NULL (zeros) in
+ * the storage dtype; dt [B, T, H] (already softplus-ed), A [H], Dskip [H] fp32;
+ * y [B, T, H, P] fp32; S_final [B, H, P, N] fp32 or NULL.  P must be 64, 1 <= chunk <= 16.
+ */
+hspec_status hspec_ssd_scan(int B, int T, int H, int P, int N, int G, int chunk, hspec_dtype dtype,
+                            const void* x, const float* dt, const float* A, const void* Bm, const void* Cm,
+                            const float* Dskip, const void* S0, float* y, float* S_final,
+                            void* workspace, size_t ws_bytes, void* stream);
+size_t hspec_ssd_scan_workspace(int B, int T, int H, int P, int N, int G, hspec_dtype dtype);
+
+/*
+ * Attention core (the KV sweep and its split reduction) on given post-norm, post-RoPE
+ * q [B, k, Hq, D], k_blk, v_blk [B, k, Hkv, D] (storage dtype): o [B, k, Hq, D] fp32.
+ */
+hspec_status hspec_paged_attn(const hspec_attn_cfg* cfg, const void* q, const void* k_blk, const void* v_blk,
+                              const void* k_cache, const void* v_cache, const int32_t* page_table,
+                              const int32_t* ctx_lens, int max_ctx_len, float* o, void* workspace,
+                              size_t ws_bytes, void* stream);
+size_t hspec_paged_attn_workspace(const hspec_attn_cfg* cfg, int max_ctx_len);
+
+/*
+ * Physical slot of every logical cache position: slots [B, max_ctx_len] int32, -1 at and past
+ * ctx_lens[b] (and for out-of-pool page ids, which also set HSPEC_DEV_BAD_PAGE in *status).
+ * status: device int32 or NULL.
+ */
+hspec_status hspec_gather_slots(int B, int max_pages, int page_size, int num_pages, const int32_t* page_table,
+                                const int32_t* ctx_lens, int max_ctx_len, int32_t* slots, int32_t* status,
+                                void* stream);
+
+/*
+ * Plain projection C [M, N] fp32 = A [M, K] W [N, K]^T (+ R [M, N] fp32 if R != NULL), A and W
+ * in the storage dtype (the GEMM used by every projection above).  K must be a multiple of 8.
+ */
+hspec_status hspec_linear(hspec_dtype dtype, int M, int N, int K, const void* A, const void* W,
+                          const float* R, float* C, void* workspace, size_t ws_bytes, void* stream);
+size_t hspec_linear_workspace(hspec_dtype dtype, int M, int N, int K);
+
+/* ------------------------------------------------------------------------- utilities */
+
+/* Copies the device status word of `workspace` to *status after synchronising `stream`. */
+hspec_status hspec_read_status(const void* workspace, int32_t* status, void* stream);
+const char* hspec_status_string(hspec_status s);
+/* Message of the last failing call on this thread ("" if none). */
+const char* hspec_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HSPEC_H */

@@ -29,6 +29,9 @@ projection.
 """
 from __future__ import annotations
 
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 
 __all__ = [
@@ -39,6 +42,13 @@ __all__ = [
 
 
 # ----------------------------------------------------------------------------- helpers
+
+def _threads() -> int:
+    try:
+        return max(1, min(16, len(os.sched_getaffinity(0))))
+    except AttributeError:  # pragma: no cover
+        return 1
+
 
 def f64(a, dtype: str | None = None) -> np.ndarray:
     """Widen a storage array to float64 (bf16 bit patterns are uint16)."""
@@ -79,9 +89,17 @@ def state_init(h_last, W_r, W_dS, H: int, P: int, N: int, block_rows: int = 1 <<
     d_S = H * P * N
     assert W_dS.shape[0] == d_S
     S = np.empty((h.shape[0], d_S))
-    for i0 in range(0, d_S, block_rows):
+
+    def rows(i0):                    # output rows are independent: blocks may run in any order
         i1 = min(d_S, i0 + block_rows)
         S[:, i0:i1] = F @ f64(W_dS[i0:i1]).T
+
+    starts = range(0, d_S, block_rows)
+    if len(starts) > 1:
+        with ThreadPoolExecutor(_threads()) as ex:
+            list(ex.map(rows, starts))
+    else:
+        rows(0)
     return S.reshape(h.shape[0], H, P, N), F
 
 

@@ -1,0 +1,691 @@
+// C ABI of the drafting step: argument validation, workspace layout, and the stream-ordered
+// launch sequence of each entry point.  Host code only; every kernel lives in a .hip file.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "hspec.h"
+#include "kernels.h"
+
+#define HSPEC_API extern "C" __attribute__((visibility("default")))
+
+using hspec::bf16;
+
+namespace {
+
+thread_local std::string g_err;
+
+hspec_status fail(hspec_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+#define HIP_TRY(expr)                                                                        \
+  do {                                                                                       \
+    hipError_t e_ = (expr);                                                                  \
+    if (e_ != hipSuccess) return fail(HSPEC_ERR_LAUNCH, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr size_t ALIGN = 256;
+
+// Bump allocator over the caller's workspace.  With base == nullptr it only measures.
+struct Arena {
+  char* base = nullptr;
+  size_t off = 0;
+  template <class T>
+  T* take(size_t count) {
+    size_t o = (off + ALIGN - 1) / ALIGN * ALIGN;
+    off = o + count * sizeof(T);
+    return base ? reinterpret_cast<T*>(base + o) : nullptr;
+  }
+  size_t size() const { return (off + ALIGN - 1) / ALIGN * ALIGN; }
+};
+
+bool is_f32(hspec_dtype d) { return d == HSPEC_F32; }
+bool dtype_ok(hspec_dtype d) { return d == HSPEC_BF16 || d == HSPEC_F32; }
+
+// A storage-dtype matrix as MFMA planes: bf16 storage is its own hi plane; fp32 storage is
+// split into (hi, lo) inside the workspace.
+struct Planes {
+  const bf16* hi = nullptr;
+  const bf16* lo = nullptr;
+};
+struct SplitSlot {
+  bf16* hi = nullptr;
+  bf16* lo = nullptr;
+  size_t n = 0;
+};
+SplitSlot reserve_split(Arena& ar, hspec_dtype d, size_t n) {
+  SplitSlot s;
+  if (is_f32(d)) {
+    s.hi = ar.take<bf16>(n);
+    s.lo = ar.take<bf16>(n);
+    s.n = n;
+  }
+  return s;
+}
+hipError_t as_planes(const void* src, hspec_dtype d, const SplitSlot& slot, Planes& out, hipStream_t st) {
+  if (!is_f32(d)) {
+    out.hi = static_cast<const bf16*>(src);
+    out.lo = nullptr;
+    return hipSuccess;
+  }
+  out.hi = slot.hi;
+  out.lo = slot.lo;
+  return hspec::launch_split_planes(static_cast<const float*>(src), slot.n, slot.hi, slot.lo, st);
+}
+
+// ------------------------------------------------------------------------- validation
+
+hspec_status check_mamba(const hspec_mamba_cfg* c, const hspec_mamba_w* w, bool full) {
+  if (!c || !w) return fail(HSPEC_ERR_NULL, "mamba config or weights is NULL");
+  if (!dtype_ok(c->dtype)) return fail(HSPEC_ERR_DTYPE, "unknown dtype %d", (int)c->dtype);
+  if (c->B <= 0 || c->d_h <= 0 || c->r <= 0 || c->H <= 0 || c->P <= 0 || c->N <= 0)
+    return fail(HSPEC_ERR_SHAPE, "non-positive mamba dimension");
+  if (c->P != 64) return fail(HSPEC_ERR_UNSUPPORTED, "P (head dim) must be 64, got %d", c->P);
+  if (c->N != 16 && c->N != 32 && c->N != 64 && c->N != 128)
+    return fail(HSPEC_ERR_UNSUPPORTED, "N (d_state) must be 16, 32, 64 or 128, got %d", c->N);
+  if (c->d_h % 8 || c->r % 8) return fail(HSPEC_ERR_UNSUPPORTED, "d_h and r must be multiples of 8");
+  if (!w->W_r || !w->W_dS) return fail(HSPEC_ERR_NULL, "W_r or W_dS is NULL");
+  if (!full) return HSPEC_OK;
+  if (c->k <= 0 || c->d_model <= 0 || c->G <= 0 || c->chunk <= 0 || c->conv_w <= 0)
+    return fail(HSPEC_ERR_SHAPE, "non-positive mamba dimension");
+  if (c->H % c->G) return fail(HSPEC_ERR_SHAPE, "H %% G != 0 (H=%d, G=%d)", c->H, c->G);
+  if (c->chunk > 16) return fail(HSPEC_ERR_UNSUPPORTED, "chunk must be <= 16, got %d", c->chunk);
+  if (c->conv_w > 8) return fail(HSPEC_ERR_UNSUPPORTED, "conv_w must be <= 8, got %d", c->conv_w);
+  if (c->d_model % 8) return fail(HSPEC_ERR_UNSUPPORTED, "d_model must be a multiple of 8");
+  if ((c->H * c->P) % c->G) return fail(HSPEC_ERR_SHAPE, "d_inner %% G != 0");
+  if (!w->W_in || !w->conv_w || !w->conv_b || !w->dt_bias || !w->A_log || !w->D || !w->gnorm_w || !w->W_out)
+    return fail(HSPEC_ERR_NULL, "a mamba weight pointer is NULL");
+  return HSPEC_OK;
+}
+
+hspec_status check_attn_cfg(const hspec_attn_cfg* c, int max_ctx_len) {
+  if (!c) return fail(HSPEC_ERR_NULL, "attention config is NULL");
+  if (!dtype_ok(c->dtype)) return fail(HSPEC_ERR_DTYPE, "unknown dtype %d", (int)c->dtype);
+  if (c->B <= 0 || c->k <= 0 || c->Hq <= 0 || c->Hkv <= 0 || c->D <= 0 || c->page_size <= 0 ||
+      c->max_pages <= 0 || c->num_pages <= 0)
+    return fail(HSPEC_ERR_SHAPE, "non-positive attention dimension");
+  if (c->Hq % c->Hkv) return fail(HSPEC_ERR_SHAPE, "Hq %% Hkv != 0 (Hq=%d, Hkv=%d)", c->Hq, c->Hkv);
+  if (c->D != 64 && c->D != 128) return fail(HSPEC_ERR_UNSUPPORTED, "D must be 64 or 128, got %d", c->D);
+  if (c->k * (c->Hq / c->Hkv) > 128)
+    return fail(HSPEC_ERR_UNSUPPORTED, "k * Hq/Hkv must be <= 128, got %d", c->k * (c->Hq / c->Hkv));
+  if (c->window < 0) return fail(HSPEC_ERR_SHAPE, "window < 0");
+  if (c->window > 0 && c->k > c->window) return fail(HSPEC_ERR_SHAPE, "k > window");
+  if (c->split_tokens < 0 || c->split_tokens % 64)
+    return fail(HSPEC_ERR_SHAPE, "split_tokens must be a non-negative multiple of 64");
+  if (max_ctx_len < 0) return fail(HSPEC_ERR_SHAPE, "max_ctx_len < 0");
+  if ((long long)c->B * c->Hkv > 65535 * 64LL) return fail(HSPEC_ERR_UNSUPPORTED, "B * Hkv too large");
+  return HSPEC_OK;
+}
+
+hspec_status check_attn_w(const hspec_attn_cfg* c, const hspec_attn_w* w) {
+  if (!w) return fail(HSPEC_ERR_NULL, "attention weights is NULL");
+  if (!w->W_q || !w->W_k || !w->W_v || !w->W_o || !w->q_norm_w || !w->k_norm_w)
+    return fail(HSPEC_ERR_NULL, "an attention weight pointer is NULL");
+  if (c->d_model <= 0 || c->d_model % 8) return fail(HSPEC_ERR_UNSUPPORTED, "d_model must be a positive multiple of 8");
+  return HSPEC_OK;
+}
+
+hspec_status check_ws(void* ws, size_t have, size_t need) {
+  if (!ws) return fail(HSPEC_ERR_WORKSPACE, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % ALIGN) return fail(HSPEC_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+  if (have < need) return fail(HSPEC_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", have, need);
+  return HSPEC_OK;
+}
+
+// ---------------------------------------------------------------------- layout + launch
+
+struct StatePlan {
+  SplitSlot h, wr, wds;
+  bf16 *F_hi = nullptr, *F_lo = nullptr;
+  bf16 *S0_hi = nullptr, *S0_lo = nullptr;
+};
+
+void plan_state(Arena& ar, const hspec_mamba_cfg& c, bool s0_planes, StatePlan& p) {
+  const size_t dS = (size_t)c.H * c.P * c.N;
+  p.h = reserve_split(ar, c.dtype, (size_t)c.B * c.d_h);
+  p.wr = reserve_split(ar, c.dtype, (size_t)c.r * c.d_h);
+  p.wds = reserve_split(ar, c.dtype, dS * c.r);
+  p.F_hi = ar.take<bf16>((size_t)c.B * c.r);
+  p.F_lo = ar.take<bf16>((size_t)c.B * c.r);
+  if (s0_planes) {
+    p.S0_hi = ar.take<bf16>((size_t)c.B * dS);
+    p.S0_lo = ar.take<bf16>((size_t)c.B * dS);
+  }
+}
+
+// F = W_r h_last (bf16 planes), then S0 = W_dS F (fp32 and/or bf16 planes).
+hspec_status run_state(const hspec_mamba_cfg& c, const hspec_mamba_w& w, const void* h_last, const StatePlan& p,
+                       float* S0_f32, hipStream_t st) {
+  Planes h, wr, wds;
+  HIP_TRY(as_planes(h_last, c.dtype, p.h, h, st));
+  HIP_TRY(as_planes(w.W_r, c.dtype, p.wr, wr, st));
+  HIP_TRY(as_planes(w.W_dS, c.dtype, p.wds, wds, st));
+  hspec::GemmArgs g1;
+  g1.A_hi = h.hi; g1.A_lo = h.lo; g1.lda = c.d_h;
+  g1.W_hi = wr.hi; g1.W_lo = wr.lo; g1.ldw = c.d_h;
+  g1.M = c.B; g1.N = c.r; g1.K = c.d_h;
+  g1.C_hi = p.F_hi; g1.C_lo = p.F_lo; g1.ldch = c.r;
+  HIP_TRY(hspec::launch_gemm(g1, st));
+  const int dS = c.H * c.P * c.N;
+  hspec::GemmArgs g2;
+  g2.A_hi = p.F_hi; g2.A_lo = p.F_lo; g2.lda = c.r;
+  g2.W_hi = wds.hi; g2.W_lo = wds.lo; g2.ldw = c.r;
+  g2.M = c.B; g2.N = dS; g2.K = c.r;
+  g2.C = S0_f32; g2.ldc = dS;
+  g2.C_hi = p.S0_hi; g2.C_lo = p.S0_lo; g2.ldch = dS;
+  HIP_TRY(hspec::launch_gemm(g2, st));
+  return HSPEC_OK;
+}
+
+struct MambaPlan {
+  StatePlan st;
+  SplitSlot u_in, win, wout;
+  bf16 *u_hi = nullptr, *u_lo = nullptr;      // normalised block input (draft step)
+  float* zx = nullptr;
+  bf16 *x_hi = nullptr, *x_lo = nullptr, *B_hi = nullptr, *B_lo = nullptr, *C_hi = nullptr, *C_lo = nullptr;
+  float* dt = nullptr;
+  float* y = nullptr;
+  bf16 *yn_hi = nullptr, *yn_lo = nullptr;
+};
+
+void plan_mamba(Arena& ar, const hspec_mamba_cfg& c, bool u_norm, MambaPlan& p) {
+  plan_state(ar, c, true, p.st);
+  const size_t M = (size_t)c.B * c.k;
+  const size_t di = (size_t)c.H * c.P, gn = (size_t)c.G * c.N;
+  const size_t dproj = 2 * di + 2 * gn + c.H;
+  if (u_norm) {
+    p.u_hi = ar.take<bf16>(M * c.d_model);
+    p.u_lo = ar.take<bf16>(M * c.d_model);
+  } else {
+    p.u_in = reserve_split(ar, c.dtype, M * c.d_model);
+  }
+  p.win = reserve_split(ar, c.dtype, dproj * c.d_model);
+  p.wout = reserve_split(ar, c.dtype, (size_t)c.d_model * di);
+  p.zx = ar.take<float>(M * dproj);
+  p.x_hi = ar.take<bf16>(M * di);
+  if (is_f32(c.dtype)) p.x_lo = ar.take<bf16>(M * di);
+  p.B_hi = ar.take<bf16>(M * gn);
+  p.B_lo = ar.take<bf16>(M * gn);
+  p.C_hi = ar.take<bf16>(M * gn);
+  p.C_lo = ar.take<bf16>(M * gn);
+  p.dt = ar.take<float>(M * c.H);
+  p.y = ar.take<float>(M * di);
+  p.yn_hi = ar.take<bf16>(M * di);
+  p.yn_lo = ar.take<bf16>(M * di);
+}
+
+// in_proj -> conv/split -> scan from S0 planes -> gated norm -> out_proj (+ residual R).
+hspec_status run_mamba_core(const hspec_mamba_cfg& c, const hspec_mamba_w& w, Planes u, const MambaPlan& p,
+                            const void* R, int r_bf16, float* out, float* S_final, hipStream_t st) {
+  const int M = c.B * c.k;
+  const int di = c.H * c.P, gn = c.G * c.N;
+  const int dproj = 2 * di + 2 * gn + c.H;
+  Planes win, wout;
+  HIP_TRY(as_planes(w.W_in, c.dtype, p.win, win, st));
+  HIP_TRY(as_planes(w.W_out, c.dtype, p.wout, wout, st));
+  hspec::GemmArgs gi;
+  gi.A_hi = u.hi; gi.A_lo = u.lo; gi.lda = c.d_model;
+  gi.W_hi = win.hi; gi.W_lo = win.lo; gi.ldw = c.d_model;
+  gi.M = M; gi.N = dproj; gi.K = c.d_model;
+  gi.C = p.zx; gi.ldc = dproj;
+  HIP_TRY(hspec::launch_gemm(gi, st));
+
+  hspec::ConvArgs ca;
+  ca.zxbcdt = p.zx; ca.conv_w = w.conv_w; ca.conv_b = w.conv_b; ca.w_bf16 = !is_f32(c.dtype);
+  ca.dt_bias = w.dt_bias;
+  ca.B = c.B; ca.T = c.k; ca.H = c.H; ca.P = c.P; ca.G = c.G; ca.N = c.N; ca.K = c.conv_w;
+  ca.x_hi = p.x_hi; ca.x_lo = p.x_lo; ca.B_hi = p.B_hi; ca.B_lo = p.B_lo; ca.C_hi = p.C_hi; ca.C_lo = p.C_lo;
+  ca.dt = p.dt;
+  HIP_TRY(hspec::launch_conv_split(ca, st));
+
+  hspec::ScanArgs sa;
+  sa.x_hi = p.x_hi; sa.x_lo = p.x_lo; sa.dt = p.dt; sa.A = w.A_log; sa.A_is_log = 1;
+  sa.B_hi = p.B_hi; sa.B_lo = p.B_lo; sa.C_hi = p.C_hi; sa.C_lo = p.C_lo; sa.Dskip = w.D;
+  sa.S0_hi = p.st.S0_hi; sa.S0_lo = p.st.S0_lo; sa.y = p.y; sa.S_final = S_final;
+  sa.B = c.B; sa.T = c.k; sa.H = c.H; sa.P = c.P; sa.N = c.N; sa.G = c.G; sa.chunk = c.chunk;
+  sa.x_ld = di; sa.bc_ld = gn; sa.dt_ld = c.H;
+  HIP_TRY(hspec::launch_ssd_scan(sa, st));
+
+  HIP_TRY(hspec::launch_gated_rmsnorm(p.y, p.zx, dproj, w.gnorm_w, M, di, c.G, c.eps, p.yn_hi, p.yn_lo, st));
+
+  hspec::GemmArgs go;
+  go.A_hi = p.yn_hi; go.A_lo = p.yn_lo; go.lda = di;
+  go.W_hi = wout.hi; go.W_lo = wout.lo; go.ldw = di;
+  go.M = M; go.N = c.d_model; go.K = di;
+  go.C = out; go.ldc = c.d_model;
+  go.R = R; go.ldr = c.d_model; go.r_bf16 = r_bf16;
+  HIP_TRY(hspec::launch_gemm(go, st));
+  return HSPEC_OK;
+}
+
+struct AttnPlan {
+  SplitSlot x_in, wq, wk, wv, wo, kc, vc, qin, kbin, vbin;
+  bf16 *xn_hi = nullptr, *xn_lo = nullptr;   // normalised input (draft step)
+  float* qkv = nullptr;
+  bf16 *q_hi = nullptr, *q_lo = nullptr, *k_hi = nullptr, *k_lo = nullptr, *v_hi = nullptr, *v_lo = nullptr;
+  float* part_o = nullptr;
+  float* part_ml = nullptr;
+  bf16 *o_hi = nullptr, *o_lo = nullptr;
+  int split = 0, max_splits = 0;
+};
+
+void plan_sweep(Arena& ar, const hspec_attn_cfg& c, int max_ctx_len, AttnPlan& p) {
+  p.split = c.split_tokens > 0 ? c.split_tokens : hspec::attention_default_split(c.B, c.Hkv, max_ctx_len);
+  p.max_splits = max_ctx_len > 0 ? (max_ctx_len + p.split - 1) / p.split : 1;
+  const int R = c.k * (c.Hq / c.Hkv);
+  const size_t units = (size_t)c.B * c.Hkv * p.max_splits;
+  if (p.max_splits > 1) {
+    p.part_o = ar.take<float>(units * R * c.D);
+    p.part_ml = ar.take<float>(units * R * 2);
+  }
+  const size_t cache = (size_t)c.num_pages * c.page_size * c.Hkv * c.D;
+  p.kc = reserve_split(ar, c.dtype, cache);
+  p.vc = reserve_split(ar, c.dtype, cache);
+}
+
+void plan_attn(Arena& ar, const hspec_attn_cfg& c, int max_ctx_len, bool x_norm, AttnPlan& p) {
+  const size_t M = (size_t)c.B * c.k;
+  const bool f32 = is_f32(c.dtype);
+  if (x_norm) {
+    p.xn_hi = ar.take<bf16>(M * c.d_model);
+    if (f32) p.xn_lo = ar.take<bf16>(M * c.d_model);
+  } else {
+    p.x_in = reserve_split(ar, c.dtype, M * c.d_model);
+  }
+  p.wq = reserve_split(ar, c.dtype, (size_t)c.Hq * c.D * c.d_model);
+  p.wk = reserve_split(ar, c.dtype, (size_t)c.Hkv * c.D * c.d_model);
+  p.wv = reserve_split(ar, c.dtype, (size_t)c.Hkv * c.D * c.d_model);
+  p.wo = reserve_split(ar, c.dtype, (size_t)c.d_model * c.Hq * c.D);
+  p.qkv = ar.take<float>(M * (c.Hq + 2 * c.Hkv) * c.D);
+  p.q_hi = ar.take<bf16>(M * c.Hq * c.D);
+  p.k_hi = ar.take<bf16>(M * c.Hkv * c.D);
+  p.v_hi = ar.take<bf16>(M * c.Hkv * c.D);
+  if (f32) {
+    p.q_lo = ar.take<bf16>(M * c.Hq * c.D);
+    p.k_lo = ar.take<bf16>(M * c.Hkv * c.D);
+    p.v_lo = ar.take<bf16>(M * c.Hkv * c.D);
+  }
+  plan_sweep(ar, c, max_ctx_len, p);
+  p.o_hi = ar.take<bf16>(M * c.Hq * c.D);
+}
+
+hspec::AttnArgs sweep_args(const hspec_attn_cfg& c, const AttnPlan& p, const int32_t* pt, const int32_t* lens,
+                           int max_ctx_len, int* status) {
+  hspec::AttnArgs a;
+  a.page_table = pt; a.ctx_lens = lens;
+  a.B = c.B; a.T = c.k; a.Hq = c.Hq; a.Hkv = c.Hkv; a.D = c.D; a.ps = c.page_size;
+  a.max_pages = c.max_pages; a.num_pages = c.num_pages; a.window = c.window;
+  a.causal = (c.flags & HSPEC_BLOCK_CAUSAL) ? 1 : 0;
+  a.max_ctx_len = max_ctx_len; a.split = p.split; a.max_splits = p.max_splits;
+  const float scale = c.scale > 0.f ? c.scale : 1.f / std::sqrt((float)c.D);
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.part_o = p.part_o; a.part_ml = p.part_ml; a.status = status;
+  return a;
+}
+
+// QKV projections -> q/k norm + RoPE -> sweep + reduce -> O projection (+ residual R).
+hspec_status run_attn_core(const hspec_attn_cfg& c, const hspec_attn_w& w, Planes xn, const void* k_cache,
+                           const void* v_cache, const int32_t* pt, const int32_t* lens, int max_ctx_len,
+                           const AttnPlan& p, const float* R, float* out, int* status, hipStream_t st) {
+  const int M = c.B * c.k;
+  const int ldq = (c.Hq + 2 * c.Hkv) * c.D;
+  Planes wq, wk, wv, wo, kc, vc;
+  HIP_TRY(as_planes(w.W_q, c.dtype, p.wq, wq, st));
+  HIP_TRY(as_planes(w.W_k, c.dtype, p.wk, wk, st));
+  HIP_TRY(as_planes(w.W_v, c.dtype, p.wv, wv, st));
+  HIP_TRY(as_planes(w.W_o, c.dtype, p.wo, wo, st));
+  HIP_TRY(as_planes(k_cache, c.dtype, p.kc, kc, st));
+  HIP_TRY(as_planes(v_cache, c.dtype, p.vc, vc, st));
+  const Planes* ws[3] = {&wq, &wk, &wv};
+  const int nrows[3] = {c.Hq * c.D, c.Hkv * c.D, c.Hkv * c.D};
+  int col = 0;
+  for (int i = 0; i < 3; ++i) {
+    hspec::GemmArgs g;
+    g.A_hi = xn.hi; g.A_lo = xn.lo; g.lda = c.d_model;
+    g.W_hi = ws[i]->hi; g.W_lo = ws[i]->lo; g.ldw = c.d_model;
+    g.M = M; g.N = nrows[i]; g.K = c.d_model;
+    g.C = p.qkv + col; g.ldc = ldq;
+    HIP_TRY(hspec::launch_gemm(g, st));
+    col += nrows[i];
+  }
+  HIP_TRY(hspec::launch_qk_norm_rope(p.qkv, w.q_norm_w, w.k_norm_w, lens, c.B, c.k, c.Hq, c.Hkv, c.D, c.eps,
+                                     c.rope_theta, p.q_hi, p.q_lo, p.k_hi, p.k_lo, p.v_hi, p.v_lo, st));
+  hspec::AttnArgs a = sweep_args(c, p, pt, lens, max_ctx_len, status);
+  a.q_hi = p.q_hi; a.q_lo = p.q_lo; a.kb_hi = p.k_hi; a.kb_lo = p.k_lo; a.vb_hi = p.v_hi; a.vb_lo = p.v_lo;
+  a.kc_hi = kc.hi; a.kc_lo = kc.lo; a.vc_hi = vc.hi; a.vc_lo = vc.lo;
+  a.o_bf16 = p.o_hi;
+  HIP_TRY(hspec::launch_attention(a, st));
+  hspec::GemmArgs g;
+  g.A_hi = p.o_hi; g.lda = c.Hq * c.D;
+  g.W_hi = wo.hi; g.W_lo = wo.lo; g.ldw = c.Hq * c.D;
+  g.M = M; g.N = c.d_model; g.K = c.Hq * c.D;
+  g.C = out; g.ldc = c.d_model;
+  g.R = R; g.ldr = c.d_model; g.r_bf16 = 0;
+  HIP_TRY(hspec::launch_gemm(g, st));
+  return HSPEC_OK;
+}
+
+struct DraftPlan {
+  MambaPlan m;
+  float* x1 = nullptr;
+  AttnPlan at;
+};
+
+void plan_draft(Arena& ar, const hspec_mamba_cfg& mc, const hspec_attn_cfg& ac, int max_ctx_len, DraftPlan& p) {
+  plan_mamba(ar, mc, true, p.m);
+  p.x1 = ar.take<float>((size_t)mc.B * mc.k * mc.d_model);
+  plan_attn(ar, ac, max_ctx_len, true, p.at);
+}
+
+int* status_word(Arena& ar) { return ar.take<int>(ALIGN / sizeof(int)); }
+
+}  // namespace
+
+// ============================================================================ C ABI
+
+HSPEC_API size_t hspec_state_init_workspace(const hspec_mamba_cfg* cfg) {
+  if (!cfg) return 0;
+  Arena ar;
+  status_word(ar);
+  StatePlan p;
+  plan_state(ar, *cfg, false, p);
+  return ar.size();
+}
+
+HSPEC_API hspec_status hspec_state_init(const hspec_mamba_cfg* cfg, const hspec_mamba_w* w, const void* h_last,
+                                        float* S0, void* workspace, size_t ws_bytes, void* stream) {
+  g_err.clear();
+  if (hspec_status s = check_mamba(cfg, w, false)) return s;
+  if (!h_last || !S0) return fail(HSPEC_ERR_NULL, "h_last or S0 is NULL");
+  if (hspec_status s = check_ws(workspace, ws_bytes, hspec_state_init_workspace(cfg))) return s;
+  hipStream_t st = (hipStream_t)stream;
+  Arena ar{(char*)workspace};
+  int* status = status_word(ar);
+  StatePlan p;
+  plan_state(ar, *cfg, false, p);
+  HIP_TRY(hspec::launch_zero_words(status, 1, st));
+  return run_state(*cfg, *w, h_last, p, S0, st);
+}
+
+HSPEC_API size_t hspec_mamba_block_scan_workspace(const hspec_mamba_cfg* cfg) {
+  if (!cfg) return 0;
+  Arena ar;
+  status_word(ar);
+  MambaPlan p;
+  plan_mamba(ar, *cfg, false, p);
+  return ar.size();
+}
+
+HSPEC_API hspec_status hspec_mamba_block_scan(const hspec_mamba_cfg* cfg, const hspec_mamba_w* w,
+                                              const void* h_last, const void* block_hidden, float* out,
+                                              float* S_final, void* workspace, size_t ws_bytes, void* stream) {
+  g_err.clear();
+  if (hspec_status s = check_mamba(cfg, w, true)) return s;
+  if (!h_last || !block_hidden || !out) return fail(HSPEC_ERR_NULL, "h_last, block_hidden or out is NULL");
+  if (hspec_status s = check_ws(workspace, ws_bytes, hspec_mamba_block_scan_workspace(cfg))) return s;
+  hipStream_t st = (hipStream_t)stream;
+  Arena ar{(char*)workspace};
+  int* status = status_word(ar);
+  MambaPlan p;
+  plan_mamba(ar, *cfg, false, p);
+  HIP_TRY(hspec::launch_zero_words(status, 1, st));
+  if (hspec_status s = run_state(*cfg, *w, h_last, p.st, nullptr, st)) return s;
+  Planes u;
+  HIP_TRY(as_planes(block_hidden, cfg->dtype, p.u_in, u, st));
+  return run_mamba_core(*cfg, *w, u, p, nullptr, 0, out, S_final, st);
+}
+
+HSPEC_API size_t hspec_target_kv_block_attn_workspace(const hspec_attn_cfg* cfg, int max_ctx_len) {
+  if (!cfg) return 0;
+  Arena ar;
+  status_word(ar);
+  AttnPlan p;
+  plan_attn(ar, *cfg, max_ctx_len < 0 ? 0 : max_ctx_len, false, p);
+  return ar.size();
+}
+
+HSPEC_API hspec_status hspec_target_kv_block_attn(const hspec_attn_cfg* cfg, const hspec_attn_w* w, const void* x,
+                                                  const void* k_cache, const void* v_cache,
+                                                  const int32_t* page_table, const int32_t* ctx_lens,
+                                                  int max_ctx_len, float* out, void* workspace, size_t ws_bytes,
+                                                  void* stream) {
+  g_err.clear();
+  if (hspec_status s = check_attn_cfg(cfg, max_ctx_len)) return s;
+  if (hspec_status s = check_attn_w(cfg, w)) return s;
+  if (!x || !k_cache || !v_cache || !page_table || !ctx_lens || !out)
+    return fail(HSPEC_ERR_NULL, "an input or output pointer is NULL");
+  if (hspec_status s = check_ws(workspace, ws_bytes, hspec_target_kv_block_attn_workspace(cfg, max_ctx_len)))
+    return s;
+  hipStream_t st = (hipStream_t)stream;
+  Arena ar{(char*)workspace};
+  int* status = status_word(ar);
+  AttnPlan p;
+  plan_attn(ar, *cfg, max_ctx_len, false, p);
+  HIP_TRY(hspec::launch_zero_words(status, 1, st));
+  Planes xn;
+  HIP_TRY(as_planes(x, cfg->dtype, p.x_in, xn, st));
+  return run_attn_core(*cfg, *w, xn, k_cache, v_cache, page_table, ctx_lens, max_ctx_len, p, nullptr, out, status, st);
+}
+
+HSPEC_API size_t hspec_draft_step_workspace(const hspec_mamba_cfg* mcfg, const hspec_attn_cfg* acfg,
+                                            int max_ctx_len) {
+  if (!mcfg || !acfg) return 0;
+  Arena ar;
+  status_word(ar);
+  DraftPlan p;
+  plan_draft(ar, *mcfg, *acfg, max_ctx_len < 0 ? 0 : max_ctx_len, p);
+  return ar.size();
+}
+
+HSPEC_API hspec_status hspec_draft_step(const hspec_mamba_cfg* mcfg, const hspec_mamba_w* mw, const float* norm1_w,
+                                        const hspec_attn_cfg* acfg, const hspec_attn_w* aw, const float* norm2_w,
+                                        const void* h_last, const void* block_emb, const void* k_cache,
+                                        const void* v_cache, const int32_t* page_table, const int32_t* ctx_lens,
+                                        int max_ctx_len, float* out, void* workspace, size_t ws_bytes, void* stream) {
+  g_err.clear();
+  if (hspec_status s = check_mamba(mcfg, mw, true)) return s;
+  if (hspec_status s = check_attn_cfg(acfg, max_ctx_len)) return s;
+  if (hspec_status s = check_attn_w(acfg, aw)) return s;
+  if (mcfg->B != acfg->B || mcfg->k != acfg->k || mcfg->d_model != acfg->d_model)
+    return fail(HSPEC_ERR_SHAPE, "mamba and attention configs disagree on B, k or d_model");
+  if (mcfg->dtype != acfg->dtype) return fail(HSPEC_ERR_DTYPE, "mamba and attention dtypes differ");
+  if (!norm1_w || !norm2_w || !h_last || !block_emb || !k_cache || !v_cache || !page_table || !ctx_lens || !out)
+    return fail(HSPEC_ERR_NULL, "an input or output pointer is NULL");
+  if (hspec_status s = check_ws(workspace, ws_bytes, hspec_draft_step_workspace(mcfg, acfg, max_ctx_len))) return s;
+  hipStream_t st = (hipStream_t)stream;
+  Arena ar{(char*)workspace};
+  int* status = status_word(ar);
+  DraftPlan p;
+  plan_draft(ar, *mcfg, *acfg, max_ctx_len, p);
+  const int M = mcfg->B * mcfg->k;
+  const bool f32 = is_f32(mcfg->dtype);
+  HIP_TRY(hspec::launch_zero_words(status, 1, st));
+  if (hspec_status s = run_state(*mcfg, *mw, h_last, p.m.st, nullptr, st)) return s;
+  HIP_TRY(hspec::launch_rmsnorm_planes(block_emb, !f32, norm1_w, M, mcfg->d_model, mcfg->eps, p.m.u_hi, p.m.u_lo, st));
+  Planes u{p.m.u_hi, p.m.u_lo};
+  if (hspec_status s = run_mamba_core(*mcfg, *mw, u, p.m, block_emb, !f32, p.x1, nullptr, st)) return s;
+  HIP_TRY(hspec::launch_rmsnorm_planes(p.x1, 0, norm2_w, M, acfg->d_model, acfg->eps, p.at.xn_hi, p.at.xn_lo, st));
+  Planes xn{p.at.xn_hi, p.at.xn_lo};
+  return run_attn_core(*acfg, *aw, xn, k_cache, v_cache, page_table, ctx_lens, max_ctx_len, p.at, p.x1, out, status,
+                       st);
+}
+
+HSPEC_API size_t hspec_ssd_scan_workspace(int B, int T, int H, int P, int N, int G, hspec_dtype dtype) {
+  Arena ar;
+  status_word(ar);
+  if (dtype == HSPEC_F32 && B > 0 && T > 0) {
+    reserve_split(ar, dtype, (size_t)B * T * H * P);
+    reserve_split(ar, dtype, (size_t)B * T * G * N);
+    reserve_split(ar, dtype, (size_t)B * T * G * N);
+    reserve_split(ar, dtype, (size_t)B * H * P * N);
+  }
+  return ar.size();
+}
+
+HSPEC_API hspec_status hspec_ssd_scan(int B, int T, int H, int P, int N, int G, int chunk, hspec_dtype dtype,
+                                      const void* x, const float* dt, const float* A, const void* Bm, const void* Cm,
+                                      const float* Dskip, const void* S0, float* y, float* S_final, void* workspace,
+                                      size_t ws_bytes, void* stream) {
+  g_err.clear();
+  if (!dtype_ok(dtype)) return fail(HSPEC_ERR_DTYPE, "unknown dtype %d", (int)dtype);
+  if (B <= 0 || T <= 0 || H <= 0 || P <= 0 || N <= 0 || G <= 0 || chunk <= 0)
+    return fail(HSPEC_ERR_SHAPE, "non-positive scan dimension");
+  if (H % G) return fail(HSPEC_ERR_SHAPE, "H %% G != 0");
+  if (P != 64) return fail(HSPEC_ERR_UNSUPPORTED, "P must be 64, got %d", P);
+  if (N != 16 && N != 32 && N != 64 && N != 128) return fail(HSPEC_ERR_UNSUPPORTED, "N must be 16/32/64/128");
+  if (chunk > 16) return fail(HSPEC_ERR_UNSUPPORTED, "chunk must be <= 16");
+  if (!x || !dt || !A || !Bm || !Cm || !Dskip || !y) return fail(HSPEC_ERR_NULL, "a scan pointer is NULL");
+  if (hspec_status s = check_ws(workspace, ws_bytes, hspec_ssd_scan_workspace(B, T, H, P, N, G, dtype))) return s;
+  hipStream_t st = (hipStream_t)stream;
+  Arena ar{(char*)workspace};
+  int* status = status_word(ar);
+  SplitSlot sx, sb, sc, ss;
+  if (dtype == HSPEC_F32) {
+    sx = reserve_split(ar, dtype, (size_t)B * T * H * P);
+    sb = reserve_split(ar, dtype, (size_t)B * T * G * N);
+    sc = reserve_split(ar, dtype, (size_t)B * T * G * N);
+    ss = reserve_split(ar, dtype, (size_t)B * H * P * N);
+  }
+  HIP_TRY(hspec::launch_zero_words(status, 1, st));
+  Planes px, pb, pc, ps;
+  HIP_TRY(as_planes(x, dtype, sx, px, st));
+  HIP_TRY(as_planes(Bm, dtype, sb, pb, st));
+  HIP_TRY(as_planes(Cm, dtype, sc, pc, st));
+  if (S0) HIP_TRY(as_planes(S0, dtype, ss, ps, st));
+  hspec::ScanArgs a;
+  a.x_hi = px.hi; a.x_lo = px.lo; a.dt = dt; a.A = A; a.A_is_log = 0;
+  a.B_hi = pb.hi; a.B_lo = pb.lo; a.C_hi = pc.hi; a.C_lo = pc.lo; a.Dskip = Dskip;
+  a.S0_hi = S0 ? ps.hi : nullptr; a.S0_lo = S0 ? ps.lo : nullptr;
+  a.y = y; a.S_final = S_final;
+  a.B = B; a.T = T; a.H = H; a.P = P; a.N = N; a.G = G; a.chunk = chunk;
+  a.x_ld = H * P; a.bc_ld = G * N; a.dt_ld = H;
+  HIP_TRY(hspec::launch_ssd_scan(a, st));
+  return HSPEC_OK;
+}
+
+HSPEC_API size_t hspec_paged_attn_workspace(const hspec_attn_cfg* cfg, int max_ctx_len) {
+  if (!cfg) return 0;
+  Arena ar;
+  status_word(ar);
+  AttnPlan p;
+  const size_t M = (size_t)cfg->B * cfg->k;
+  p.qin = reserve_split(ar, cfg->dtype, M * cfg->Hq * cfg->D);
+  p.kbin = reserve_split(ar, cfg->dtype, M * cfg->Hkv * cfg->D);
+  p.vbin = reserve_split(ar, cfg->dtype, M * cfg->Hkv * cfg->D);
+  plan_sweep(ar, *cfg, max_ctx_len < 0 ? 0 : max_ctx_len, p);
+  return ar.size();
+}
+
+HSPEC_API hspec_status hspec_paged_attn(const hspec_attn_cfg* cfg, const void* q, const void* k_blk,
+                                        const void* v_blk, const void* k_cache, const void* v_cache,
+                                        const int32_t* page_table, const int32_t* ctx_lens, int max_ctx_len, float* o,
+                                        void* workspace, size_t ws_bytes, void* stream) {
+  g_err.clear();
+  if (hspec_status s = check_attn_cfg(cfg, max_ctx_len)) return s;
+  if (!q || !k_blk || !v_blk || !k_cache || !v_cache || !page_table || !ctx_lens || !o)
+    return fail(HSPEC_ERR_NULL, "an input or output pointer is NULL");
+  if (hspec_status s = check_ws(workspace, ws_bytes, hspec_paged_attn_workspace(cfg, max_ctx_len))) return s;
+  hipStream_t st = (hipStream_t)stream;
+  Arena ar{(char*)workspace};
+  int* status = status_word(ar);
+  AttnPlan p;
+  const size_t M = (size_t)cfg->B * cfg->k;
+  p.qin = reserve_split(ar, cfg->dtype, M * cfg->Hq * cfg->D);
+  p.kbin = reserve_split(ar, cfg->dtype, M * cfg->Hkv * cfg->D);
+  p.vbin = reserve_split(ar, cfg->dtype, M * cfg->Hkv * cfg->D);
+  plan_sweep(ar, *cfg, max_ctx_len, p);
+  HIP_TRY(hspec::launch_zero_words(status, 1, st));
+  Planes pq, pk, pv, kc, vc;
+  HIP_TRY(as_planes(q, cfg->dtype, p.qin, pq, st));
+  HIP_TRY(as_planes(k_blk, cfg->dtype, p.kbin, pk, st));
+  HIP_TRY(as_planes(v_blk, cfg->dtype, p.vbin, pv, st));
+  HIP_TRY(as_planes(k_cache, cfg->dtype, p.kc, kc, st));
+  HIP_TRY(as_planes(v_cache, cfg->dtype, p.vc, vc, st));
+  hspec::AttnArgs a = sweep_args(*cfg, p, page_table, ctx_lens, max_ctx_len, status);
+  a.q_hi = pq.hi; a.q_lo = pq.lo; a.kb_hi = pk.hi; a.kb_lo = pk.lo; a.vb_hi = pv.hi; a.vb_lo = pv.lo;
+  a.kc_hi = kc.hi; a.kc_lo = kc.lo; a.vc_hi = vc.hi; a.vc_lo = vc.lo;
+  a.o_f32 = o;
+  HIP_TRY(hspec::launch_attention(a, st));
+  return HSPEC_OK;
+}
+
+HSPEC_API hspec_status hspec_gather_slots(int B, int max_pages, int page_size, int num_pages,
+                                          const int32_t* page_table, const int32_t* ctx_lens, int max_ctx_len,
+                                          int32_t* slots, int32_t* status, void* stream) {
+  g_err.clear();
+  if (B <= 0 || max_pages <= 0 || page_size <= 0 || num_pages <= 0 || max_ctx_len < 0)
+    return fail(HSPEC_ERR_SHAPE, "non-positive gather dimension");
+  if (!page_table || !ctx_lens || (!slots && max_ctx_len > 0)) return fail(HSPEC_ERR_NULL, "a gather pointer is NULL");
+  HIP_TRY(hspec::launch_gather_slots(B, max_pages, page_size, num_pages, page_table, ctx_lens, max_ctx_len, slots,
+                                     status, (hipStream_t)stream));
+  return HSPEC_OK;
+}
+
+HSPEC_API size_t hspec_linear_workspace(hspec_dtype dtype, int M, int N, int K) {
+  Arena ar;
+  status_word(ar);
+  if (M > 0 && N > 0 && K > 0) {
+    reserve_split(ar, dtype, (size_t)M * K);
+    reserve_split(ar, dtype, (size_t)N * K);
+  }
+  return ar.size();
+}
+
+HSPEC_API hspec_status hspec_linear(hspec_dtype dtype, int M, int N, int K, const void* A, const void* W,
+                                    const float* R, float* C, void* workspace, size_t ws_bytes, void* stream) {
+  g_err.clear();
+  if (!dtype_ok(dtype)) return fail(HSPEC_ERR_DTYPE, "unknown dtype %d", (int)dtype);
+  if (M <= 0 || N <= 0 || K <= 0) return fail(HSPEC_ERR_SHAPE, "non-positive GEMM dimension");
+  if (K % 8) return fail(HSPEC_ERR_UNSUPPORTED, "K must be a multiple of 8");
+  if (!A || !W || !C) return fail(HSPEC_ERR_NULL, "A, W or C is NULL");
+  if (hspec_status s = check_ws(workspace, ws_bytes, hspec_linear_workspace(dtype, M, N, K))) return s;
+  hipStream_t st = (hipStream_t)stream;
+  Arena ar{(char*)workspace};
+  int* status = status_word(ar);
+  SplitSlot sa = reserve_split(ar, dtype, (size_t)M * K), sw = reserve_split(ar, dtype, (size_t)N * K);
+  HIP_TRY(hspec::launch_zero_words(status, 1, st));
+  Planes pa, pw;
+  HIP_TRY(as_planes(A, dtype, sa, pa, st));
+  HIP_TRY(as_planes(W, dtype, sw, pw, st));
+  hspec::GemmArgs g;
+  g.A_hi = pa.hi; g.A_lo = pa.lo; g.lda = K;
+  g.W_hi = pw.hi; g.W_lo = pw.lo; g.ldw = K;
+  g.M = M; g.N = N; g.K = K;
+  g.C = C; g.ldc = N; g.R = R; g.ldr = N; g.r_bf16 = 0;
+  HIP_TRY(hspec::launch_gemm(g, st));
+  return HSPEC_OK;
+}
+
+HSPEC_API hspec_status hspec_read_status(const void* workspace, int32_t* status, void* stream) {
+  g_err.clear();
+  if (!workspace || !status) return fail(HSPEC_ERR_NULL, "workspace or status is NULL");
+  hipStream_t st = (hipStream_t)stream;
+  HIP_TRY(hipMemcpyAsync(status, workspace, sizeof(int32_t), hipMemcpyDeviceToHost, st));
+  HIP_TRY(hipStreamSynchronize(st));
+  return HSPEC_OK;
+}
+
+HSPEC_API const char* hspec_status_string(hspec_status s) {
+  switch (s) {
+    case HSPEC_OK: return "ok";
+    case HSPEC_ERR_NULL: return "null pointer";
+    case HSPEC_ERR_SHAPE: return "bad shape";
+    case HSPEC_ERR_DTYPE: return "bad dtype";
+    case HSPEC_ERR_UNSUPPORTED: return "unsupported dimension";
+    case HSPEC_ERR_WORKSPACE: return "workspace too small or misaligned";
+    case HSPEC_ERR_LAUNCH: return "kernel launch failed";
+  }
+  return "unknown status";
+}
+
+HSPEC_API const char* hspec_last_error(void) { return g_err.c_str(); }

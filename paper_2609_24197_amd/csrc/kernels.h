@@ -1,0 +1,99 @@
+// Internal launchers of the HIP kernels (not part of the C ABI).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace hspec {
+
+typedef __bf16 bf16;
+
+// C[M,N] = A[M,K] * W[N,K]^T (+ R), fp32 accumulate.  *_lo planes are optional.
+struct GemmArgs {
+  const bf16* A_hi = nullptr; const bf16* A_lo = nullptr; int lda = 0;
+  const bf16* W_hi = nullptr; const bf16* W_lo = nullptr; int ldw = 0;
+  int M = 0, N = 0, K = 0;
+  float* C = nullptr; int ldc = 0;             // fp32 result (optional)
+  const void* R = nullptr; int ldr = 0; int r_bf16 = 0;   // residual added (optional)
+  bf16* C_hi = nullptr; bf16* C_lo = nullptr; int ldch = 0;  // bf16 planes of the result
+};
+hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
+
+// Paged block attention (split-K sweep over the target cache + block keys, then reduce).
+struct AttnArgs {
+  const bf16 *q_hi = nullptr, *q_lo = nullptr;        // [B, T, Hq, D] post-RoPE
+  const bf16 *kb_hi = nullptr, *kb_lo = nullptr;      // [B, T, Hkv, D] post-RoPE
+  const bf16 *vb_hi = nullptr, *vb_lo = nullptr;
+  const bf16 *kc_hi = nullptr, *kc_lo = nullptr;      // [num_pages, ps, Hkv, D]
+  const bf16 *vc_hi = nullptr, *vc_lo = nullptr;
+  const int32_t* page_table = nullptr;                // [B, max_pages]
+  const int32_t* ctx_lens = nullptr;                  // [B]
+  int B = 0, T = 0, Hq = 0, Hkv = 0, D = 0, ps = 0, max_pages = 0, num_pages = 0;
+  int window = 0, causal = 0, max_ctx_len = 0, split = 0, max_splits = 0;
+  float scale_log2 = 0.f;
+  float* part_o = nullptr;    // [B*Hkv*max_splits, R, D]
+  float* part_ml = nullptr;   // [B*Hkv*max_splits, R, 2]
+  float* o_f32 = nullptr;     // [B, T, Hq, D] (one of o_f32 / o_bf16)
+  bf16* o_bf16 = nullptr;
+  int* status = nullptr;
+};
+hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
+size_t attention_partials_bytes(int B, int Hkv, int max_splits, int R, int D);
+int attention_default_split(int B, int Hkv, int max_ctx_len);
+
+hipError_t launch_gather_slots(int B, int max_pages, int ps, int num_pages, const int32_t* page_table,
+                               const int32_t* ctx_lens, int max_ctx_len, int32_t* slots, int* status,
+                               hipStream_t s);
+
+// Chunked SSD scan from an injected state.
+struct ScanArgs {
+  const bf16 *x_hi = nullptr, *x_lo = nullptr;        // [B, T, H, P]
+  const float* dt = nullptr;                          // [B, T, H] (post-softplus)
+  const float* A = nullptr;                           // [H]: A, or A_log when A_is_log
+  int A_is_log = 0;                                   // A_h = -exp(A_log[h])
+  const bf16 *B_hi = nullptr, *B_lo = nullptr;        // [B, T, G, N]
+  const bf16 *C_hi = nullptr, *C_lo = nullptr;
+  const float* Dskip = nullptr;                       // [H]
+  const bf16 *S0_hi = nullptr, *S0_lo = nullptr;      // [B, H, P, N] or null
+  float* y = nullptr;                                 // [B, T, H, P]
+  float* S_final = nullptr;                           // [B, H, P, N] or null
+  int B = 0, T = 0, H = 0, P = 0, N = 0, G = 0, chunk = 0;
+  int x_ld = 0;      // elements between consecutive tokens of x (>= H*P)
+  int bc_ld = 0;     // elements between consecutive tokens of B and C (>= G*N)
+  int dt_ld = 0;     // elements between consecutive tokens of dt (>= H)
+};
+hipError_t launch_ssd_scan(const ScanArgs& a, hipStream_t s);
+
+// Elementwise / normalisation kernels.
+// out = x / sqrt(mean(x^2) + eps) * w, rows of n; x is fp32 or bf16; outputs bf16 hi/lo planes.
+hipError_t launch_rmsnorm_planes(const void* x, int x_bf16, const float* w, int rows, int n, float eps,
+                                 bf16* out_hi, bf16* out_lo, hipStream_t s);
+// Depthwise causal conv (zero left state) + SiLU over the xBC slice of zxbcdt, split into
+// x (bf16 planes) and B, C (bf16 planes); dt = softplus(dt_raw + dt_bias).
+struct ConvArgs {
+  const float* zxbcdt = nullptr;    // [B*T, d_in_proj]
+  const void* conv_w = nullptr;     // [conv_dim, K] storage dtype
+  const void* conv_b = nullptr;     // [conv_dim]
+  int w_bf16 = 1;
+  const float* dt_bias = nullptr;   // [H]
+  int B = 0, T = 0, H = 0, P = 0, G = 0, N = 0, K = 0;
+  bf16 *x_hi = nullptr, *x_lo = nullptr;   // [B*T, H*P]
+  bf16 *B_hi = nullptr, *B_lo = nullptr;   // [B*T, G*N]
+  bf16 *C_hi = nullptr, *C_lo = nullptr;
+  float* dt = nullptr;                     // [B*T, H]
+};
+hipError_t launch_conv_split(const ConvArgs& a, hipStream_t s);
+// yn = RMSNorm_group(y * SiLU(z)) * w -> bf16 planes.  z rows have stride z_ld.
+hipError_t launch_gated_rmsnorm(const float* y, const float* z, int z_ld, const float* w, int rows,
+                                int n, int G, float eps, bf16* out_hi, bf16* out_lo, hipStream_t s);
+// q/k per-head RMSNorm + RoPE at position ctx_len + j; v copied.  qkv rows [Hq*D | Hkv*D | Hkv*D].
+hipError_t launch_qk_norm_rope(const float* qkv, const float* qw, const float* kw, const int32_t* ctx_lens,
+                               int B, int T, int Hq, int Hkv, int D, float eps, double theta,
+                               bf16* q_hi, bf16* q_lo, bf16* k_hi, bf16* k_lo, bf16* v_hi, bf16* v_lo,
+                               hipStream_t s);
+// fp32 -> bf16 hi/lo planes (lo optional).
+hipError_t launch_split_planes(const float* x, size_t n, bf16* hi, bf16* lo, hipStream_t s);
+// Zero n int32 words (device status, counters) with a kernel, graph-capture safe.
+hipError_t launch_zero_words(int* p, int n, hipStream_t s);
+
+}  // namespace hspec

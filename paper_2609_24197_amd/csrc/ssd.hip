@@ -1,0 +1,241 @@
+// Chunked SSD scan of the Mamba-2 selective recurrence from an injected initial state
+// (H-Spec Sec. 3.3.1: the Mamba kernel starts from the projected last-token state and
+// evaluates every draft position in one pass).
+//
+// Per head (scalar decay a_t = exp(dt_t A)), within a chunk with l_t = sum_{u<=t} dt_u A:
+//   y_t = exp(l_t) C_t S_in^T + sum_{s<=t} exp(l_t - l_s) dt_s (C_t . B_s) x_s + D x_t
+//   S_out = exp(l_end) S_in + sum_s exp(l_end - l_s) dt_s x_s (outer) B_s
+// One wave owns one (request, head).  C S_in^T (16 x N x 64) and C B^T (16 x N x 16) run on
+// v_mfma_f32_16x16x32_bf16; operands given as bf16 hi/lo planes use three products so fp32
+// values survive.  The 16x16 decay-weighted mixing matrix and the x tile go through LDS and
+// the intra-chunk product is done in fp32 on the VALU.  The chunk-local cumulative sum of
+// dt*A is a 16-lane shuffle scan.  When the block fits one chunk and no final state is
+// requested, the initial state is read straight from global memory into MFMA fragments;
+// otherwise the fp32 state lives in LDS between chunks.
+#include "common.h"
+#include "kernels.h"
+
+namespace hspec {
+
+namespace {
+
+constexpr int P = 64;
+constexpr int QMAX = 16;
+
+template <int N, bool MULTI>
+struct ScanLds {
+  static constexpr int XT = P * (QMAX + 1);          // x^T tile, fp32, padded rows
+  static constexpr int MM = QMAX * (QMAX + 1);        // mixing matrix, fp32
+  static constexpr int BT = MULTI ? N * (QMAX + 1) : 0;   // B^T tile, fp32
+  static constexpr int ST = MULTI ? P * (N + 1) : 0;      // state, fp32, padded rows
+  static constexpr int BYTES = 4 * (XT + MM + BT + ST);
+};
+
+__device__ __forceinline__ bf16x8 ld8_or0(const bf16* p, bool ok) { return ok ? ld8(p) : zero8(); }
+
+__device__ __forceinline__ void split8(const float* v, bf16x8& hi, bf16x8& lo) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const bf16 h = f2bf(v[e]);
+    hi[e] = h;
+    lo[e] = f2bf(v[e] - bf2f(h));
+  }
+}
+
+template <int N, bool MULTI>
+__global__ void __launch_bounds__(64) ssd_scan_kernel(ScanArgs a) {
+  constexpr int NS = (N + 31) / 32;
+  using LD = ScanLds<N, MULTI>;
+  extern __shared__ __align__(16) float sm[];
+  float* xT = sm;                       // [P][QMAX+1]
+  float* Mm = xT + LD::XT;              // [QMAX][QMAX+1]
+  float* Bt = Mm + LD::MM;              // [N][QMAX+1]
+  float* S = Bt + LD::BT;               // [P][N+1]
+
+  const int H = a.H, T = a.T, G = a.G;
+  const int b = blockIdx.x / H, h = blockIdx.x % H;
+  const int grp = h / (H / G);
+  const int lane = threadIdx.x, g4 = lane >> 4, l16 = lane & 15;
+  const float Ah = a.A_is_log ? -__expf(a.A[h]) : a.A[h], Dh = a.Dskip[h];
+  const size_t s0_off = ((size_t)b * H + h) * P * N;
+
+  if constexpr (MULTI) {
+    for (int p = 0; p < P; ++p) {
+      for (int n = lane; n < N; n += 64) {
+        float v = 0.f;
+        if (a.S0_hi) {
+          v = bf2f(a.S0_hi[s0_off + p * N + n]);
+          if (a.S0_lo) v += bf2f(a.S0_lo[s0_off + p * N + n]);
+        }
+        S[p * (N + 1) + n] = v;
+      }
+    }
+    __syncthreads();
+  }
+
+  for (int c0 = 0; c0 < T; c0 += a.chunk) {
+    const int Qc = min(a.chunk, T - c0);
+    // dt and the inclusive cumulative sum of dt*A over the chunk (lanes 0..15)
+    const float dtv = l16 < Qc ? a.dt[(size_t)(b * T + c0 + l16) * a.dt_ld + h] : 0.f;
+    float cum = dtv * Ah;
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) {
+      const float v = __shfl_up(cum, off, 16);
+      if (l16 >= off) cum += v;
+    }
+    // x^T tile in LDS: lane = head channel p
+    for (int s = 0; s < QMAX; ++s) {
+      float v = 0.f;
+      if (s < Qc) {
+        const size_t off = (size_t)(b * T + c0 + s) * a.x_ld + (size_t)h * P + lane;
+        v = bf2f(a.x_hi[off]);
+        if (a.x_lo) v += bf2f(a.x_lo[off]);
+      }
+      xT[lane * (QMAX + 1) + s] = v;
+    }
+    // C (A operand, rows t) and B (B operand, columns s) fragments over n
+    bf16x8 cf[NS], cfl[NS], bfr[NS], bfl[NS];
+    const size_t tok_t = (size_t)(b * T + c0 + l16) * a.bc_ld + (size_t)grp * N;
+#pragma unroll
+    for (int ns = 0; ns < NS; ++ns) {
+      const int n = 32 * ns + 8 * g4;
+      const bool ok = l16 < Qc && n < N;
+      cf[ns] = ld8_or0(a.C_hi + tok_t + n, ok);
+      cfl[ns] = a.C_lo ? ld8_or0(a.C_lo + tok_t + n, ok) : zero8();
+      bfr[ns] = ld8_or0(a.B_hi + tok_t + n, ok);
+      bfl[ns] = a.B_lo ? ld8_or0(a.B_lo + tok_t + n, ok) : zero8();
+    }
+    // state term C S^T: lane gets rows t = 4 g4 + i, column p = 16 pb + l16
+    f32x4 ys[4];
+#pragma unroll
+    for (int pb = 0; pb < 4; ++pb) {
+      ys[pb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const int p = 16 * pb + l16;
+#pragma unroll
+      for (int ns = 0; ns < NS; ++ns) {
+        const int n = 32 * ns + 8 * g4;
+        bf16x8 sh, sl;
+        bool has_lo;
+        if constexpr (MULTI) {
+          float v[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = n + e < N ? S[p * (N + 1) + n + e] : 0.f;
+          split8(v, sh, sl);
+          has_lo = true;
+        } else {
+          const bool ok = a.S0_hi != nullptr && n < N;
+          sh = ld8_or0(a.S0_hi + s0_off + (size_t)p * N + n, ok);
+          has_lo = a.S0_lo != nullptr;
+          sl = has_lo ? ld8_or0(a.S0_lo + s0_off + (size_t)p * N + n, ok) : zero8();
+        }
+        ys[pb] = mma16(cf[ns], sh, ys[pb]);
+        if (a.C_lo) ys[pb] = mma16(cfl[ns], sh, ys[pb]);
+        if (has_lo) ys[pb] = mma16(cf[ns], sl, ys[pb]);
+      }
+    }
+    // C B^T: lane gets rows t = 4 g4 + i, column s = l16
+    f32x4 cb = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ns = 0; ns < NS; ++ns) {
+      cb = mma16(cf[ns], bfr[ns], cb);
+      if (a.C_lo) cb = mma16(cfl[ns], bfr[ns], cb);
+      if (a.B_lo) cb = mma16(cf[ns], bfl[ns], cb);
+    }
+    const float ell_s = __shfl(cum, l16);            // l_s for this lane's column s
+    const float dt_s = __shfl(dtv, l16);
+    float ell_t[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int t = 4 * g4 + i;
+      ell_t[i] = __shfl(cum, t);
+      const bool ok = l16 <= t && t < Qc;
+      Mm[t * (QMAX + 1) + l16] = ok ? cb[i] * __expf(ell_t[i] - ell_s) * dt_s : 0.f;
+    }
+    if constexpr (MULTI) {
+      // B^T tile for the state update: Bt[n][s]
+      for (int s = 0; s < QMAX; ++s)
+        for (int n = lane; n < N; n += 64) {
+          float v = 0.f;
+          if (s < Qc) {
+            const size_t off = (size_t)(b * T + c0 + s) * a.bc_ld + (size_t)grp * N + n;
+            v = bf2f(a.B_hi[off]);
+            if (a.B_lo) v += bf2f(a.B_lo[off]);
+          }
+          Bt[n * (QMAX + 1) + s] = v;
+        }
+    }
+    __syncthreads();
+    // y = exp(l_t) (C S^T) + M x + D x
+#pragma unroll
+    for (int pb = 0; pb < 4; ++pb) {
+      const int p = 16 * pb + l16;
+      const float* xr = xT + p * (QMAX + 1);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t = 4 * g4 + i;
+        if (t >= Qc) continue;
+        const float* mr = Mm + t * (QMAX + 1);
+        float acc = __expf(ell_t[i]) * ys[pb][i] + Dh * xr[t];
+        for (int s = 0; s <= t; ++s) acc += mr[s] * xr[s];
+        a.y[(size_t)(b * T + c0 + t) * H * P + (size_t)h * P + p] = acc;
+      }
+    }
+    if constexpr (MULTI) {
+      // S <- exp(l_end) S + sum_s exp(l_end - l_s) dt_s x_s (outer) B_s ; lane = row p
+      const float ell_end = __shfl(cum, Qc - 1);
+      const float dec = __expf(ell_end);
+      float wx[QMAX];
+#pragma unroll
+      for (int s = 0; s < QMAX; ++s) {
+        const float w = __shfl(dtv, s) * __expf(ell_end - __shfl(cum, s));
+        wx[s] = s < Qc ? w * xT[lane * (QMAX + 1) + s] : 0.f;
+      }
+      float* Sr = S + lane * (N + 1);
+      for (int n = 0; n < N; ++n) {
+        const float* br = Bt + n * (QMAX + 1);
+        float acc = dec * Sr[n];
+#pragma unroll
+        for (int s = 0; s < QMAX; ++s) acc += wx[s] * br[s];
+        Sr[n] = acc;
+      }
+    }
+    __syncthreads();
+  }
+
+  if (a.S_final) {
+    if constexpr (MULTI) {
+      for (int p = 0; p < P; ++p)
+        for (int n = lane; n < N; n += 64) a.S_final[s0_off + p * N + n] = S[p * (N + 1) + n];
+    }
+  }
+}
+
+template <int N>
+hipError_t launch_n(const ScanArgs& a, hipStream_t s) {
+  const bool multi = a.S_final != nullptr || a.T > a.chunk;
+  constexpr int lds_multi = ScanLds<N, true>::BYTES, lds_single = ScanLds<N, false>::BYTES;
+  if (multi) {
+    auto kern = ssd_scan_kernel<N, true>;
+    hipLaunchKernelGGL(kern, dim3(a.B * a.H), dim3(64), lds_multi, s, a);
+  } else {
+    auto kern = ssd_scan_kernel<N, false>;
+    hipLaunchKernelGGL(kern, dim3(a.B * a.H), dim3(64), lds_single, s, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_ssd_scan(const ScanArgs& a, hipStream_t s) {
+  if (a.B <= 0 || a.T <= 0 || a.H <= 0) return hipSuccess;
+  if (a.P != P || a.chunk < 1 || a.chunk > QMAX) return hipErrorInvalidValue;
+  switch (a.N) {
+    case 16: return launch_n<16>(a, s);
+    case 32: return launch_n<32>(a, s);
+    case 64: return launch_n<64>(a, s);
+    case 128: return launch_n<128>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace hspec

@@ -1,0 +1,138 @@
+"""The C ABI on a host without a GPU: every declared symbol is exported, and host-checkable
+argument errors return their status before anything touches the device."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2609_24197_amd import hspec, inputs as I
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hspec.h")
+FAKE = C.c_void_p(1 << 20)        # never dereferenced: validation fails first
+
+
+def _lib():
+    if not os.path.exists(hspec.lib_path()):
+        pytest.skip("libhspec.so not built")
+    return hspec.lib()
+
+
+def declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(hspec_[a-z_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported():
+    L = _lib()
+    names = declared()
+    assert len(names) >= 18, names
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(hspec.EXPORTS), set(names) ^ set(hspec.EXPORTS)
+
+
+def test_status_strings():
+    L = _lib()
+    for s in range(7):
+        assert L.hspec_status_string(s)
+    assert L.hspec_status_string(99) == b"unknown status"
+
+
+def _ws_big():
+    return C.c_void_p(1 << 20), 1 << 40
+
+
+def test_linear_validation():
+    L = _lib()
+    ws, n = _ws_big()
+    assert L.hspec_linear(0, 0, 8, 8, FAKE, FAKE, None, FAKE, ws, n, None) == 2
+    assert L.hspec_linear(0, 4, 8, 7, FAKE, FAKE, None, FAKE, ws, n, None) == 4
+    assert L.hspec_linear(0, 4, 8, 8, None, FAKE, None, FAKE, ws, n, None) == 1
+    assert L.hspec_linear(7, 4, 8, 8, FAKE, FAKE, None, FAKE, ws, n, None) == 3
+    assert L.hspec_linear(0, 4, 8, 8, FAKE, FAKE, None, FAKE, ws, 16, None) == 5
+    assert L.hspec_linear(0, 4, 8, 8, FAKE, FAKE, None, FAKE, C.c_void_p((1 << 20) + 8), n, None) == 5
+    assert b"aligned" in L.hspec_last_error()
+    assert L.hspec_linear(0, 4, 8, 8, FAKE, FAKE, None, FAKE, None, n, None) == 5
+
+
+def test_scan_validation():
+    L = _lib()
+    ws, n = _ws_big()
+    args = [FAKE] * 9
+    ok = (2, 16, 4, 64, 128, 1, 16, 0)
+    def call(B=2, T=16, H=4, P=64, N=128, G=1, chunk=16, dt=0, ptrs=args):
+        return L.hspec_ssd_scan(B, T, H, P, N, G, chunk, dt, *ptrs, ws, n, None)
+    assert call(P=32) == 4
+    assert call(N=96) == 4
+    assert call(G=3) == 2
+    assert call(chunk=17) == 4
+    assert call(chunk=0) == 2
+    assert call(dt=5) == 3
+    assert call(ptrs=[None] + args[1:]) == 1
+    assert ok
+
+
+def _attn_cfg(**kw):
+    cfg = I.CONFIGS[3]
+    c = hspec.attn_cfg(cfg, 512, 20000)
+    for k, v in kw.items():
+        setattr(c, k, v)
+    return c
+
+
+def test_attention_validation():
+    L = _lib()
+    ws, n = _ws_big()
+    def call(c, maxL=8192):
+        return L.hspec_paged_attn(C.byref(c), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, maxL, FAKE, ws, n, None)
+    assert call(_attn_cfg(Hkv=5)) == 2
+    assert call(_attn_cfg(D=96)) == 4
+    assert call(_attn_cfg(k=64)) == 4           # k * g = 256 query rows
+    assert call(_attn_cfg(window=-1)) == 2
+    assert call(_attn_cfg(window=8)) == 2       # k > window
+    assert call(_attn_cfg(split_tokens=100)) == 2
+    assert call(_attn_cfg(page_size=0)) == 2
+    assert call(_attn_cfg(dtype=9)) == 3
+    assert call(_attn_cfg(), maxL=-1) == 2
+    c = _attn_cfg()
+    assert L.hspec_paged_attn(C.byref(c), FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, 8192, FAKE, ws, n, None) == 1
+
+
+def test_draft_step_validation():
+    L = _lib()
+    ws, n = _ws_big()
+    cfg = I.CONFIGS[3]
+    mc, mw = hspec.mamba_cfg(cfg), hspec.MambaW(*([FAKE.value] * 10))
+    aw = hspec.AttnW(*([FAKE.value] * 6))
+
+    def call(mc, ac):
+        return L.hspec_draft_step(C.byref(mc), C.byref(mw), FAKE, C.byref(ac), C.byref(aw), FAKE, FAKE, FAKE, FAKE,
+                                  FAKE, FAKE, FAKE, 8192, FAKE, ws, n, None)
+    ac = _attn_cfg()
+    bad = hspec.mamba_cfg(cfg.replace(B=63))
+    assert call(bad, ac) == 2
+    assert call(hspec.mamba_cfg(cfg.replace(dtype="f32")), ac) == 3
+    assert call(hspec.mamba_cfg(cfg.replace(P=32)), ac) == 4
+    assert call(hspec.mamba_cfg(cfg.replace(G=3)), ac) == 2
+    assert call(hspec.mamba_cfg(cfg.replace(chunk=32)), ac) == 4
+    mw0 = hspec.MambaW(*([FAKE.value] * 9 + [None]))
+    assert L.hspec_draft_step(C.byref(mc), C.byref(mw0), FAKE, C.byref(ac), C.byref(aw), FAKE, FAKE, FAKE, FAKE,
+                              FAKE, FAKE, FAKE, 8192, FAKE, ws, n, None) == 1
+
+
+def test_workspace_queries_are_consistent():
+    _lib()
+    for num in (1, 2, 3, 5):
+        cfg = I.CONFIGS[num]
+        a = hspec.draft_step_workspace(cfg, 1024, 30000, 4096)
+        b = hspec.draft_step_workspace(cfg, 1024, 30000, 16384)
+        assert 0 < a <= b
+        assert a % 256 == 0
+        assert hspec.mamba_block_scan_workspace(cfg) > 0
+        assert hspec.paged_attn_workspace(cfg, 1024, 30000, 4096) > 0
+    # the state projection of config 3 keeps S0 on chip only as bf16 planes: 2 x 2 bytes
+    cfg = I.CONFIGS[3]
+    assert hspec.mamba_block_scan_workspace(cfg) >= 4 * cfg.B * cfg.d_S

@@ -1,0 +1,125 @@
+"""GPU parity of the layer-level calls and the drafting step against the float64 oracle."""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+import oracle.hspec_oracle as O  # noqa: E402
+from gpu_util import assert_close, dev, empty, host  # noqa: E402
+from paper_2609_24197_amd import hspec, inputs as I  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+SMALL = {
+    "cfg1": I.CONFIGS[1],
+    "small_bf16": I.StepConfig(name="s", B=3, k=16, d_model=512, H=8, P=64, N=128, G=1, chunk=16, Hq=32, Hkv=8,
+                               D=128, lengths="list:300,0,77"),
+    "k7_chunk4_g2": I.StepConfig(name="s", B=2, k=7, d_model=256, H=4, P=64, N=16, G=2, chunk=4, Hq=8, Hkv=2,
+                                 D=128, lengths="list:45,200"),
+    "window_causal": I.StepConfig(name="s", B=2, k=16, d_model=256, H=4, P=64, N=128, G=1, chunk=8, Hq=32, Hkv=8,
+                                  D=128, lengths="list:900,100", window=256, block_causal=True),
+}
+
+
+def _weights(cfg, seed=0):
+    W = I.make_weights(cfg, seed)
+    return W, dev(W)
+
+
+@pytest.mark.parametrize("name", sorted(SMALL))
+def test_mamba_block_scan(name):
+    cfg = SMALL[name]
+    print(f"[mamba_block_scan] {name}", flush=True)
+    W, Wd = _weights(cfg, 1)
+    x = I.make_inputs(cfg, seed=1)
+    d = dev(dict(h_last=x["h_last"], u=x["block_emb"]))
+    ws = hspec.workspace(hspec.mamba_block_scan_workspace(cfg))
+    out = empty((cfg.B, cfg.k, cfg.d_model))
+    Sf = empty((cfg.B, cfg.H, cfg.P, cfg.N))
+    hspec.mamba_block_scan(cfg, Wd, d["h_last"], d["u"], out, ws, S_final=Sf)
+    S0, _ = O.state_init(x["h_last"], W["W_r"], W["W_dS"], cfg.H, cfg.P, cfg.N)
+    ref, parts = O.mamba_mixer(O.f64(x["block_emb"]), S0, W, cfg, return_parts=True)
+    assert_close(host(out), ref, "out")
+    assert_close(host(Sf), parts["S_final"], "S_final")
+
+
+@pytest.mark.parametrize("name", sorted(SMALL))
+def test_target_kv_block_attn(name):
+    cfg = SMALL[name]
+    print(f"[target_kv_block_attn] {name}", flush=True)
+    W, Wd = _weights(cfg, 2)
+    x = I.make_inputs(cfg, seed=2, extra_pages=2)
+    xin = I.normal("attn_x", (cfg.B, cfg.k, cfg.d_model), 1.0, 2, cfg.dtype)
+    d = dev(dict(x, xin=xin))
+    maxL = int(max(x["ctx_lens"]))
+    ws = hspec.workspace(hspec.target_kv_block_attn_workspace(cfg, x["page_table"].shape[1], x["num_pages"], maxL))
+    out = empty((cfg.B, cfg.k, cfg.d_model))
+    hspec.target_kv_block_attn(cfg, Wd, d["xin"], d, out, ws, maxL)
+    ref = O.attention_layer(O.f64(xin), W, x, cfg)
+    assert_close(host(out), ref, "out")
+    assert hspec.read_status(ws) == 0
+
+
+def _draft(cfg, W, Wd, x, maxL=None):
+    d = dev(x)
+    maxL = int(max(x["ctx_lens"])) if maxL is None else maxL
+    ws = hspec.workspace(hspec.draft_step_workspace(cfg, x["page_table"].shape[1], x["num_pages"], maxL))
+    out = empty((cfg.B, cfg.k, cfg.d_model))
+    hspec.draft_step(cfg, Wd, d, out, ws, maxL)
+    return host(out), hspec.read_status(ws)
+
+
+@pytest.mark.parametrize("name", sorted(SMALL))
+def test_draft_step_small(name):
+    cfg = SMALL[name]
+    print(f"[draft_step] {name}", flush=True)
+    W, Wd = _weights(cfg, 3)
+    x = I.make_inputs(cfg, seed=3)
+    out, st = _draft(cfg, W, Wd, x)
+    assert st == 0
+    assert_close(out, O.draft_step(W, x, cfg), "out")
+
+
+def test_draft_step_zero_inputs():
+    """e = 0 and h_last = 0: out = W_o mean(V over cache and block) per query head."""
+    cfg = SMALL["small_bf16"]
+    W, Wd = _weights(cfg, 4)
+    x = I.make_inputs(cfg, seed=4)
+    x["h_last"] = np.zeros_like(x["h_last"])
+    x["block_emb"] = np.zeros_like(x["block_emb"])
+    out, _ = _draft(cfg, W, Wd, x)
+    assert_close(out, O.draft_step(W, x, cfg), "out")
+
+
+def test_draft_step_deterministic():
+    cfg = SMALL["small_bf16"]
+    W, Wd = _weights(cfg, 5)
+    x = I.make_inputs(cfg, seed=5)
+    a, _ = _draft(cfg, W, Wd, x)
+    b, _ = _draft(cfg, W, Wd, x)
+    assert np.array_equal(a, b)
+
+
+@pytest.mark.slow
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("num", [2, 3, 4, 5])
+def test_draft_step_full_config(num):
+    """The full-size workloads, in the launch configuration the benchmark times.  The oracle
+    recomputes the first and the last request of the batch (all positions, all outputs)."""
+    import torch
+    cfg = I.CONFIGS[num]
+    print(f"[draft_step full] config {num}: {cfg}", flush=True)
+    W = I.make_weights(cfg, 0)
+    x = I.make_inputs(cfg, 0)
+    Wd = dev(W)
+    out, st = _draft(cfg, W, Wd, x)
+    assert st == 0
+    del Wd
+    torch.cuda.empty_cache()
+    req = sorted({0, cfg.B - 1})
+    print(f"  oracle on requests {req}", flush=True)
+    ref = O.draft_step(W, x, cfg, requests=req)
+    assert np.all(np.isfinite(out))
+    assert_close(out[req], ref[req], f"config {num}")

@@ -1,0 +1,258 @@
+"""GPU parity of the primitives (GEMM, gather, KV sweep, SSD scan, state projection) against
+the float64 oracle, through the C ABI."""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+import oracle.hspec_oracle as O  # noqa: E402
+from gpu_util import assert_close, dev, empty, host  # noqa: E402
+from paper_2609_24197_amd import hspec, inputs as I  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+def _small_attn_cfg(**kw):
+    base = dict(name="t", B=3, k=16, d_model=256, H=4, P=64, N=16, G=1, chunk=16, Hq=32, Hkv=8, D=128,
+                lengths="list:130,0,77", dtype="bf16")
+    base.update(kw)
+    return I.StepConfig(**base)
+
+
+# ------------------------------------------------------------------------------- GEMM
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("M,N,K", [(4, 256, 256), (64, 1000, 512), (100, 384, 264), (128, 512, 1024),
+                                   (300, 700, 4096), (1, 4096, 4096)])
+def test_linear(dtype, M, N, K):
+    print(f"[linear] dtype={dtype} M={M} N={N} K={K}", flush=True)
+    A = I.normal("lin_A", (M, K), 1.0, 0, dtype)
+    W = I.normal("lin_W", (N, K), K ** -0.5, 0, dtype)
+    R = I.normal("lin_R", (M, N), 1.0, 0, "f32")
+    d = dev(dict(A=A, W=W, R=R))
+    code = hspec.F32 if dtype == "f32" else hspec.BF16
+    ws = hspec.workspace(hspec.linear_workspace(code, M, N, K))
+    out = empty((M, N))
+    hspec.linear(code, d["A"], d["W"], out, ws, R=d["R"])
+    ref = O.f64(A) @ O.f64(W).T + R
+    assert_close(host(out), ref, "C")
+
+
+# ----------------------------------------------------------------------------- gather
+
+def test_gather_slots_bit_exact():
+    cfg = _small_attn_cfg(B=5, lengths="list:1,16,17,300,0")
+    x = I.make_inputs(cfg, seed=1, extra_pages=5, pad_pages=2)
+    d = dev(dict(page_table=x["page_table"], ctx_lens=x["ctx_lens"]))
+    maxL = 320
+    slots = empty((cfg.B, maxL), "i32")
+    st = empty((1,), "i32")
+    st.zero_()
+    hspec.gather_slots(d["page_table"], d["ctx_lens"], cfg.page_size, x["num_pages"], maxL, slots, st)
+    ref = O.gather_slots(x["page_table"], x["ctx_lens"], cfg.page_size, maxL)
+    assert np.array_equal(host(slots), ref)
+    assert int(host(st)[0]) == 0
+
+
+def test_gather_slots_flags_bad_page():
+    pt = np.array([[0, 7, 1]], np.int32)        # page id 7 is outside a pool of 3 pages
+    d = dev(dict(page_table=pt, ctx_lens=np.array([40], np.int32)))
+    slots = empty((1, 48), "i32")
+    st = empty((1,), "i32")
+    st.zero_()
+    hspec.gather_slots(d["page_table"], d["ctx_lens"], 16, 3, 48, slots, st)
+    s = host(slots)[0]
+    assert np.array_equal(s[:16], np.arange(16)) and np.all(s[16:32] == -1)
+    assert np.array_equal(s[32:40], 16 + np.arange(8)) and np.all(s[40:] == -1)
+    assert int(host(st)[0]) & hspec.DEV_BAD_PAGE
+
+
+# ------------------------------------------------------------------------- KV sweep
+
+def _run_attn(cfg, x, max_ctx_len=None, split=0):
+    cfg = cfg.replace(split_tokens=split)
+    d = dev(x)
+    maxL = int(max(x["ctx_lens"])) if max_ctx_len is None else max_ctx_len
+    ws = hspec.workspace(hspec.paged_attn_workspace(cfg, x["page_table"].shape[1], x["num_pages"], maxL))
+    o = empty((cfg.B, cfg.k, cfg.Hq, cfg.D))
+    hspec.paged_attn(cfg, d, o, ws, maxL)
+    return host(o), hspec.read_status(ws)
+
+
+def _ref_attn(cfg, x):
+    return O.paged_attention(x["q"], x["k_blk"], x["v_blk"], x["k_cache"], x["v_cache"], x["page_table"],
+                             x["ctx_lens"], page_size=cfg.page_size, window=cfg.window,
+                             block_causal=cfg.block_causal)
+
+
+ATTN_CASES = {
+    "cfg1_f32": I.CONFIGS[1],
+    "bf16_ragged": _small_attn_cfg(),
+    "k7_g4": _small_attn_cfg(k=7, lengths="list:1000,37,16"),
+    "g8_128rows": _small_attn_cfg(Hq=64, lengths="list:500,1,260"),
+    "d64_mha": _small_attn_cfg(Hq=4, Hkv=4, D=64, k=5, lengths="list:33,64,200"),
+    "window": _small_attn_cfg(window=100, lengths="list:1000,5,333"),
+    "causal": _small_attn_cfg(block_causal=True),
+    "causal_window": _small_attn_cfg(block_causal=True, window=64, lengths="list:700,64,65"),
+    "empty_ctx": _small_attn_cfg(B=2, lengths="list:0,0"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(ATTN_CASES))
+def test_paged_attn(name):
+    cfg = ATTN_CASES[name]
+    print(f"[paged_attn] {name} {cfg}", flush=True)
+    x = I.make_attn_inputs(cfg, seed=2, extra_pages=3)
+    o, st = _run_attn(cfg, x)
+    assert st == 0
+    assert_close(o, _ref_attn(cfg, x), name)
+
+
+def test_paged_attn_split_invariance():
+    """Split sizes 64 .. whole context agree to fp32 rounding; each split size is deterministic."""
+    cfg = _small_attn_cfg(B=2, lengths="list:1000,450")
+    x = I.make_attn_inputs(cfg, seed=3)
+    ref = _ref_attn(cfg, x)
+    outs = {}
+    for split in (64, 128, 448, 1024):
+        o, st = _run_attn(cfg, x, split=split)
+        o2, _ = _run_attn(cfg, x, split=split)
+        assert np.array_equal(o, o2), f"split {split} not deterministic"
+        assert_close(o, ref, f"split={split}")
+        outs[split] = o
+    base = outs[1024]
+    for s, o in outs.items():
+        assert np.max(np.abs(o - base)) <= 1e-5 * max(1.0, np.max(np.abs(base))), s
+
+
+def test_paged_attn_page_permutation_bitwise():
+    cfg = _small_attn_cfg()
+    x = I.make_attn_inputs(cfg, seed=4, extra_pages=4)
+    a, _ = _run_attn(cfg, x)
+    perm = np.random.default_rng(0).permutation(x["num_pages"])
+    y = dict(x)
+    for key in ("k_cache", "v_cache"):
+        arr = np.empty_like(x[key])
+        arr[perm] = x[key]
+        y[key] = arr
+    y["page_table"] = np.where(x["page_table"] >= 0, perm[np.maximum(x["page_table"], 0)], -1).astype(np.int32)
+    b, _ = _run_attn(cfg, y)
+    assert np.array_equal(a, b)
+
+
+def test_paged_attn_poisoned_slots():
+    """NaN/inf in unreferenced pages and in slots at or past ctx_len change nothing."""
+    cfg = _small_attn_cfg(lengths="list:130,3,77")
+    x = I.make_attn_inputs(cfg, seed=5, extra_pages=6)
+    a, _ = _run_attn(cfg, x)
+    y = dict(x)
+    kc, vc = x["k_cache"].copy(), x["v_cache"].copy()
+    used = np.zeros(x["num_pages"], bool)
+    for b, L in enumerate(x["ctx_lens"]):
+        n = (int(L) + 15) // 16
+        pages = x["page_table"][b, :n]
+        used[pages] = True
+        if L % 16:
+            last = pages[-1]
+            kc[last, L % 16:] = 0x7FC0   # bf16 NaN
+            vc[last, L % 16:] = 0x7F80   # bf16 +inf
+    kc[~used] = 0x7FC0
+    vc[~used] = 0xFF80
+    y["k_cache"], y["v_cache"] = kc, vc
+    b_, _ = _run_attn(cfg, y)
+    assert np.array_equal(a, b_)
+
+
+def test_paged_attn_single_key_and_mean():
+    """P1 on the GPU: ctx_len 0 and k = 1 returns v_blk; identical keys return the mean of V."""
+    cfg = _small_attn_cfg(B=1, k=1, lengths="list:0")
+    x = I.make_attn_inputs(cfg, seed=6)
+    o, _ = _run_attn(cfg, x)
+    vb = O.f64(x["v_blk"])[0, 0]
+    assert np.allclose(o[0, 0], np.repeat(vb, cfg.g, axis=0), rtol=0, atol=1e-6)
+    cfg = _small_attn_cfg(B=1, k=4, lengths="list:37")
+    x = I.make_attn_inputs(cfg, seed=7)
+    x["k_cache"][:] = x["k_cache"][0, 0]
+    x["k_blk"][:] = x["k_cache"][0, 0]
+    o, _ = _run_attn(cfg, x)
+    assert_close(o, _ref_attn(cfg, x), "identical keys")
+
+
+def test_paged_attn_flags_bad_inputs():
+    """Out-of-pool page ids and over-long context lengths are flagged, not faulted on."""
+    cfg = _small_attn_cfg(B=2, lengths="list:40,20")
+    x = I.make_attn_inputs(cfg, seed=8)
+    x["page_table"] = x["page_table"].copy()
+    x["page_table"][0, 1] = x["num_pages"] + 100
+    _, st = _run_attn(cfg, x)
+    assert st & hspec.DEV_BAD_PAGE
+    x = I.make_attn_inputs(cfg, seed=8)
+    x["ctx_lens"] = np.array([40, 20000], np.int32)
+    _, st = _run_attn(cfg, x, max_ctx_len=48)
+    assert st & hspec.DEV_BAD_CTX_LEN
+
+
+# ------------------------------------------------------------------------------- scan
+
+SCAN_CASES = [
+    # B, T, H, N, G, chunk, dtype, with S0, final state
+    (2, 16, 8, 128, 1, 16, "bf16", True, False),
+    (2, 16, 8, 128, 1, 16, "bf16", True, True),
+    (1, 4, 8, 16, 1, 4, "f32", True, True),
+    (2, 7, 4, 128, 2, 4, "bf16", True, True),
+    (2, 32, 4, 128, 1, 8, "bf16", True, True),
+    (1, 16, 4, 16, 1, 1, "bf16", False, True),
+    (3, 5, 6, 64, 3, 2, "f32", True, False),
+    (2, 16, 4, 32, 1, 16, "bf16", False, False),
+]
+
+
+@pytest.mark.parametrize("case", SCAN_CASES, ids=[str(c) for c in SCAN_CASES])
+def test_ssd_scan(case):
+    B, T, H, N, G, chunk, dtype, with_s0, fin = case
+    print(f"[ssd_scan] {case}", flush=True)
+    s = I.make_scan_inputs(B, T, H, 64, N, G, seed=T + H, dtype=dtype, s0=with_s0)
+    d = dev({k: v for k, v in s.items() if v is not None})
+    code = hspec.F32 if dtype == "f32" else hspec.BF16
+    ws = hspec.workspace(hspec.ssd_scan_workspace(B, T, H, 64, N, G, code))
+    y = empty((B, T, H, 64))
+    Sf = empty((B, H, 64, N)) if fin else None
+    hspec.ssd_scan(B, T, H, 64, N, G, chunk, code, d["x"], d["dt"], d["A"], d["Bm"], d["Cm"], d["Dskip"],
+                   d.get("S0"), y, Sf, ws)
+    yr, Sr = O.ssd_sequential(s["x"], s["dt"], s["A"], s["Bm"], s["Cm"], s["Dskip"], s["S0"])
+    assert_close(host(y), yr, "y")
+    if fin:
+        assert_close(host(Sf), Sr, "S_final")
+
+
+def test_ssd_scan_zero_input_zero_state():
+    """x = 0 and S0 = 0 give y = 0 and S_final = 0 exactly, for any dt, B, C."""
+    B, T, H, N, G = 2, 16, 4, 128, 1
+    s = I.make_scan_inputs(B, T, H, 64, N, G, seed=1)
+    s["x"] = np.zeros_like(s["x"])
+    d = dev({k: v for k, v in s.items() if v is not None})
+    ws = hspec.workspace(hspec.ssd_scan_workspace(B, T, H, 64, N, G, hspec.BF16))
+    y = empty((B, T, H, 64))
+    Sf = empty((B, H, 64, N))
+    hspec.ssd_scan(B, T, H, 64, N, G, 16, hspec.BF16, d["x"], d["dt"], d["A"], d["Bm"], d["Cm"], d["Dskip"],
+                   None, y, Sf, ws)
+    assert not np.any(host(y)) and not np.any(host(Sf))
+
+
+# -------------------------------------------------------------------- state projection
+
+@pytest.mark.parametrize("cfg", [I.CONFIGS[1], _small_attn_cfg(B=5, d_model=512, H=8, N=128),
+                                 _small_attn_cfg(B=70, d_model=256, H=4, N=128)],
+                         ids=["cfg1", "b5", "b70"])
+def test_state_init(cfg):
+    W = I.make_weights(cfg, seed=3, skip=("W_in", "W_out", "W_q", "W_k", "W_v", "W_o"))
+    x = I.make_inputs(cfg, seed=3)
+    d = dev(dict(W_r=W["W_r"], W_dS=W["W_dS"], h_last=x["h_last"]))
+    Wd = dict(d, W_in=None, conv_w=None, conv_b=None, dt_bias=None, A_log=None, D=None, gnorm_w=None, W_out=None)
+    ws = hspec.workspace(hspec.state_init_workspace(cfg))
+    S0 = empty((cfg.B, cfg.H, cfg.P, cfg.N))
+    hspec.state_init(cfg, Wd, d["h_last"], S0, ws)
+    ref, _ = O.state_init(x["h_last"], W["W_r"], W["W_dS"], cfg.H, cfg.P, cfg.N)
+    assert_close(host(S0), ref, "S0")
