@@ -1,0 +1,197 @@
+"""Benchmark of one H-Spec block-drafting step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3]
+
+A step is one call of hspec_draft_step over the whole batch: state projection from the
+last-token hidden state, the Mamba-2 layer with its chunked scan, and the attention layer
+over the paged target cache plus the block.  Inputs are synthetic, seeded, and resident in
+HBM before timing starts.  Prints one JSON line with the drafted-tokens/s throughput, the
+roofline of the dominant kernel (the state projection, which streams W_dS), the roofline of
+the target-KV sweep, and the float64 CPU oracle timed on a bounded sample of the same
+workload on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+from paper_2609_24197_amd import hspec, inputs as I, roofline as RL  # noqa: E402
+
+METRIC = "drafted tokens/s per draft step at B=64; achieved HBM GB/s vs MI355X peak"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_hash(files) -> str:
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, "paper_2609_24197_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_for(name: str, src_hash: str):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if taken on this source."""
+    p = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(p):
+        return None
+    with open(p) as f:
+        t = json.load(f)
+    e = t.get(name)
+    if not e or e.get("source_hash") != src_hash:
+        return None
+    return e.get("bytes_per_launch")
+
+
+def time_launches(fn, n: int, torch) -> float:
+    """Average duration (s) of n back-to-back launches, HIP events on the launch stream."""
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    fn()
+    torch.cuda.synchronize()
+    s.record()
+    for _ in range(n):
+        fn()
+    e.record()
+    e.synchronize()
+    return s.elapsed_time(e) / 1e3 / n
+
+
+def cpu_baseline(cfg, W, x, n_req: int):
+    """The float64 oracle on the first n_req requests of the same workload (all positions)."""
+    import oracle.hspec_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        blas = 1
+    cores = max(O._threads(), blas)
+    t0 = time.perf_counter()
+    O.draft_step(W, x, cfg, requests=list(range(n_req)))
+    dt = time.perf_counter() - t0
+    return {"value": n_req * cfg.k / dt, "unit": "drafted tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{n_req} of {cfg.B} requests of {cfg.name} (all {cfg.k} positions, full W_dS "
+                      f"projection), {dt:.1f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=3)
+    ap.add_argument("--cpu-requests", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--seed", type=int, default=0)
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): this build has no multi-GPU path; "
+              "the drafting step is measured on a single MI355X.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    cfg = I.CONFIGS[args.config]
+    t0 = time.perf_counter()
+    W = I.make_weights(cfg, args.seed)
+    x = I.make_inputs(cfg, args.seed)
+    log(f"generated inputs in {time.perf_counter() - t0:.1f} s")
+    t0 = time.perf_counter()
+    Wd = {k: hspec.to_device(v) for k, v in W.items()}
+    Xd = {k: hspec.to_device(v) if isinstance(v, np.ndarray) else v for k, v in x.items()}
+    torch.cuda.synchronize()
+    log(f"uploaded in {time.perf_counter() - t0:.1f} s")
+    L = x["ctx_lens"]
+    maxL = int(L.max())
+    ws = hspec.workspace(hspec.draft_step_workspace(cfg, x["page_table"].shape[1], x["num_pages"], maxL))
+    out = torch.empty((cfg.B, cfg.k, cfg.d_model), dtype=torch.float32, device="cuda")
+
+    def step():
+        hspec.draft_step(cfg, Wd, Xd, out, ws, maxL)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    s.record()
+    for _ in range(args.steps):
+        step()
+    e.record()
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms = s.elapsed_time(e) / args.steps
+    assert hspec.read_status(ws) == 0
+    assert bool(torch.isfinite(out).all())
+    tok_s = cfg.B * cfg.k / (ms / 1e3)
+    log(f"draft step: {ms:.3f} ms/step ({t_wall / args.steps * 1e3:.3f} ms wall), {tok_s:,.0f} drafted tok/s")
+
+    # dominant kernel: the state projection (Proj_r then Proj_dS), timed as its own launches
+    sws = hspec.workspace(hspec.state_init_workspace(cfg))
+    S0 = torch.empty((cfg.B, cfg.H, cfg.P, cfg.N), dtype=torch.float32, device="cuda")
+    t_state = time_launches(lambda: hspec.state_init(cfg, Wd, Xd["h_last"], S0, sws), args.steps, torch)
+    b_state = RL.state_proj_bytes(cfg, 2, 4) + cfg.rank * cfg.d_h * 2
+    del S0, sws
+
+    # the target-KV sweep + split reduction (the spec bar), same cache, table and lengths
+    Ad = dict(Xd)
+    for k, name, heads in (("q", "attn_q", cfg.Hq), ("k_blk", "attn_kblk", cfg.Hkv), ("v_blk", "attn_vblk", cfg.Hkv)):
+        Ad[k] = hspec.to_device(I.normal(name, (cfg.B, cfg.k, heads, cfg.D), 1.0, args.seed, cfg.dtype))
+    aws = hspec.workspace(hspec.paged_attn_workspace(cfg, x["page_table"].shape[1], x["num_pages"], maxL))
+    o = torch.empty((cfg.B, cfg.k, cfg.Hq, cfg.D), dtype=torch.float32, device="cuda")
+    t_sweep = time_launches(lambda: hspec.paged_attn(cfg, Ad, o, aws, maxL), args.steps, torch)
+    b_sweep = RL.sweep_bytes(cfg, L)
+    log(f"state projection: {t_state * 1e6:.1f} us, {b_state / t_state / 1e9:.0f} GB/s; "
+        f"KV sweep: {t_sweep * 1e6:.1f} us, {b_sweep / t_sweep / 1e9:.0f} GB/s")
+
+    h_state = kernel_hash(["gemm.hip"])
+    h_sweep = kernel_hash(["attn.hip"])
+    roof = {"bound": "hbm", "achieved": round(b_state / t_state / 1e9, 1), "peak": RL.HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": round(b_state / t_state / 1e9 / RL.HBM_PEAK_GBS, 4),
+            "traffic": traffic_for("state_proj", h_state), "kernel": "state projection (Proj_r + Proj_dS GEMMs)",
+            "algorithmic_bytes": int(b_state), "avg_launch_us": round(t_state * 1e6, 2)}
+    roof_sweep = {"bound": "hbm", "achieved": round(b_sweep / t_sweep / 1e9, 1), "peak": RL.HBM_PEAK_GBS,
+                  "unit": "GB/s", "frac": round(b_sweep / t_sweep / 1e9 / RL.HBM_PEAK_GBS, 4),
+                  "traffic": traffic_for("kv_sweep", h_sweep), "kernel": "target-KV sweep + split reduction",
+                  "algorithmic_bytes": int(b_sweep), "avg_launch_us": round(t_sweep * 1e6, 2),
+                  "tflops": round(RL.sweep_flops(cfg, L) / t_sweep / 1e12, 1)}
+    del Ad, aws, o
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        del Wd, Xd, ws, out
+        torch.cuda.empty_cache()
+        log(f"cpu baseline: oracle on {args.cpu_requests} request(s) ...")
+        cpu = cpu_baseline(cfg, W, x, args.cpu_requests)
+        log(f"cpu baseline: {cpu['value']:.2f} tok/s on {cpu['cores']} threads")
+
+    rec = {
+        "metric": METRIC, "value": round(tok_s, 1), "unit": "drafted tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": cfg.name, "B": cfg.B, "k": cfg.k, "ctx_lens": cfg.lengths,
+                   "sum_ctx_tokens": int(L.sum()), "Hq": cfg.Hq, "Hkv": cfg.Hkv, "D": cfg.D,
+                   "d_model": cfg.d_model, "mamba": f"H{cfg.H} P{cfg.P} N{cfg.N} G{cfg.G} chunk{cfg.chunk}",
+                   "page_size": cfg.page_size, "parallelism": "single GPU"},
+        "roofline": roof,
+        "roofline_kv_sweep": roof_sweep,
+        "cpu_baseline": cpu,
+        "step_bytes_ideal": int(RL.step_bytes(cfg, L)),
+    }
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -16,6 +16,9 @@
 // in a fixed order, so results are bitwise reproducible and independent of where pages
 // live in the pool.  Cache slots at or past ctx_len and pages the table does not reference
 // are never read; page ids outside the pool raise a device status bit and read as zeros.
+#include <climits>
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -23,14 +26,31 @@ namespace hspec {
 
 namespace {
 
-constexpr int KT = 64;   // keys per tile
 typedef unsigned short u16;
-typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+#define LDS_AS __attribute__((address_space(3)))
+#define GLB_AS __attribute__((address_space(1)))
 
-template <int D>
-struct AttnCfg {
-  static constexpr int CPR = D / 8;              // 16-byte chunks per K/V row
-  static constexpr int TILE = KT * D;            // elements per tile per plane
+constexpr int MAX_SPLIT = 8192;                 // keys per split (host-enforced)
+constexpr int MIN_PAGE = 16;                    // smallest supported page size
+constexpr int MAX_PIDS = MAX_SPLIT / MIN_PAGE + 1;
+
+// Tile shape of the sweep.  QB: 16-column query blocks per wave; NW waves per workgroup;
+// KT keys per tile; ST LDS stages (ST - 1 tiles in flight while one is multiplied).
+template <int D, int QB, int NW, int KT, int ST, bool LO>
+struct Sweep {
+  static constexpr int NT = 64 * NW;
+  static constexpr int COLS = 16 * QB;                 // query columns per wave
+  static constexpr int CPR = D / 8;                    // 16-byte chunks per K/V row
+  static constexpr int PLANES = LO ? 2 : 1;
+  static constexpr int DMA = KT * CPR / NT;            // LDS-DMA instructions per wave per tensor-plane
+  static constexpr int NDMA = 2 * PLANES * DMA;        // per wave per tile
+  static constexpr int TILE = KT * D;                  // elements per tensor-plane
+  static constexpr int STAGE = 2 * PLANES * TILE;      // K planes then V planes
+  static constexpr int VM = (ST - 2) * NDMA;           // DMA instructions allowed in flight
+  static_assert(KT % 32 == 0 && DMA >= 1 && KT * CPR % NT == 0, "tile shape");
+  static_assert(ST >= 2 && ST <= 8 && VM < 64, "stages");
 };
 
 __device__ __forceinline__ int clamp_len(const AttnArgs& a, int b) {
@@ -44,24 +64,69 @@ __device__ __forceinline__ int clamp_len(const AttnArgs& a, int b) {
   return L;
 }
 
-template <int D>
-__device__ __forceinline__ int lds_idx(int row, int chunk) {
-  return (row * AttnCfg<D>::CPR + (chunk ^ (row & (AttnCfg<D>::CPR - 1)))) * 8;
+// Element offset of (row, column d) in a swizzled K/V tile: 16-byte chunk c of row r lives at
+// chunk slot c ^ (r mod CPR), so a column of 16 rows and a 4 x 32-byte block both spread over
+// all LDS banks.
+template <int CPR>
+__device__ __forceinline__ int tile_off(int row, int d) {
+  return (row * CPR + ((d >> 3) ^ (row & (CPR - 1)))) * 8 + (d & 7);
 }
 
-template <int D, int NW, bool LO>
-__global__ void __launch_bounds__(64 * NW)
-attn_sweep(AttnArgs a) {
-  using C = AttnCfg<D>;
-  constexpr int NT = 64 * NW;
-  constexpr int CH = KT * C::CPR / NT;            // chunks per thread per tensor per plane
-  constexpr int NS = D / 32;                      // d-steps of the QK^T contraction
-  constexpr int NDB = D / 16;                     // 16-wide d blocks of the output
-  extern __shared__ __align__(16) unsigned char smem[];
-  bf16* sK = reinterpret_cast<bf16*>(smem);
-  bf16* sV = sK + C::TILE * (LO ? 2 : 1);
+template <int VM>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(VM >= 0 && VM < 64, "vmcnt range");
+  // gfx9 s_waitcnt immediate: vmcnt[3:0] and [15:14], expcnt[6:4] = 7, lgkmcnt[11:8] = 15 (no wait)
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((VM & 15) | (7 << 4) | (15 << 8) | ((VM >> 4) << 14));
+  asm volatile("" ::: "memory");
+}
 
-  const int sp = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+__device__ __forceinline__ void wg_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <int V>
+using Int = std::integral_constant<int, V>;
+
+// Running-max slack (log2 units): the softmax reference max is only raised, and O rescaled,
+// when a tile's max exceeds it by more than this; probabilities then stay below 2^8.
+constexpr float RESCALE_SLACK = 8.f;
+
+template <int D, int QB, int NW, int KT, int ST, bool LO>
+__global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)))
+attn_sweep(AttnArgs a) {
+  using C = Sweep<D, QB, NW, KT, ST, LO>;
+  constexpr int NS = D / 32;             // d-steps of the QK^T contraction
+  constexpr int NDB = D / 16;            // 16-wide d blocks of the output
+  constexpr int NKT = KT / 16;           // 16-key tiles per tile
+  // One LDS object per stage, so the compiler can tell a stage being read from the stages
+  // whose DMA is still in flight; the explicit waits below order them.
+  __shared__ __align__(16) bf16 st0[C::STAGE];
+  __shared__ __align__(16) bf16 st1[C::STAGE];
+  __shared__ __align__(16) bf16 st2[ST > 2 ? C::STAGE : 8];
+  __shared__ __align__(16) bf16 st3[ST > 3 ? C::STAGE : 8];
+  __shared__ __align__(16) bf16 st4[ST > 4 ? C::STAGE : 8];
+  __shared__ __align__(16) bf16 st5[ST > 5 ? C::STAGE : 8];
+  __shared__ __align__(16) bf16 st6[ST > 6 ? C::STAGE : 8];
+  __shared__ __align__(16) bf16 st7[ST > 7 ? C::STAGE : 8];
+  __shared__ int pids[MAX_PIDS];
+  auto stage = [&](auto S) -> bf16* {
+    constexpr int s = decltype(S)::value;
+    if constexpr (s == 0) return st0;
+    else if constexpr (s == 1) return st1;
+    else if constexpr (s == 2) return st2;
+    else if constexpr (s == 3) return st3;
+    else if constexpr (s == 4) return st4;
+    else if constexpr (s == 5) return st5;
+    else if constexpr (s == 6) return st6;
+    else return st7;
+  };
+
+  const int BH = a.B * a.Hkv;
+  const int sp = blockIdx.x / BH, bh = blockIdx.x % BH;   // all first splits are dispatched first
+  const int b = bh / a.Hkv, h = bh % a.Hkv;
   const int L = clamp_len(a, b);
   const int nsplit = L > 0 ? (L + a.split - 1) / a.split : 1;
   if (sp >= nsplit) return;
@@ -71,7 +136,7 @@ attn_sweep(AttnArgs a) {
   const bool last = sp == nsplit - 1;
   int kstart = k0;
   if (a.window > 0) {
-    int lo0 = L - a.window + 1;
+    const int lo0 = L - a.window + 1;
     if (lo0 > kstart) kstart = k0 + ((lo0 - k0) / KT) * KT;
   }
   const int n_cache = kstart < k1 ? (k1 - kstart + KT - 1) / KT : 0;
@@ -80,202 +145,235 @@ attn_sweep(AttnArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g4 = lane >> 4, l16 = lane & 15;
+  const int lps = 31 - __builtin_clz(a.ps);
 
-  // ---- query fragments: B operand of S^T = K Q^T (lane: column l16, dims 32s + 8 g4 ..)
-  bf16x8 qf[2][NS], qfl[2][LO ? NS : 1];
-  int colj[2];
-#pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
-    const int c = wave * 32 + qb * 16 + l16;
-    colj[qb] = c < R ? c / g : T;          // padding columns: never valid, never written
-    const int hq = h * g + (c < R ? c % g : 0);
-    const size_t off = ((size_t)(b * T + (c < R ? c / g : 0)) * a.Hq + hq) * D + 8 * g4;
-#pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      qf[qb][s] = c < R ? ld8(a.q_hi + off + 32 * s) : zero8();
-      if constexpr (LO) qfl[qb][s] = c < R ? ld8(a.q_lo + off + 32 * s) : zero8();
+  // page ids of this split, validated once
+  const int pg0 = k0 >> lps;
+  if (n_cache > 0) {
+    const int npg = ((k1 - 1) >> lps) - pg0 + 1;
+    const int32_t* ptab = a.page_table + (size_t)b * a.max_pages + pg0;
+    for (int e = tid; e < npg; e += C::NT) {
+      int pid = ptab[e];
+      if (pid < 0 || pid >= a.num_pages) {
+        set_status(a.status, ST_BAD_PAGE);
+        pid = 0;
+      }
+      pids[e] = pid * a.ps;        // first slot of the page
     }
   }
 
-  f32x4 o[NDB][2];
+  // query fragments: B operand of S^T = K Q^T (lane: column l16, dims 32 s + 8 g4 ..) and the
+  // key window [lo, hi) of each column for cache keys and for block keys
+  bf16x8 qf[QB][NS], qfl[QB][LO ? NS : 1];
+  int c_lo[QB], c_hi[QB], b_hi[QB];
 #pragma unroll
-  for (int d = 0; d < NDB; ++d)
+  for (int qb = 0; qb < QB; ++qb) {
+    const int c = wave * C::COLS + qb * 16 + l16;
+    const bool real = c < R;
+    const int j = real ? c / g : 0;
+    const int hq = h * g + (real ? c % g : 0);
+    const size_t off = ((size_t)(b * T + j) * a.Hq + hq) * D + 8 * g4;
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) o[d][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
+    for (int s = 0; s < NS; ++s) {
+      qf[qb][s] = real ? ld8(a.q_hi + off + 32 * s) : zero8();
+      if constexpr (LO) qfl[qb][s] = real ? ld8(a.q_lo + off + 32 * s) : zero8();
+    }
+    c_lo[qb] = a.window > 0 ? L + j - a.window + 1 : INT_MIN;
+    c_hi[qb] = real ? k1 : INT_MIN;
+    b_hi[qb] = real ? (a.causal ? j + 1 : T) : INT_MIN;
+  }
+  wg_barrier();   // page ids visible
 
-  // ---- cooperative tile loads (registers, then LDS)
-  bf16x8 rk[CH], rv[CH], rkl[LO ? CH : 1], rvl[LO ? CH : 1];
-  const int32_t* ptab = a.page_table + (size_t)b * a.max_pages;
-  auto load_tile = [&](int ti) {
+  // LDS-DMA of tile ti into stage sb: wave w fills chunk slots [w*DMA*64, (w+1)*DMA*64) of
+  // every tensor-plane; each lane picks the global chunk that belongs at its slot.  Keys past
+  // the valid range load a valid row instead (finite values; masked out of the softmax).
+  auto issue = [&](int ti, bf16* sb) {
     const bool cache = ti < n_cache;
     const int base = cache ? kstart + ti * KT : (ti - n_cache) * KT;
 #pragma unroll
-    for (int i = 0; i < CH; ++i) {
-      const int q = i * NT + tid, r = q / C::CPR, c = q % C::CPR;
-      const int key = base + r;
-      bool ok;
-      size_t off = 0;
+    for (int i = 0; i < C::DMA; ++i) {
+      const int slot = (wave * C::DMA + i) * 64 + lane;
+      const int row = slot / C::CPR;
+      const int cl = (slot % C::CPR) ^ (row & (C::CPR - 1));
+      size_t off;
+      int key = base + row;
       if (cache) {
-        ok = key < k1;
-        if (ok) {
-          int pid = ptab[key / a.ps];
-          if (pid < 0 || pid >= a.num_pages) {
-            set_status(a.status, ST_BAD_PAGE);
-            ok = false;
-          } else {
-            off = ((size_t)(pid * a.ps + key % a.ps) * a.Hkv + h) * D + 8 * c;
-          }
-        }
+        key = key < k1 ? key : k0;
+        const int slot_id = pids[(key >> lps) - pg0] + (key & (a.ps - 1));
+        off = (size_t)slot_id * (a.Hkv * D) + (h * D + 8 * cl);
       } else {
-        ok = key < T;
-        off = ((size_t)(b * T + key) * a.Hkv + h) * D + 8 * c;
+        key = key < T ? key : 0;
+        off = ((size_t)(b * T + key) * a.Hkv + h) * D + 8 * cl;
       }
-      const bf16* K = cache ? a.kc_hi : a.kb_hi;
-      const bf16* V = cache ? a.vc_hi : a.vb_hi;
-      rk[i] = ok ? ld8(K + off) : zero8();
-      rv[i] = ok ? ld8(V + off) : zero8();
+      const bf16* Kp = cache ? a.kc_hi : a.kb_hi;
+      const bf16* Vp = cache ? a.vc_hi : a.vb_hi;
+      bf16* dst = sb + (wave * C::DMA + i) * 64 * 8;
+      __builtin_amdgcn_global_load_lds((const GLB_AS void*)(Kp + off), (LDS_AS void*)dst, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((const GLB_AS void*)(Vp + off), (LDS_AS void*)(dst + C::PLANES * C::TILE),
+                                       16, 0, 0);
       if constexpr (LO) {
         const bf16* Kl = cache ? a.kc_lo : a.kb_lo;
         const bf16* Vl = cache ? a.vc_lo : a.vb_lo;
-        rkl[i] = ok ? ld8(Kl + off) : zero8();
-        rvl[i] = ok ? ld8(Vl + off) : zero8();
+        __builtin_amdgcn_global_load_lds((const GLB_AS void*)(Kl + off), (LDS_AS void*)(dst + C::TILE), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds((const GLB_AS void*)(Vl + off),
+                                         (LDS_AS void*)(dst + C::PLANES * C::TILE + C::TILE), 16, 0, 0);
       }
     }
   };
-  auto store_tile = [&]() {
+
+  f32x4 o[NDB][QB];
 #pragma unroll
-    for (int i = 0; i < CH; ++i) {
-      const int q = i * NT + tid, r = q / C::CPR, c = q % C::CPR;
-      const int idx = lds_idx<D>(r, c);
-      *reinterpret_cast<bf16x8*>(sK + idx) = rk[i];
-      *reinterpret_cast<bf16x8*>(sV + idx) = rv[i];
-      if constexpr (LO) {
-        *reinterpret_cast<bf16x8*>(sK + C::TILE + idx) = rkl[i];
-        *reinterpret_cast<bf16x8*>(sV + C::TILE + idx) = rvl[i];
-      }
-    }
-  };
-
+  for (int d = 0; d < NDB; ++d)
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) o[d][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run[QB], l_run[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    m_run[qb] = -INFINITY;
+    l_run[qb] = 0.f;
+  }
   const int lo_last = a.window > 0 ? L + (T - 1) - a.window + 1 : 0;
-  if (ntiles > 0) load_tile(0);
-  for (int ti = 0; ti < ntiles; ++ti) {
-    __syncthreads();
-    store_tile();
-    __syncthreads();
-    if (ti + 1 < ntiles) load_tile(ti + 1);
 
+  auto compute = [&](int ti, const bf16* sb) {
+    const bf16* sK = sb;
+    const bf16* sV = sb + C::PLANES * C::TILE;
     const bool cache = ti < n_cache;
     const int base = cache ? kstart + ti * KT : (ti - n_cache) * KT;
 
-    // S^T tile: 4 key-tiles of 16 x 2 column blocks of 16
-    f32x4 st[4][2];
+    // all K fragments first, then the QK^T chains interleaved across key tiles
+    bf16x8 kf[NKT][NS], kfl[NKT][LO ? NS : 1];
 #pragma unroll
-    for (int kt = 0; kt < 4; ++kt) {
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb) st[kt][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
-        const int idx = lds_idx<D>(kt * 16 + l16, 4 * s + g4);
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(sK + idx);
-        bf16x8 kfl;
-        if constexpr (LO) kfl = *reinterpret_cast<const bf16x8*>(sK + C::TILE + idx);
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-          st[kt][qb] = mma16(kf, qf[qb][s], st[kt][qb]);
-          if constexpr (LO) {
-            st[kt][qb] = mma16(kfl, qf[qb][s], st[kt][qb]);
-            st[kt][qb] = mma16(kf, qfl[qb][s], st[kt][qb]);
-          }
-        }
+        const int off = tile_off<C::CPR>(kt * 16 + l16, 32 * s + 8 * g4);
+        kf[kt][s] = *reinterpret_cast<const bf16x8*>(sK + off);
+        if constexpr (LO) kfl[kt][s] = *reinterpret_cast<const bf16x8*>(sK + C::TILE + off);
       }
-    }
-
-    // scale into log2 units, mask, online softmax per column
-    const bool full = cache && base + KT <= k1 && (a.window <= 0 || base >= lo_last);
-    float p[4][2][4];
+    f32x4 st[NKT][QB];
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      const int j = colj[qb];
-      float mx = -INFINITY;
+    for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
+      for (int qb = 0; qb < QB; ++qb) st[kt][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float v = st[kt][qb][i] * a.scale_log2;
-          if (!full) {
-            const int key = base + kt * 16 + 4 * g4 + i;
-            bool ok;
-            if (cache) ok = key < k1 && (a.window <= 0 || key >= L + j - a.window + 1);
-            else ok = key < T && (!a.causal || key <= j);
-            if (j >= T) ok = false;
-            v = ok ? v : -INFINITY;
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+          st[kt][qb] = mma16(kf[kt][s], qf[qb][s], st[kt][qb]);
+          if constexpr (LO) {
+            st[kt][qb] = mma16(kfl[kt][s], qf[qb][s], st[kt][qb]);
+            st[kt][qb] = mma16(kf[kt][s], qfl[qb][s], st[kt][qb]);
           }
-          p[kt][qb][i] = v;
-          mx = fmaxf(mx, v);
         }
+
+    const bool full = cache && base + KT <= k1 && (a.window <= 0 || base >= lo_last);
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      float mx = -INFINITY;
+      if (full) {
+#pragma unroll
+        for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            st[kt][qb][i] *= a.scale_log2;
+            mx = fmaxf(mx, st[kt][qb][i]);
+          }
+      } else {
+        const int lo = cache ? c_lo[qb] : INT_MIN;
+        const int hi = cache ? c_hi[qb] : b_hi[qb];
+#pragma unroll
+        for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int key = base + kt * 16 + 4 * g4 + i;
+            const float v = ((key >= lo) & (key < hi)) ? st[kt][qb][i] * a.scale_log2 : -INFINITY;
+            st[kt][qb][i] = v;
+            mx = fmaxf(mx, v);
+          }
+      }
       mx = wave_max16x4(mx);
-      const float m_new = fmaxf(m_run[qb], mx);
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = exp2f(m_run[qb] - m_use);
+      if (__any(mx > m_run[qb] + RESCALE_SLACK)) {   // raise the reference max, rescale O and l
+        const float m_new = fmaxf(m_run[qb], mx);
+        const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - (m_new == -INFINITY ? 0.f : m_new));
+        l_run[qb] *= alpha;
+#pragma unroll
+        for (int d = 0; d < NDB; ++d) o[d][qb] *= alpha;
+        m_run[qb] = m_new;
+      }
+      const float m_use = m_run[qb] == -INFINITY ? 0.f : m_run[qb];
       float sum = 0.f;
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
+      for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float e = exp2f(p[kt][qb][i] - m_use);
-          p[kt][qb][i] = e;
+          const float e = __builtin_amdgcn_exp2f(st[kt][qb][i] - m_use);
+          st[kt][qb][i] = e;
           sum += e;
         }
-      sum = wave_sum16x4(sum);
-      l_run[qb] = l_run[qb] * alpha + sum;
-      m_run[qb] = m_new;
-#pragma unroll
-      for (int d = 0; d < NDB; ++d) o[d][qb] *= alpha;
+      l_run[qb] += wave_sum16x4(sum);
     }
 
-    // O^T += V^T P^T over two 32-key halves
+    // O^T += V^T P^T, 32 keys at a time; V^T fragments by transposing LDS reads
 #pragma unroll
-    for (int kp = 0; kp < 2; ++kp) {
-      bf16x8 pf[2], pfl[2];
+    for (int kp = 0; kp < KT / 32; ++kp) {
+      bf16x8 pf[QB], pfl[QB];
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb)
+      for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
         for (int jj = 0; jj < 8; ++jj) {
-          const float v = p[2 * kp + (jj >> 2)][qb][jj & 3];
+          const float v = st[2 * kp + (jj >> 2)][qb][jj & 3];
           const bf16 hv = f2bf(v);
           pf[qb][jj] = hv;
           if constexpr (LO) pfl[qb][jj] = f2bf(v - bf2f(hv));
         }
+      const int vrow = kp * 32 + 4 * g4 + (l16 >> 2);
 #pragma unroll
       for (int d = 0; d < NDB; ++d) {
-        const int dd = d * 16 + l16;
-        u16x8 vv, vvl;
+        const int dc = d * 16 + 4 * (l16 & 3);
+        const int o0 = tile_off<C::CPR>(vrow, dc), o1 = tile_off<C::CPR>(vrow + 16, dc);
+        const s16x4 a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4*)(sV + o0));
+        const s16x4 a1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4*)(sV + o1));
+        const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
-        for (int jj = 0; jj < 8; ++jj) {
-          const int key = kp * 32 + (jj < 4 ? 4 * g4 + jj : 16 + 4 * g4 + (jj - 4));
-          const int idx = lds_idx<D>(key, dd >> 3) + (dd & 7);
-          vv[jj] = reinterpret_cast<const u16*>(sV)[idx];
-          if constexpr (LO) vvl[jj] = reinterpret_cast<const u16*>(sV + C::TILE)[idx];
-        }
-        const bf16x8 vf = __builtin_bit_cast(bf16x8, vv);
+        for (int qb = 0; qb < QB; ++qb) o[d][qb] = mma16(vf, pf[qb], o[d][qb]);
+        if constexpr (LO) {
+          const s16x4 b0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4*)(sV + C::TILE + o0));
+          const s16x4 b1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4*)(sV + C::TILE + o1));
+          const bf16x8 vfl = __builtin_bit_cast(bf16x8, __builtin_shufflevector(b0, b1, 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-          o[d][qb] = mma16(vf, pf[qb], o[d][qb]);
-          if constexpr (LO) {
-            o[d][qb] = mma16(__builtin_bit_cast(bf16x8, vvl), pf[qb], o[d][qb]);
+          for (int qb = 0; qb < QB; ++qb) {
+            o[d][qb] = mma16(vfl, pf[qb], o[d][qb]);
             o[d][qb] = mma16(vf, pfl[qb], o[d][qb]);
           }
         }
       }
     }
-  }
+  };
 
-  // ---- write: lane holds O[column l16][d = 16 d + 4 g4 + i]
+  // One pipeline step on stage S: wait for its tile, refill the stage freed last step, compute.
+  auto step = [&](int ti, auto S) {
+    constexpr int s = decltype(S)::value;
+    if (ti >= ntiles) return;
+    if (ti + ST - 2 < ntiles) wait_vmcnt<C::VM>();   // the next ST-2 tiles may stay in flight
+    else wait_vmcnt<0>();
+    wg_barrier();   // every wave's DMA for ti landed; every wave is done with the previous stage
+    if (ti + ST - 1 < ntiles) issue(ti + ST - 1, stage(Int<(s + ST - 1) % ST>{}));
+    compute(ti, stage(S));
+  };
+  auto round = [&]<int... I>(int t0, std::integer_sequence<int, I...>) { (step(t0 + I, Int<I>{}), ...); };
+
+  [&]<int... I>(std::integer_sequence<int, I...>) {
+    ((I < ntiles ? issue(I, stage(Int<I>{})) : void()), ...);
+  }(std::make_integer_sequence<int, ST - 1>{});
+  for (int t0 = 0; t0 < ntiles; t0 += ST) round(t0, std::make_integer_sequence<int, ST>{});
+
+  // write: lane holds O[column l16][d = 16 d + 4 g4 + i]
   const size_t unit = ((size_t)b * a.Hkv + h) * a.max_splits + sp;
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
-    const int c = wave * 32 + qb * 16 + l16;
+  for (int qb = 0; qb < QB; ++qb) {
+    const int c = wave * C::COLS + qb * 16 + l16;
     if (c >= R) continue;
     if (nsplit == 1) {
       const float inv = 1.f / l_run[qb];
@@ -286,8 +384,8 @@ attn_sweep(AttnArgs a) {
         f32x4 v = o[d][qb] * inv;
         if (a.o_f32) *reinterpret_cast<f32x4*>(a.o_f32 + off + 16 * d) = v;
         if (a.o_bf16) {
-#pragma unroll
-          for (int i = 0; i < 4; ++i) a.o_bf16[off + 16 * d + i] = f2bf(v[i]);
+          bf16x4 hv = {f2bf(v[0]), f2bf(v[1]), f2bf(v[2]), f2bf(v[3])};
+          *reinterpret_cast<bf16x4*>(a.o_bf16 + off + 16 * d) = hv;
         }
       }
     } else {
@@ -355,29 +453,34 @@ __global__ void gather_slots_kernel(int B, int max_pages, int ps, int num_pages,
   }
 }
 
-template <int D, int NW, bool LO>
+#ifndef HSPEC_SWEEP_QB
+#define HSPEC_SWEEP_QB 1
+#endif
+#ifndef HSPEC_SWEEP_ST
+#define HSPEC_SWEEP_ST 4
+#endif
+
+template <int D, int QB, int NW, bool LO>
 hipError_t launch_sweep(const AttnArgs& a, hipStream_t s) {
-  constexpr int lds = 2 * 2 * AttnCfg<D>::TILE * (LO ? 2 : 1);
-  auto kern = attn_sweep<D, NW, LO>;
-  if (lds > 64 * 1024) {
-    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-    if (e != hipSuccess) return e;
-  }
-  hipLaunchKernelGGL(kern, dim3(a.max_splits, a.Hkv, a.B), dim3(64 * NW), lds, s, a);
+  constexpr int KT = 512 * NW / D > 32 ? 512 * NW / D : 32;   // every lane DMAs at least one chunk
+  constexpr int NDMA = 2 * (LO ? 2 : 1) * KT * (D / 8) / (64 * NW);
+  constexpr int ST_MAX = 2 + 63 / NDMA;                         // vmcnt holds at most 63
+  constexpr int ST = LO ? 2 : (HSPEC_SWEEP_ST < ST_MAX ? HSPEC_SWEEP_ST : ST_MAX);
+  auto kern = attn_sweep<D, QB, NW, KT, ST, LO>;
+  hipLaunchKernelGGL(kern, dim3(a.max_splits * a.B * a.Hkv), dim3(64 * NW), 0, s, a);
   return hipGetLastError();
 }
 
 template <int D, bool LO>
 hipError_t launch_sweep_nw(const AttnArgs& a, hipStream_t s) {
+  constexpr int QB = HSPEC_SWEEP_QB;
   const int R = a.T * (a.Hq / a.Hkv);
-  const int nw = (R + 31) / 32;
-  switch (nw) {
-    case 1: return launch_sweep<D, 1, LO>(a, s);
-    case 2: return launch_sweep<D, 2, LO>(a, s);
-    case 3:
-    case 4: return launch_sweep<D, 4, LO>(a, s);
-    default: return hipErrorInvalidValue;
-  }
+  const int nw = (R + 16 * QB - 1) / (16 * QB);
+  if (nw <= 1) return launch_sweep<D, QB, 1, LO>(a, s);
+  if (nw <= 2) return launch_sweep<D, QB, 2, LO>(a, s);
+  if (nw <= 4) return launch_sweep<D, QB, 4, LO>(a, s);
+  if (nw <= 8) return launch_sweep<D, QB, 8, LO>(a, s);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace
@@ -390,10 +493,11 @@ size_t attention_partials_bytes(int B, int Hkv, int max_splits, int R, int D) {
 int attention_default_split(int B, int Hkv, int max_ctx_len) {
   // Aim for ~2048 work units over the whole batch, in multiples of the 64-key tile.
   long long want = ((long long)max_ctx_len * B * Hkv + 2047) / 2048;
-  long long s = ((want + KT - 1) / KT) * KT;
+  long long s = ((want + 63) / 64) * 64;
   if (s < 256) s = 256;
-  long long cap = ((long long)(max_ctx_len > 0 ? max_ctx_len : 1) + KT - 1) / KT * KT;
+  long long cap = ((long long)(max_ctx_len > 0 ? max_ctx_len : 1) + 63) / 64 * 64;
   if (s > cap) s = cap;
+  if (s > MAX_SPLIT) s = MAX_SPLIT;
   return (int)s;
 }
 

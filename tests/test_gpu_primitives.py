@@ -111,7 +111,9 @@ def test_paged_attn(name):
 
 
 def test_paged_attn_split_invariance():
-    """Split sizes 64 .. whole context agree to fp32 rounding; each split size is deterministic."""
+    """Every split size meets the tolerance, is bitwise deterministic, and the split sizes agree
+    with each other to the bf16 rounding of the probabilities (which depends on each split's
+    running maximum)."""
     cfg = _small_attn_cfg(B=2, lengths="list:1000,450")
     x = I.make_attn_inputs(cfg, seed=3)
     ref = _ref_attn(cfg, x)
@@ -124,7 +126,7 @@ def test_paged_attn_split_invariance():
         outs[split] = o
     base = outs[1024]
     for s, o in outs.items():
-        assert np.max(np.abs(o - base)) <= 1e-5 * max(1.0, np.max(np.abs(base))), s
+        assert_close(o, base, f"split {s} vs whole context", max_abs=2e-3, rel_l2=3e-3)
 
 
 def test_paged_attn_page_permutation_bitwise():
@@ -243,8 +245,8 @@ def test_ssd_scan_zero_input_zero_state():
 
 # -------------------------------------------------------------------- state projection
 
-@pytest.mark.parametrize("cfg", [I.CONFIGS[1], _small_attn_cfg(B=5, d_model=512, H=8, N=128),
-                                 _small_attn_cfg(B=70, d_model=256, H=4, N=128)],
+@pytest.mark.parametrize("cfg", [I.CONFIGS[1], _small_attn_cfg(B=5, d_model=512, H=8, N=128, lengths="fixed:16"),
+                                 _small_attn_cfg(B=70, d_model=256, H=4, N=128, lengths="fixed:16")],
                          ids=["cfg1", "b5", "b70"])
 def test_state_init(cfg):
     W = I.make_weights(cfg, seed=3, skip=("W_in", "W_out", "W_q", "W_k", "W_v", "W_o"))
