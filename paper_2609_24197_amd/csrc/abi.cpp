@@ -123,7 +123,13 @@ hspec_status check_attn_cfg(const hspec_attn_cfg* c, int max_ctx_len) {
   if (c->split_tokens < 0 || c->split_tokens % 64)
     return fail(HSPEC_ERR_SHAPE, "split_tokens must be a non-negative multiple of 64");
   if (max_ctx_len < 0) return fail(HSPEC_ERR_SHAPE, "max_ctx_len < 0");
-  if ((long long)c->B * c->Hkv > 65535 * 64LL) return fail(HSPEC_ERR_UNSUPPORTED, "B * Hkv too large");
+  if (c->B > 32767) return fail(HSPEC_ERR_UNSUPPORTED, "B must be <= 32767");
+  if (c->page_size < 16 || (c->page_size & (c->page_size - 1)))
+    return fail(HSPEC_ERR_UNSUPPORTED, "page_size must be a power of two >= 16, got %d", c->page_size);
+  if (c->split_tokens > 8192) return fail(HSPEC_ERR_UNSUPPORTED, "split_tokens must be <= 8192");
+  const int split = c->split_tokens > 0 ? c->split_tokens : hspec::attention_default_split(c->B, c->Hkv, max_ctx_len);
+  if (max_ctx_len > 0 && (max_ctx_len + split - 1) / split > 256)
+    return fail(HSPEC_ERR_UNSUPPORTED, "max_ctx_len / split_tokens gives more than 256 splits");
   return HSPEC_OK;
 }
 
@@ -275,6 +281,7 @@ struct AttnPlan {
   bf16 *q_hi = nullptr, *q_lo = nullptr, *k_hi = nullptr, *k_lo = nullptr, *v_hi = nullptr, *v_lo = nullptr;
   float* part_o = nullptr;
   float* part_ml = nullptr;
+  int32_t* units = nullptr;
   bf16 *o_hi = nullptr, *o_lo = nullptr;
   int split = 0, max_splits = 0;
 };
@@ -284,6 +291,7 @@ void plan_sweep(Arena& ar, const hspec_attn_cfg& c, int max_ctx_len, AttnPlan& p
   p.max_splits = max_ctx_len > 0 ? (max_ctx_len + p.split - 1) / p.split : 1;
   const int R = c.k * (c.Hq / c.Hkv);
   const size_t units = (size_t)c.B * c.Hkv * p.max_splits;
+  p.units = ar.take<int32_t>((size_t)c.B * p.max_splits);
   if (p.max_splits > 1) {
     p.part_o = ar.take<float>(units * R * c.D);
     p.part_ml = ar.take<float>(units * R * 2);
@@ -329,7 +337,7 @@ hspec::AttnArgs sweep_args(const hspec_attn_cfg& c, const AttnPlan& p, const int
   a.max_ctx_len = max_ctx_len; a.split = p.split; a.max_splits = p.max_splits;
   const float scale = c.scale > 0.f ? c.scale : 1.f / std::sqrt((float)c.D);
   a.scale_log2 = scale * 1.4426950408889634f;
-  a.part_o = p.part_o; a.part_ml = p.part_ml; a.status = status;
+  a.part_o = p.part_o; a.part_ml = p.part_ml; a.status = status; a.units = p.units;
   return a;
 }
 

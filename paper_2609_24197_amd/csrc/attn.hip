@@ -64,12 +64,17 @@ __device__ __forceinline__ int clamp_len(const AttnArgs& a, int b) {
   return L;
 }
 
-// Element offset of (row, column d) in a swizzled K/V tile: 16-byte chunk c of row r lives at
-// chunk slot c ^ (r mod CPR), so a column of 16 rows and a 4 x 32-byte block both spread over
-// all LDS banks.
+// Element offset of (row, column d) in a swizzled K/V tile.  16-byte chunk c of row r lives at
+// chunk slot c ^ f(r).  For 256-byte rows f(r) = 2 (r mod 8) + (r / 8 mod 2): the 16 rows read
+// by one 16-lane K fragment load land on 16 different slots, and the 8 rows x 32 bytes read by
+// each half-wave of a transposing V load land on 8 different slot pairs, so neither access
+// pattern has bank conflicts.  Shorter rows use c ^ (r mod CPR).
 template <int CPR>
 __device__ __forceinline__ int tile_off(int row, int d) {
-  return (row * CPR + ((d >> 3) ^ (row & (CPR - 1)))) * 8 + (d & 7);
+  int f;
+  if constexpr (CPR == 16) f = ((row & 7) << 1) | ((row >> 3) & 1);
+  else f = row & (CPR - 1);
+  return (row * CPR + ((d >> 3) ^ f)) * 8 + (d & 7);
 }
 
 template <int VM>
@@ -124,13 +129,24 @@ attn_sweep(AttnArgs a) {
     else return st7;
   };
 
-  const int BH = a.B * a.Hkv;
-  const int sp = blockIdx.x / BH, bh = blockIdx.x % BH;   // all first splits are dispatched first
-  const int b = bh / a.Hkv, h = bh % a.Hkv;
+  __shared__ int s_item;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g4 = lane >> 4, l16 = lane & 15;
+  const int lps = 31 - __builtin_clz(a.ps);
+  const int g = a.Hq / a.Hkv, T = a.T, R = T * g;
+  const int n_items = a.status[1];
+
+  // Persistent workgroups pull (request, split, KV head) items, longest splits first.
+  for (;;) {
+  __syncthreads();                    // the previous item is finished by every wave
+  if (tid == 0) s_item = atomicAdd(a.status + 2, 1);
+  __syncthreads();
+  const int item = s_item;
+  if (item >= n_items) break;
+  const int packed = a.units[item / a.Hkv];
+  const int b = packed >> 16, sp = packed & 0xffff, h = item % a.Hkv;
   const int L = clamp_len(a, b);
   const int nsplit = L > 0 ? (L + a.split - 1) / a.split : 1;
-  if (sp >= nsplit) return;
-  const int g = a.Hq / a.Hkv, T = a.T, R = T * g;
   const int k0 = sp * a.split;
   const int k1 = min(L, k0 + a.split);
   const bool last = sp == nsplit - 1;
@@ -142,10 +158,6 @@ attn_sweep(AttnArgs a) {
   const int n_cache = kstart < k1 ? (k1 - kstart + KT - 1) / KT : 0;
   const int n_block = last ? (T + KT - 1) / KT : 0;
   const int ntiles = n_cache + n_block;
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int g4 = lane >> 4, l16 = lane & 15;
-  const int lps = 31 - __builtin_clz(a.ps);
 
   // page ids of this split, validated once
   const int pg0 = k0 >> lps;
@@ -182,7 +194,7 @@ attn_sweep(AttnArgs a) {
     c_hi[qb] = real ? k1 : INT_MIN;
     b_hi[qb] = real ? (a.causal ? j + 1 : T) : INT_MIN;
   }
-  wg_barrier();   // page ids visible
+  __syncthreads();   // page ids visible (LDS writes waited for, unlike the pipeline barrier)
 
   // LDS-DMA of tile ti into stage sb: wave w fills chunk slots [w*DMA*64, (w+1)*DMA*64) of
   // every tensor-plane; each lane picks the global chunk that belongs at its slot.  Keys past
@@ -194,7 +206,7 @@ attn_sweep(AttnArgs a) {
     for (int i = 0; i < C::DMA; ++i) {
       const int slot = (wave * C::DMA + i) * 64 + lane;
       const int row = slot / C::CPR;
-      const int cl = (slot % C::CPR) ^ (row & (C::CPR - 1));
+      const int cl = (tile_off<C::CPR>(row, 8 * (slot % C::CPR)) / 8 - row * C::CPR);   // chunk stored here
       size_t off;
       int key = base + row;
       if (cache) {
@@ -268,6 +280,27 @@ attn_sweep(AttnArgs a) {
           }
         }
 
+    // V^T fragments (transposing LDS reads), issued before the softmax to hide their latency
+    bf16x8 vf[KT / 32][NDB], vfl[KT / 32][LO ? NDB : 1];
+    {
+      const int vrow = 4 * g4 + (l16 >> 2);
+#pragma unroll
+      for (int kp = 0; kp < KT / 32; ++kp)
+#pragma unroll
+        for (int d = 0; d < NDB; ++d) {
+          const int dc = d * 16 + 4 * (l16 & 3);
+          const int o0 = tile_off<C::CPR>(kp * 32 + vrow, dc), o1 = tile_off<C::CPR>(kp * 32 + vrow + 16, dc);
+          const s16x4 a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4*)(sV + o0));
+          const s16x4 a1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4*)(sV + o1));
+          vf[kp][d] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
+          if constexpr (LO) {
+            const s16x4 b0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4*)(sV + C::TILE + o0));
+            const s16x4 b1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4*)(sV + C::TILE + o1));
+            vfl[kp][d] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(b0, b1, 0, 1, 2, 3, 4, 5, 6, 7));
+          }
+        }
+    }
+
     const bool full = cache && base + KT <= k1 && (a.window <= 0 || base >= lo_last);
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
@@ -315,7 +348,7 @@ attn_sweep(AttnArgs a) {
       l_run[qb] += wave_sum16x4(sum);
     }
 
-    // O^T += V^T P^T, 32 keys at a time; V^T fragments by transposing LDS reads
+    // O^T += V^T P^T, 32 keys at a time (V^T fragments were read before the softmax)
 #pragma unroll
     for (int kp = 0; kp < KT / 32; ++kp) {
       bf16x8 pf[QB], pfl[QB];
@@ -328,24 +361,15 @@ attn_sweep(AttnArgs a) {
           pf[qb][jj] = hv;
           if constexpr (LO) pfl[qb][jj] = f2bf(v - bf2f(hv));
         }
-      const int vrow = kp * 32 + 4 * g4 + (l16 >> 2);
 #pragma unroll
       for (int d = 0; d < NDB; ++d) {
-        const int dc = d * 16 + 4 * (l16 & 3);
-        const int o0 = tile_off<C::CPR>(vrow, dc), o1 = tile_off<C::CPR>(vrow + 16, dc);
-        const s16x4 a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4*)(sV + o0));
-        const s16x4 a1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4*)(sV + o1));
-        const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb) o[d][qb] = mma16(vf, pf[qb], o[d][qb]);
+        for (int qb = 0; qb < QB; ++qb) o[d][qb] = mma16(vf[kp][d], pf[qb], o[d][qb]);
         if constexpr (LO) {
-          const s16x4 b0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4*)(sV + C::TILE + o0));
-          const s16x4 b1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4*)(sV + C::TILE + o1));
-          const bf16x8 vfl = __builtin_bit_cast(bf16x8, __builtin_shufflevector(b0, b1, 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
           for (int qb = 0; qb < QB; ++qb) {
-            o[d][qb] = mma16(vfl, pf[qb], o[d][qb]);
-            o[d][qb] = mma16(vf, pfl[qb], o[d][qb]);
+            o[d][qb] = mma16(vfl[kp][d], pf[qb], o[d][qb]);
+            o[d][qb] = mma16(vf[kp][d], pfl[qb], o[d][qb]);
           }
         }
       }
@@ -398,37 +422,87 @@ attn_sweep(AttnArgs a) {
       }
     }
   }
+  }   // item loop
 }
 
-// One workgroup per (request, KV head): o = sum_s O_s 2^(m_s - m*) / sum_s l_s 2^(m_s - m*).
+// Work list of the sweep: every (request, split) once, the full splits first and then the
+// last splits by decreasing length, so the persistent workgroups finish close together.
+// One workgroup; also resets the item queue.
+__global__ void __launch_bounds__(256) attn_plan(AttnArgs a) {
+  __shared__ int s_full;
+  if (threadIdx.x == 0) {
+    int full = 0;
+    for (int b = 0; b < a.B; ++b) {
+      const int L = clamp_len(a, b);
+      const int ns = L > 0 ? (L + a.split - 1) / a.split : 1;
+      for (int sp = 0; sp < ns - 1; ++sp) a.units[full++] = (b << 16) | sp;
+    }
+    s_full = full;
+    a.status[1] = (full + a.B) * a.Hkv;
+    a.status[2] = 0;
+  }
+  __syncthreads();
+  const int full = s_full;
+  for (int b = threadIdx.x; b < a.B; b += blockDim.x) {
+    const int L = clamp_len(a, b);
+    const int ns = L > 0 ? (L + a.split - 1) / a.split : 1;
+    const int rem = L - (ns - 1) * a.split;
+    int rank = 0;
+    for (int o = 0; o < a.B; ++o) {
+      const int Lo = clamp_len(a, o);
+      const int no = Lo > 0 ? (Lo + a.split - 1) / a.split : 1;
+      const int ro = Lo - (no - 1) * a.split;
+      rank += (ro > rem) || (ro == rem && o < b);
+    }
+    a.units[full + rank] = (b << 16) | (ns - 1);
+  }
+}
+
+// One workgroup per (request, KV head, 16 query columns): per column the split weights
+// 2^(m_s - m*) / sum_s l_s 2^(m_s - m*) go to LDS once, then o = sum_s w_s O_s streams the
+// partial outputs in a fixed split order.
+constexpr int RED_COLS = 16;
+constexpr int RED_MAX_SPLITS = 256;
+
 __global__ void __launch_bounds__(256) attn_reduce(AttnArgs a) {
-  const int b = blockIdx.x / a.Hkv, h = blockIdx.x % a.Hkv;
+  __shared__ float w[RED_COLS][RED_MAX_SPLITS + 1];
+  const int g = a.Hq / a.Hkv, T = a.T, R = T * g, D = a.D;
+  const int cblocks = (R + RED_COLS - 1) / RED_COLS;
+  const int bh = blockIdx.x / cblocks, c0 = (blockIdx.x % cblocks) * RED_COLS;
+  const int b = bh / a.Hkv, h = bh % a.Hkv;
   const int L = clamp_len(a, b);
   const int nsplit = L > 0 ? (L + a.split - 1) / a.split : 1;
   if (nsplit == 1) return;
-  const int g = a.Hq / a.Hkv, T = a.T, R = T * g, D = a.D;
   const size_t unit0 = ((size_t)b * a.Hkv + h) * a.max_splits;
-  const int nq = D / 4;
-  for (int it = threadIdx.x; it < R * nq; it += blockDim.x) {
-    const int c = it / nq, d4 = (it % nq) * 4;
+  for (int c = threadIdx.x; c < RED_COLS; c += blockDim.x) {
+    if (c0 + c >= R) continue;
     float mstar = -INFINITY;
-    for (int s = 0; s < nsplit; ++s) mstar = fmaxf(mstar, a.part_ml[((unit0 + s) * R + c) * 2]);
+    for (int s = 0; s < nsplit; ++s) mstar = fmaxf(mstar, a.part_ml[((unit0 + s) * R + c0 + c) * 2]);
     const float m_use = mstar == -INFINITY ? 0.f : mstar;
     float lsum = 0.f;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     for (int s = 0; s < nsplit; ++s) {
-      const float* ml = a.part_ml + ((unit0 + s) * R + c) * 2;
-      const float w = exp2f(ml[0] - m_use);
-      lsum += ml[1] * w;
-      acc += *reinterpret_cast<const f32x4*>(a.part_o + ((unit0 + s) * R + c) * D + d4) * w;
+      const float* ml = a.part_ml + ((unit0 + s) * R + c0 + c) * 2;
+      const float e = exp2f(ml[0] - m_use);
+      w[c][s] = e;
+      lsum += ml[1] * e;
     }
-    acc *= 1.f / lsum;
+    const float inv = 1.f / lsum;
+    for (int s = 0; s < nsplit; ++s) w[c][s] *= inv;
+  }
+  __syncthreads();
+  const int nq = D / 4;
+  for (int it = threadIdx.x; it < RED_COLS * nq; it += blockDim.x) {
+    const int cc = it / nq, c = c0 + cc, d4 = (it % nq) * 4;
+    if (c >= R) continue;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < nsplit; ++s)
+      acc += *reinterpret_cast<const f32x4*>(a.part_o + ((unit0 + s) * R + c) * D + d4) * w[cc][s];
     const int j = c / g, hq = h * g + c % g;
     const size_t off = ((size_t)(b * T + j) * a.Hq + hq) * D + d4;
     if (a.o_f32) *reinterpret_cast<f32x4*>(a.o_f32 + off) = acc;
     if (a.o_bf16) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) a.o_bf16[off + i] = f2bf(acc[i]);
+      bf16x4 hv = {f2bf(acc[0]), f2bf(acc[1]), f2bf(acc[2]), f2bf(acc[3])};
+      *reinterpret_cast<bf16x4*>(a.o_bf16 + off) = hv;
     }
   }
 }
@@ -457,7 +531,7 @@ __global__ void gather_slots_kernel(int B, int max_pages, int ps, int num_pages,
 #define HSPEC_SWEEP_QB 1
 #endif
 #ifndef HSPEC_SWEEP_ST
-#define HSPEC_SWEEP_ST 4
+#define HSPEC_SWEEP_ST 3
 #endif
 
 template <int D, int QB, int NW, bool LO>
@@ -467,7 +541,21 @@ hipError_t launch_sweep(const AttnArgs& a, hipStream_t s) {
   constexpr int ST_MAX = 2 + 63 / NDMA;                         // vmcnt holds at most 63
   constexpr int ST = LO ? 2 : (HSPEC_SWEEP_ST < ST_MAX ? HSPEC_SWEEP_ST : ST_MAX);
   auto kern = attn_sweep<D, QB, NW, KT, ST, LO>;
-  hipLaunchKernelGGL(kern, dim3(a.max_splits * a.B * a.Hkv), dim3(64 * NW), 0, s, a);
+  static int slots_of[64] = {};   // resident workgroups per device (persistent grid size)
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  int& slots = slots_of[dev & 63];
+  if (slots == 0) {
+    int cus = 0, per_cu = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 64 * NW, 0);
+    if (e != hipSuccess) return e;
+    slots = cus * (per_cu > 0 ? per_cu : 1);
+  }
+  const long long items = (long long)a.B * a.max_splits * a.Hkv;
+  const int grid = (int)(items < slots ? items : slots);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * NW), 0, s, a);
   return hipGetLastError();
 }
 
@@ -491,25 +579,32 @@ size_t attention_partials_bytes(int B, int Hkv, int max_splits, int R, int D) {
 }
 
 int attention_default_split(int B, int Hkv, int max_ctx_len) {
-  // Aim for ~2048 work units over the whole batch, in multiples of the 64-key tile.
-  long long want = ((long long)max_ctx_len * B * Hkv + 2047) / 2048;
+  // About 1024 (request, split, head) items of the longest requests: enough to fill every
+  // resident workgroup slot, few enough that split partials and unit start-up stay small.
+  long long want = ((long long)max_ctx_len * B * Hkv + 1023) / 1024;
   long long s = ((want + 63) / 64) * 64;
   if (s < 256) s = 256;
   long long cap = ((long long)(max_ctx_len > 0 ? max_ctx_len : 1) + 63) / 64 * 64;
   if (s > cap) s = cap;
   if (s > MAX_SPLIT) s = MAX_SPLIT;
+  const long long min_for_256 = ((long long)max_ctx_len + 255) / 256;   // at most 256 splits
+  if (s < min_for_256) s = (min_for_256 + 63) / 64 * 64;
   return (int)s;
 }
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   const bool lo = a.q_lo != nullptr;
-  hipError_t e;
+  hipLaunchKernelGGL(attn_plan, dim3(1), dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   if (a.D == 128) e = lo ? launch_sweep_nw<128, true>(a, s) : launch_sweep_nw<128, false>(a, s);
   else if (a.D == 64) e = lo ? launch_sweep_nw<64, true>(a, s) : launch_sweep_nw<64, false>(a, s);
   else return hipErrorInvalidValue;
   if (e != hipSuccess) return e;
   if (a.max_splits > 1) {
-    hipLaunchKernelGGL(attn_reduce, dim3(a.B * a.Hkv), dim3(256), 0, s, a);
+    const int R = a.T * (a.Hq / a.Hkv);
+    const int cblocks = (R + RED_COLS - 1) / RED_COLS;
+    hipLaunchKernelGGL(attn_reduce, dim3(a.B * a.Hkv * cblocks), dim3(256), 0, s, a);
     e = hipGetLastError();
   }
   return e;

@@ -35,10 +35,12 @@ struct AttnArgs {
   float* part_ml = nullptr;   // [B*Hkv*max_splits, R, 2]
   float* o_f32 = nullptr;     // [B, T, Hq, D] (one of o_f32 / o_bf16)
   bf16* o_bf16 = nullptr;
-  int* status = nullptr;
+  int* status = nullptr;      // device status word; status[1] = work items, status[2] = queue
+  int32_t* units = nullptr;   // [B * max_splits] work list (request << 16 | split), longest first
 };
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
 size_t attention_partials_bytes(int B, int Hkv, int max_splits, int R, int D);
+constexpr int kStatusWords = 64;   // int32 words reserved at the start of every workspace
 int attention_default_split(int B, int Hkv, int max_ctx_len);
 
 hipError_t launch_gather_slots(int B, int max_pages, int ps, int num_pages, const int32_t* page_table,
