@@ -1,6 +1,7 @@
 """Benchmark of one H-Spec block-drafting step on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3]
+    python bench.py --counters      # one launch of each measured kernel, for rocprofv3 --pmc
 
 A step is one call of hspec_draft_step over the whole batch: state projection from the
 last-token hidden state, the Mamba-2 layer with its chunked scan, and the attention layer
@@ -84,15 +85,55 @@ def cpu_baseline(cfg, W, x, n_req: int):
                       f"projection), {dt:.1f} s wall"}
 
 
+def sweep_inputs(cfg, Xd, x, seed, torch):
+    """Block queries/keys/values for the KV sweep over the same cache, table and lengths."""
+    Ad = dict(Xd)
+    for k, name, heads in (("q", "attn_q", cfg.Hq), ("k_blk", "attn_kblk", cfg.Hkv), ("v_blk", "attn_vblk", cfg.Hkv)):
+        Ad[k] = hspec.to_device(I.normal(name, (cfg.B, cfg.k, heads, cfg.D), 1.0, seed, cfg.dtype))
+    maxL = int(x["ctx_lens"].max())
+    aws = hspec.workspace(hspec.paged_attn_workspace(cfg, x["page_table"].shape[1], x["num_pages"], maxL))
+    o = torch.empty((cfg.B, cfg.k, cfg.Hq, cfg.D), dtype=torch.float32, device="cuda")
+    return Ad, aws, o
+
+
+def counters(cfg, seed, torch):
+    """One launch each of a 1 GiB device copy (to calibrate the byte counters), the state
+    projection and the KV sweep, for FETCH_SIZE / WRITE_SIZE collection under rocprofv3."""
+    src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+    log("copy: 1 GiB")
+    W = I.make_weights(cfg, seed, skip=("W_in", "W_out", "W_q", "W_k", "W_v", "W_o"))
+    x = I.make_inputs(cfg, seed)
+    Wd = {k: hspec.to_device(W[k]) for k in ("W_r", "W_dS")}
+    S0 = torch.empty((cfg.B, cfg.H, cfg.P, cfg.N), dtype=torch.float32, device="cuda")
+    sws = hspec.workspace(hspec.state_init_workspace(cfg))
+    hspec.state_init(cfg, Wd, hspec.to_device(x["h_last"]), S0, sws)
+    torch.cuda.synchronize()
+    log("state projection: 1 launch")
+    del Wd, S0, sws
+    Xd = {k: hspec.to_device(v) if isinstance(v, np.ndarray) else v for k, v in x.items()
+          if k not in ("h_last", "block_emb")}
+    Ad, aws, o = sweep_inputs(cfg, Xd, x, seed, torch)
+    hspec.paged_attn(cfg, Ad, o, aws, int(x["ctx_lens"].max()))
+    torch.cuda.synchronize()
+    log("KV sweep: 1 launch")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=3)
-    ap.add_argument("--cpu-requests", type=int, default=2)
+    ap.add_argument("--cpu-requests", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--counters", action="store_true",
+                    help="launch each measured kernel once (for rocprofv3 --pmc) and exit")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -104,6 +145,9 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     cfg = I.CONFIGS[args.config]
+    if args.counters:
+        counters(cfg, args.seed, torch)
+        return
     t0 = time.perf_counter()
     W = I.make_weights(cfg, args.seed)
     x = I.make_inputs(cfg, args.seed)
@@ -146,11 +190,7 @@ def main():
     del S0, sws
 
     # the target-KV sweep + split reduction (the spec bar), same cache, table and lengths
-    Ad = dict(Xd)
-    for k, name, heads in (("q", "attn_q", cfg.Hq), ("k_blk", "attn_kblk", cfg.Hkv), ("v_blk", "attn_vblk", cfg.Hkv)):
-        Ad[k] = hspec.to_device(I.normal(name, (cfg.B, cfg.k, heads, cfg.D), 1.0, args.seed, cfg.dtype))
-    aws = hspec.workspace(hspec.paged_attn_workspace(cfg, x["page_table"].shape[1], x["num_pages"], maxL))
-    o = torch.empty((cfg.B, cfg.k, cfg.Hq, cfg.D), dtype=torch.float32, device="cuda")
+    Ad, aws, o = sweep_inputs(cfg, Xd, x, args.seed, torch)
     t_sweep = time_launches(lambda: hspec.paged_attn(cfg, Ad, o, aws, maxL), args.steps, torch)
     b_sweep = RL.sweep_bytes(cfg, L)
     log(f"state projection: {t_state * 1e6:.1f} us, {b_state / t_state / 1e9:.0f} GB/s; "

@@ -21,9 +21,10 @@
  *     call returns without synchronising.  Calls on different streams with disjoint
  *     workspaces may run concurrently.
  *   - Workspace: caller-provided device scratch of at least the size returned by the matching
- *     *_workspace() query; 256-byte aligned.  Its first 4 bytes are a device status word that
- *     the call resets and the kernels OR bits into (HSPEC_DEV_*); read it after the stream
- *     completes with hspec_read_status().
+ *     *_workspace() query; 256-byte aligned.  Its first 256 bytes are reserved: the first
+ *     int32 is a device status word that the call resets and the kernels OR bits into
+ *     (HSPEC_DEV_*), read it after the stream completes with hspec_read_status(); the rest
+ *     holds the work-queue counters of the attention sweep.
  *   - Errors: host-checkable problems (NULL pointers, non-positive or inconsistent sizes,
  *     unsupported dimensions, a too-small workspace) return an error before anything is
  *     enqueued.  A failed launch returns HSPEC_ERR_LAUNCH.  hspec_last_error() gives a
@@ -95,13 +96,16 @@ typedef struct {
 /*
  * Attention layer configuration (Sec. 3.3.2; App. B.2 "Unified attention implementation").
  *   Hq query heads, Hkv KV heads (Hq % Hkv == 0, query head q reads KV head q / (Hq/Hkv)),
- *   D head dim (64 or 128), k * Hq/Hkv <= 128.  The target cache is two pools
+ *   D head dim (64 or 128), k * Hq/Hkv <= 128, B <= 32767, page_size a power of two >= 16.
+ *   The target cache is two pools
  *   [num_pages, page_size, Hkv, D] (K stored after RoPE), addressed through page_table
  *   [B, max_pages] int32 and ctx_lens [B] int32: cache position i of request b lives in
  *   slot page_table[b, i / page_size] * page_size + i % page_size.  Block position j sits at
  *   RoPE position ctx_lens[b] + j.  window > 0 hides cache position p from the query at
  *   position pos when pos - p >= window (sliding window; requires k <= window).
- *   split_tokens: context length per split of the KV sweep (multiple of 64), 0 = automatic.
+ *   split_tokens: context length per split of the KV sweep (multiple of 64, at most 8192,
+ *   and at least max_ctx_len / 256 so that no request has more than 256 splits), 0 = automatic.
+ *   A setting outside these limits returns HSPEC_ERR_UNSUPPORTED.
  *   scale: softmax scale, 0 = 1/sqrt(D).  rope_theta: RoPE base (rotate-half pairing).
  */
 typedef struct {

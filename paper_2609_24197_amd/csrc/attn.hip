@@ -427,34 +427,61 @@ attn_sweep(AttnArgs a) {
 
 // Work list of the sweep: every (request, split) once, the full splits first and then the
 // last splits by decreasing length, so the persistent workgroups finish close together.
-// One workgroup; also resets the item queue.
-__global__ void __launch_bounds__(256) attn_plan(AttnArgs a) {
-  __shared__ int s_full;
-  if (threadIdx.x == 0) {
-    int full = 0;
-    for (int b = 0; b < a.B; ++b) {
+// One workgroup of PLAN_THREADS: the full splits are placed by a block-wide prefix sum over
+// requests, the last splits by rank (requests beyond PLAN_RANK_MAX keep their own order).
+// Also resets the item queue.
+constexpr int PLAN_THREADS = 1024;
+constexpr int PLAN_RANK_MAX = 4096;
+
+__global__ void __launch_bounds__(PLAN_THREADS) attn_plan(AttnArgs a) {
+  __shared__ int s_rem[PLAN_RANK_MAX];
+  __shared__ int s_scan[PLAN_THREADS];
+  __shared__ int s_base;
+  const int tid = threadIdx.x;
+  const bool ranked = a.B <= PLAN_RANK_MAX;
+  if (tid == 0) s_base = 0;
+  __syncthreads();
+  for (int b0 = 0; b0 < a.B; b0 += PLAN_THREADS) {
+    const int b = b0 + tid;
+    int nfull = 0;
+    if (b < a.B) {
       const int L = clamp_len(a, b);
       const int ns = L > 0 ? (L + a.split - 1) / a.split : 1;
-      for (int sp = 0; sp < ns - 1; ++sp) a.units[full++] = (b << 16) | sp;
+      nfull = ns - 1;
+      if (ranked) s_rem[b] = L - nfull * a.split;
     }
-    s_full = full;
-    a.status[1] = (full + a.B) * a.Hkv;
-    a.status[2] = 0;
+    s_scan[tid] = nfull;
+    __syncthreads();
+    for (int o = 1; o < PLAN_THREADS; o <<= 1) {
+      const int v = tid >= o ? s_scan[tid - o] : 0;
+      __syncthreads();
+      s_scan[tid] += v;
+      __syncthreads();
+    }
+    const int first = s_base + s_scan[tid] - nfull;
+    for (int sp = 0; sp < nfull; ++sp) a.units[first + sp] = (b << 16) | sp;
+    __syncthreads();
+    if (tid == PLAN_THREADS - 1) s_base += s_scan[tid];
+    __syncthreads();
   }
-  __syncthreads();
-  const int full = s_full;
-  for (int b = threadIdx.x; b < a.B; b += blockDim.x) {
+  const int full = s_base;
+  for (int b = tid; b < a.B; b += PLAN_THREADS) {
     const int L = clamp_len(a, b);
     const int ns = L > 0 ? (L + a.split - 1) / a.split : 1;
-    const int rem = L - (ns - 1) * a.split;
-    int rank = 0;
-    for (int o = 0; o < a.B; ++o) {
-      const int Lo = clamp_len(a, o);
-      const int no = Lo > 0 ? (Lo + a.split - 1) / a.split : 1;
-      const int ro = Lo - (no - 1) * a.split;
-      rank += (ro > rem) || (ro == rem && o < b);
+    int rank = b;
+    if (ranked) {
+      const int rem = s_rem[b];
+      rank = 0;
+      for (int o = 0; o < a.B; ++o) {
+        const int ro = s_rem[o];
+        rank += (ro > rem) || (ro == rem && o < b);
+      }
     }
     a.units[full + rank] = (b << 16) | (ns - 1);
+  }
+  if (tid == 0) {
+    a.status[1] = (full + a.B) * a.Hkv;
+    a.status[2] = 0;
   }
 }
 
@@ -594,7 +621,7 @@ int attention_default_split(int B, int Hkv, int max_ctx_len) {
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   const bool lo = a.q_lo != nullptr;
-  hipLaunchKernelGGL(attn_plan, dim3(1), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(attn_plan, dim3(1), dim3(PLAN_THREADS), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (a.D == 128) e = lo ? launch_sweep_nw<128, true>(a, s) : launch_sweep_nw<128, false>(a, s);

@@ -154,12 +154,12 @@ def attn_cfg(cfg: I.StepConfig, max_pages: int, num_pages: int) -> AttnCfg:
 
 
 def mamba_w(W: dict) -> MambaW:
-    return MambaW(*(ptr(W[n]) for n in ("W_r", "W_dS", "W_in", "conv_w", "conv_b", "dt_bias", "A_log", "D",
+    return MambaW(*(ptr(W.get(n)) for n in ("W_r", "W_dS", "W_in", "conv_w", "conv_b", "dt_bias", "A_log", "D",
                                          "gnorm_w", "W_out")))
 
 
 def attn_w(W: dict) -> AttnW:
-    return AttnW(*(ptr(W[n]) for n in ("W_q", "W_k", "W_v", "W_o", "q_norm_w", "k_norm_w")))
+    return AttnW(*(ptr(W.get(n)) for n in ("W_q", "W_k", "W_v", "W_o", "q_norm_w", "k_norm_w")))
 
 
 def read_status(ws) -> int:
