@@ -23,6 +23,13 @@ sequential per-token recurrence.  ``ssd_chunked`` is a second float64
 formulation (the SSD chunk algebra) kept only so that tests can pin the
 sequential one against an independent derivation.
 
+Pins: every primitive here (state projection layout, conv, pointwise functions,
+RoPE, slot map, naive attention, the recurrence) is checked against textbook
+special cases, closed forms and library routines.  The composed functions
+``mamba_mixer``, ``attention_layer`` and ``draft_step`` are pinned only through
+their parts and whole-function properties (zero input, causality, decay rate,
+residual structure, dense-cache attention); beyond those they are parity unpinned.
+
 Inputs are storage arrays: bf16 as uint16 bit patterns, or float32/float64.
 They are widened to float64 here, block by block for the large state
 projection.
