@@ -72,12 +72,18 @@ enum { HSPEC_DEV_BAD_PAGE = 1, HSPEC_DEV_BAD_CTX_LEN = 2 };
  *   (P must be 64), N = d_state (16, 32, 64 or 128), G groups of B/C (H % G == 0),
  *   chunk = SSD chunk length (1..16), conv_w = causal conv width (1..8), eps of every RMSNorm.
  *   d_inner = H*P, d_S = H*P*N.  d_h, r, d_model must be multiples of 8.
+ *   flags: HSPEC_W_DS_PACKED when hspec_mamba_w.W_dS points at the packed layout written by
+ *   hspec_pack_w_ds (bf16 storage, r a multiple of 32), else 0.
  */
 typedef struct {
   int B, k, d_model, d_h, r, H, P, N, G, chunk, conv_w;
+  unsigned flags;
   hspec_dtype dtype;
   float eps;
 } hspec_mamba_cfg;
+
+/* hspec_mamba_cfg.flags */
+enum { HSPEC_W_DS_PACKED = 1u << 0 };
 
 /*
  * Mamba weights.  Matrices are [out, in] row-major in the storage dtype:
@@ -169,6 +175,21 @@ hspec_status hspec_draft_step(const hspec_mamba_cfg* mcfg, const hspec_mamba_w* 
                               const void* v_cache, const int32_t* page_table, const int32_t* ctx_lens,
                               int max_ctx_len, float* out, void* workspace, size_t ws_bytes, void* stream);
 size_t hspec_draft_step_workspace(const hspec_mamba_cfg* mcfg, const hspec_attn_cfg* acfg, int max_ctx_len);
+
+/* ------------------------------------------------------------- weight preparation */
+
+/*
+ * Packed layout of W_dS for the state projection (Sec. 3.3.1, Proj_dS), written once when
+ * the weights are loaded, never per step.  The projection streams W_dS from HBM once per
+ * step; this layout lets every wave read whole 1 KB blocks that are already MFMA operand
+ * fragments.  Block (s, t) holds rows 16t..16t+15 and columns 32s..32s+31 of W_dS and
+ * starts at byte ((s * d_S/16) + t) * 1024; inside it, the 8 consecutive columns
+ * 32s + 8c .. +7 of row 16t + i are the 16 bytes at (i + 16c) * 16.
+ * W_dS [d_S, r] row-major bf16 in, W_packed (hspec_pack_w_ds_bytes bytes) out, both device
+ * memory; d_S % 16 == 0 and r % 32 == 0, else HSPEC_ERR_UNSUPPORTED.  Asynchronous on stream.
+ */
+size_t hspec_pack_w_ds_bytes(int d_S, int r);
+hspec_status hspec_pack_w_ds(int d_S, int r, const void* W_dS, void* W_packed, void* stream);
 
 /* --------------------------------------------------- primitives (same kernels as above) */
 

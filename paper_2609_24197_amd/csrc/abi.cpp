@@ -2,8 +2,11 @@
 // launch sequence of each entry point.  Host code only; every kernel lives in a .hip file.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <array>
 #include <cmath>
 #include <cstdarg>
+#include <initializer_list>
 #include <cstdio>
 #include <string>
 
@@ -83,6 +86,22 @@ hipError_t as_planes(const void* src, hspec_dtype d, const SplitSlot& slot, Plan
   return hspec::launch_split_planes(static_cast<const float*>(src), slot.n, slot.hi, slot.lo, st);
 }
 
+// Split-K scratch shared by a sequence of GEMMs on one stream, sized for the largest.
+struct GemmScratch {
+  float* p = nullptr;
+  size_t cap = 0;
+};
+GemmScratch reserve_gemm(Arena& ar, hspec_dtype d, std::initializer_list<std::array<int, 3>> mnk) {
+  GemmScratch s;
+  for (const auto& x : mnk) s.cap = std::max(s.cap, hspec::gemm_scratch_elems(x[0], x[1], x[2], true, is_f32(d)));
+  if (s.cap) s.p = ar.take<float>(s.cap);
+  return s;
+}
+void use_scratch(hspec::GemmArgs& g, const GemmScratch& s) {
+  g.part = s.p;
+  g.part_cap = s.cap;
+}
+
 // ------------------------------------------------------------------------- validation
 
 hspec_status check_mamba(const hspec_mamba_cfg* c, const hspec_mamba_w* w, bool full) {
@@ -94,6 +113,9 @@ hspec_status check_mamba(const hspec_mamba_cfg* c, const hspec_mamba_w* w, bool 
   if (c->N != 16 && c->N != 32 && c->N != 64 && c->N != 128)
     return fail(HSPEC_ERR_UNSUPPORTED, "N (d_state) must be 16, 32, 64 or 128, got %d", c->N);
   if (c->d_h % 8 || c->r % 8) return fail(HSPEC_ERR_UNSUPPORTED, "d_h and r must be multiples of 8");
+  if (c->flags & ~(unsigned)HSPEC_W_DS_PACKED) return fail(HSPEC_ERR_UNSUPPORTED, "unknown mamba flags 0x%x", c->flags);
+  if ((c->flags & HSPEC_W_DS_PACKED) && (is_f32(c->dtype) || c->r % 32))
+    return fail(HSPEC_ERR_UNSUPPORTED, "a packed W_dS needs bf16 storage and r %% 32 == 0");
   if (!w->W_r || !w->W_dS) return fail(HSPEC_ERR_NULL, "W_r or W_dS is NULL");
   if (!full) return HSPEC_OK;
   if (c->k <= 0 || c->d_model <= 0 || c->G <= 0 || c->chunk <= 0 || c->conv_w <= 0)
@@ -152,6 +174,7 @@ hspec_status check_ws(void* ws, size_t have, size_t need) {
 
 struct StatePlan {
   SplitSlot h, wr, wds;
+  GemmScratch gs;
   bf16 *F_hi = nullptr, *F_lo = nullptr;
   bf16 *S0_hi = nullptr, *S0_lo = nullptr;
 };
@@ -163,6 +186,7 @@ void plan_state(Arena& ar, const hspec_mamba_cfg& c, bool s0_planes, StatePlan& 
   p.wds = reserve_split(ar, c.dtype, dS * c.r);
   p.F_hi = ar.take<bf16>((size_t)c.B * c.r);
   p.F_lo = ar.take<bf16>((size_t)c.B * c.r);
+  p.gs = reserve_gemm(ar, c.dtype, {{c.B, c.r, c.d_h}, {c.B, (int)dS, c.r}});
   if (s0_planes) {
     p.S0_hi = ar.take<bf16>((size_t)c.B * dS);
     p.S0_lo = ar.take<bf16>((size_t)c.B * dS);
@@ -181,6 +205,7 @@ hspec_status run_state(const hspec_mamba_cfg& c, const hspec_mamba_w& w, const v
   g1.W_hi = wr.hi; g1.W_lo = wr.lo; g1.ldw = c.d_h;
   g1.M = c.B; g1.N = c.r; g1.K = c.d_h;
   g1.C_hi = p.F_hi; g1.C_lo = p.F_lo; g1.ldch = c.r;
+  use_scratch(g1, p.gs);
   HIP_TRY(hspec::launch_gemm(g1, st));
   const int dS = c.H * c.P * c.N;
   hspec::GemmArgs g2;
@@ -189,6 +214,8 @@ hspec_status run_state(const hspec_mamba_cfg& c, const hspec_mamba_w& w, const v
   g2.M = c.B; g2.N = dS; g2.K = c.r;
   g2.C = S0_f32; g2.ldc = dS;
   g2.C_hi = p.S0_hi; g2.C_lo = p.S0_lo; g2.ldch = dS;
+  g2.w_packed = (c.flags & HSPEC_W_DS_PACKED) ? 1 : 0;
+  use_scratch(g2, p.gs);
   HIP_TRY(hspec::launch_gemm(g2, st));
   return HSPEC_OK;
 }
@@ -202,6 +229,7 @@ struct MambaPlan {
   float* dt = nullptr;
   float* y = nullptr;
   bf16 *yn_hi = nullptr, *yn_lo = nullptr;
+  GemmScratch gs;
 };
 
 void plan_mamba(Arena& ar, const hspec_mamba_cfg& c, bool u_norm, MambaPlan& p) {
@@ -228,6 +256,7 @@ void plan_mamba(Arena& ar, const hspec_mamba_cfg& c, bool u_norm, MambaPlan& p) 
   p.y = ar.take<float>(M * di);
   p.yn_hi = ar.take<bf16>(M * di);
   p.yn_lo = ar.take<bf16>(M * di);
+  p.gs = reserve_gemm(ar, c.dtype, {{(int)M, (int)dproj, c.d_model}, {(int)M, c.d_model, (int)di}});
 }
 
 // in_proj -> conv/split -> scan from S0 planes -> gated norm -> out_proj (+ residual R).
@@ -244,6 +273,7 @@ hspec_status run_mamba_core(const hspec_mamba_cfg& c, const hspec_mamba_w& w, Pl
   gi.W_hi = win.hi; gi.W_lo = win.lo; gi.ldw = c.d_model;
   gi.M = M; gi.N = dproj; gi.K = c.d_model;
   gi.C = p.zx; gi.ldc = dproj;
+  use_scratch(gi, p.gs);
   HIP_TRY(hspec::launch_gemm(gi, st));
 
   hspec::ConvArgs ca;
@@ -270,6 +300,7 @@ hspec_status run_mamba_core(const hspec_mamba_cfg& c, const hspec_mamba_w& w, Pl
   go.M = M; go.N = c.d_model; go.K = di;
   go.C = out; go.ldc = c.d_model;
   go.R = R; go.ldr = c.d_model; go.r_bf16 = r_bf16;
+  use_scratch(go, p.gs);
   HIP_TRY(hspec::launch_gemm(go, st));
   return HSPEC_OK;
 }
@@ -284,6 +315,7 @@ struct AttnPlan {
   int32_t* units = nullptr;
   bf16 *o_hi = nullptr, *o_lo = nullptr;
   int split = 0, max_splits = 0;
+  GemmScratch gs;
 };
 
 void plan_sweep(Arena& ar, const hspec_attn_cfg& c, int max_ctx_len, AttnPlan& p) {
@@ -325,6 +357,8 @@ void plan_attn(Arena& ar, const hspec_attn_cfg& c, int max_ctx_len, bool x_norm,
   }
   plan_sweep(ar, c, max_ctx_len, p);
   p.o_hi = ar.take<bf16>(M * c.Hq * c.D);
+  p.gs = reserve_gemm(ar, c.dtype, {{(int)M, c.Hq * c.D, c.d_model}, {(int)M, c.Hkv * c.D, c.d_model},
+                                    {(int)M, c.d_model, c.Hq * c.D}});
 }
 
 hspec::AttnArgs sweep_args(const hspec_attn_cfg& c, const AttnPlan& p, const int32_t* pt, const int32_t* lens,
@@ -363,6 +397,7 @@ hspec_status run_attn_core(const hspec_attn_cfg& c, const hspec_attn_w& w, Plane
     g.W_hi = ws[i]->hi; g.W_lo = ws[i]->lo; g.ldw = c.d_model;
     g.M = M; g.N = nrows[i]; g.K = c.d_model;
     g.C = p.qkv + col; g.ldc = ldq;
+    use_scratch(g, p.gs);
     HIP_TRY(hspec::launch_gemm(g, st));
     col += nrows[i];
   }
@@ -379,6 +414,7 @@ hspec_status run_attn_core(const hspec_attn_cfg& c, const hspec_attn_w& w, Plane
   g.M = M; g.N = c.d_model; g.K = c.Hq * c.D;
   g.C = out; g.ldc = c.d_model;
   g.R = R; g.ldr = c.d_model; g.r_bf16 = 0;
+  use_scratch(g, p.gs);
   HIP_TRY(hspec::launch_gemm(g, st));
   return HSPEC_OK;
 }
@@ -645,6 +681,7 @@ HSPEC_API size_t hspec_linear_workspace(hspec_dtype dtype, int M, int N, int K) 
   if (M > 0 && N > 0 && K > 0) {
     reserve_split(ar, dtype, (size_t)M * K);
     reserve_split(ar, dtype, (size_t)N * K);
+    reserve_gemm(ar, dtype, {{M, N, K}});
   }
   return ar.size();
 }
@@ -661,6 +698,7 @@ HSPEC_API hspec_status hspec_linear(hspec_dtype dtype, int M, int N, int K, cons
   Arena ar{(char*)workspace};
   int* status = status_word(ar);
   SplitSlot sa = reserve_split(ar, dtype, (size_t)M * K), sw = reserve_split(ar, dtype, (size_t)N * K);
+  const GemmScratch gs = reserve_gemm(ar, dtype, {{M, N, K}});
   HIP_TRY(hspec::launch_zero_words(status, 1, st));
   Planes pa, pw;
   HIP_TRY(as_planes(A, dtype, sa, pa, st));
@@ -670,7 +708,23 @@ HSPEC_API hspec_status hspec_linear(hspec_dtype dtype, int M, int N, int K, cons
   g.W_hi = pw.hi; g.W_lo = pw.lo; g.ldw = K;
   g.M = M; g.N = N; g.K = K;
   g.C = C; g.ldc = N; g.R = R; g.ldr = N; g.r_bf16 = 0;
+  use_scratch(g, gs);
   HIP_TRY(hspec::launch_gemm(g, st));
+  return HSPEC_OK;
+}
+
+HSPEC_API size_t hspec_pack_w_ds_bytes(int d_S, int r) {
+  if (d_S <= 0 || r <= 0 || d_S % 16 || r % 32) return 0;
+  return (size_t)d_S * r * sizeof(bf16);
+}
+
+HSPEC_API hspec_status hspec_pack_w_ds(int d_S, int r, const void* W_dS, void* W_packed, void* stream) {
+  g_err.clear();
+  if (d_S <= 0 || r <= 0) return fail(HSPEC_ERR_SHAPE, "non-positive W_dS dimension");
+  if (d_S % 16 || r % 32) return fail(HSPEC_ERR_UNSUPPORTED, "packing needs d_S %% 16 == 0 and r %% 32 == 0");
+  if (!W_dS || !W_packed) return fail(HSPEC_ERR_NULL, "W_dS or W_packed is NULL");
+  HIP_TRY(hspec::launch_pack_w(static_cast<const bf16*>(W_dS), d_S, r, static_cast<bf16*>(W_packed),
+                               (hipStream_t)stream));
   return HSPEC_OK;
 }
 

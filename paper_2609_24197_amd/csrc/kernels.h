@@ -16,8 +16,17 @@ struct GemmArgs {
   float* C = nullptr; int ldc = 0;             // fp32 result (optional)
   const void* R = nullptr; int ldr = 0; int r_bf16 = 0;   // residual added (optional)
   bf16* C_hi = nullptr; bf16* C_lo = nullptr; int ldch = 0;  // bf16 planes of the result
+  float* part = nullptr; size_t part_cap = 0;  // split-K scratch (fp32 elements), optional
+  int w_packed = 0;   // W_hi is in the fragment-major packed layout (launch_pack_w)
 };
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
+// fp32 elements of split-K scratch that launch_gemm uses for an M x N x K product when
+// given at least that much (0: the shape is never split).
+size_t gemm_scratch_elems(int M, int N, int K, bool a_lo, bool w_lo);
+// Rewrites a row-major bf16 W[N, K] (N % 16 == 0, K % 32 == 0) into the packed layout that
+// launch_gemm streams when w_packed is set: 1 KB blocks (k-step s, 16-row tile t) at
+// ((s * N/16) + t) * 1024 bytes, each one 16x32 MFMA operand fragment.
+hipError_t launch_pack_w(const bf16* W, int N, int K, bf16* Wp, hipStream_t s);
 
 // Paged block attention (split-K sweep over the target cache + block keys, then reduce).
 struct AttnArgs {

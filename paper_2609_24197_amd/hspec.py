@@ -19,6 +19,7 @@ _lib = None
 
 BF16, F32 = 0, 1
 BLOCK_CAUSAL = 1
+W_DS_PACKED = 1
 DEV_BAD_PAGE, DEV_BAD_CTX_LEN = 1, 2
 STATUS = {0: "HSPEC_OK", 1: "HSPEC_ERR_NULL", 2: "HSPEC_ERR_SHAPE", 3: "HSPEC_ERR_DTYPE",
           4: "HSPEC_ERR_UNSUPPORTED", 5: "HSPEC_ERR_WORKSPACE", 6: "HSPEC_ERR_LAUNCH"}
@@ -26,7 +27,7 @@ STATUS = {0: "HSPEC_OK", 1: "HSPEC_ERR_NULL", 2: "HSPEC_ERR_SHAPE", 3: "HSPEC_ER
 
 class MambaCfg(C.Structure):
     _fields_ = [(n, C.c_int) for n in ("B", "k", "d_model", "d_h", "r", "H", "P", "N", "G", "chunk", "conv_w")] + [
-        ("dtype", C.c_int), ("eps", C.c_float)]
+        ("flags", C.c_uint), ("dtype", C.c_int), ("eps", C.c_float)]
 
 
 class MambaW(C.Structure):
@@ -75,6 +76,8 @@ EXPORTS = {
                                                       C.c_void_p]),
     "hspec_linear": (C.c_int, [C.c_int] * 4 + [C.c_void_p] * 5 + [C.c_size_t, C.c_void_p]),
     "hspec_linear_workspace": (C.c_size_t, [C.c_int] * 4),
+    "hspec_pack_w_ds_bytes": (C.c_size_t, [C.c_int, C.c_int]),
+    "hspec_pack_w_ds": (C.c_int, [C.c_int, C.c_int, C.c_void_p, C.c_void_p, C.c_void_p]),
     "hspec_read_status": (C.c_int, [C.c_void_p, C.POINTER(C.c_int32), C.c_void_p]),
     "hspec_status_string": (C.c_char_p, [C.c_int]),
     "hspec_last_error": (C.c_char_p, []),
@@ -142,9 +145,11 @@ def dtype_code(cfg: I.StepConfig) -> int:
     return F32 if cfg.dtype == "f32" else BF16
 
 
-def mamba_cfg(cfg: I.StepConfig) -> MambaCfg:
+def mamba_cfg(cfg: I.StepConfig, W: dict | None = None) -> MambaCfg:
+    """The Mamba config; W_DS_PACKED is set when W carries "W_dS_packed" (see pack_w_ds)."""
+    flags = W_DS_PACKED if W is not None and W.get("W_dS_packed") is not None else 0
     return MambaCfg(cfg.B, cfg.k, cfg.d_model, cfg.d_h, cfg.rank, cfg.H, cfg.P, cfg.N, cfg.G, cfg.chunk,
-                    cfg.conv_w, dtype_code(cfg), cfg.eps)
+                    cfg.conv_w, flags, dtype_code(cfg), cfg.eps)
 
 
 def attn_cfg(cfg: I.StepConfig, max_pages: int, num_pages: int) -> AttnCfg:
@@ -154,8 +159,20 @@ def attn_cfg(cfg: I.StepConfig, max_pages: int, num_pages: int) -> AttnCfg:
 
 
 def mamba_w(W: dict) -> MambaW:
-    return MambaW(*(ptr(W.get(n)) for n in ("W_r", "W_dS", "W_in", "conv_w", "conv_b", "dt_bias", "A_log", "D",
-                                         "gnorm_w", "W_out")))
+    """Weight pointers; a "W_dS_packed" entry replaces W_dS (pair it with mamba_cfg(cfg, W))."""
+    names = ("W_r", "W_dS", "W_in", "conv_w", "conv_b", "dt_bias", "A_log", "D", "gnorm_w", "W_out")
+    return MambaW(*(ptr(W.get("W_dS_packed", W.get("W_dS")) if n == "W_dS" else W.get(n)) for n in names))
+
+
+def pack_w_ds(W_dS, d_S: int, r: int):
+    """The packed copy of a bf16 W_dS [d_S, r] device tensor (hspec_pack_w_ds), as a new tensor."""
+    import torch
+    nbytes = lib().hspec_pack_w_ds_bytes(int(d_S), int(r))
+    if nbytes == 0:
+        raise HspecError(4, "W_dS shape cannot be packed")
+    out = torch.empty(nbytes // 2, dtype=torch.bfloat16, device=W_dS.device)
+    _check(lib().hspec_pack_w_ds(int(d_S), int(r), ptr(W_dS), ptr(out), stream_ptr()))
+    return out
 
 
 def attn_w(W: dict) -> AttnW:
@@ -177,7 +194,7 @@ def draft_step_workspace(cfg, max_pages, num_pages, max_ctx_len) -> int:
 
 def draft_step(cfg, W: dict, X: dict, out, ws, max_ctx_len: int):
     """out [B, k, d_model] fp32 = one drafting step (see hspec_draft_step)."""
-    mc = mamba_cfg(cfg)
+    mc = mamba_cfg(cfg, W)
     ac = attn_cfg(cfg, X["page_table"].shape[1], X["k_cache"].shape[0])
     mw, aw = mamba_w(W), attn_w(W)
     _check(lib().hspec_draft_step(C.byref(mc), C.byref(mw), ptr(W["norm1_w"]), C.byref(ac), C.byref(aw),
@@ -192,7 +209,7 @@ def mamba_block_scan_workspace(cfg) -> int:
 
 
 def mamba_block_scan(cfg, W, h_last, u, out, ws, S_final=None):
-    mc, mw = mamba_cfg(cfg), mamba_w(W)
+    mc, mw = mamba_cfg(cfg, W), mamba_w(W)
     _check(lib().hspec_mamba_block_scan(C.byref(mc), C.byref(mw), ptr(h_last), ptr(u), ptr(out), ptr(S_final),
                                         ptr(ws), ws.numel(), stream_ptr()))
 
@@ -216,7 +233,7 @@ def state_init_workspace(cfg) -> int:
 
 
 def state_init(cfg, W, h_last, S0, ws):
-    mc, mw = mamba_cfg(cfg), mamba_w(W)
+    mc, mw = mamba_cfg(cfg, W), mamba_w(W)
     _check(lib().hspec_state_init(C.byref(mc), C.byref(mw), ptr(h_last), ptr(S0), ptr(ws), ws.numel(),
                                   stream_ptr()))
 

@@ -123,6 +123,35 @@ def test_draft_step_validation():
                               FAKE, FAKE, FAKE, 8192, FAKE, ws, n, None) == 1
 
 
+def test_packed_w_ds_validation():
+    L = _lib()
+    ws, n = _ws_big()
+    assert L.hspec_pack_w_ds_bytes(1 << 20, 4096) == (1 << 20) * 4096 * 2
+    assert L.hspec_pack_w_ds_bytes(24, 4096) == 0
+    assert L.hspec_pack_w_ds_bytes(1 << 20, 4008) == 0
+    assert L.hspec_pack_w_ds(0, 32, FAKE, FAKE, None) == 2
+    assert L.hspec_pack_w_ds(24, 32, FAKE, FAKE, None) == 4
+    assert L.hspec_pack_w_ds(16, 40, FAKE, FAKE, None) == 4
+    assert L.hspec_pack_w_ds(16, 32, None, FAKE, None) == 1
+    # the packed flag needs bf16 storage and r % 32 == 0; unknown flags are rejected
+    cfg = I.CONFIGS[3]
+    mw = hspec.MambaW(*([FAKE.value] * 10))
+    S0 = FAKE
+
+    def state(mc):
+        return L.hspec_state_init(C.byref(mc), C.byref(mw), FAKE, S0, ws, n, None)
+    mc = hspec.mamba_cfg(cfg)
+    mc.flags = 2
+    assert state(mc) == 4
+    mc = hspec.mamba_cfg(cfg.replace(dtype="f32"))
+    mc.flags = hspec.W_DS_PACKED
+    assert state(mc) == 4
+    mc = hspec.mamba_cfg(cfg.replace(r=4104))
+    mc.flags = hspec.W_DS_PACKED
+    assert state(mc) == 4
+    assert b"packed" in L.hspec_last_error()
+
+
 def test_workspace_queries_are_consistent():
     _lib()
     for num in (1, 2, 3, 5):

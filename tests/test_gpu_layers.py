@@ -82,6 +82,18 @@ def test_draft_step_small(name):
     assert_close(out, O.draft_step(W, x, cfg), "out")
 
 
+@pytest.mark.parametrize("name", ["small_bf16", "window_causal"])
+def test_draft_step_packed(name):
+    """The drafting step with W_dS in the packed layout gives the same outputs."""
+    cfg = SMALL[name]
+    W, Wd = _weights(cfg, 6)
+    x = I.make_inputs(cfg, seed=6)
+    Wd["W_dS_packed"] = hspec.pack_w_ds(Wd.pop("W_dS"), cfg.d_S, cfg.rank)
+    out, st = _draft(cfg, W, Wd, x)
+    assert st == 0
+    assert_close(out, O.draft_step(W, x, cfg), "out")
+
+
 def test_draft_step_zero_inputs():
     """e = 0 and h_last = 0: out = W_o mean(V over cache and block) per query head."""
     cfg = SMALL["small_bf16"]
@@ -114,6 +126,8 @@ def test_draft_step_full_config(num):
     W = I.make_weights(cfg, 0)
     x = I.make_inputs(cfg, 0)
     Wd = dev(W)
+    if cfg.dtype == "bf16":   # the benchmark streams the packed W_dS
+        Wd["W_dS_packed"] = hspec.pack_w_ds(Wd.pop("W_dS"), cfg.d_S, cfg.rank)
     out, st = _draft(cfg, W, Wd, x)
     assert st == 0
     del Wd

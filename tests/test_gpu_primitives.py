@@ -25,7 +25,8 @@ def _small_attn_cfg(**kw):
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("M,N,K", [(4, 256, 256), (64, 1000, 512), (100, 384, 264), (128, 512, 1024),
-                                   (300, 700, 4096), (1, 4096, 4096)])
+                                   (300, 700, 4096), (1, 4096, 4096), (48, 5000, 4096), (20, 3000, 1024),
+                                   (8, 300, 264), (64, 200000, 160)])
 def test_linear(dtype, M, N, K):
     print(f"[linear] dtype={dtype} M={M} N={N} K={K}", flush=True)
     A = I.normal("lin_A", (M, K), 1.0, 0, dtype)
@@ -244,6 +245,40 @@ def test_ssd_scan_zero_input_zero_state():
 
 
 # -------------------------------------------------------------------- state projection
+
+def _pack_host(W, r):
+    """The packed W_dS layout as the header describes it: block (s, t) at ((s*T + t) * 1024)
+    bytes, row 16t+i, columns 32s+8c..+7 at (i + 16c) * 16 bytes inside the block."""
+    d_S = W.shape[0]
+    T, S = d_S // 16, r // 32
+    blk = W.reshape(T, 16, S, 4, 8)              # [t, i, s, c, e]
+    return np.ascontiguousarray(blk.transpose(2, 0, 3, 1, 4)).reshape(-1)   # [s, t, c, i, e]
+
+
+@pytest.mark.parametrize("d_S,r", [(16, 32), (4096, 256), (2048, 96)])
+def test_pack_w_ds_layout(d_S, r):
+    """Packing is pure data movement: bit-exact against the host re-layout."""
+    W = I.normal("pack_W", (d_S, r), 1.0, 0, "bf16")
+    d = dev(dict(W=W))
+    packed = hspec.pack_w_ds(d["W"], d_S, r)
+    got = packed.view(dtype=__import__("torch").int16).cpu().numpy().view(np.uint16)
+    assert np.array_equal(got, _pack_host(W, r))
+
+
+@pytest.mark.parametrize("B", [1, 5, 40, 64])
+def test_state_init_packed(B):
+    """Proj_dS from the packed W_dS (the layout the benchmark streams) against the oracle."""
+    cfg = _small_attn_cfg(B=B, d_model=512, H=8, N=128, lengths="fixed:16")
+    W = I.make_weights(cfg, seed=7, skip=("W_in", "W_out", "W_q", "W_k", "W_v", "W_o"))
+    x = I.make_inputs(cfg, seed=7)
+    d = dev(dict(W_r=W["W_r"], W_dS=W["W_dS"], h_last=x["h_last"]))
+    Wd = dict(W_r=d["W_r"], W_dS_packed=hspec.pack_w_ds(d["W_dS"], cfg.d_S, cfg.rank))
+    ws = hspec.workspace(hspec.state_init_workspace(cfg))
+    S0 = empty((cfg.B, cfg.H, cfg.P, cfg.N))
+    hspec.state_init(cfg, Wd, d["h_last"], S0, ws)
+    ref, _ = O.state_init(x["h_last"], W["W_r"], W["W_dS"], cfg.H, cfg.P, cfg.N)
+    assert_close(host(S0), ref, "S0")
+
 
 @pytest.mark.parametrize("cfg", [I.CONFIGS[1], _small_attn_cfg(B=5, d_model=512, H=8, N=128, lengths="fixed:16"),
                                  _small_attn_cfg(B=70, d_model=256, H=4, N=128, lengths="fixed:16")],
