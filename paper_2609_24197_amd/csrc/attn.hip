@@ -77,24 +77,6 @@ __device__ __forceinline__ int tile_off(int row, int d) {
   return (row * CPR + ((d >> 3) ^ f)) * 8 + (d & 7);
 }
 
-template <int VM>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(VM >= 0 && VM < 64, "vmcnt range");
-  // gfx9 s_waitcnt immediate: vmcnt[3:0] and [15:14], expcnt[6:4] = 7, lgkmcnt[11:8] = 15 (no wait)
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_waitcnt((VM & 15) | (7 << 4) | (15 << 8) | ((VM >> 4) << 14));
-  asm volatile("" ::: "memory");
-}
-
-__device__ __forceinline__ void wg_barrier() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-
-template <int V>
-using Int = std::integral_constant<int, V>;
-
 // Running-max slack (log2 units): the softmax reference max is only raised, and O rescaled,
 // when a tile's max exceeds it by more than this; probabilities then stay below 2^8.
 constexpr float RESCALE_SLACK = 8.f;

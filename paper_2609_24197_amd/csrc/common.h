@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace hspec {
 
 typedef __bf16 bf16;
@@ -67,6 +69,27 @@ __device__ __forceinline__ float wave_sum(float v) {
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
   return v;
 }
+
+// Wait until at most VM vector-memory operations (loads, LDS DMA) of this wave are pending.
+template <int VM>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(VM >= 0 && VM < 64, "vmcnt range");
+  // gfx9 s_waitcnt immediate: vmcnt[3:0] and [15:14], expcnt[6:4] = 7, lgkmcnt[11:8] = 15 (no wait)
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((VM & 15) | (7 << 4) | (15 << 8) | ((VM >> 4) << 14));
+  asm volatile("" ::: "memory");
+}
+
+// Workgroup barrier without the memory fence of __syncthreads (which would also wait for
+// every outstanding global load); callers order LDS traffic with explicit waits.
+__device__ __forceinline__ void wg_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <int V>
+using Int = std::integral_constant<int, V>;
 
 __device__ __forceinline__ void set_status(int* st, int bit) {
   if (st) atomicOr(st, bit);

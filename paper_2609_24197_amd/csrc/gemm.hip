@@ -22,6 +22,8 @@
 // HBM efficiency; the packed layout (launch_pack_w) stores every 16x32 operand fragment as
 // one contiguous 1 KB block, k-step-major, so that the whole grid sweeps W in address order
 // with non-temporal loads.
+#include <utility>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -453,6 +455,201 @@ hipError_t launch_skinny_a(const GemmArgs& g, const SkPlan& p, hipStream_t s) {
   return launch_skinny_m<4, ALO>(g, p, s);
 }
 
+// ------------------------------------------------------------- pipelined dense path
+//
+// Many rows (M >= 128): 128 x 128 output tiles, 4 waves of 64 x 64 (v_mfma_f32_32x32x16_bf16).
+// A and W k-tiles (64 wide) go straight from global memory into LDS (global_load_lds_dwordx4),
+// ST stages deep, so ST-1 tiles are in flight while one is multiplied; every LDS stage is its
+// own object so that the compiler's wait for outstanding LDS DMA names only the stage being
+// read.  Rows past M or N re-read the last valid row (their results are never stored); K must
+// be a multiple of 64.
+
+template <int TM, int TN, bool ALO, int ST>
+struct DmaCfg {
+  static constexpr int NT = 256;
+  static constexpr int BM = 2 * TM * 32, BN = 2 * TN * 32;
+  static constexpr int SA = BM * BK, SW = BN * BK;                  // elements per plane per stage
+  static constexpr int STAGE = SA * (ALO ? 2 : 1) + SW;
+  static constexpr int A_I = BM * CPR / NT, W_I = BN * CPR / NT;   // DMA instructions per wave
+  static constexpr int NI = A_I * (ALO ? 2 : 1) + W_I;
+  static constexpr int VM = (ST - 2) * NI;
+  static_assert(BM * CPR % NT == 0 && BN * CPR % NT == 0 && VM < 64 && ST >= 2 && ST <= 4, "dma gemm shape");
+};
+
+__device__ __forceinline__ void dma16(const bf16* src, bf16* lds) {
+  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                   (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+
+template <int VM>
+__device__ __forceinline__ void wait_vm_lgkm0() {
+  // vmcnt <= VM and every LDS read of this wave complete
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((VM & 15) | (7 << 4) | (0 << 8) | ((VM >> 4) << 14));
+  asm volatile("" ::: "memory");
+}
+
+// Epilogue of a 32x32 accumulator block: lane holds rows 8(i/4)+4(l/32)+i%4 of column l%32.
+__device__ __forceinline__ void store_block32(const GemmArgs& g, const f32x16& acc, int mb, int nb, int lane) {
+  const int n = nb + (lane & 31);
+  if (n >= g.N) return;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int m = mb + 8 * (i / 4) + 4 * (lane >> 5) + (i % 4);
+    if (m >= g.M) continue;
+    float v = acc[i];
+    if (g.R) {
+      v += g.r_bf16 ? bf2f(reinterpret_cast<const bf16*>(g.R)[(size_t)m * g.ldr + n])
+                    : reinterpret_cast<const float*>(g.R)[(size_t)m * g.ldr + n];
+    }
+    if (g.C) g.C[(size_t)m * g.ldc + n] = v;
+    if (g.C_hi) {
+      const bf16 h = f2bf(v);
+      g.C_hi[(size_t)m * g.ldch + n] = h;
+      if (g.C_lo) g.C_lo[(size_t)m * g.ldch + n] = f2bf(v - bf2f(h));
+    }
+  }
+}
+
+template <int TM, int TN, bool ALO, int ST>
+__global__ void __launch_bounds__(256) gemm_dma_kernel(GemmArgs g) {
+  using C = DmaCfg<TM, TN, ALO, ST>;
+  // one LDS object per (stage, operand): the A planes and the W tile of stage s
+  constexpr int PA = C::SA * (ALO ? 2 : 1);
+  __shared__ __align__(16) bf16 A0s[PA], W0s[C::SW];
+  __shared__ __align__(16) bf16 A1s[PA], W1s[C::SW];
+  __shared__ __align__(16) bf16 A2s[ST > 2 ? PA : 8], W2s[ST > 2 ? C::SW : 8];
+  __shared__ __align__(16) bf16 A3s[ST > 3 ? PA : 8], W3s[ST > 3 ? C::SW : 8];
+  auto sa_of = [&](auto I) -> bf16* {
+    if constexpr (decltype(I)::value == 0) return A0s;
+    else if constexpr (decltype(I)::value == 1) return A1s;
+    else if constexpr (decltype(I)::value == 2) return A2s;
+    else return A3s;
+  };
+  auto sw_of = [&](auto I) -> bf16* {
+    if constexpr (decltype(I)::value == 0) return W0s;
+    else if constexpr (decltype(I)::value == 1) return W1s;
+    else if constexpr (decltype(I)::value == 2) return W2s;
+    else return W3s;
+  };
+
+  const int mt_count = (g.M + C::BM - 1) / C::BM;
+  const int nt_count = (g.N + C::BN - 1) / C::BN;
+  int mt, nt;
+  tile_of(blockIdx.x, mt_count * nt_count, mt_count, mt, nt);
+  const int m0 = mt * C::BM, n0 = nt * C::BN;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / 2, wn = wave % 2;
+
+  const int rows_a = min(C::BM, g.M - m0), rows_w = min(C::BN, g.N - n0);
+  const bf16* A0 = g.A_hi + (size_t)m0 * g.lda;
+  const bf16* Al0 = (ALO ? g.A_lo : g.A_hi) + (size_t)m0 * g.lda;
+  const bf16* W0 = g.W_hi + (size_t)n0 * g.ldw;
+
+  // unit u (16 bytes) of a stage plane: row u / 8, stored chunk u % 8 = logical chunk ^ (row & 7)
+  auto issue = [&](int t, bf16* L, bf16* LW) {
+    const int k0 = t * BK;
+#pragma unroll
+    for (int i = 0; i < C::A_I; ++i) {
+      const int u0 = (i * 4 + wave) * 64, u = u0 + lane, row = u >> 3, k = k0 + 8 * ((u & 7) ^ (row & 7));
+      const size_t off = (size_t)min(row, rows_a - 1) * g.lda + k;
+      dma16(A0 + off, L + u0 * 8);
+      if constexpr (ALO) dma16(Al0 + off, L + C::SA + u0 * 8);
+    }
+#pragma unroll
+    for (int i = 0; i < C::W_I; ++i) {
+      const int u0 = (i * 4 + wave) * 64, u = u0 + lane, row = u >> 3, k = k0 + 8 * ((u & 7) ^ (row & 7));
+      dma16(W0 + (size_t)min(row, rows_w - 1) * g.ldw + k, LW + u0 * 8);
+    }
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int b = 0; b < TN; ++b)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[a][b][i] = 0.f;
+
+  auto compute = [&](const bf16* L, const bf16* LW) {
+    const bf16* sA = L;
+    const bf16* sAl = L + C::SA;
+    const bf16* sW = LW;
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      const int ch = 2 * ks + (lane >> 5);
+      bf16x8 fa[TM], fal[ALO ? TM : 1], fw[TN];
+#pragma unroll
+      for (int a = 0; a < TM; ++a) {
+        const int r = (wm * TM + a) * 32 + (lane & 31);
+        fa[a] = *reinterpret_cast<const bf16x8*>(sA + 8 * swz(r, ch));
+        if constexpr (ALO) fal[a] = *reinterpret_cast<const bf16x8*>(sAl + 8 * swz(r, ch));
+      }
+#pragma unroll
+      for (int b = 0; b < TN; ++b) {
+        const int r = (wn * TN + b) * 32 + (lane & 31);
+        fw[b] = *reinterpret_cast<const bf16x8*>(sW + 8 * swz(r, ch));
+      }
+#pragma unroll
+      for (int a = 0; a < TM; ++a)
+#pragma unroll
+        for (int b = 0; b < TN; ++b) {
+          acc[a][b] = mma32(fa[a], fw[b], acc[a][b]);
+          if constexpr (ALO) acc[a][b] = mma32(fal[a], fw[b], acc[a][b]);
+        }
+    }
+  };
+
+  const int nk = (g.K + BK - 1) / BK;
+  // prologue without branches (tiles past the end re-read the last one into unused stages),
+  // so that the compiler's record of which stage each pending DMA fills stays exact
+  [&]<int... I>(std::integer_sequence<int, I...>) {
+    (issue(min(I, nk - 1), sa_of(Int<I>{}), sw_of(Int<I>{})), ...);
+  }(std::make_integer_sequence<int, ST - 1>{});
+  // steady state: straight-line rounds of ST steps, each waiting for its own tile only
+  auto steady = [&](int t, auto S) {
+    wait_vm_lgkm0<C::VM>();
+    wg_barrier();   // tile t is in LDS for every wave; every wave is done reading tile t-1
+    constexpr int N = (decltype(S)::value + ST - 1) % ST;
+    issue(t + ST - 1, sa_of(Int<N>{}), sw_of(Int<N>{}));
+    compute(sa_of(S), sw_of(S));
+  };
+  auto step = [&](int t, auto S) {
+    if (t + ST - 2 < nk) wait_vm_lgkm0<C::VM>();
+    else wait_vm_lgkm0<0>();
+    wg_barrier();
+    constexpr int N = (decltype(S)::value + ST - 1) % ST;
+    if (t + ST - 1 < nk) issue(t + ST - 1, sa_of(Int<N>{}), sw_of(Int<N>{}));
+    compute(sa_of(S), sw_of(S));
+  };
+  int t0 = 0;
+  for (; t0 + 2 * ST - 2 < nk; t0 += ST) {
+    [&]<int... I>(std::integer_sequence<int, I...>) {
+      (steady(t0 + I, Int<I>{}), ...);
+    }(std::make_integer_sequence<int, ST>{});
+  }
+  for (; t0 < nk; t0 += ST) {
+    [&]<int... I>(std::integer_sequence<int, I...>) {
+      ((t0 + I < nk ? step(t0 + I, Int<I>{}) : void()), ...);
+    }(std::make_integer_sequence<int, ST>{});
+  }
+
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int b = 0; b < TN; ++b)
+      store_block32(g, acc[a][b], m0 + (wm * TM + a) * 32, n0 + (wn * TN + b) * 32, lane);
+}
+
+template <int TM, int TN, bool ALO, int ST>
+hipError_t launch_dma(const GemmArgs& g, hipStream_t s) {
+  using C = DmaCfg<TM, TN, ALO, ST>;
+  const int tiles = ((g.M + C::BM - 1) / C::BM) * ((g.N + C::BN - 1) / C::BN);
+  hipLaunchKernelGGL((gemm_dma_kernel<TM, TN, ALO, ST>), dim3(tiles), dim3(C::NT), 0, s, g);
+  return hipGetLastError();
+}
+
 template <int WM, int WN, int TM, int TN, bool ALO, bool WLO>
 hipError_t launch_one(const GemmArgs& g, hipStream_t s) {
   using C = GemmCfg<WM, WN, TM, TN, ALO, WLO>;
@@ -517,6 +714,8 @@ hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
     return g.A_lo ? launch_skinny_a<true>(g, p, s) : launch_skinny_a<false>(g, p, s);
   }
   if (g.M <= 64) return launch_cfg<1, 4, 2, 2>(g, s);      // 64 x 256: weight streaming
+  if (!g.W_lo && g.K % BK == 0)
+    return g.A_lo ? launch_dma<2, 2, true, 3>(g, s) : launch_dma<2, 2, false, 4>(g, s);
   if (g.M <= 128) return launch_cfg<2, 2, 2, 4>(g, s);     // 128 x 256
   return launch_cfg<2, 2, 2, 2>(g, s);                     // 128 x 128: dense
 }
