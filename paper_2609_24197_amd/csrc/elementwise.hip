@@ -31,6 +31,33 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return t;
 }
 
+// 8 consecutive elements as fp32 (one 16-byte bf16 load or two 16-byte fp32 loads).
+__device__ __forceinline__ void load8(const bf16* p, float (&v)[8]) {
+  const bf16x8 x = ld8(p);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = bf2f(x[e]);
+}
+__device__ __forceinline__ void load8(const float* p, float (&v)[8]) {
+  const f32x4 a = *reinterpret_cast<const f32x4*>(p), b = *reinterpret_cast<const f32x4*>(p + 4);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    v[e] = a[e];
+    v[4 + e] = b[e];
+  }
+}
+__device__ __forceinline__ void put8(bf16* hi, bf16* lo, size_t i, const float (&v)[8]) {
+  bf16x8 h, l;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    h[e] = f2bf(v[e]);
+    l[e] = f2bf(v[e] - bf2f(h[e]));
+  }
+  *reinterpret_cast<bf16x8*>(hi + i) = h;
+  if (lo) *reinterpret_cast<bf16x8*>(lo + i) = l;
+}
+
+// One workgroup per row, 8 elements per thread and step (n % 8 == 0); the second pass re-reads
+// the row from cache.
 template <typename T>
 __global__ void __launch_bounds__(256) rmsnorm_kernel(const T* x, const float* w, int n, float eps,
                                                       bf16* hi, bf16* lo) {
@@ -38,13 +65,22 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const T* x, const float* w
   const size_t row = blockIdx.x;
   const T* xr = x + row * n;
   float ss = 0.f;
-  for (int i = threadIdx.x; i < n; i += blockDim.x) {
-    const float v = to_f32(xr[i]);
-    ss += v * v;
+  for (int i = threadIdx.x * 8; i < n; i += blockDim.x * 8) {
+    float v[8];
+    load8(xr + i, v);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ss += v[e] * v[e];
   }
   ss = block_sum(ss, red);
   const float r = rsqrtf(ss / n + eps);
-  for (int i = threadIdx.x; i < n; i += blockDim.x) put_planes(hi, lo, row * n + i, to_f32(xr[i]) * r * w[i]);
+  for (int i = threadIdx.x * 8; i < n; i += blockDim.x * 8) {
+    float v[8], g[8];
+    load8(xr + i, v);
+    load8(w + i, g);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = v[e] * r * g[e];
+    put8(hi, lo, row * n + i, v);
+  }
 }
 
 template <typename T>
@@ -73,7 +109,70 @@ __global__ void __launch_bounds__(256) conv_split_kernel(ConvArgs a) {
   }
 }
 
-// One workgroup per (row, group).
+// Vectorised causal conv: a thread owns 4 consecutive channels of one request and walks its
+// T tokens in order with the last 8 inputs in registers, so zx is read once.  Needs the xBC and
+// dt parts of a zx row 16-byte aligned (checked by the launcher).
+template <typename T>
+__global__ void __launch_bounds__(256) conv_split4_kernel(ConvArgs a) {
+  const int di = a.H * a.P, gn = a.G * a.N, cdim = di + 2 * gn;
+  const int dproj = 2 * di + 2 * gn + a.H;
+  const int b = blockIdx.y;
+  const int c = (blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (c >= cdim + a.H) return;
+  const float* zrow = a.zxbcdt + (size_t)b * a.T * dproj;
+  if (c >= cdim) {                                   // dt = softplus(dt_raw + dt_bias), 4 heads
+    const int hh = c - cdim;
+    for (int t = 0; t < a.T; ++t) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(zrow + (size_t)t * dproj + 2 * di + 2 * gn + hh);
+      f32x4 o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = softplus(v[e] + a.dt_bias[hh + e]);
+      *reinterpret_cast<f32x4*>(a.dt + ((size_t)b * a.T + t) * a.H + hh) = o;
+    }
+    return;
+  }
+  const T* cw = reinterpret_cast<const T*>(a.conv_w);
+  const T* cb = reinterpret_cast<const T*>(a.conv_b);
+  // taps right-aligned in an 8-wide window: wp[j] multiplies the input 7 - j tokens back
+  float wp[8][4], bias[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    bias[e] = to_f32(cb[c + e]);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) wp[j][e] = j >= 8 - a.K ? to_f32(cw[(size_t)(c + e) * a.K + j - (8 - a.K)]) : 0.f;
+  }
+  f32x4 hist[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) hist[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  bf16* ohi;
+  bf16* olo;
+  int ld, col;
+  if (c < di) { ohi = a.x_hi; olo = a.x_lo; ld = di; col = c; }
+  else if (c < di + gn) { ohi = a.B_hi; olo = a.B_lo; ld = gn; col = c - di; }
+  else { ohi = a.C_hi; olo = a.C_lo; ld = gn; col = c - di - gn; }
+  for (int t = 0; t < a.T; ++t) {
+#pragma unroll
+    for (int j = 0; j < 7; ++j) hist[j] = hist[j + 1];
+    hist[7] = *reinterpret_cast<const f32x4*>(zrow + (size_t)t * dproj + di + c);
+    bf16x4 h, l;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float v = bias[e];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v += wp[j][e] * hist[j][e];
+      v = silu(v);
+      h[e] = f2bf(v);
+      l[e] = f2bf(v - bf2f(h[e]));
+    }
+    const size_t o = ((size_t)b * a.T + t) * ld + col;
+    *reinterpret_cast<bf16x4*>(ohi + o) = h;
+    if (olo) *reinterpret_cast<bf16x4*>(olo + o) = l;
+  }
+}
+
+// One workgroup per (row, group); 8 elements per thread and step.  VEC: y and z rows can be
+// read as 16-byte vectors.
+template <bool VEC>
 __global__ void __launch_bounds__(256) gated_rmsnorm_kernel(const float* y, const float* z, int z_ld,
                                                             const float* w, int n, int G, float eps,
                                                             bf16* hi, bf16* lo) {
@@ -82,58 +181,88 @@ __global__ void __launch_bounds__(256) gated_rmsnorm_kernel(const float* y, cons
   const int gi = blockIdx.x % G, gs = n / G;
   const float* yr = y + row * n + (size_t)gi * gs;
   const float* zr = z + row * z_ld + (size_t)gi * gs;
+  auto gated8 = [&](int i, float (&v)[8]) {
+    float zz[8];
+    if constexpr (VEC) {
+      load8(yr + i, v);
+      load8(zr + i, zz);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        v[e] = yr[i + e];
+        zz[e] = zr[i + e];
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] *= silu(zz[e]);
+  };
   float ss = 0.f;
-  for (int i = threadIdx.x; i < gs; i += blockDim.x) {
-    const float v = yr[i] * silu(zr[i]);
-    ss += v * v;
+  for (int i = threadIdx.x * 8; i < gs; i += blockDim.x * 8) {
+    float v[8];
+    gated8(i, v);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ss += v[e] * v[e];
   }
   ss = block_sum(ss, red);
   const float r = rsqrtf(ss / gs + eps);
-  for (int i = threadIdx.x; i < gs; i += blockDim.x)
-    put_planes(hi, lo, row * n + (size_t)gi * gs + i, yr[i] * silu(zr[i]) * r * w[gi * gs + i]);
+  for (int i = threadIdx.x * 8; i < gs; i += blockDim.x * 8) {
+    float v[8], g[8];
+    gated8(i, v);
+    load8(w + (size_t)gi * gs + i, g);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = v[e] * r * g[e];
+    put8(hi, lo, row * n + (size_t)gi * gs + i, v);
+  }
 }
 
-// One wave per (token, head) of q, k and v.  Lane i < D/2 owns the rotate-half pair (i, i + D/2).
-__global__ void __launch_bounds__(64) qk_norm_rope_kernel(const float* qkv, const float* qw, const float* kw,
-                                                          const int32_t* ctx_lens, int T, int Hq, int Hkv,
-                                                          int D, float eps, double theta, bf16* q_hi,
-                                                          bf16* q_lo, bf16* k_hi, bf16* k_lo, bf16* v_hi,
-                                                          bf16* v_lo) {
+// One workgroup (4 waves) per token.  A head's D/2 rotate-half pairs (i, i + D/2) sit on D/2
+// consecutive lanes, so a wave holds 64 / (D/2) heads at a time; the rotation angle of pair i
+// is the same for every head of the token and is computed once per thread (in fp64, reduced
+// modulo 2 pi, then fp32 sin/cos).
+__global__ void __launch_bounds__(256) qk_norm_rope_kernel(const float* qkv, const float* qw, const float* kw,
+                                                           const int32_t* ctx_lens, int T, int Hq, int Hkv,
+                                                           int D, float eps, double theta, bf16* q_hi,
+                                                           bf16* q_lo, bf16* k_hi, bf16* k_lo, bf16* v_hi,
+                                                           bf16* v_lo) {
   const int nh = Hq + 2 * Hkv;
-  const int tok = blockIdx.x / nh, head = blockIdx.x % nh;
+  const int tok = blockIdx.x;
   const int b = tok / T, j = tok % T;
-  const int lane = threadIdx.x, half = D / 2;
-  const float* src = qkv + (size_t)tok * nh * D + (size_t)head * D;
-  const bool act = lane < half;
-  const float x1 = act ? src[lane] : 0.f, x2 = act ? src[lane + half] : 0.f;
-  if (head >= Hq + Hkv) {                     // v: copy
-    if (act) {
-      const size_t o = ((size_t)tok * Hkv + (head - Hq - Hkv)) * D;
-      put_planes(v_hi, v_lo, o + lane, x1);
-      put_planes(v_hi, v_lo, o + lane + half, x2);
-    }
-    return;
-  }
-  const bool isq = head < Hq;
-  const float* g = isq ? qw : kw;
-  const float ss = wave_sum(x1 * x1 + x2 * x2);
-  const float r = rsqrtf(ss / D + eps);
-  const float a1 = act ? x1 * r * g[lane] : 0.f, a2 = act ? x2 * r * g[lane + half] : 0.f;
-  // angle in fp64: pos * theta^(-2i/D), reduced modulo 2 pi before the fp32 sin/cos
+  const int half = D / 2, hpw = 64 / half;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i = lane % half, hsub = lane / half;
   const double pos = (double)ctx_lens[b] + j;
-  const double inv = pow(theta, -2.0 * (double)lane / (double)D);
-  double phi = pos * inv;
+  double phi = pos * pow(theta, -2.0 * (double)i / (double)D);
   const double two_pi = 6.283185307179586476925286766559;
   phi -= two_pi * rint(phi / two_pi);
   float sn, cs;
   sincosf((float)phi, &sn, &cs);
-  if (!act) return;
-  const float o1 = a1 * cs - a2 * sn, o2 = a2 * cs + a1 * sn;
-  bf16* hi = isq ? q_hi : k_hi;
-  bf16* lo = isq ? q_lo : k_lo;
-  const size_t o = isq ? ((size_t)tok * Hq + head) * D : ((size_t)tok * Hkv + (head - Hq)) * D;
-  put_planes(hi, lo, o + lane, o1);
-  put_planes(hi, lo, o + lane + half, o2);
+  const float* src_tok = qkv + (size_t)tok * nh * D;
+  for (int h0 = wave * hpw; h0 < nh; h0 += 4 * hpw) {
+    const int head = h0 + hsub;
+    const bool act = head < nh;
+    const float* src = src_tok + (size_t)(act ? head : 0) * D;
+    const float x1 = act ? src[i] : 0.f, x2 = act ? src[i + half] : 0.f;
+    // sum of squares over the head's D/2 lanes (every lane takes part in the exchange)
+    float ss = x1 * x1 + x2 * x2;
+    for (int off = half / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+    if (!act) continue;
+    if (head >= Hq + Hkv) {                    // v heads: copy
+      const size_t o = ((size_t)tok * Hkv + (head - Hq - Hkv)) * D;
+      put_planes(v_hi, v_lo, o + i, x1);
+      put_planes(v_hi, v_lo, o + i + half, x2);
+      continue;
+    }
+    const bool isq = head < Hq;
+    const float* g = isq ? qw : kw;
+    const float r = rsqrtf(ss / D + eps);
+    const float a1 = x1 * r * g[i], a2 = x2 * r * g[i + half];
+    const float o1 = a1 * cs - a2 * sn, o2 = a2 * cs + a1 * sn;
+    bf16* hi = isq ? q_hi : k_hi;
+    bf16* lo = isq ? q_lo : k_lo;
+    const size_t o = isq ? ((size_t)tok * Hq + head) * D : ((size_t)tok * Hkv + (head - Hq)) * D;
+    put_planes(hi, lo, o + i, o1);
+    put_planes(hi, lo, o + i + half, o2);
+  }
 }
 
 __global__ void split_kernel(const float* x, size_t n, bf16* hi, bf16* lo) {
@@ -158,7 +287,15 @@ hipError_t launch_rmsnorm_planes(const void* x, int x_bf16, const float* w, int 
 }
 
 hipError_t launch_conv_split(const ConvArgs& a, hipStream_t s) {
-  const int total = a.H * a.P + 2 * a.G * a.N + a.H;
+  const int di = a.H * a.P, gn = a.G * a.N;
+  const int dproj = 2 * di + 2 * gn + a.H;
+  const int total = di + 2 * gn + a.H;
+  if (dproj % 4 == 0 && di % 4 == 0 && gn % 4 == 0 && a.H % 4 == 0 && a.K <= 8) {
+    dim3 grid((total / 4 + 255) / 256, a.B);
+    if (a.w_bf16) hipLaunchKernelGGL(conv_split4_kernel<bf16>, grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(conv_split4_kernel<float>, grid, dim3(256), 0, s, a);
+    return hipGetLastError();
+  }
   dim3 grid((total + 255) / 256, a.B * a.T);
   if (a.w_bf16) hipLaunchKernelGGL(conv_split_kernel<bf16>, grid, dim3(256), 0, s, a);
   else hipLaunchKernelGGL(conv_split_kernel<float>, grid, dim3(256), 0, s, a);
@@ -168,7 +305,10 @@ hipError_t launch_conv_split(const ConvArgs& a, hipStream_t s) {
 hipError_t launch_gated_rmsnorm(const float* y, const float* z, int z_ld, const float* w, int rows, int n, int G,
                                 float eps, bf16* out_hi, bf16* out_lo, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(gated_rmsnorm_kernel, dim3(rows * G), dim3(256), 0, s, y, z, z_ld, w, n, G, eps, out_hi, out_lo);
+  if (z_ld % 4 == 0 && (n / G) % 4 == 0)
+    hipLaunchKernelGGL(gated_rmsnorm_kernel<true>, dim3(rows * G), dim3(256), 0, s, y, z, z_ld, w, n, G, eps, out_hi, out_lo);
+  else
+    hipLaunchKernelGGL(gated_rmsnorm_kernel<false>, dim3(rows * G), dim3(256), 0, s, y, z, z_ld, w, n, G, eps, out_hi, out_lo);
   return hipGetLastError();
 }
 
@@ -176,7 +316,7 @@ hipError_t launch_qk_norm_rope(const float* qkv, const float* qw, const float* k
                                int T, int Hq, int Hkv, int D, float eps, double theta, bf16* q_hi, bf16* q_lo,
                                bf16* k_hi, bf16* k_lo, bf16* v_hi, bf16* v_lo, hipStream_t s) {
   if (B * T <= 0) return hipSuccess;
-  hipLaunchKernelGGL(qk_norm_rope_kernel, dim3(B * T * (Hq + 2 * Hkv)), dim3(64), 0, s, qkv, qw, kw, ctx_lens, T,
+  hipLaunchKernelGGL(qk_norm_rope_kernel, dim3(B * T), dim3(256), 0, s, qkv, qw, kw, ctx_lens, T,
                      Hq, Hkv, D, eps, theta, q_hi, q_lo, k_hi, k_lo, v_hi, v_lo);
   return hipGetLastError();
 }

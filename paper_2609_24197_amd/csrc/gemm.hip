@@ -184,10 +184,23 @@ gemm_kernel(GemmArgs g) {
 
 // ---------------------------------------------------------------- weight-streaming path
 
-constexpr int SK_KC = 128;                  // k per LDS chunk of A
+#ifndef HSPEC_SK_KC
+#define HSPEC_SK_KC 128
+#endif
+#ifndef HSPEC_SK_P
+#define HSPEC_SK_P 4
+#endif
+#ifndef HSPEC_SK_NW
+#define HSPEC_SK_NW 8
+#endif
+constexpr int SK_KC = HSPEC_SK_KC;          // k per LDS chunk of A
 constexpr int SK_STEP = 32;                 // k per MFMA (16x16x32)
-constexpr int SK_SPC = SK_KC / SK_STEP;     // k-steps per chunk; also the W prefetch depth
+constexpr int SK_SPC = SK_KC / SK_STEP;     // k-steps per chunk
+constexpr int SK_CPR = SK_KC / 8;           // 16-byte pieces per row of an A chunk
+constexpr int SK_P = HSPEC_SK_P;            // W prefetch depth (k-steps in flight per wave)
+static_assert(SK_SPC % SK_P == 0, "prefetch depth must divide the chunk");
 constexpr int SK_OOB = 0x7fffff00;          // buffer offset beyond every range: reads zeros
+typedef uint32_t v2u32 __attribute__((ext_vector_type(2)));
 
 template <int MT, int NTW, int NW, bool ALO>
 struct SkCfg {
@@ -198,6 +211,8 @@ struct SkCfg {
   static constexpr int STAGE = PLANE * (ALO ? 2 : 1);
   static constexpr int CHUNKS = STAGE / 8;            // 16-byte pieces per stage
   static constexpr int A_PT = (CHUNKS + NT - 1) / NT;
+  static constexpr int BNW = NTW * 16;                // columns per wave
+  static constexpr int PITCH = BNW + 4;               // fp32 row pitch of the epilogue staging
 };
 
 __device__ __forceinline__ void lds_barrier() {
@@ -208,76 +223,99 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("" ::: "memory");
 }
 
-// C[M, N] (or split-K partials) for M <= 16 * MT.  Workgroup = (column tile, k-part); wave w
-// owns NTW 16-column tiles and all rows.  A chunk (k0, k0 + 128) of every A plane sits in LDS
-// with the 16-byte piece c of row m at c ^ (m & 15), so the fragment reads of 16 rows hit
-// distinct banks.
-template <int MT, int NTW, int NW, bool ALO, bool PK>
+// Buffer resource over [base, base + bytes); a range of 0 bytes makes every access a no-op
+// (loads return zeros, stores are dropped).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf(const void* base, long long bytes) {
+  const int n = bytes <= 0 ? 0 : (int)(bytes > 0x7fffffffLL ? 0x7fffffff : bytes);
+  return __builtin_amdgcn_make_buffer_rsrc((void*)base, 0, __builtin_amdgcn_readfirstlane(n), 0x00020000);
+}
+
+// Work items are (column tile, k-part) pairs; a workgroup takes items blockIdx.x, +gridDim.x,
+// ... so that with a grid of one workgroup per CU the loads of its next tile are already in
+// flight while the epilogue of the current one stores.  Wave w owns NTW 16-column tiles and
+// all rows of an item.  The A chunk (k0, k0 + SK_KC) of every A plane sits in LDS with the
+// 16-byte piece c of row m at c ^ (m & 15), so the fragment reads of 16 rows hit distinct
+// banks.  Every global access is an unconditional buffer access whose range check does the
+// bounds work, which keeps the compiler's counts of outstanding loads exact across tiles.
+template <int MT, int NTW, int NW, bool ALO, bool PK, bool RES>
 __global__ void __launch_bounds__(64 * NW)
-skinny_kernel(GemmArgs g, int kper) {
+skinny_kernel(GemmArgs g, int kper, int nitems) {
   using S = SkCfg<MT, NTW, NW, ALO>;
   __shared__ __align__(16) bf16 sA[2 * S::STAGE];
+  __shared__ __align__(16) float stg_all[NW * 16 * S::PITCH];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int ntiles = (g.N + S::BN - 1) / S::BN;
-  const int tile = blockIdx.x % ntiles, kp = blockIdx.x / ntiles;
-  const int kb = kp * kper, ke = min(g.K, kb + kper);
-  const int nsteps = (ke - kb) / SK_STEP;
-  const int nch = (ke - kb + SK_KC - 1) / SK_KC;
-  const int n_w = tile * S::BN + wave * NTW * 16;
+  const int ntile16 = g.N / 16;
+  const bool split = nitems > ntiles;
 
-  // W: lane l needs row n_w + 16 j + l % 16 at k offset 8 (l / 16) of each k-step.
-  // Row-major: one buffer resource over the wave's rows (rows past N read as zeros).
-  // Packed: per k-step, the wave's NTW tiles are one contiguous range of 1 KB fragments.
-  const int rows_w = max(0, min(NTW * 16, g.N - n_w));
-  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(g.W_hi + (size_t)min(n_w, g.N) * g.ldw), 0, __builtin_amdgcn_readfirstlane(rows_w * g.ldw * 2),
-      0x00020000);
-  int voff[NTW];
+  struct Item {
+    int tile, kp, kb, ke, nsteps, nch, n_w;
+  };
+  auto item_of = [&](int it) {
+    Item r;
+    r.tile = it % ntiles;
+    r.kp = it / ntiles;
+    r.kb = r.kp * kper;
+    r.ke = min(g.K, r.kb + kper);
+    r.nsteps = (r.ke - r.kb) / SK_STEP;
+    r.nch = (r.ke - r.kb + SK_KC - 1) / SK_KC;
+    r.n_w = r.tile * S::BN + wave * S::BNW;
+    return r;
+  };
+
+  // ---- W stream: lane l needs row n_w + 16 j + l % 16 at k offset 8 (l / 16) of each k-step
+  int vrow[NTW];
 #pragma unroll
   for (int j = 0; j < NTW; ++j)
-    voff[j] = PK ? j * 1024 + lane * 16 : ((16 * j + (lane & 15)) * g.ldw + kb + 8 * (lane >> 4)) * 2;
-  const int ntile = g.N / 16, t0 = min(n_w / 16, ntile);
-  const int tiles_w = min(NTW, ntile - t0);
-
-  bf16x8 wr[SK_SPC][NTW];
-  auto load_w = [&](int st, bf16x8 (&slot)[NTW]) {
+    vrow[j] = PK ? j * 1024 + lane * 16 : ((16 * j + (lane & 15)) * g.ldw + 8 * (lane >> 4)) * 2;
+  int p_it = blockIdx.x, p_st = 0;          // next k-step to prefetch
+  Item p_item = item_of(p_it);
+  bf16x8 wr[SK_P][NTW];
+  auto load_w_next = [&](bf16x8 (&slot)[NTW]) {
+    const bool live = p_it < nitems && p_st < p_item.nsteps;
     if constexpr (PK) {
-      const bool live = st < nsteps;
-      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-          (void*)(g.W_hi + ((size_t)(kb / SK_STEP + (live ? st : 0)) * ntile + t0) * 512), 0,
-          __builtin_amdgcn_readfirstlane(live ? tiles_w * 1024 : 0), 0x00020000);
+      const int t0 = min(p_item.n_w / 16, ntile16);
+      const __amdgpu_buffer_rsrc_t rs =
+          buf(g.W_hi + ((size_t)(p_item.kb / SK_STEP + (live ? p_st : 0)) * ntile16 + t0) * 512,
+              live ? (long long)min(NTW, ntile16 - t0) * 1024 : 0);
 #pragma unroll
       for (int j = 0; j < NTW; ++j)   // aux 2: non-temporal, W is read once
-        slot[j] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rs, voff[j], 0, 2));
+        slot[j] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rs, vrow[j], 0, 2));
     } else {
+      const int rows = live ? max(0, min(S::BNW, g.N - p_item.n_w)) : 0;
+      const __amdgpu_buffer_rsrc_t rs = buf(g.W_hi + (size_t)min(p_item.n_w, g.N) * g.ldw, (long long)rows * g.ldw * 2);
+      const int koff = (p_item.kb + p_st * SK_STEP) * 2;
 #pragma unroll
-      for (int j = 0; j < NTW; ++j) {
-        const int off = st < nsteps ? voff[j] + st * SK_STEP * 2 : SK_OOB;
-        slot[j] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, 0));
-      }
+      for (int j = 0; j < NTW; ++j)
+        slot[j] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rs, vrow[j] + koff, 0, 0));
+    }
+    if (++p_st == p_item.nch * SK_SPC) {
+      p_st = 0;
+      p_it += gridDim.x;
+      p_item = item_of(p_it);
     }
   };
 
-  // A: buffer resources over the M rows of each plane (rows past M and pieces past ke read
-  // as zeros), so every load below is unconditional and the wait counts stay exact.
-  const __amdgpu_buffer_rsrc_t ra_hi = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)g.A_hi, 0, __builtin_amdgcn_readfirstlane(g.M * g.lda * 2), 0x00020000);
-  const __amdgpu_buffer_rsrc_t ra_lo = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(ALO ? g.A_lo : g.A_hi), 0, __builtin_amdgcn_readfirstlane(g.M * g.lda * 2), 0x00020000);
+  // ---- A stream: chunks of the items in order, staged through registers into LDS
+  const __amdgpu_buffer_rsrc_t ra_hi = buf(g.A_hi, (long long)g.M * g.lda * 2);
+  const __amdgpu_buffer_rsrc_t ra_lo = buf(ALO ? g.A_lo : g.A_hi, (long long)g.M * g.lda * 2);
+  int a_it = blockIdx.x, a_c = 0;           // next A chunk to load
+  Item a_item = item_of(a_it);
   bf16x8 ar[S::A_PT];
-  auto load_a = [&](int c) {
-    const int k0 = kb + c * SK_KC;
+  auto load_a_next = [&]() {
+    const bool live = a_it < nitems;
+    const int k0 = a_item.kb + a_c * SK_KC;
 #pragma unroll
     for (int i = 0; i < S::A_PT; ++i) {
       const int q = tid + i * S::NT;
       if (S::CHUNKS % S::NT != 0 && q >= S::CHUNKS) continue;
-      const int plane = q / (S::ROWS * 16), rem = q % (S::ROWS * 16), m = rem / 16, cc = rem % 16;
+      const int plane = q / (S::ROWS * SK_CPR), rem = q % (S::ROWS * SK_CPR), m = rem / SK_CPR, cc = rem % SK_CPR;
       const int k = k0 + 8 * cc;
-      const int off = (c < nch && k < ke) ? (m * g.lda + k) * 2 : SK_OOB;
-      if constexpr ((S::ROWS * 16) % S::NT == 0) {
+      const int off = (live && k < a_item.ke) ? (m * g.lda + k) * 2 : SK_OOB;
+      if constexpr ((S::ROWS * SK_CPR) % S::NT == 0) {
         // the plane of piece i is the same in every lane
-        const bool lo = (i * S::NT) / (S::ROWS * 16) != 0;
+        const bool lo = (i * S::NT) / (S::ROWS * SK_CPR) != 0;
         ar[i] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(lo ? ra_lo : ra_hi, off, 0, 0));
       } else {
         // lanes of both planes: each lane reads its own piece; the other load reads zeros
@@ -286,6 +324,11 @@ skinny_kernel(GemmArgs g, int kper) {
         ar[i] = __builtin_bit_cast(bf16x8, h | l);
       }
     }
+    if (++a_c == a_item.nch) {
+      a_c = 0;
+      a_it += gridDim.x;
+      a_item = item_of(a_it);
+    }
   };
   auto store_a = [&](int stage) {
     bf16* dst = sA + stage * S::STAGE;
@@ -293,78 +336,116 @@ skinny_kernel(GemmArgs g, int kper) {
     for (int i = 0; i < S::A_PT; ++i) {
       const int q = tid + i * S::NT;
       if (S::CHUNKS % S::NT != 0 && q >= S::CHUNKS) continue;
-      const int plane = q / (S::ROWS * 16), rem = q % (S::ROWS * 16), m = rem / 16, cc = rem % 16;
+      const int plane = q / (S::ROWS * SK_CPR), rem = q % (S::ROWS * SK_CPR), m = rem / SK_CPR, cc = rem % SK_CPR;
       *reinterpret_cast<bf16x8*>(dst + plane * S::PLANE + m * SK_KC + 8 * (cc ^ (m & 15))) = ar[i];
     }
   };
 
-  f32x4 acc[MT][NTW];
-#pragma unroll
-  for (int t = 0; t < MT; ++t)
-#pragma unroll
-    for (int j = 0; j < NTW; ++j) acc[t][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // ---- epilogue geometry: after staging, lane owns 4 consecutive columns of one row
+  float* stg = stg_all + wave * 16 * S::PITCH;
+  constexpr int LPR = S::BNW / 4;                    // lanes per row
+  constexpr int RPP = 64 / LPR < 16 ? 64 / LPR : 16; // rows per pass
+  const int lr = lane / LPR, c4 = (lane % LPR) * 4;
 
-  load_a(0);
+  if (blockIdx.x >= nitems) return;
 #pragma unroll
-  for (int p = 0; p < SK_SPC; ++p) load_w(p, wr[p]);
+  for (int p = 0; p < SK_P; ++p) load_w_next(wr[p]);
+  load_a_next();
   store_a(0);
   lds_barrier();
-  for (int c = 0; c < nch; ++c) {
-    const bf16* sa = sA + (c & 1) * S::STAGE;
-    load_a(c + 1);
-#pragma unroll
-    for (int ks = 0; ks < SK_SPC; ++ks) {
-      bf16x8 fa[MT], fl[ALO ? MT : 1];
-#pragma unroll
-      for (int t = 0; t < MT; ++t) {
-        const int m = 16 * t + (lane & 15), cc = 4 * ks + (lane >> 4);
-        const bf16* p = sa + m * SK_KC + 8 * (cc ^ (m & 15));
-        fa[t] = *reinterpret_cast<const bf16x8*>(p);
-        if constexpr (ALO) fl[t] = *reinterpret_cast<const bf16x8*>(p + S::PLANE);
-      }
-#pragma unroll
-      for (int t = 0; t < MT; ++t)
-#pragma unroll
-        for (int j = 0; j < NTW; ++j) {
-          acc[t][j] = mma16(fa[t], wr[ks][j], acc[t][j]);
-          if constexpr (ALO) acc[t][j] = mma16(fl[t], wr[ks][j], acc[t][j]);
-        }
-      load_w((c + 1) * SK_SPC + ks, wr[ks]);
-      __builtin_amdgcn_sched_barrier(0);   // keep each step's refill behind its own MFMAs
-    }
-    store_a((c + 1) & 1);
-    lds_barrier();
-  }
+  int gc = 0;   // chunks consumed by this workgroup: A stage gc & 1
 
-  // lane holds rows 16 t + 4 (l / 16) + i of column 16 j + l % 16
-  const bool split = gridDim.x > ntiles;
+  for (int it = blockIdx.x; it < nitems; it += gridDim.x) {
+    const Item cur = item_of(it);
+    f32x4 acc[MT][NTW];
 #pragma unroll
-  for (int t = 0; t < MT; ++t)
+    for (int t = 0; t < MT; ++t)
 #pragma unroll
-    for (int j = 0; j < NTW; ++j) {
-      const int n = n_w + 16 * j + (lane & 15);
-      if (n >= g.N) continue;
+      for (int j = 0; j < NTW; ++j) acc[t][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    for (int c = 0; c < cur.nch; ++c, ++gc) {
+      const bf16* sa = sA + (gc & 1) * S::STAGE;
+      load_a_next();
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int m = 16 * t + 4 * (lane >> 4) + i;
-        if (m >= g.M) continue;
-        float v = acc[t][j][i];
-        if (split) {
-          g.part[((size_t)kp * g.M + m) * g.N + n] = v;
-          continue;
+      for (int ks = 0; ks < SK_SPC; ++ks) {
+        bf16x8 fa[MT], fl[ALO ? MT : 1];
+#pragma unroll
+        for (int t = 0; t < MT; ++t) {
+          const int m = 16 * t + (lane & 15), cc = 4 * ks + (lane >> 4);
+          const bf16* p = sa + m * SK_KC + 8 * (cc ^ (m & 15));
+          fa[t] = *reinterpret_cast<const bf16x8*>(p);
+          if constexpr (ALO) fl[t] = *reinterpret_cast<const bf16x8*>(p + S::PLANE);
         }
-        if (g.R) {
-          v += g.r_bf16 ? bf2f(reinterpret_cast<const bf16*>(g.R)[(size_t)m * g.ldr + n])
-                        : reinterpret_cast<const float*>(g.R)[(size_t)m * g.ldr + n];
+#pragma unroll
+        for (int t = 0; t < MT; ++t)
+#pragma unroll
+          for (int j = 0; j < NTW; ++j) {
+            acc[t][j] = mma16(fa[t], wr[ks % SK_P][j], acc[t][j]);
+            if constexpr (ALO) acc[t][j] = mma16(fl[t], wr[ks % SK_P][j], acc[t][j]);
+          }
+        load_w_next(wr[ks % SK_P]);
+        __builtin_amdgcn_sched_barrier(0);   // keep each step's refill behind its own MFMAs
+      }
+      store_a((gc + 1) & 1);
+      lds_barrier();
+    }
+
+    // Epilogue (N % 4 == 0): each 16-row slab of the accumulators goes through this wave's LDS
+    // staging so that lanes store whole 16-byte pieces of rows.  Outputs outside [0, M) x [0, N)
+    // and absent outputs fall outside their buffer's range and are dropped.
+    const int n0 = cur.n_w;
+    const int cols = max(0, min(S::BNW, g.N - n0));
+    const long long rows_span = (long long)(g.M - 1);
+    const __amdgpu_buffer_rsrc_t r_part =
+        buf(split ? g.part + ((size_t)cur.kp * g.M) * g.N + min(n0, g.N) : nullptr,
+            split && cols ? (rows_span * g.N + cols) * 4 : 0);
+    const __amdgpu_buffer_rsrc_t r_c =
+        buf(g.C ? g.C + min(n0, g.N) : nullptr, !split && g.C && cols ? (rows_span * g.ldc + cols) * 4 : 0);
+    const __amdgpu_buffer_rsrc_t r_hi =
+        buf(g.C_hi ? g.C_hi + min(n0, g.N) : nullptr, !split && g.C_hi && cols ? (rows_span * g.ldch + cols) * 2 : 0);
+    const __amdgpu_buffer_rsrc_t r_lo =
+        buf(g.C_lo ? g.C_lo + min(n0, g.N) : nullptr, !split && g.C_lo && cols ? (rows_span * g.ldch + cols) * 2 : 0);
+    // residual R (RES: present and not split-K): one of the two loads reads, the other is empty
+    const bool rf = RES && !g.r_bf16, rb = RES && g.r_bf16;
+    [[maybe_unused]] const __amdgpu_buffer_rsrc_t r_rf =
+        buf(rf ? reinterpret_cast<const float*>(g.R) + min(n0, g.N) : nullptr, !split && rf && cols ? (rows_span * g.ldr + cols) * 4 : 0);
+    [[maybe_unused]] const __amdgpu_buffer_rsrc_t r_rb =
+        buf(rb ? reinterpret_cast<const bf16*>(g.R) + min(n0, g.N) : nullptr, !split && rb && cols ? (rows_span * g.ldr + cols) * 2 : 0);
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+#pragma unroll
+      for (int j = 0; j < NTW; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) stg[(4 * (lane >> 4) + i) * S::PITCH + 16 * j + (lane & 15)] = acc[t][j][i];
+#pragma unroll
+      for (int pass = 0; pass < 16 / RPP; ++pass) {
+        const int r = pass * RPP + lr;
+        const int m = 16 * t + r;
+        const bool ok = lane < LPR * RPP && m < g.M && c4 < cols;
+        f32x4 v = *reinterpret_cast<const f32x4*>(stg + r * S::PITCH + c4);
+        if constexpr (RES) {
+          const int o4 = ok ? (m * g.ldr + c4) * 4 : SK_OOB;
+          const int o2 = ok ? (m * g.ldr + c4) * 2 : SK_OOB;
+          const f32x4 addf = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r_rf, o4, 0, 0));
+          const bf16x4 addb = __builtin_bit_cast(bf16x4, __builtin_amdgcn_raw_buffer_load_b64(r_rb, o2, 0, 0));
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] += addf[e] + bf2f(addb[e]);
         }
-        if (g.C) g.C[(size_t)m * g.ldc + n] = v;
-        if (g.C_hi) {
-          const bf16 h = f2bf(v);
-          g.C_hi[(size_t)m * g.ldch + n] = h;
-          if (g.C_lo) g.C_lo[(size_t)m * g.ldch + n] = f2bf(v - bf2f(h));
+        bf16x4 h, l;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          h[e] = f2bf(v[e]);
+          l[e] = f2bf(v[e] - bf2f(h[e]));
         }
+        // aux 16 (sc1): measured to disturb the concurrent non-temporal W stream least
+        const u32x4 vb = __builtin_bit_cast(u32x4, v);
+        __builtin_amdgcn_raw_buffer_store_b128(vb, r_part, ok ? (m * g.N + c4) * 4 : SK_OOB, 0, 16);
+        __builtin_amdgcn_raw_buffer_store_b128(vb, r_c, ok ? (m * g.ldc + c4) * 4 : SK_OOB, 0, 16);
+        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2u32, h), r_hi, ok ? (m * g.ldch + c4) * 2 : SK_OOB, 0, 16);
+        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2u32, l), r_lo, ok ? (m * g.ldch + c4) * 2 : SK_OOB, 0, 16);
       }
     }
+  }
 }
 
 // Sum of the split-K partials in k-part order, then the usual epilogue.
@@ -399,7 +480,7 @@ int device_cus() {
   return cus[dev];
 }
 
-constexpr int SK_NW = 8;
+constexpr int SK_NW = HSPEC_SK_NW;
 
 // Launch shape of the weight-streaming path: wide N uses 4 column tiles per wave; narrow N
 // uses 1 and splits K until the grid covers the chip twice.
@@ -410,7 +491,7 @@ struct SkPlan {
 
 SkPlan skinny_plan(int M, int N, int K, bool w_lo, int cus) {
   SkPlan p;
-  if (M > 64 || w_lo || K % SK_STEP != 0) return p;
+  if (M > 64 || w_lo || K % SK_STEP != 0 || N % 4 != 0) return p;
   p.use = true;
   const int want = 2 * cus;
   int tiles = (N + SK_NW * 64 - 1) / (SK_NW * 64);
@@ -430,9 +511,13 @@ SkPlan skinny_plan(int M, int N, int K, bool w_lo, int cus) {
 template <int MT, int NTW, bool ALO, bool PK>
 hipError_t launch_skinny_t(const GemmArgs& g, const SkPlan& p, hipStream_t s) {
   using S = SkCfg<MT, NTW, SK_NW, ALO>;
-  auto kern = skinny_kernel<MT, NTW, SK_NW, ALO, PK>;
-  const int ntiles = (g.N + S::BN - 1) / S::BN;
-  hipLaunchKernelGGL(kern, dim3(ntiles * p.ksplit), dim3(S::NT), 0, s, g, p.kper);
+  // the residual is added by the reduction when K is split
+  auto kern = (g.R && p.ksplit == 1 && !PK) ? skinny_kernel<MT, NTW, SK_NW, ALO, PK, !PK>
+                                            : skinny_kernel<MT, NTW, SK_NW, ALO, PK, false>;
+  const int nitems = ((g.N + S::BN - 1) / S::BN) * p.ksplit;
+  // one workgroup per CU walks several items when there are more items than CUs
+  const int grid = p.ksplit == 1 && nitems > device_cus() ? device_cus() : nitems;
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(S::NT), 0, s, g, p.kper, nitems);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.ksplit == 1) return e;
   const size_t total = (size_t)g.M * g.N;
@@ -705,7 +790,8 @@ size_t gemm_scratch_elems(int M, int N, int K, bool a_lo, bool w_lo) {
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
   SkPlan p = skinny_plan(g.M, g.N, g.K, g.W_lo != nullptr, device_cus());
-  if (g.w_packed && (!p.use || g.N % 16 || g.W_lo)) return hipErrorInvalidValue;   // packed W needs this path
+  if ((g.C && g.ldc % 4) || (g.C_hi && g.ldch % 4) || (g.R && g.ldr % 4)) p.use = false;   // 16-byte stores
+  if (g.w_packed && (!p.use || g.N % 16 || g.W_lo || g.R)) return hipErrorInvalidValue;   // packed W: this path, no residual
   if (p.use) {
     if (p.ksplit > 1 && (!g.part || g.part_cap < (size_t)p.ksplit * g.M * g.N)) {
       p.ksplit = 1;
