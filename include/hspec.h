@@ -73,7 +73,7 @@ enum { HSPEC_DEV_BAD_PAGE = 1, HSPEC_DEV_BAD_CTX_LEN = 2 };
  *   chunk = SSD chunk length (1..16), conv_w = causal conv width (1..8), eps of every RMSNorm.
  *   d_inner = H*P, d_S = H*P*N.  d_h, r, d_model must be multiples of 8.
  *   flags: HSPEC_W_DS_PACKED when hspec_mamba_w.W_dS points at the packed layout written by
- *   hspec_pack_w_ds (bf16 storage, r a multiple of 32), else 0.
+ *   hspec_pack_w_ds (bf16 storage, r a multiple of 64), else 0.
  */
 typedef struct {
   int B, k, d_model, d_h, r, H, P, N, G, chunk, conv_w;
@@ -186,7 +186,7 @@ size_t hspec_draft_step_workspace(const hspec_mamba_cfg* mcfg, const hspec_attn_
  * starts at byte ((s * d_S/16) + t) * 1024; inside it, the 8 consecutive columns
  * 32s + 8c .. +7 of row 16t + i are the 16 bytes at (i + 16c) * 16.
  * W_dS [d_S, r] row-major bf16 in, W_packed (hspec_pack_w_ds_bytes bytes) out, both device
- * memory; d_S % 16 == 0 and r % 32 == 0, else HSPEC_ERR_UNSUPPORTED.  Asynchronous on stream.
+ * memory; d_S % 16 == 0 and r % 64 == 0, else HSPEC_ERR_UNSUPPORTED.  Asynchronous on stream.
  */
 size_t hspec_pack_w_ds_bytes(int d_S, int r);
 hspec_status hspec_pack_w_ds(int d_S, int r, const void* W_dS, void* W_packed, void* stream);

@@ -114,8 +114,8 @@ hspec_status check_mamba(const hspec_mamba_cfg* c, const hspec_mamba_w* w, bool 
     return fail(HSPEC_ERR_UNSUPPORTED, "N (d_state) must be 16, 32, 64 or 128, got %d", c->N);
   if (c->d_h % 8 || c->r % 8) return fail(HSPEC_ERR_UNSUPPORTED, "d_h and r must be multiples of 8");
   if (c->flags & ~(unsigned)HSPEC_W_DS_PACKED) return fail(HSPEC_ERR_UNSUPPORTED, "unknown mamba flags 0x%x", c->flags);
-  if ((c->flags & HSPEC_W_DS_PACKED) && (is_f32(c->dtype) || c->r % 32))
-    return fail(HSPEC_ERR_UNSUPPORTED, "a packed W_dS needs bf16 storage and r %% 32 == 0");
+  if ((c->flags & HSPEC_W_DS_PACKED) && (is_f32(c->dtype) || c->r % 64))
+    return fail(HSPEC_ERR_UNSUPPORTED, "a packed W_dS needs bf16 storage and r %% 64 == 0");
   if (!w->W_r || !w->W_dS) return fail(HSPEC_ERR_NULL, "W_r or W_dS is NULL");
   if (!full) return HSPEC_OK;
   if (c->k <= 0 || c->d_model <= 0 || c->G <= 0 || c->chunk <= 0 || c->conv_w <= 0)
@@ -714,14 +714,14 @@ HSPEC_API hspec_status hspec_linear(hspec_dtype dtype, int M, int N, int K, cons
 }
 
 HSPEC_API size_t hspec_pack_w_ds_bytes(int d_S, int r) {
-  if (d_S <= 0 || r <= 0 || d_S % 16 || r % 32) return 0;
+  if (d_S <= 0 || r <= 0 || d_S % 16 || r % 64) return 0;
   return (size_t)d_S * r * sizeof(bf16);
 }
 
 HSPEC_API hspec_status hspec_pack_w_ds(int d_S, int r, const void* W_dS, void* W_packed, void* stream) {
   g_err.clear();
   if (d_S <= 0 || r <= 0) return fail(HSPEC_ERR_SHAPE, "non-positive W_dS dimension");
-  if (d_S % 16 || r % 32) return fail(HSPEC_ERR_UNSUPPORTED, "packing needs d_S %% 16 == 0 and r %% 32 == 0");
+  if (d_S % 16 || r % 64) return fail(HSPEC_ERR_UNSUPPORTED, "packing needs d_S %% 16 == 0 and r %% 64 == 0");
   if (!W_dS || !W_packed) return fail(HSPEC_ERR_NULL, "W_dS or W_packed is NULL");
   HIP_TRY(hspec::launch_pack_w(static_cast<const bf16*>(W_dS), d_S, r, static_cast<bf16*>(W_packed),
                                (hipStream_t)stream));

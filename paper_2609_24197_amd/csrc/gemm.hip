@@ -630,7 +630,6 @@ __global__ void __launch_bounds__(256) gemm_dma_kernel(GemmArgs g) {
   const int rows_a = min(C::BM, g.M - m0), rows_w = min(C::BN, g.N - n0);
   const bf16* A0 = g.A_hi + (size_t)m0 * g.lda;
   const bf16* Al0 = (ALO ? g.A_lo : g.A_hi) + (size_t)m0 * g.lda;
-  const bf16* W0 = g.W_hi + (size_t)n0 * g.ldw;
 
   // unit u (16 bytes) of a stage plane: row u / 8, stored chunk u % 8 = logical chunk ^ (row & 7)
   auto issue = [&](int t, bf16* L, bf16* LW) {
@@ -645,7 +644,12 @@ __global__ void __launch_bounds__(256) gemm_dma_kernel(GemmArgs g) {
 #pragma unroll
     for (int i = 0; i < C::W_I; ++i) {
       const int u0 = (i * 4 + wave) * 64, u = u0 + lane, row = u >> 3, k = k0 + 8 * ((u & 7) ^ (row & 7));
-      dma16(W0 + (size_t)min(row, rows_w - 1) * g.ldw + k, LW + u0 * 8);
+      const int n = n0 + min(row, rows_w - 1);
+      // packed W: 1 KB fragment (k-step k / 32, 16-row tile n / 16), piece (n % 16) + 16 (k % 32) / 8
+      const size_t woff = g.w_packed
+          ? ((((size_t)(k >> 5) * (g.N >> 4) + (n >> 4)) * 64 + (n & 15) + 16 * ((k & 31) >> 3)) * 8)
+          : (size_t)n * g.ldw + k;
+      dma16(g.W_hi + woff, LW + u0 * 8);
     }
   };
 
@@ -657,31 +661,37 @@ __global__ void __launch_bounds__(256) gemm_dma_kernel(GemmArgs g) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[a][b][i] = 0.f;
 
+  // Fragments of k-step ks + 1 are read while the MFMAs of k-step ks run.
   auto compute = [&](const bf16* L, const bf16* LW) {
     const bf16* sA = L;
     const bf16* sAl = L + C::SA;
     const bf16* sW = LW;
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
+    bf16x8 fa[2][TM], fal[2][ALO ? TM : 1], fw[2][TN];
+    auto frags = [&](int ks, int buf) {
       const int ch = 2 * ks + (lane >> 5);
-      bf16x8 fa[TM], fal[ALO ? TM : 1], fw[TN];
 #pragma unroll
       for (int a = 0; a < TM; ++a) {
         const int r = (wm * TM + a) * 32 + (lane & 31);
-        fa[a] = *reinterpret_cast<const bf16x8*>(sA + 8 * swz(r, ch));
-        if constexpr (ALO) fal[a] = *reinterpret_cast<const bf16x8*>(sAl + 8 * swz(r, ch));
+        fa[buf][a] = *reinterpret_cast<const bf16x8*>(sA + 8 * swz(r, ch));
+        if constexpr (ALO) fal[buf][a] = *reinterpret_cast<const bf16x8*>(sAl + 8 * swz(r, ch));
       }
 #pragma unroll
       for (int b = 0; b < TN; ++b) {
         const int r = (wn * TN + b) * 32 + (lane & 31);
-        fw[b] = *reinterpret_cast<const bf16x8*>(sW + 8 * swz(r, ch));
+        fw[buf][b] = *reinterpret_cast<const bf16x8*>(sW + 8 * swz(r, ch));
       }
+    };
+    frags(0, 0);
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      if (ks + 1 < BK / 16) frags(ks + 1, (ks + 1) & 1);
+      const int cb = ks & 1;
 #pragma unroll
       for (int a = 0; a < TM; ++a)
 #pragma unroll
         for (int b = 0; b < TN; ++b) {
-          acc[a][b] = mma32(fa[a], fw[b], acc[a][b]);
-          if constexpr (ALO) acc[a][b] = mma32(fal[a], fw[b], acc[a][b]);
+          acc[a][b] = mma32(fa[cb][a], fw[cb][b], acc[a][b]);
+          if constexpr (ALO) acc[a][b] = mma32(fal[cb][a], fw[cb][b], acc[a][b]);
         }
     }
   };
@@ -791,7 +801,7 @@ hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
   SkPlan p = skinny_plan(g.M, g.N, g.K, g.W_lo != nullptr, device_cus());
   if ((g.C && g.ldc % 4) || (g.C_hi && g.ldch % 4) || (g.R && g.ldr % 4)) p.use = false;   // 16-byte stores
-  if (g.w_packed && (!p.use || g.N % 16 || g.W_lo || g.R)) return hipErrorInvalidValue;   // packed W: this path, no residual
+  if (g.w_packed && (g.N % 16 || g.K % BK || g.W_lo || g.R)) return hipErrorInvalidValue;   // packed W: no residual
   if (p.use) {
     if (p.ksplit > 1 && (!g.part || g.part_cap < (size_t)p.ksplit * g.M * g.N)) {
       p.ksplit = 1;
@@ -799,7 +809,7 @@ hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
     }
     return g.A_lo ? launch_skinny_a<true>(g, p, s) : launch_skinny_a<false>(g, p, s);
   }
-  if (g.M <= 64) return launch_cfg<1, 4, 2, 2>(g, s);      // 64 x 256: weight streaming
+  if (g.M <= 64 && !g.w_packed) return launch_cfg<1, 4, 2, 2>(g, s);      // 64 x 256: weight streaming
   if (!g.W_lo && g.K % BK == 0)
     return g.A_lo ? launch_dma<2, 2, true, 3>(g, s) : launch_dma<2, 2, false, 4>(g, s);
   if (g.M <= 128) return launch_cfg<2, 2, 2, 4>(g, s);     // 128 x 256

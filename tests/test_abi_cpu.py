@@ -129,10 +129,10 @@ def test_packed_w_ds_validation():
     assert L.hspec_pack_w_ds_bytes(1 << 20, 4096) == (1 << 20) * 4096 * 2
     assert L.hspec_pack_w_ds_bytes(24, 4096) == 0
     assert L.hspec_pack_w_ds_bytes(1 << 20, 4008) == 0
-    assert L.hspec_pack_w_ds(0, 32, FAKE, FAKE, None) == 2
-    assert L.hspec_pack_w_ds(24, 32, FAKE, FAKE, None) == 4
-    assert L.hspec_pack_w_ds(16, 40, FAKE, FAKE, None) == 4
-    assert L.hspec_pack_w_ds(16, 32, None, FAKE, None) == 1
+    assert L.hspec_pack_w_ds(0, 64, FAKE, FAKE, None) == 2
+    assert L.hspec_pack_w_ds(24, 64, FAKE, FAKE, None) == 4
+    assert L.hspec_pack_w_ds(16, 96, FAKE, FAKE, None) == 4
+    assert L.hspec_pack_w_ds(16, 64, None, FAKE, None) == 1
     # the packed flag needs bf16 storage and r % 32 == 0; unknown flags are rejected
     cfg = I.CONFIGS[3]
     mw = hspec.MambaW(*([FAKE.value] * 10))
@@ -146,7 +146,7 @@ def test_packed_w_ds_validation():
     mc = hspec.mamba_cfg(cfg.replace(dtype="f32"))
     mc.flags = hspec.W_DS_PACKED
     assert state(mc) == 4
-    mc = hspec.mamba_cfg(cfg.replace(r=4104))
+    mc = hspec.mamba_cfg(cfg.replace(r=4128))
     mc.flags = hspec.W_DS_PACKED
     assert state(mc) == 4
     assert b"packed" in L.hspec_last_error()
