@@ -390,16 +390,27 @@ hspec_status run_attn_core(const hspec_attn_cfg& c, const hspec_attn_w& w, Plane
   HIP_TRY(as_planes(v_cache, c.dtype, p.vc, vc, st));
   const Planes* ws[3] = {&wq, &wk, &wv};
   const int nrows[3] = {c.Hq * c.D, c.Hkv * c.D, c.Hkv * c.D};
-  int col = 0;
-  for (int i = 0; i < 3; ++i) {
+  if (!wq.lo) {
+    // one product over the three row segments [W_q; W_k; W_v]
     hspec::GemmArgs g;
     g.A_hi = xn.hi; g.A_lo = xn.lo; g.lda = c.d_model;
-    g.W_hi = ws[i]->hi; g.W_lo = ws[i]->lo; g.ldw = c.d_model;
-    g.M = M; g.N = nrows[i]; g.K = c.d_model;
-    g.C = p.qkv + col; g.ldc = ldq;
+    g.W_hi = wq.hi; g.W2 = wk.hi; g.W3 = wv.hi; g.N1 = nrows[0]; g.N2 = nrows[1]; g.ldw = c.d_model;
+    g.M = M; g.N = ldq; g.K = c.d_model;
+    g.C = p.qkv; g.ldc = ldq;
     use_scratch(g, p.gs);
     HIP_TRY(hspec::launch_gemm(g, st));
-    col += nrows[i];
+  } else {
+    int col = 0;
+    for (int i = 0; i < 3; ++i) {
+      hspec::GemmArgs g;
+      g.A_hi = xn.hi; g.A_lo = xn.lo; g.lda = c.d_model;
+      g.W_hi = ws[i]->hi; g.W_lo = ws[i]->lo; g.ldw = c.d_model;
+      g.M = M; g.N = nrows[i]; g.K = c.d_model;
+      g.C = p.qkv + col; g.ldc = ldq;
+      use_scratch(g, p.gs);
+      HIP_TRY(hspec::launch_gemm(g, st));
+      col += nrows[i];
+    }
   }
   HIP_TRY(hspec::launch_qk_norm_rope(p.qkv, w.q_norm_w, w.k_norm_w, lens, c.B, c.k, c.Hq, c.Hkv, c.D, c.eps,
                                      c.rope_theta, p.q_hi, p.q_lo, p.k_hi, p.k_lo, p.v_hi, p.v_lo, st));

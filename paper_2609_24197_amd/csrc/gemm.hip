@@ -627,9 +627,18 @@ __global__ void __launch_bounds__(256) gemm_dma_kernel(GemmArgs g) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / 2, wn = wave % 2;
 
-  const int rows_a = min(C::BM, g.M - m0), rows_w = min(C::BN, g.N - n0);
+  const int rows_a = min(C::BM, g.M - m0);
   const bf16* A0 = g.A_hi + (size_t)m0 * g.lda;
   const bf16* Al0 = (ALO ? g.A_lo : g.A_hi) + (size_t)m0 * g.lda;
+  // W row segment of this tile (tiles never straddle a segment boundary)
+  const bf16* wbase = g.W_hi;
+  int wseg0 = 0, wseg1 = g.N;
+  if (g.W2) {
+    if (n0 >= g.N1 + g.N2) { wbase = g.W3; wseg0 = g.N1 + g.N2; }
+    else if (n0 >= g.N1) { wbase = g.W2; wseg0 = g.N1; wseg1 = g.N1 + g.N2; }
+    else wseg1 = g.N1;
+  }
+  const int rows_w = min(C::BN, wseg1 - n0);
 
   // unit u (16 bytes) of a stage plane: row u / 8, stored chunk u % 8 = logical chunk ^ (row & 7)
   auto issue = [&](int t, bf16* L, bf16* LW) {
@@ -648,8 +657,8 @@ __global__ void __launch_bounds__(256) gemm_dma_kernel(GemmArgs g) {
       // packed W: 1 KB fragment (k-step k / 32, 16-row tile n / 16), piece (n % 16) + 16 (k % 32) / 8
       const size_t woff = g.w_packed
           ? ((((size_t)(k >> 5) * (g.N >> 4) + (n >> 4)) * 64 + (n & 15) + 16 * ((k & 31) >> 3)) * 8)
-          : (size_t)n * g.ldw + k;
-      dma16(g.W_hi + woff, LW + u0 * 8);
+          : (size_t)(n - wseg0) * g.ldw + k;
+      dma16(wbase + woff, LW + u0 * 8);
     }
   };
 
@@ -799,6 +808,25 @@ size_t gemm_scratch_elems(int M, int N, int K, bool a_lo, bool w_lo) {
 
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
+  if (g.W2) {
+    const bool dma = g.M > 64 && !g.W_lo && !g.w_packed && g.K % BK == 0 && g.N1 % 128 == 0 && g.N2 % 128 == 0;
+    if (dma) return g.A_lo ? launch_dma<2, 2, true, 3>(g, s) : launch_dma<2, 2, false, 4>(g, s);
+    // one launch per segment, each writing its own column range of C
+    const bf16* ws[3] = {g.W_hi, g.W2, g.W3};
+    const int n0s[3] = {0, g.N1, g.N1 + g.N2}, ns[3] = {g.N1, g.N2, g.N - g.N1 - g.N2};
+    for (int i = 0; i < 3; ++i) {
+      GemmArgs h = g;
+      h.W2 = h.W3 = nullptr;
+      h.W_hi = ws[i];
+      h.N = ns[i];
+      if (h.C) h.C += n0s[i];
+      if (h.C_hi) h.C_hi += n0s[i];
+      if (h.C_lo) h.C_lo += n0s[i];
+      if (h.R) h.R = h.r_bf16 ? (const void*)((const bf16*)h.R + n0s[i]) : (const void*)((const float*)h.R + n0s[i]);
+      if (hipError_t e = launch_gemm(h, s)) return e;
+    }
+    return hipSuccess;
+  }
   SkPlan p = skinny_plan(g.M, g.N, g.K, g.W_lo != nullptr, device_cus());
   if ((g.C && g.ldc % 4) || (g.C_hi && g.ldch % 4) || (g.R && g.ldr % 4)) p.use = false;   // 16-byte stores
   if (g.w_packed && (g.N % 16 || g.K % BK || g.W_lo || g.R)) return hipErrorInvalidValue;   // packed W: no residual

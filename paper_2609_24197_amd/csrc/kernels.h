@@ -18,6 +18,9 @@ struct GemmArgs {
   bf16* C_hi = nullptr; bf16* C_lo = nullptr; int ldch = 0;  // bf16 planes of the result
   float* part = nullptr; size_t part_cap = 0;  // split-K scratch (fp32 elements), optional
   int w_packed = 0;   // W_hi is in the fragment-major packed layout (launch_pack_w)
+  // Optional row segments of W (bf16, not packed): rows [0, N1) come from W_hi, [N1, N1 + N2)
+  // from W2 and [N1 + N2, N) from W3, each with leading dimension ldw.
+  const bf16* W2 = nullptr; const bf16* W3 = nullptr; int N1 = 0, N2 = 0;
 };
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
 // fp32 elements of split-K scratch that launch_gemm uses for an M x N x K product when

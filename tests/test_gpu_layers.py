@@ -20,6 +20,9 @@ SMALL = {
                                  D=128, lengths="list:45,200"),
     "window_causal": I.StepConfig(name="s", B=2, k=16, d_model=256, H=4, P=64, N=128, G=1, chunk=8, Hq=32, Hkv=8,
                                   D=128, lengths="list:900,100", window=256, block_causal=True),
+    # B*k = 160 rows: the pipelined dense GEMMs, the fused Q/K/V product with a ragged last tile
+    "m160_fused_qkv": I.StepConfig(name="s", B=10, k=16, d_model=320, H=5, P=64, N=32, G=1, chunk=16, Hq=8,
+                                   Hkv=2, D=128, lengths="uniform:1:700"),
 }
 
 
