@@ -47,7 +47,11 @@ struct GemmCfg {
   static constexpr int LDS_BYTES = 2 * (LDS_A * (ALO ? 2 : 1) + LDS_W * (WLO ? 2 : 1));
 };
 
-__device__ __forceinline__ int swz(int row, int chunk) { return row * CPR + (chunk ^ (row & 7)); }
+// LDS position (16-byte units) of chunk `chunk` of tile row `row`: the chunk is XOR-ed with
+// (row / 2) % 8 so that the 16 rows one ds_read_b128 pass serves (two per 256-byte bank line)
+// fall on 16 distinct 4-bank groups.
+__device__ __forceinline__ int swz_key(int row) { return (row >> 1) & 7; }
+__device__ __forceinline__ int swz(int row, int chunk) { return row * CPR + (chunk ^ swz_key(row)); }
 
 __device__ __forceinline__ bf16x8 ld_chunk(const bf16* base, int ld, int row, int col, int rows, int K) {
   if (row < rows && col < K) return ld8(base + (size_t)row * ld + col);
@@ -640,26 +644,33 @@ __global__ void __launch_bounds__(256) gemm_dma_kernel(GemmArgs g) {
   }
   const int rows_w = min(C::BN, wseg1 - n0);
 
-  // unit u (16 bytes) of a stage plane: row u / 8, stored chunk u % 8 = logical chunk ^ (row & 7)
+  // unit u (16 bytes) of a stage plane: row u / 8, stored chunk u % 8 = logical chunk ^ swz_key(row).
+  // Source offsets of k-tile 0 per lane; k-tile t adds t * (a_step, w_step) elements.
+  size_t a_off[C::A_I], w_off[C::W_I];
+#pragma unroll
+  for (int i = 0; i < C::A_I; ++i) {
+    const int u = (i * 4 + wave) * 64 + lane, row = u >> 3, k = 8 * ((u & 7) ^ swz_key(row));
+    a_off[i] = (size_t)min(row, rows_a - 1) * g.lda + k;
+  }
+#pragma unroll
+  for (int i = 0; i < C::W_I; ++i) {
+    const int u = (i * 4 + wave) * 64 + lane, row = u >> 3, k = 8 * ((u & 7) ^ swz_key(row));
+    const int n = n0 + min(row, rows_w - 1);
+    // packed W: 1 KB fragment (k-step k / 32, 16-row tile n / 16), piece (n % 16) + 16 (k % 32) / 8
+    w_off[i] = g.w_packed ? ((((size_t)(k >> 5) * (g.N >> 4) + (n >> 4)) * 64 + (n & 15) + 16 * ((k & 31) >> 3)) * 8)
+                          : (size_t)(n - wseg0) * g.ldw + k;
+  }
+  const size_t w_step = g.w_packed ? (size_t)2 * (g.N >> 4) * 512 : (size_t)BK;
   auto issue = [&](int t, bf16* L, bf16* LW) {
-    const int k0 = t * BK;
+    const size_t ka = (size_t)t * BK, kw = (size_t)t * w_step;
 #pragma unroll
     for (int i = 0; i < C::A_I; ++i) {
-      const int u0 = (i * 4 + wave) * 64, u = u0 + lane, row = u >> 3, k = k0 + 8 * ((u & 7) ^ (row & 7));
-      const size_t off = (size_t)min(row, rows_a - 1) * g.lda + k;
-      dma16(A0 + off, L + u0 * 8);
-      if constexpr (ALO) dma16(Al0 + off, L + C::SA + u0 * 8);
+      const int u0 = (i * 4 + wave) * 64;
+      dma16(A0 + a_off[i] + ka, L + u0 * 8);
+      if constexpr (ALO) dma16(Al0 + a_off[i] + ka, L + C::SA + u0 * 8);
     }
 #pragma unroll
-    for (int i = 0; i < C::W_I; ++i) {
-      const int u0 = (i * 4 + wave) * 64, u = u0 + lane, row = u >> 3, k = k0 + 8 * ((u & 7) ^ (row & 7));
-      const int n = n0 + min(row, rows_w - 1);
-      // packed W: 1 KB fragment (k-step k / 32, 16-row tile n / 16), piece (n % 16) + 16 (k % 32) / 8
-      const size_t woff = g.w_packed
-          ? ((((size_t)(k >> 5) * (g.N >> 4) + (n >> 4)) * 64 + (n & 15) + 16 * ((k & 31) >> 3)) * 8)
-          : (size_t)(n - wseg0) * g.ldw + k;
-      dma16(wbase + woff, LW + u0 * 8);
-    }
+    for (int i = 0; i < C::W_I; ++i) dma16(wbase + w_off[i] + kw, LW + (i * 4 + wave) * 64 * 8);
   };
 
   f32x16 acc[TM][TN];
@@ -694,6 +705,7 @@ __global__ void __launch_bounds__(256) gemm_dma_kernel(GemmArgs g) {
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
       if (ks + 1 < BK / 16) frags(ks + 1, (ks + 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);   // the next k-step's LDS reads go out before these MFMAs
       const int cb = ks & 1;
 #pragma unroll
       for (int a = 0; a < TM; ++a)
