@@ -22,6 +22,13 @@
 #include "common.h"
 #include "kernels.h"
 
+#ifndef HSPEC_SWEEP_WPE
+#define HSPEC_SWEEP_WPE 2   // waves per SIMD the sweep's register budget is sized for
+#endif
+#ifndef HSPEC_SWEEP_AUX
+#define HSPEC_SWEEP_AUX 2   // cache-policy bits of the cache K/V loads (2: non-temporal)
+#endif
+
 namespace hspec {
 
 namespace {
@@ -82,7 +89,7 @@ __device__ __forceinline__ int tile_off(int row, int d) {
 constexpr float RESCALE_SLACK = 8.f;
 
 template <int D, int QB, int NW, int KT, int ST, bool LO>
-__global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(HSPEC_SWEEP_WPE)))
 attn_sweep(AttnArgs a) {
   using C = Sweep<D, QB, NW, KT, ST, LO>;
   constexpr int NS = D / 32;             // d-steps of the QK^T contraction
@@ -202,9 +209,10 @@ attn_sweep(AttnArgs a) {
       const bf16* Kp = cache ? a.kc_hi : a.kb_hi;
       const bf16* Vp = cache ? a.vc_hi : a.vb_hi;
       bf16* dst = sb + (wave * C::DMA + i) * 64 * 8;
-      __builtin_amdgcn_global_load_lds((const GLB_AS void*)(Kp + off), (LDS_AS void*)dst, 16, 0, 0);
+      // the cache is read once per step: non-temporal loads (HSPEC_SWEEP_AUX cache-policy bits)
+      __builtin_amdgcn_global_load_lds((const GLB_AS void*)(Kp + off), (LDS_AS void*)dst, 16, 0, HSPEC_SWEEP_AUX);
       __builtin_amdgcn_global_load_lds((const GLB_AS void*)(Vp + off), (LDS_AS void*)(dst + C::PLANES * C::TILE),
-                                       16, 0, 0);
+                                       16, 0, HSPEC_SWEEP_AUX);
       if constexpr (LO) {
         const bf16* Kl = cache ? a.kc_lo : a.kb_lo;
         const bf16* Vl = cache ? a.vc_lo : a.vb_lo;
@@ -542,10 +550,14 @@ __global__ void gather_slots_kernel(int B, int max_pages, int ps, int num_pages,
 #ifndef HSPEC_SWEEP_ST
 #define HSPEC_SWEEP_ST 3
 #endif
+#ifndef HSPEC_SWEEP_KT
+#define HSPEC_SWEEP_KT 32   // keys per tile (at least; a multiple of 32)
+#endif
 
 template <int D, int QB, int NW, bool LO>
 hipError_t launch_sweep(const AttnArgs& a, hipStream_t s) {
-  constexpr int KT = 512 * NW / D > 32 ? 512 * NW / D : 32;   // every lane DMAs at least one chunk
+  constexpr int KT0 = 512 * NW / D > 32 ? 512 * NW / D : 32;  // every lane DMAs at least one chunk
+  constexpr int KT = KT0 > HSPEC_SWEEP_KT ? KT0 : HSPEC_SWEEP_KT;
   constexpr int NDMA = 2 * (LO ? 2 : 1) * KT * (D / 8) / (64 * NW);
   constexpr int ST_MAX = 2 + 63 / NDMA;                         // vmcnt holds at most 63
   constexpr int ST = LO ? 2 : (HSPEC_SWEEP_ST < ST_MAX ? HSPEC_SWEEP_ST : ST_MAX);
