@@ -323,7 +323,7 @@ void plan_sweep(Arena& ar, const hspec_attn_cfg& c, int max_ctx_len, AttnPlan& p
   p.max_splits = max_ctx_len > 0 ? (max_ctx_len + p.split - 1) / p.split : 1;
   const int R = c.k * (c.Hq / c.Hkv);
   const size_t units = (size_t)c.B * c.Hkv * p.max_splits;
-  p.units = ar.take<int32_t>((size_t)c.B * p.max_splits);
+  p.units = ar.take<int32_t>((size_t)2 * c.B * p.max_splits);
   if (p.max_splits > 1) {
     p.part_o = ar.take<float>(units * R * c.D);
     p.part_ml = ar.take<float>(units * R * 2);

@@ -125,16 +125,19 @@ attn_sweep(AttnArgs a) {
   const int g = a.Hq / a.Hkv, T = a.T, R = T * g;
   const int n_items = a.status[1];
 
-  // Persistent workgroups pull (request, split, KV head) items, longest splits first.
+  // Persistent workgroups pull (request, split, KV head) items, longest splits first.  The
+  // next item is claimed while the last round of the current one is multiplied.
+  int next = -1;   // thread 0: item claimed ahead
   for (;;) {
   __syncthreads();                    // the previous item is finished by every wave
-  if (tid == 0) s_item = atomicAdd(a.status + 2, 1);
+  if (tid == 0) s_item = next >= 0 ? next : atomicAdd(a.status + 2, 1);
+  next = -1;
   __syncthreads();
   const int item = s_item;
   if (item >= n_items) break;
-  const int packed = a.units[item / a.Hkv];
-  const int b = packed >> 16, sp = packed & 0xffff, h = item % a.Hkv;
-  const int L = clamp_len(a, b);
+  const int2 unit_e = *reinterpret_cast<const int2*>(a.units + 2 * (item / a.Hkv));
+  const int b = unit_e.x >> 16, sp = unit_e.x & 0xffff, h = item % a.Hkv;
+  const int L = unit_e.y;   // validated by the work-list kernel
   const int nsplit = L > 0 ? (L + a.split - 1) / a.split : 1;
   const int k0 = sp * a.split;
   const int k1 = min(L, k0 + a.split);
@@ -147,21 +150,6 @@ attn_sweep(AttnArgs a) {
   const int n_cache = kstart < k1 ? (k1 - kstart + KT - 1) / KT : 0;
   const int n_block = last ? (T + KT - 1) / KT : 0;
   const int ntiles = n_cache + n_block;
-
-  // page ids of this split, validated once
-  const int pg0 = k0 >> lps;
-  if (n_cache > 0) {
-    const int npg = ((k1 - 1) >> lps) - pg0 + 1;
-    const int32_t* ptab = a.page_table + (size_t)b * a.max_pages + pg0;
-    for (int e = tid; e < npg; e += C::NT) {
-      int pid = ptab[e];
-      if (pid < 0 || pid >= a.num_pages) {
-        set_status(a.status, ST_BAD_PAGE);
-        pid = 0;
-      }
-      pids[e] = pid * a.ps;        // first slot of the page
-    }
-  }
 
   // query fragments: B operand of S^T = K Q^T (lane: column l16, dims 32 s + 8 g4 ..) and the
   // key window [lo, hi) of each column for cache keys and for block keys
@@ -183,6 +171,21 @@ attn_sweep(AttnArgs a) {
     c_hi[qb] = real ? k1 : INT_MIN;
     b_hi[qb] = real ? (a.causal ? j + 1 : T) : INT_MIN;
   }
+  // page ids of this split, validated once
+  const int pg0 = k0 >> lps;
+  if (n_cache > 0) {
+    const int npg = ((k1 - 1) >> lps) - pg0 + 1;
+    const int32_t* ptab = a.page_table + (size_t)b * a.max_pages + pg0;
+    for (int e = tid; e < npg; e += C::NT) {
+      int pid = ptab[e];
+      if (pid < 0 || pid >= a.num_pages) {
+        set_status(a.status, ST_BAD_PAGE);
+        pid = 0;
+      }
+      pids[e] = pid * a.ps;        // first slot of the page
+    }
+  }
+
   __syncthreads();   // page ids visible (LDS writes waited for, unlike the pipeline barrier)
 
   // LDS-DMA of tile ti into stage sb: wave w fills chunk slots [w*DMA*64, (w+1)*DMA*64) of
@@ -381,7 +384,10 @@ attn_sweep(AttnArgs a) {
   [&]<int... I>(std::integer_sequence<int, I...>) {
     ((I < ntiles ? issue(I, stage(Int<I>{})) : void()), ...);
   }(std::make_integer_sequence<int, ST - 1>{});
-  for (int t0 = 0; t0 < ntiles; t0 += ST) round(t0, std::make_integer_sequence<int, ST>{});
+  for (int t0 = 0; t0 < ntiles; t0 += ST) {
+    if (tid == 0 && t0 + ST >= ntiles) next = (int)atomicInc(reinterpret_cast<unsigned*>(a.status + 2), 0xffffffffu);
+    round(t0, std::make_integer_sequence<int, ST>{});
+  }
 
   // write: lane holds O[column l16][d = 16 d + 4 g4 + i]
   const size_t unit = ((size_t)b * a.Hkv + h) * a.max_splits + sp;
@@ -415,8 +421,9 @@ attn_sweep(AttnArgs a) {
   }   // item loop
 }
 
-// Work list of the sweep: every (request, split) once, the full splits first and then the
-// last splits by decreasing length, so the persistent workgroups finish close together.
+// Work list of the sweep: every (request, split) once, as (request << 16 | split, context
+// length), the full splits first and then the last splits by decreasing length, so the
+// persistent workgroups finish close together.
 // One workgroup of PLAN_THREADS: the full splits are placed by a block-wide prefix sum over
 // requests, the last splits by rank (requests beyond PLAN_RANK_MAX keep their own order).
 // Also resets the item queue.
@@ -433,9 +440,9 @@ __global__ void __launch_bounds__(PLAN_THREADS) attn_plan(AttnArgs a) {
   __syncthreads();
   for (int b0 = 0; b0 < a.B; b0 += PLAN_THREADS) {
     const int b = b0 + tid;
-    int nfull = 0;
+    int nfull = 0, L = 0;
     if (b < a.B) {
-      const int L = clamp_len(a, b);
+      L = clamp_len(a, b);
       const int ns = L > 0 ? (L + a.split - 1) / a.split : 1;
       nfull = ns - 1;
       if (ranked) s_rem[b] = L - nfull * a.split;
@@ -449,7 +456,10 @@ __global__ void __launch_bounds__(PLAN_THREADS) attn_plan(AttnArgs a) {
       __syncthreads();
     }
     const int first = s_base + s_scan[tid] - nfull;
-    for (int sp = 0; sp < nfull; ++sp) a.units[first + sp] = (b << 16) | sp;
+    for (int sp = 0; sp < nfull; ++sp) {
+      a.units[2 * (first + sp)] = (b << 16) | sp;
+      a.units[2 * (first + sp) + 1] = L;
+    }
     __syncthreads();
     if (tid == PLAN_THREADS - 1) s_base += s_scan[tid];
     __syncthreads();
@@ -467,7 +477,8 @@ __global__ void __launch_bounds__(PLAN_THREADS) attn_plan(AttnArgs a) {
         rank += (ro > rem) || (ro == rem && o < b);
       }
     }
-    a.units[full + rank] = (b << 16) | (ns - 1);
+    a.units[2 * (full + rank)] = (b << 16) | (ns - 1);
+    a.units[2 * (full + rank) + 1] = L;
   }
   if (tid == 0) {
     a.status[1] = (full + a.B) * a.Hkv;

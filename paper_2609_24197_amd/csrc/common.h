@@ -80,6 +80,15 @@ __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("" ::: "memory");
 }
 
+template <int VM>
+__device__ __forceinline__ void wait_vm_lgkm0() {
+  // vmcnt <= VM and every LDS access of this wave complete
+  static_assert(VM >= 0 && VM < 64, "vmcnt range");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((VM & 15) | (7 << 4) | (0 << 8) | ((VM >> 4) << 14));
+  asm volatile("" ::: "memory");
+}
+
 // Workgroup barrier without the memory fence of __syncthreads (which would also wait for
 // every outstanding global load); callers order LDS traffic with explicit waits.
 __device__ __forceinline__ void wg_barrier() {

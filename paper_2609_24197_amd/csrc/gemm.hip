@@ -570,14 +570,6 @@ __device__ __forceinline__ void dma16(const bf16* src, bf16* lds) {
                                    (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
 }
 
-template <int VM>
-__device__ __forceinline__ void wait_vm_lgkm0() {
-  // vmcnt <= VM and every LDS read of this wave complete
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_waitcnt((VM & 15) | (7 << 4) | (0 << 8) | ((VM >> 4) << 14));
-  asm volatile("" ::: "memory");
-}
-
 // Epilogue of a 32x32 accumulator block: lane holds rows 8(i/4)+4(l/32)+i%4 of column l%32.
 __device__ __forceinline__ void store_block32(const GemmArgs& g, const f32x16& acc, int mb, int nb, int lane) {
   const int n = nb + (lane & 31);

@@ -48,7 +48,7 @@ struct AttnArgs {
   float* o_f32 = nullptr;     // [B, T, Hq, D] (one of o_f32 / o_bf16)
   bf16* o_bf16 = nullptr;
   int* status = nullptr;      // device status word; status[1] = work items, status[2] = queue
-  int32_t* units = nullptr;   // [B * max_splits] work list (request << 16 | split), longest first
+  int32_t* units = nullptr;   // [B * max_splits][2] work list (request << 16 | split, length)
 };
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
 size_t attention_partials_bytes(int B, int Hkv, int max_splits, int R, int D);
