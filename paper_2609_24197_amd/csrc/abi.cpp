@@ -468,7 +468,7 @@ HSPEC_API hspec_status hspec_state_init(const hspec_mamba_cfg* cfg, const hspec_
   int* status = status_word(ar);
   StatePlan p;
   plan_state(ar, *cfg, false, p);
-  HIP_TRY(hspec::launch_zero_words(status, 1, st));
+  HIP_TRY(hspec::launch_zero_words(status, hspec::kStatusClear, st));
   return run_state(*cfg, *w, h_last, p, S0, st);
 }
 
@@ -493,7 +493,7 @@ HSPEC_API hspec_status hspec_mamba_block_scan(const hspec_mamba_cfg* cfg, const 
   int* status = status_word(ar);
   MambaPlan p;
   plan_mamba(ar, *cfg, false, p);
-  HIP_TRY(hspec::launch_zero_words(status, 1, st));
+  HIP_TRY(hspec::launch_zero_words(status, hspec::kStatusClear, st));
   if (hspec_status s = run_state(*cfg, *w, h_last, p.st, nullptr, st)) return s;
   Planes u;
   HIP_TRY(as_planes(block_hidden, cfg->dtype, p.u_in, u, st));
@@ -526,7 +526,9 @@ HSPEC_API hspec_status hspec_target_kv_block_attn(const hspec_attn_cfg* cfg, con
   int* status = status_word(ar);
   AttnPlan p;
   plan_attn(ar, *cfg, max_ctx_len, false, p);
-  HIP_TRY(hspec::launch_zero_words(status, 1, st));
+  // the sweep's work list is the call's first kernel and clears the status words
+  HIP_TRY(hspec::launch_attention_plan(sweep_args(*cfg, p, page_table, ctx_lens, max_ctx_len, status),
+                                       hspec::kStatusClear, st));
   Planes xn;
   HIP_TRY(as_planes(x, cfg->dtype, p.x_in, xn, st));
   return run_attn_core(*cfg, *w, xn, k_cache, v_cache, page_table, ctx_lens, max_ctx_len, p, nullptr, out, status, st);
@@ -564,7 +566,9 @@ HSPEC_API hspec_status hspec_draft_step(const hspec_mamba_cfg* mcfg, const hspec
   plan_draft(ar, *mcfg, *acfg, max_ctx_len, p);
   const int M = mcfg->B * mcfg->k;
   const bool f32 = is_f32(mcfg->dtype);
-  HIP_TRY(hspec::launch_zero_words(status, 1, st));
+  // the sweep's work list is the call's first kernel and clears the status words
+  HIP_TRY(hspec::launch_attention_plan(sweep_args(*acfg, p.at, page_table, ctx_lens, max_ctx_len, status),
+                                       hspec::kStatusClear, st));
   if (hspec_status s = run_state(*mcfg, *mw, h_last, p.m.st, nullptr, st)) return s;
   HIP_TRY(hspec::launch_rmsnorm_planes(block_emb, !f32, norm1_w, M, mcfg->d_model, mcfg->eps, p.m.u_hi, p.m.u_lo, st));
   Planes u{p.m.u_hi, p.m.u_lo};
@@ -611,7 +615,7 @@ HSPEC_API hspec_status hspec_ssd_scan(int B, int T, int H, int P, int N, int G, 
     sc = reserve_split(ar, dtype, (size_t)B * T * G * N);
     ss = reserve_split(ar, dtype, (size_t)B * H * P * N);
   }
-  HIP_TRY(hspec::launch_zero_words(status, 1, st));
+  HIP_TRY(hspec::launch_zero_words(status, hspec::kStatusClear, st));
   Planes px, pb, pc, ps;
   HIP_TRY(as_planes(x, dtype, sx, px, st));
   HIP_TRY(as_planes(Bm, dtype, sb, pb, st));
@@ -659,7 +663,9 @@ HSPEC_API hspec_status hspec_paged_attn(const hspec_attn_cfg* cfg, const void* q
   p.kbin = reserve_split(ar, cfg->dtype, M * cfg->Hkv * cfg->D);
   p.vbin = reserve_split(ar, cfg->dtype, M * cfg->Hkv * cfg->D);
   plan_sweep(ar, *cfg, max_ctx_len, p);
-  HIP_TRY(hspec::launch_zero_words(status, 1, st));
+  // the sweep's work list is the call's first kernel and clears the status words
+  HIP_TRY(hspec::launch_attention_plan(sweep_args(*cfg, p, page_table, ctx_lens, max_ctx_len, status),
+                                       hspec::kStatusClear, st));
   Planes pq, pk, pv, kc, vc;
   HIP_TRY(as_planes(q, cfg->dtype, p.qin, pq, st));
   HIP_TRY(as_planes(k_blk, cfg->dtype, p.kbin, pk, st));
@@ -710,7 +716,7 @@ HSPEC_API hspec_status hspec_linear(hspec_dtype dtype, int M, int N, int K, cons
   int* status = status_word(ar);
   SplitSlot sa = reserve_split(ar, dtype, (size_t)M * K), sw = reserve_split(ar, dtype, (size_t)N * K);
   const GemmScratch gs = reserve_gemm(ar, dtype, {{M, N, K}});
-  HIP_TRY(hspec::launch_zero_words(status, 1, st));
+  HIP_TRY(hspec::launch_zero_words(status, hspec::kStatusClear, st));
   Planes pa, pw;
   HIP_TRY(as_planes(A, dtype, sa, pa, st));
   HIP_TRY(as_planes(W, dtype, sw, pw, st));

@@ -426,15 +426,17 @@ attn_sweep(AttnArgs a) {
 // persistent workgroups finish close together.
 // One workgroup of PLAN_THREADS: the full splits are placed by a block-wide prefix sum over
 // requests, the last splits by rank (requests beyond PLAN_RANK_MAX keep their own order).
-// Also resets the item queue.
+// Also resets the item queue and, as the first kernel of a call, its status words.
 constexpr int PLAN_THREADS = 1024;
 constexpr int PLAN_RANK_MAX = 4096;
 
-__global__ void __launch_bounds__(PLAN_THREADS) attn_plan(AttnArgs a) {
+__global__ void __launch_bounds__(PLAN_THREADS) attn_plan(AttnArgs a, int clear_words) {
   __shared__ int s_rem[PLAN_RANK_MAX];
   __shared__ int s_scan[PLAN_THREADS];
   __shared__ int s_base;
   const int tid = threadIdx.x;
+  if (tid < clear_words) a.status[tid] = 0;   // a call's first kernel clears its status words
+  __syncthreads();
   const bool ranked = a.B <= PLAN_RANK_MAX;
   if (tid == 0) s_base = 0;
   __syncthreads();
@@ -486,45 +488,63 @@ __global__ void __launch_bounds__(PLAN_THREADS) attn_plan(AttnArgs a) {
   }
 }
 
-// One workgroup per (request, KV head, 16 query columns): per column the split weights
-// 2^(m_s - m*) / sum_s l_s 2^(m_s - m*) go to LDS once, then o = sum_s w_s O_s streams the
-// partial outputs in a fixed split order.
+// Split reduction.  One workgroup per (request, KV head, 16 query columns), one thread per
+// (column, 4 dims) and 2 per thread: every thread loads the running max, sum and partial
+// output of each split for its column at once, then o = sum_s O_s 2^(m_s - m*) / sum_s l_s
+// 2^(m_s - m*) in split order.
 constexpr int RED_COLS = 16;
-constexpr int RED_MAX_SPLITS = 256;
+constexpr int RED_THREADS = 256;
+constexpr int RED_NS = 4;   // splits whose loads are all issued together; more take further rounds
 
-__global__ void __launch_bounds__(256) attn_reduce(AttnArgs a) {
-  __shared__ float w[RED_COLS][RED_MAX_SPLITS + 1];
-  const int g = a.Hq / a.Hkv, T = a.T, R = T * g, D = a.D;
+__global__ void __launch_bounds__(RED_THREADS) attn_reduce(AttnArgs a) {
+  const int g = a.Hq / a.Hkv, T = a.T, R = T * g, D = a.D, nq = D / 4;
   const int cblocks = (R + RED_COLS - 1) / RED_COLS;
   const int bh = blockIdx.x / cblocks, c0 = (blockIdx.x % cblocks) * RED_COLS;
   const int b = bh / a.Hkv, h = bh % a.Hkv;
-  const int L = clamp_len(a, b);
+  int L = a.ctx_lens[b];
+  const int cap = min(a.max_pages * a.ps, a.max_ctx_len);
+  L = L < 0 ? 0 : (L > cap ? cap : L);   // out-of-range lengths were flagged by the sweep
   const int nsplit = L > 0 ? (L + a.split - 1) / a.split : 1;
   if (nsplit == 1) return;
   const size_t unit0 = ((size_t)b * a.Hkv + h) * a.max_splits;
-  for (int c = threadIdx.x; c < RED_COLS; c += blockDim.x) {
-    if (c0 + c >= R) continue;
+  for (int it = threadIdx.x; it < RED_COLS * nq; it += RED_THREADS) {
+    const int c = c0 + it / nq, d4 = (it % nq) * 4;
+    if (c >= R) continue;
+    // per round of RED_NS splits: running maxima, sums and partial outputs, all loads in flight
+    // together; with at most RED_NS splits the maxima are known after the one round
+    float m[RED_NS], l[RED_NS];
+    f32x4 o[RED_NS];
+    auto fetch = [&](int s0) {
+#pragma unroll
+      for (int i = 0; i < RED_NS; ++i) {
+        const bool in = s0 + i < nsplit;
+        const size_t u = (unit0 + s0 + (in ? i : 0)) * R + c;
+        m[i] = in ? a.part_ml[u * 2] : -INFINITY;
+        l[i] = in ? a.part_ml[u * 2 + 1] : 0.f;
+        o[i] = in ? *reinterpret_cast<const f32x4*>(a.part_o + u * D + d4) : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    };
     float mstar = -INFINITY;
-    for (int s = 0; s < nsplit; ++s) mstar = fmaxf(mstar, a.part_ml[((unit0 + s) * R + c0 + c) * 2]);
+    if (nsplit <= RED_NS) {
+      fetch(0);
+#pragma unroll
+      for (int i = 0; i < RED_NS; ++i) mstar = fmaxf(mstar, m[i]);
+    } else {
+      for (int sp = 0; sp < nsplit; ++sp) mstar = fmaxf(mstar, a.part_ml[((unit0 + sp) * R + c) * 2]);
+    }
     const float m_use = mstar == -INFINITY ? 0.f : mstar;
     float lsum = 0.f;
-    for (int s = 0; s < nsplit; ++s) {
-      const float* ml = a.part_ml + ((unit0 + s) * R + c0 + c) * 2;
-      const float e = exp2f(ml[0] - m_use);
-      w[c][s] = e;
-      lsum += ml[1] * e;
-    }
-    const float inv = 1.f / lsum;
-    for (int s = 0; s < nsplit; ++s) w[c][s] *= inv;
-  }
-  __syncthreads();
-  const int nq = D / 4;
-  for (int it = threadIdx.x; it < RED_COLS * nq; it += blockDim.x) {
-    const int cc = it / nq, c = c0 + cc, d4 = (it % nq) * 4;
-    if (c >= R) continue;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int s = 0; s < nsplit; ++s)
-      acc += *reinterpret_cast<const f32x4*>(a.part_o + ((unit0 + s) * R + c) * D + d4) * w[cc][s];
+    for (int s0 = 0; s0 < nsplit; s0 += RED_NS) {
+      if (nsplit > RED_NS) fetch(s0);
+#pragma unroll
+      for (int i = 0; i < RED_NS; ++i) {
+        const float e = exp2f(m[i] - m_use);
+        lsum += l[i] * e;
+        acc += o[i] * e;
+      }
+    }
+    acc *= 1.f / lsum;
     const int j = c / g, hq = h * g + c % g;
     const size_t off = ((size_t)(b * T + j) * a.Hq + hq) * D + d4;
     if (a.o_f32) *reinterpret_cast<f32x4*>(a.o_f32 + off) = acc;
@@ -624,11 +644,14 @@ int attention_default_split(int B, int Hkv, int max_ctx_len) {
   return (int)s;
 }
 
+hipError_t launch_attention_plan(const AttnArgs& a, int clear_words, hipStream_t s) {
+  hipLaunchKernelGGL(attn_plan, dim3(1), dim3(PLAN_THREADS), 0, s, a, clear_words);
+  return hipGetLastError();
+}
+
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   const bool lo = a.q_lo != nullptr;
-  hipLaunchKernelGGL(attn_plan, dim3(1), dim3(PLAN_THREADS), 0, s, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  hipError_t e = hipSuccess;
   if (a.D == 128) e = lo ? launch_sweep_nw<128, true>(a, s) : launch_sweep_nw<128, false>(a, s);
   else if (a.D == 64) e = lo ? launch_sweep_nw<64, true>(a, s) : launch_sweep_nw<64, false>(a, s);
   else return hipErrorInvalidValue;

@@ -47,12 +47,16 @@ struct AttnArgs {
   float* part_ml = nullptr;   // [B*Hkv*max_splits, R, 2]
   float* o_f32 = nullptr;     // [B, T, Hq, D] (one of o_f32 / o_bf16)
   bf16* o_bf16 = nullptr;
-  int* status = nullptr;      // device status word; status[1] = work items, status[2] = queue
+  int* status = nullptr;      // device status word; status[1] = work items, status[2] = queue (zero at launch)
   int32_t* units = nullptr;   // [B * max_splits][2] work list (request << 16 | split, length)
 };
+// Work list of the sweep (reads only B, ctx_lens, split and the table sizes of a); clears
+// status[0, clear_words) first.  Must precede launch_attention on the stream.
+hipError_t launch_attention_plan(const AttnArgs& a, int clear_words, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
 size_t attention_partials_bytes(int B, int Hkv, int max_splits, int R, int D);
 constexpr int kStatusWords = 64;   // int32 words reserved at the start of every workspace
+constexpr int kStatusClear = 4;    // cleared at the start of every call: status bits, work items, queue
 int attention_default_split(int B, int Hkv, int max_ctx_len);
 
 hipError_t launch_gather_slots(int B, int max_pages, int ps, int num_pages, const int32_t* page_table,
