@@ -225,6 +225,21 @@ hspec_status hspec_paged_attn(const hspec_attn_cfg* cfg, const void* q, const vo
 size_t hspec_paged_attn_workspace(const hspec_attn_cfg* cfg, int max_ctx_len);
 
 /*
+ * hspec_paged_attn in separately launched phases, for timing one kernel at a time: the work
+ * list (which also clears the workspace status words), the KV sweep (with any fp32 -> bf16
+ * plane conversion of its inputs), and the cross-split reduction.  `phases` is an OR of the
+ * flags below; a call with all three is hspec_paged_attn.  The phases of one attention must
+ * run in this order, on one stream, with the same arguments and workspace: a sweep or a
+ * reduction whose predecessors have not run on this workspace reads an undefined work list
+ * or undefined partials, and its behaviour is undefined.  Unknown bits: HSPEC_ERR_UNSUPPORTED.
+ */
+enum { HSPEC_PHASE_WORKLIST = 1u << 0, HSPEC_PHASE_SWEEP = 1u << 1, HSPEC_PHASE_REDUCE = 1u << 2 };
+hspec_status hspec_paged_attn_phase(const hspec_attn_cfg* cfg, const void* q, const void* k_blk, const void* v_blk,
+                                    const void* k_cache, const void* v_cache, const int32_t* page_table,
+                                    const int32_t* ctx_lens, int max_ctx_len, float* o, void* workspace,
+                                    size_t ws_bytes, unsigned phases, void* stream);
+
+/*
  * Physical slot of every logical cache position: slots [B, max_ctx_len] int32, -1 at and past
  * ctx_lens[b] (and for out-of-pool page ids, which also set HSPEC_DEV_BAD_PAGE in *status).
  * status: device int32 or NULL.

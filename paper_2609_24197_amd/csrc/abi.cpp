@@ -645,14 +645,17 @@ HSPEC_API size_t hspec_paged_attn_workspace(const hspec_attn_cfg* cfg, int max_c
   return ar.size();
 }
 
-HSPEC_API hspec_status hspec_paged_attn(const hspec_attn_cfg* cfg, const void* q, const void* k_blk,
-                                        const void* v_blk, const void* k_cache, const void* v_cache,
-                                        const int32_t* page_table, const int32_t* ctx_lens, int max_ctx_len, float* o,
-                                        void* workspace, size_t ws_bytes, void* stream) {
+HSPEC_API hspec_status hspec_paged_attn_phase(const hspec_attn_cfg* cfg, const void* q, const void* k_blk,
+                                              const void* v_blk, const void* k_cache, const void* v_cache,
+                                              const int32_t* page_table, const int32_t* ctx_lens, int max_ctx_len,
+                                              float* o, void* workspace, size_t ws_bytes, unsigned phases,
+                                              void* stream) {
   g_err.clear();
   if (hspec_status s = check_attn_cfg(cfg, max_ctx_len)) return s;
   if (!q || !k_blk || !v_blk || !k_cache || !v_cache || !page_table || !ctx_lens || !o)
     return fail(HSPEC_ERR_NULL, "an input or output pointer is NULL");
+  if (phases & ~(unsigned)(HSPEC_PHASE_WORKLIST | HSPEC_PHASE_SWEEP | HSPEC_PHASE_REDUCE))
+    return fail(HSPEC_ERR_UNSUPPORTED, "unknown phase bits 0x%x", phases);
   if (hspec_status s = check_ws(workspace, ws_bytes, hspec_paged_attn_workspace(cfg, max_ctx_len))) return s;
   hipStream_t st = (hipStream_t)stream;
   Arena ar{(char*)workspace};
@@ -664,20 +667,35 @@ HSPEC_API hspec_status hspec_paged_attn(const hspec_attn_cfg* cfg, const void* q
   p.vbin = reserve_split(ar, cfg->dtype, M * cfg->Hkv * cfg->D);
   plan_sweep(ar, *cfg, max_ctx_len, p);
   // the sweep's work list is the call's first kernel and clears the status words
-  HIP_TRY(hspec::launch_attention_plan(sweep_args(*cfg, p, page_table, ctx_lens, max_ctx_len, status),
-                                       hspec::kStatusClear, st));
+  if (phases & HSPEC_PHASE_WORKLIST)
+    HIP_TRY(hspec::launch_attention_plan(sweep_args(*cfg, p, page_table, ctx_lens, max_ctx_len, status),
+                                         hspec::kStatusClear, st));
+  if (!(phases & (HSPEC_PHASE_SWEEP | HSPEC_PHASE_REDUCE))) return HSPEC_OK;
   Planes pq, pk, pv, kc, vc;
-  HIP_TRY(as_planes(q, cfg->dtype, p.qin, pq, st));
-  HIP_TRY(as_planes(k_blk, cfg->dtype, p.kbin, pk, st));
-  HIP_TRY(as_planes(v_blk, cfg->dtype, p.vbin, pv, st));
-  HIP_TRY(as_planes(k_cache, cfg->dtype, p.kc, kc, st));
-  HIP_TRY(as_planes(v_cache, cfg->dtype, p.vc, vc, st));
+  if (phases & HSPEC_PHASE_SWEEP) {
+    HIP_TRY(as_planes(q, cfg->dtype, p.qin, pq, st));
+    HIP_TRY(as_planes(k_blk, cfg->dtype, p.kbin, pk, st));
+    HIP_TRY(as_planes(v_blk, cfg->dtype, p.vbin, pv, st));
+    HIP_TRY(as_planes(k_cache, cfg->dtype, p.kc, kc, st));
+    HIP_TRY(as_planes(v_cache, cfg->dtype, p.vc, vc, st));
+  }
   hspec::AttnArgs a = sweep_args(*cfg, p, page_table, ctx_lens, max_ctx_len, status);
   a.q_hi = pq.hi; a.q_lo = pq.lo; a.kb_hi = pk.hi; a.kb_lo = pk.lo; a.vb_hi = pv.hi; a.vb_lo = pv.lo;
   a.kc_hi = kc.hi; a.kc_lo = kc.lo; a.vc_hi = vc.hi; a.vc_lo = vc.lo;
   a.o_f32 = o;
-  HIP_TRY(hspec::launch_attention(a, st));
+  const unsigned parts = ((phases & HSPEC_PHASE_SWEEP) ? hspec::ATTN_SWEEP : 0u) |
+                         ((phases & HSPEC_PHASE_REDUCE) ? hspec::ATTN_REDUCE : 0u);
+  HIP_TRY(hspec::launch_attention(a, st, parts));
   return HSPEC_OK;
+}
+
+HSPEC_API hspec_status hspec_paged_attn(const hspec_attn_cfg* cfg, const void* q, const void* k_blk,
+                                        const void* v_blk, const void* k_cache, const void* v_cache,
+                                        const int32_t* page_table, const int32_t* ctx_lens, int max_ctx_len, float* o,
+                                        void* workspace, size_t ws_bytes, void* stream) {
+  return hspec_paged_attn_phase(cfg, q, k_blk, v_blk, k_cache, v_cache, page_table, ctx_lens, max_ctx_len, o,
+                                workspace, ws_bytes, HSPEC_PHASE_WORKLIST | HSPEC_PHASE_SWEEP | HSPEC_PHASE_REDUCE,
+                                stream);
 }
 
 HSPEC_API hspec_status hspec_gather_slots(int B, int max_pages, int page_size, int num_pages,

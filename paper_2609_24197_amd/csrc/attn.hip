@@ -123,7 +123,7 @@ attn_sweep(AttnArgs a) {
   const int g4 = lane >> 4, l16 = lane & 15;
   const int lps = 31 - __builtin_clz(a.ps);
   const int g = a.Hq / a.Hkv, T = a.T, R = T * g;
-  const int n_items = a.status[1];
+  const int n_items = min(a.status[1], a.B * a.max_splits * a.Hkv);   // work-list length, capped at its array
 
   // Persistent workgroups pull (request, split, KV head) items, longest splits first.  The
   // next item is claimed while the last round of the current one is multiplied.
@@ -649,14 +649,16 @@ hipError_t launch_attention_plan(const AttnArgs& a, int clear_words, hipStream_t
   return hipGetLastError();
 }
 
-hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
+hipError_t launch_attention(const AttnArgs& a, hipStream_t s, unsigned parts) {
   const bool lo = a.q_lo != nullptr;
   hipError_t e = hipSuccess;
-  if (a.D == 128) e = lo ? launch_sweep_nw<128, true>(a, s) : launch_sweep_nw<128, false>(a, s);
-  else if (a.D == 64) e = lo ? launch_sweep_nw<64, true>(a, s) : launch_sweep_nw<64, false>(a, s);
-  else return hipErrorInvalidValue;
-  if (e != hipSuccess) return e;
-  if (a.max_splits > 1) {
+  if (parts & ATTN_SWEEP) {
+    if (a.D == 128) e = lo ? launch_sweep_nw<128, true>(a, s) : launch_sweep_nw<128, false>(a, s);
+    else if (a.D == 64) e = lo ? launch_sweep_nw<64, true>(a, s) : launch_sweep_nw<64, false>(a, s);
+    else return hipErrorInvalidValue;
+    if (e != hipSuccess) return e;
+  }
+  if ((parts & ATTN_REDUCE) && a.max_splits > 1) {
     const int R = a.T * (a.Hq / a.Hkv);
     const int cblocks = (R + RED_COLS - 1) / RED_COLS;
     hipLaunchKernelGGL(attn_reduce, dim3(a.B * a.Hkv * cblocks), dim3(256), 0, s, a);

@@ -53,7 +53,8 @@ struct AttnArgs {
 // Work list of the sweep (reads only B, ctx_lens, split and the table sizes of a); clears
 // status[0, clear_words) first.  Must precede launch_attention on the stream.
 hipError_t launch_attention_plan(const AttnArgs& a, int clear_words, hipStream_t s);
-hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
+enum : unsigned { ATTN_SWEEP = 1u, ATTN_REDUCE = 2u };   // parts of launch_attention
+hipError_t launch_attention(const AttnArgs& a, hipStream_t s, unsigned parts = ATTN_SWEEP | ATTN_REDUCE);
 size_t attention_partials_bytes(int B, int Hkv, int max_splits, int R, int D);
 constexpr int kStatusWords = 64;   // int32 words reserved at the start of every workspace
 constexpr int kStatusClear = 4;    // cleared at the start of every call: status bits, work items, queue

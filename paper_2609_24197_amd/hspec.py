@@ -72,6 +72,8 @@ EXPORTS = {
     "hspec_paged_attn": (C.c_int, [C.POINTER(AttnCfg)] + [C.c_void_p] * 7 + [C.c_int, C.c_void_p, C.c_void_p,
                                                                           C.c_size_t, C.c_void_p]),
     "hspec_paged_attn_workspace": (C.c_size_t, [C.POINTER(AttnCfg), C.c_int]),
+    "hspec_paged_attn_phase": (C.c_int, [C.POINTER(AttnCfg)] + [C.c_void_p] * 7 + [C.c_int, C.c_void_p, C.c_void_p,
+                                                                                C.c_size_t, C.c_uint, C.c_void_p]),
     "hspec_gather_slots": (C.c_int, [C.c_int] * 4 + [C.c_void_p, C.c_void_p, C.c_int, C.c_void_p, C.c_void_p,
                                                       C.c_void_p]),
     "hspec_linear": (C.c_int, [C.c_int] * 4 + [C.c_void_p] * 5 + [C.c_size_t, C.c_void_p]),
@@ -252,11 +254,18 @@ def paged_attn_workspace(cfg, max_pages, num_pages, max_ctx_len) -> int:
     return lib().hspec_paged_attn_workspace(C.byref(ac), int(max_ctx_len))
 
 
-def paged_attn(cfg, X, o, ws, max_ctx_len, acfg: AttnCfg | None = None):
+PHASE_WORKLIST, PHASE_SWEEP, PHASE_REDUCE = 1, 2, 4
+
+
+def paged_attn(cfg, X, o, ws, max_ctx_len, acfg: AttnCfg | None = None, phases: int | None = None):
+    """All of the attention core, or (phases: OR of PHASE_*) some of its launches in order."""
     ac = acfg or attn_cfg(cfg, X["page_table"].shape[1], X["k_cache"].shape[0])
-    _check(lib().hspec_paged_attn(C.byref(ac), ptr(X["q"]), ptr(X["k_blk"]), ptr(X["v_blk"]), ptr(X["k_cache"]),
-                                  ptr(X["v_cache"]), ptr(X["page_table"]), ptr(X["ctx_lens"]), int(max_ctx_len),
-                                  ptr(o), ptr(ws), ws.numel(), stream_ptr()))
+    args = (C.byref(ac), ptr(X["q"]), ptr(X["k_blk"]), ptr(X["v_blk"]), ptr(X["k_cache"]), ptr(X["v_cache"]),
+            ptr(X["page_table"]), ptr(X["ctx_lens"]), int(max_ctx_len), ptr(o), ptr(ws), ws.numel())
+    if phases is None:
+        _check(lib().hspec_paged_attn(*args, stream_ptr()))
+    else:
+        _check(lib().hspec_paged_attn_phase(*args, int(phases), stream_ptr()))
 
 
 def gather_slots(page_table, ctx_lens, page_size, num_pages, max_ctx_len, slots, status=None):

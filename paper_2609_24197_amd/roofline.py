@@ -16,10 +16,11 @@ def kv_bytes_per_token(Hkv: int, D: int, elem_bytes: int) -> int:
 
 
 def sweep_bytes(cfg, ctx_lens, elem_bytes: int = 2) -> int:
-    """Target-KV attention sweep plus its split reduction, one launch pair.
+    """Algorithmic bytes of the target-KV attention (sweep and split reduction together).
 
     Per context token: K and V rows of every KV head.  Per block position:
-    its query heads, the block K/V, and the fp32 output row.
+    its query heads, the block K/V, and the fp32 output row.  Split partials are not
+    algorithmic bytes.
     """
     ctx = int(sum(int(L) for L in ctx_lens))
     per_tok = kv_bytes_per_token(cfg.Hkv, cfg.D, elem_bytes)

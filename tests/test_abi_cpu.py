@@ -101,6 +101,18 @@ def test_attention_validation():
     assert L.hspec_paged_attn(C.byref(c), FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, 8192, FAKE, ws, n, None) == 1
 
 
+def test_paged_attn_phase_validation():
+    L = _lib()
+    ws, n = _ws_big()
+    c = _attn_cfg()
+    def call(phases, c=c):
+        return L.hspec_paged_attn_phase(C.byref(c), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 8192, FAKE, ws, n,
+                                        phases, None)
+    assert call(8) == 4 and "phase" in hspec.lib().hspec_last_error().decode()
+    assert call(0x100 | hspec.PHASE_SWEEP) == 4
+    assert call(hspec.PHASE_SWEEP, _attn_cfg(Hkv=5)) == 2   # the config is checked for every phase
+
+
 def test_draft_step_validation():
     L = _lib()
     ws, n = _ws_big()

@@ -130,6 +130,21 @@ def test_paged_attn_split_invariance():
         assert_close(o, base, f"split {s} vs whole context", max_abs=2e-3, rel_l2=3e-3)
 
 
+def test_paged_attn_phases_bitwise():
+    """The work list, sweep and reduction launched one call each give the one-call result."""
+    cfg = _small_attn_cfg(B=3, lengths="list:1000,37,450").replace(split_tokens=256)
+    x = I.make_attn_inputs(cfg, seed=6)
+    whole, _ = _run_attn(cfg, x, split=256)
+    d = dev(x)
+    maxL = int(max(x["ctx_lens"]))
+    ws = hspec.workspace(hspec.paged_attn_workspace(cfg, x["page_table"].shape[1], x["num_pages"], maxL))
+    o = empty((cfg.B, cfg.k, cfg.Hq, cfg.D))
+    for ph in (hspec.PHASE_WORKLIST, hspec.PHASE_SWEEP, hspec.PHASE_REDUCE):
+        hspec.paged_attn(cfg, d, o, ws, maxL, phases=ph)
+    assert hspec.read_status(ws) == 0
+    assert np.array_equal(host(o), whole)
+
+
 def test_paged_attn_page_permutation_bitwise():
     cfg = _small_attn_cfg()
     x = I.make_attn_inputs(cfg, seed=4, extra_pages=4)
