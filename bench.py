@@ -9,7 +9,9 @@ over the paged target cache plus the block.  Inputs are synthetic, seeded, and r
 HBM before timing starts.  Prints one JSON line with the drafted-tokens/s throughput, the
 roofline of the dominant kernel (the state projection, which streams W_dS), the roofline of
 the target-KV sweep, and the float64 CPU oracle timed on a bounded sample of the same
-workload on this host.
+workload on this host.  Each kernel of a roofline figure is timed with HIP events around its
+own launches, each launch right after one drafting step, so that it runs at the clock and
+cache state it has inside the step.
 """
 from __future__ import annotations
 
@@ -55,33 +57,48 @@ def traffic_for(name: str, src_hash: str):
     return e.get("bytes_per_launch")
 
 
-def time_launches(fn, n: int, torch) -> float:
-    """Average duration (s) of n back-to-back launches, HIP events on the launch stream."""
-    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    fn()
-    torch.cuda.synchronize()
-    s.record()
-    for _ in range(n):
-        fn()
-    e.record()
-    e.synchronize()
-    return s.elapsed_time(e) / 1e3 / n
-
-
-def time_sweep_kernel(cfg, Ad, o, aws, maxL, n: int, torch) -> float:
-    """Average duration (s) of the KV-sweep kernel alone: each attention runs its work list,
-    sweep and split reduction as separate launches, with HIP events around the sweep."""
+def time_in_step(fn, n: int, warmup: int, context, torch) -> float:
+    """Average duration (s) of fn's launches, each preceded by `context()` (one drafting step),
+    HIP events on the launch stream around fn: the kernels are timed at the clock and cache
+    state they see inside a step."""
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
-    hspec.paged_attn(cfg, Ad, o, aws, maxL)
-    torch.cuda.synchronize()
-    for s, e in ev:
-        hspec.paged_attn(cfg, Ad, o, aws, maxL, phases=hspec.PHASE_WORKLIST)
+    for i in range(warmup + n):
+        context()
+        if i < warmup:
+            fn()
+            continue
+        s, e = ev[i - warmup]
         s.record()
-        hspec.paged_attn(cfg, Ad, o, aws, maxL, phases=hspec.PHASE_SWEEP)
+        fn()
         e.record()
-        hspec.paged_attn(cfg, Ad, o, aws, maxL, phases=hspec.PHASE_REDUCE)
     torch.cuda.synchronize()
     return sum(s.elapsed_time(e) for s, e in ev) / 1e3 / n
+
+
+def time_attention(cfg, Ad, o, aws, maxL, n: int, warmup: int, context, torch):
+    """Average durations (s) of the KV-sweep kernel and of the whole attention core (work list,
+    sweep, split reduction), each attention call preceded by `context()`, one drafting step,
+    so that the sweep is timed at the clock and cache state it sees inside a step (the same
+    kernel runs measurably slower back to back, or right after a long weight stream).  HIP
+    events on the launch stream bracket the sweep launch, and separately the whole core."""
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(n)]
+    for i in range(warmup + n):
+        context()
+        if i < warmup:
+            hspec.paged_attn(cfg, Ad, o, aws, maxL)
+            continue
+        e = ev[i - warmup]
+        e[0].record()
+        hspec.paged_attn(cfg, Ad, o, aws, maxL, phases=hspec.PHASE_WORKLIST)
+        e[1].record()
+        hspec.paged_attn(cfg, Ad, o, aws, maxL, phases=hspec.PHASE_SWEEP)
+        e[2].record()
+        hspec.paged_attn(cfg, Ad, o, aws, maxL, phases=hspec.PHASE_REDUCE)
+        e[3].record()
+    torch.cuda.synchronize()
+    t_sweep = sum(e[1].elapsed_time(e[2]) for e in ev) / 1e3 / n
+    t_core = sum(e[0].elapsed_time(e[3]) for e in ev) / 1e3 / n
+    return t_sweep, t_core
 
 
 def cpu_baseline(cfg, W, x, n_req: int):
@@ -205,16 +222,16 @@ def main():
     # dominant kernel: the state projection (Proj_r then Proj_dS), timed as its own launches
     sws = hspec.workspace(hspec.state_init_workspace(cfg))
     S0 = torch.empty((cfg.B, cfg.H, cfg.P, cfg.N), dtype=torch.float32, device="cuda")
-    t_state = time_launches(lambda: hspec.state_init(cfg, Wd, Xd["h_last"], S0, sws), args.steps, torch)
+    state = lambda: hspec.state_init(cfg, Wd, Xd["h_last"], S0, sws)  # noqa: E731
+    t_state = time_in_step(state, args.steps, args.warmup, step, torch)
     b_state = RL.state_proj_bytes(cfg, 2, 4) + cfg.rank * cfg.d_h * 2
-    del S0, sws
 
     # the target-KV sweep (the spec bar), same cache, table and lengths: the sweep kernel
     # alone, and the whole attention core (work list + sweep + split reduction)
     Ad, aws, o = sweep_inputs(cfg, Xd, x, args.seed, torch)
-    t_sweep = time_sweep_kernel(cfg, Ad, o, aws, maxL, args.steps, torch)
-    t_core = time_launches(lambda: hspec.paged_attn(cfg, Ad, o, aws, maxL), args.steps, torch)
+    t_sweep, t_core = time_attention(cfg, Ad, o, aws, maxL, args.steps, args.warmup, step, torch)
     b_sweep = RL.sweep_bytes(cfg, L)
+    del S0, sws
     log(f"state projection: {t_state * 1e6:.1f} us, {b_state / t_state / 1e9:.0f} GB/s; "
         f"KV sweep kernel: {t_sweep * 1e6:.1f} us, {b_sweep / t_sweep / 1e9:.0f} GB/s; "
         f"with work list and split reduction: {t_core * 1e6:.1f} us, {b_sweep / t_core / 1e9:.0f} GB/s")
