@@ -247,7 +247,7 @@ void plan_mamba(Arena& ar, const hspec_mamba_cfg& c, bool u_norm, MambaPlan& p) 
   p.wout = reserve_split(ar, c.dtype, (size_t)c.d_model * di);
   p.zx = ar.take<float>(M * dproj);
   p.x_hi = ar.take<bf16>(M * di);
-  if (is_f32(c.dtype)) p.x_lo = ar.take<bf16>(M * di);
+  p.x_lo = ar.take<bf16>(M * di);   // x feeds the state update: kept as hi/lo planes
   p.B_hi = ar.take<bf16>(M * gn);
   p.B_lo = ar.take<bf16>(M * gn);
   p.C_hi = ar.take<bf16>(M * gn);

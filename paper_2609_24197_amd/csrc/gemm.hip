@@ -22,6 +22,7 @@
 // HBM efficiency; the packed layout (launch_pack_w) stores every 16x32 operand fragment as
 // one contiguous 1 KB block, k-step-major, so that the whole grid sweeps W in address order
 // with non-temporal loads.
+#include <algorithm>
 #include <utility>
 
 #include "common.h"
@@ -547,23 +548,40 @@ hipError_t launch_skinny_a(const GemmArgs& g, const SkPlan& p, hipStream_t s) {
 // ------------------------------------------------------------- pipelined dense path
 //
 // Many rows (M >= 128): 128 x 128 output tiles, 4 waves of 64 x 64 (v_mfma_f32_32x32x16_bf16).
-// A and W k-tiles (64 wide) go straight from global memory into LDS (global_load_lds_dwordx4),
-// ST stages deep, so ST-1 tiles are in flight while one is multiplied; every LDS stage is its
-// own object so that the compiler's wait for outstanding LDS DMA names only the stage being
-// read.  Rows past M or N re-read the last valid row (their results are never stored); K must
-// be a multiple of 64.
+// A and W k-tiles (KT = 64 or 32 wide) go straight from global memory into LDS
+// (global_load_lds_dwordx4), ST stages deep, so ST-1 tiles are in flight while one is
+// multiplied; every LDS stage is its own object so that the compiler's wait for outstanding
+// LDS DMA names only the stage being read.  Rows past M or N re-read the last valid row (their
+// results are never stored); K must be a multiple of KT.  With KT = 32 a workgroup needs at
+// most 72 KB of LDS, so two share a CU and each covers the other's waits for memory.
 
-template <int TM, int TN, bool ALO, int ST>
+template <int TM, int TN, bool ALO, int ST, int KT>
 struct DmaCfg {
   static constexpr int NT = 256;
   static constexpr int BM = 2 * TM * 32, BN = 2 * TN * 32;
-  static constexpr int SA = BM * BK, SW = BN * BK;                  // elements per plane per stage
+  static constexpr int CPRT = KT / 8;                               // 16-byte units per tile row
+  static constexpr int SA = BM * KT, SW = BN * KT;                  // elements per plane per stage
   static constexpr int STAGE = SA * (ALO ? 2 : 1) + SW;
-  static constexpr int A_I = BM * CPR / NT, W_I = BN * CPR / NT;   // DMA instructions per wave
+  static constexpr int A_I = BM * CPRT / NT, W_I = BN * CPRT / NT; // DMA instructions per wave
   static constexpr int NI = A_I * (ALO ? 2 : 1) + W_I;
   static constexpr int VM = (ST - 2) * NI;
-  static_assert(BM * CPR % NT == 0 && BN * CPR % NT == 0 && VM < 64 && ST >= 2 && ST <= 4, "dma gemm shape");
+  static_assert(KT == 64 || KT == 32, "k-tile");
+  static_assert(BM * CPRT % NT == 0 && BN * CPRT % NT == 0 && VM < 64 && ST >= 2 && ST <= 4, "dma gemm shape");
 };
+
+// LDS unit (16 bytes) of logical chunk `chunk` of tile row `row` in a KT-wide tile.  Rows of
+// 128 bytes (KT = 64) XOR the chunk with (row / 2) mod 8, rows of 64 bytes (KT = 32) with
+// (row / 4) mod 4: either way the 16 rows read by each 16-lane group of a fragment load fall
+// on 16 distinct 16-byte bank groups.
+template <int KT>
+__device__ __forceinline__ int swz_key_t(int row) {
+  if constexpr (KT == 64) return (row >> 1) & 7;
+  else return (row >> 2) & 3;
+}
+template <int KT>
+__device__ __forceinline__ int swz_t(int row, int chunk) {
+  return row * (KT / 8) + (chunk ^ swz_key_t<KT>(row));
+}
 
 __device__ __forceinline__ void dma16(const bf16* src, bf16* lds) {
   __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
@@ -592,9 +610,9 @@ __device__ __forceinline__ void store_block32(const GemmArgs& g, const f32x16& a
   }
 }
 
-template <int TM, int TN, bool ALO, int ST>
+template <int TM, int TN, bool ALO, int ST, int KT>
 __global__ void __launch_bounds__(256) gemm_dma_kernel(GemmArgs g) {
-  using C = DmaCfg<TM, TN, ALO, ST>;
+  using C = DmaCfg<TM, TN, ALO, ST, KT>;
   // one LDS object per (stage, operand): the A planes and the W tile of stage s
   constexpr int PA = C::SA * (ALO ? 2 : 1);
   __shared__ __align__(16) bf16 A0s[PA], W0s[C::SW];
@@ -636,25 +654,27 @@ __global__ void __launch_bounds__(256) gemm_dma_kernel(GemmArgs g) {
   }
   const int rows_w = min(C::BN, wseg1 - n0);
 
-  // unit u (16 bytes) of a stage plane: row u / 8, stored chunk u % 8 = logical chunk ^ swz_key(row).
-  // Source offsets of k-tile 0 per lane; k-tile t adds t * (a_step, w_step) elements.
+  // unit u (16 bytes) of a stage plane: row u / CPRT, stored chunk u % CPRT = logical chunk ^
+  // swz_key_t(row).  Source offsets of k-tile 0 per lane; k-tile t adds t * (a_step, w_step).
   size_t a_off[C::A_I], w_off[C::W_I];
 #pragma unroll
   for (int i = 0; i < C::A_I; ++i) {
-    const int u = (i * 4 + wave) * 64 + lane, row = u >> 3, k = 8 * ((u & 7) ^ swz_key(row));
+    const int u = (i * 4 + wave) * 64 + lane, row = u / C::CPRT;
+    const int k = 8 * ((u % C::CPRT) ^ swz_key_t<KT>(row));
     a_off[i] = (size_t)min(row, rows_a - 1) * g.lda + k;
   }
 #pragma unroll
   for (int i = 0; i < C::W_I; ++i) {
-    const int u = (i * 4 + wave) * 64 + lane, row = u >> 3, k = 8 * ((u & 7) ^ swz_key(row));
+    const int u = (i * 4 + wave) * 64 + lane, row = u / C::CPRT;
+    const int k = 8 * ((u % C::CPRT) ^ swz_key_t<KT>(row));
     const int n = n0 + min(row, rows_w - 1);
     // packed W: 1 KB fragment (k-step k / 32, 16-row tile n / 16), piece (n % 16) + 16 (k % 32) / 8
     w_off[i] = g.w_packed ? ((((size_t)(k >> 5) * (g.N >> 4) + (n >> 4)) * 64 + (n & 15) + 16 * ((k & 31) >> 3)) * 8)
                           : (size_t)(n - wseg0) * g.ldw + k;
   }
-  const size_t w_step = g.w_packed ? (size_t)2 * (g.N >> 4) * 512 : (size_t)BK;
+  const size_t w_step = g.w_packed ? (size_t)(KT / 32) * (g.N >> 4) * 512 : (size_t)KT;
   auto issue = [&](int t, bf16* L, bf16* LW) {
-    const size_t ka = (size_t)t * BK, kw = (size_t)t * w_step;
+    const size_t ka = (size_t)t * KT, kw = (size_t)t * w_step;
 #pragma unroll
     for (int i = 0; i < C::A_I; ++i) {
       const int u0 = (i * 4 + wave) * 64;
@@ -684,19 +704,19 @@ __global__ void __launch_bounds__(256) gemm_dma_kernel(GemmArgs g) {
 #pragma unroll
       for (int a = 0; a < TM; ++a) {
         const int r = (wm * TM + a) * 32 + (lane & 31);
-        fa[buf][a] = *reinterpret_cast<const bf16x8*>(sA + 8 * swz(r, ch));
-        if constexpr (ALO) fal[buf][a] = *reinterpret_cast<const bf16x8*>(sAl + 8 * swz(r, ch));
+        fa[buf][a] = *reinterpret_cast<const bf16x8*>(sA + 8 * swz_t<KT>(r, ch));
+        if constexpr (ALO) fal[buf][a] = *reinterpret_cast<const bf16x8*>(sAl + 8 * swz_t<KT>(r, ch));
       }
 #pragma unroll
       for (int b = 0; b < TN; ++b) {
         const int r = (wn * TN + b) * 32 + (lane & 31);
-        fw[buf][b] = *reinterpret_cast<const bf16x8*>(sW + 8 * swz(r, ch));
+        fw[buf][b] = *reinterpret_cast<const bf16x8*>(sW + 8 * swz_t<KT>(r, ch));
       }
     };
     frags(0, 0);
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      if (ks + 1 < BK / 16) frags(ks + 1, (ks + 1) & 1);
+    for (int ks = 0; ks < KT / 16; ++ks) {
+      if (ks + 1 < KT / 16) frags(ks + 1, (ks + 1) & 1);
       __builtin_amdgcn_sched_barrier(0);   // the next k-step's LDS reads go out before these MFMAs
       const int cb = ks & 1;
 #pragma unroll
@@ -709,7 +729,7 @@ __global__ void __launch_bounds__(256) gemm_dma_kernel(GemmArgs g) {
     }
   };
 
-  const int nk = (g.K + BK - 1) / BK;
+  const int nk = (g.K + KT - 1) / KT;
   // prologue without branches (tiles past the end re-read the last one into unused stages),
   // so that the compiler's record of which stage each pending DMA fills stays exact
   [&]<int... I>(std::integer_sequence<int, I...>) {
@@ -750,11 +770,350 @@ __global__ void __launch_bounds__(256) gemm_dma_kernel(GemmArgs g) {
       store_block32(g, acc[a][b], m0 + (wm * TM + a) * 32, n0 + (wn * TN + b) * 32, lane);
 }
 
-template <int TM, int TN, bool ALO, int ST>
+template <int TM, int TN, bool ALO, int ST, int KT>
 hipError_t launch_dma(const GemmArgs& g, hipStream_t s) {
-  using C = DmaCfg<TM, TN, ALO, ST>;
+  using C = DmaCfg<TM, TN, ALO, ST, KT>;
   const int tiles = ((g.M + C::BM - 1) / C::BM) * ((g.N + C::BN - 1) / C::BN);
-  hipLaunchKernelGGL((gemm_dma_kernel<TM, TN, ALO, ST>), dim3(tiles), dim3(C::NT), 0, s, g);
+  hipLaunchKernelGGL((gemm_dma_kernel<TM, TN, ALO, ST, KT>), dim3(tiles), dim3(C::NT), 0, s, g);
+  return hipGetLastError();
+}
+
+#ifndef HSPEC_DMA_KT
+#define HSPEC_DMA_KT 32
+#endif
+// The dense products of the step (M = B k rows): 128 x 128 tiles, KT-wide k-tiles.
+hipError_t launch_dense(const GemmArgs& g, hipStream_t s) {
+  if constexpr (HSPEC_DMA_KT == 32)
+    return g.A_lo ? launch_dma<2, 2, true, 3, 32>(g, s) : launch_dma<2, 2, false, 4, 32>(g, s);
+  else
+    return g.A_lo ? launch_dma<2, 2, true, 3, 64>(g, s) : launch_dma<2, 2, false, 4, 64>(g, s);
+}
+
+// ---------------------------------------------------------------------------------------
+// Large products (M >= 512, the block positions of many requests): 256 x 256 output tiles,
+// eight waves of 128 x 64 each (4 x 2 blocks of 32 x 32).  A wave reads 0.75 KB of LDS
+// fragments per v_mfma_f32_32x32x16_bf16 (0.625 KB with an A lo plane), so the fragment reads
+// of two waves per SIMD stay below the CU's LDS bandwidth at the full MFMA rate; with 64 x 64
+// per wave they would need all of it.  32-wide k-tiles come into LDS by DMA, 3 stages deep.
+// With few tiles (tiles mod CUs small) the last tiles are split over K: unit u < full is
+// whole tile u, the others are (tile, k-part) pairs whose fp32 partials a fix-up kernel sums
+// in k-part order, so the result does not depend on scheduling.
+constexpr int GB_BM = 256, GB_BN = 256, GB_KT = 32, GB_NT = 512, GB_ST = 3;
+
+template <bool ALO>
+struct BigCfg {
+  static constexpr int CPRT = GB_KT / 8;                           // 16-byte units per tile row
+  static constexpr int SA = GB_BM * GB_KT, SW = GB_BN * GB_KT;     // elements per plane per stage
+  static constexpr int A_I = GB_BM * CPRT / GB_NT, W_I = GB_BN * CPRT / GB_NT;   // DMA per wave
+  static constexpr int NI = A_I * (ALO ? 2 : 1) + W_I;
+  static constexpr int VM = (GB_ST - 2) * NI;
+  static_assert(GB_BM * CPRT % GB_NT == 0 && GB_BN * CPRT % GB_NT == 0 && VM < 64, "big gemm shape");
+};
+
+// Work division of a large product (host-computed, passed to the kernels).
+struct BigPlan {
+  int mt = 0, nt = 0;       // tile grid
+  int full = 0;             // units [0, full): whole tiles (virtual ids)
+  int splits = 1, kper = 0; // remaining tiles: `splits` k-parts of kper k-tiles
+  int units = 0;
+};
+
+template <bool ALO>
+__global__ void __launch_bounds__(GB_NT) gemm_big_kernel(GemmArgs g, BigPlan p) {
+  using C = BigCfg<ALO>;
+  constexpr int PA = C::SA * (ALO ? 2 : 1);
+  __shared__ __align__(16) bf16 A0s[PA], W0s[C::SW];
+  __shared__ __align__(16) bf16 A1s[PA], W1s[C::SW];
+  __shared__ __align__(16) bf16 A2s[PA], W2s[C::SW];
+  auto sa_of = [&](auto I) -> bf16* {
+    if constexpr (decltype(I)::value == 0) return A0s;
+    else if constexpr (decltype(I)::value == 1) return A1s;
+    else return A2s;
+  };
+  auto sw_of = [&](auto I) -> bf16* {
+    if constexpr (decltype(I)::value == 0) return W0s;
+    else if constexpr (decltype(I)::value == 1) return W1s;
+    else return W2s;
+  };
+  constexpr int TM = 4, TN = 2;
+
+  // unit -> (tile, k-tile range)
+  const int nk_all = g.K / GB_KT;
+  int v, kb, ke;
+  const int u = blockIdx.x;
+  if (u < p.full) {
+    int mt_, nt_;
+    tile_of(u, p.full, p.mt, mt_, nt_);
+    v = nt_ * p.mt + mt_;
+    kb = 0;
+    ke = nk_all;
+  } else {
+    const int r = u - p.full;
+    v = p.full + r / p.splits;
+    kb = (r % p.splits) * p.kper;
+    ke = min(nk_all, kb + p.kper);
+  }
+  const int mt = v % p.mt, nt = v / p.mt;
+  const int m0 = mt * GB_BM, n0 = nt * GB_BN;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / 4, wn = wave % 4;
+
+  const int rows_a = min(GB_BM, g.M - m0);
+  const bf16* A0 = g.A_hi + (size_t)m0 * g.lda;
+  const bf16* Al0 = (ALO ? g.A_lo : g.A_hi) + (size_t)m0 * g.lda;
+  const bf16* wbase = g.W_hi;   // W row segment of this tile (tiles never straddle one)
+  int wseg0 = 0, wseg1 = g.N;
+  if (g.W2) {
+    if (n0 >= g.N1 + g.N2) { wbase = g.W3; wseg0 = g.N1 + g.N2; }
+    else if (n0 >= g.N1) { wbase = g.W2; wseg0 = g.N1; wseg1 = g.N1 + g.N2; }
+    else wseg1 = g.N1;
+  }
+  const int rows_w = min(GB_BN, wseg1 - n0);
+
+  // unit q (16 bytes) of a stage plane: row q / 4, stored chunk q % 4 = logical chunk ^ key(row).
+  // Element offsets (32-bit: host-checked) from the tile's first row, at k-tile kb.
+  const bf16* Ab = A0 + (size_t)kb * GB_KT;
+  const bf16* Alb = Al0 + (size_t)kb * GB_KT;
+  const bf16* Wb = wbase + (size_t)(n0 - wseg0) * g.ldw + (size_t)kb * GB_KT;
+  int a_off[C::A_I], w_off[C::W_I];
+#pragma unroll
+  for (int i = 0; i < C::A_I; ++i) {
+    const int q = (i * 8 + wave) * 64 + lane, row = q / C::CPRT;
+    a_off[i] = min(row, rows_a - 1) * g.lda + 8 * ((q % C::CPRT) ^ swz_key_t<GB_KT>(row));
+  }
+#pragma unroll
+  for (int i = 0; i < C::W_I; ++i) {
+    const int q = (i * 8 + wave) * 64 + lane, row = q / C::CPRT;
+    w_off[i] = min(row, rows_w - 1) * g.ldw + 8 * ((q % C::CPRT) ^ swz_key_t<GB_KT>(row));
+  }
+  auto issue = [&](int t, bf16* L, bf16* LW) {
+    const int k = t * GB_KT;
+#pragma unroll
+    for (int i = 0; i < C::A_I; ++i) {
+      const int q0 = (i * 8 + wave) * 64;
+      dma16(Ab + (a_off[i] + k), L + q0 * 8);
+      if constexpr (ALO) dma16(Alb + (a_off[i] + k), L + C::SA + q0 * 8);
+    }
+#pragma unroll
+    for (int i = 0; i < C::W_I; ++i) dma16(Wb + (w_off[i] + k), LW + (i * 8 + wave) * 64 * 8);
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int b = 0; b < TN; ++b)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[a][b][i] = 0.f;
+
+  // fragments of k-step ks + 1 are read while the MFMAs of k-step ks run
+  auto compute = [&](const bf16* L, const bf16* LW) {
+    const bf16* sA = L;
+    const bf16* sAl = L + C::SA;
+    bf16x8 fa[2][TM], fal[2][ALO ? TM : 1], fw[2][TN];
+    auto frags = [&](int ks, int buf) {
+      const int ch = 2 * ks + (lane >> 5);
+#pragma unroll
+      for (int a = 0; a < TM; ++a) {
+        const int r = (wm * TM + a) * 32 + (lane & 31);
+        fa[buf][a] = *reinterpret_cast<const bf16x8*>(sA + 8 * swz_t<GB_KT>(r, ch));
+        if constexpr (ALO) fal[buf][a] = *reinterpret_cast<const bf16x8*>(sAl + 8 * swz_t<GB_KT>(r, ch));
+      }
+#pragma unroll
+      for (int b = 0; b < TN; ++b) {
+        const int r = (wn * TN + b) * 32 + (lane & 31);
+        fw[buf][b] = *reinterpret_cast<const bf16x8*>(LW + 8 * swz_t<GB_KT>(r, ch));
+      }
+    };
+    frags(0, 0);
+#pragma unroll
+    for (int ks = 0; ks < GB_KT / 16; ++ks) {
+      if (ks + 1 < GB_KT / 16) frags(ks + 1, (ks + 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);
+      const int cb = ks & 1;
+#pragma unroll
+      for (int a = 0; a < TM; ++a)
+#pragma unroll
+        for (int b = 0; b < TN; ++b) {
+          acc[a][b] = mma32(fa[cb][a], fw[cb][b], acc[a][b]);
+          if constexpr (ALO) acc[a][b] = mma32(fal[cb][a], fw[cb][b], acc[a][b]);
+        }
+    }
+  };
+
+  const int nk = ke - kb;
+  [&]<int... I>(std::integer_sequence<int, I...>) {
+    (issue(min(I, nk - 1), sa_of(Int<I>{}), sw_of(Int<I>{})), ...);
+  }(std::make_integer_sequence<int, GB_ST - 1>{});
+  auto steady = [&](int t, auto S) {
+    wait_vm_lgkm0<C::VM>();
+    wg_barrier();
+    constexpr int N = (decltype(S)::value + GB_ST - 1) % GB_ST;
+    issue(t + GB_ST - 1, sa_of(Int<N>{}), sw_of(Int<N>{}));
+    compute(sa_of(S), sw_of(S));
+  };
+  auto step = [&](int t, auto S) {
+    if (t + GB_ST - 2 < nk) wait_vm_lgkm0<C::VM>();
+    else wait_vm_lgkm0<0>();
+    wg_barrier();
+    constexpr int N = (decltype(S)::value + GB_ST - 1) % GB_ST;
+    if (t + GB_ST - 1 < nk) issue(t + GB_ST - 1, sa_of(Int<N>{}), sw_of(Int<N>{}));
+    compute(sa_of(S), sw_of(S));
+  };
+  int t0 = 0;
+  for (; t0 + 2 * GB_ST - 2 < nk; t0 += GB_ST) {
+    [&]<int... I>(std::integer_sequence<int, I...>) {
+      (steady(t0 + I, Int<I>{}), ...);
+    }(std::make_integer_sequence<int, GB_ST>{});
+  }
+  for (; t0 < nk; t0 += GB_ST) {
+    [&]<int... I>(std::integer_sequence<int, I...>) {
+      ((t0 + I < nk ? step(t0 + I, Int<I>{}) : void()), ...);
+    }(std::make_integer_sequence<int, GB_ST>{});
+  }
+
+  if (u < p.full) {
+#pragma unroll
+    for (int a = 0; a < TM; ++a)
+#pragma unroll
+      for (int b = 0; b < TN; ++b)
+        store_block32(g, acc[a][b], m0 + (wm * TM + a) * 32, n0 + (wn * TN + b) * 32, lane);
+  } else {
+    // partial of k-part r % splits: [unit][256][256] fp32; lane holds rows 8(i/4)+4(l/32)+i%4
+    float* part = g.part + (size_t)(u - p.full) * GB_BM * GB_BN;
+#pragma unroll
+    for (int a = 0; a < TM; ++a)
+#pragma unroll
+      for (int b = 0; b < TN; ++b)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int r = (wm * TM + a) * 32 + 8 * (i / 4) + 4 * (lane >> 5) + (i % 4);
+          part[r * GB_BN + (wn * TN + b) * 32 + (lane & 31)] = acc[a][b][i];
+        }
+  }
+}
+
+// Sum of the k-parts of the split tiles in k-part order, then the usual epilogue.  One thread
+// per 4 consecutive columns: 16-byte loads of the parts, 8 at a time, then of the residual;
+// 16-byte stores.  VEC needs N, ldc, ldr and ldch % 4 == 0.
+template <bool VEC>
+__global__ void __launch_bounds__(256) gemm_big_fixup(GemmArgs g, BigPlan p) {
+  constexpr int GROUP = 8;   // k-parts whose loads are issued together
+  const int tiles = p.mt * p.nt - p.full;
+  const size_t per = (size_t)GB_BM * GB_BN;
+  const size_t quads = (size_t)tiles * per / 4;
+  for (size_t q = (size_t)blockIdx.x * 256 + threadIdx.x; q < quads; q += (size_t)gridDim.x * 256) {
+    const int tl = (int)(q / (per / 4));
+    const int rc = (int)(q % (per / 4)) * 4;
+    const int v = p.full + tl;
+    const int m = (v % p.mt) * GB_BM + rc / GB_BN, n0 = (v / p.mt) * GB_BN + rc % GB_BN;
+    if (m >= g.M || n0 >= g.N) continue;
+    const float* src = g.part + (size_t)tl * p.splits * per + rc;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < p.splits; k0 += GROUP) {
+      f32x4 part[GROUP];
+#pragma unroll
+      for (int k = 0; k < GROUP; ++k)
+        part[k] = k0 + k < p.splits ? *reinterpret_cast<const f32x4*>(src + (size_t)(k0 + k) * per)
+                                    : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int k = 0; k < GROUP; ++k) acc += part[k];   // absent parts add +0
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int n = n0 + e;
+      if constexpr (!VEC) {
+        if (n >= g.N) break;
+        float s = acc[e];
+        if (g.R) {
+          s += g.r_bf16 ? bf2f(reinterpret_cast<const bf16*>(g.R)[(size_t)m * g.ldr + n])
+                        : reinterpret_cast<const float*>(g.R)[(size_t)m * g.ldr + n];
+        }
+        if (g.C) g.C[(size_t)m * g.ldc + n] = s;
+        if (g.C_hi) {
+          const bf16 h = f2bf(s);
+          g.C_hi[(size_t)m * g.ldch + n] = h;
+          if (g.C_lo) g.C_lo[(size_t)m * g.ldch + n] = f2bf(s - bf2f(h));
+        }
+      }
+    }
+    if constexpr (VEC) {
+      if (g.R) {
+        if (g.r_bf16) {
+          const bf16x4 r = *reinterpret_cast<const bf16x4*>(reinterpret_cast<const bf16*>(g.R) + (size_t)m * g.ldr + n0);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[e] += bf2f(r[e]);
+        } else {
+          acc += *reinterpret_cast<const f32x4*>(reinterpret_cast<const float*>(g.R) + (size_t)m * g.ldr + n0);
+        }
+      }
+      if (g.C) *reinterpret_cast<f32x4*>(g.C + (size_t)m * g.ldc + n0) = acc;
+      if (g.C_hi) {
+        bf16x4 h, l;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          h[e] = f2bf(acc[e]);
+          l[e] = f2bf(acc[e] - bf2f(h[e]));
+        }
+        *reinterpret_cast<bf16x4*>(g.C_hi + (size_t)m * g.ldch + n0) = h;
+        if (g.C_lo) *reinterpret_cast<bf16x4*>(g.C_lo + (size_t)m * g.ldch + n0) = l;
+      }
+    }
+  }
+}
+
+// Whether the 256 x 256 path serves a product, and its work division for `cus` CUs: whole
+// tiles for every full round, the tiles of a short last round split over K so that the round
+// fills the chip (at least 4 k-tiles per part).
+bool big_ok(const GemmArgs& g) {
+  if (g.M < 512 || g.W_lo || g.w_packed || g.K % GB_KT) return false;
+  // 32-bit element offsets inside a tile's rows of A and W
+  if ((long long)GB_BM * g.lda >= (1ll << 31) || (long long)GB_BN * g.ldw >= (1ll << 31)) return false;
+  if (g.W2 && (g.N1 % GB_BN || g.N2 % GB_BN)) return false;
+  return true;
+}
+BigPlan big_plan(int M, int N, int K, int cus) {
+  BigPlan p;
+  p.mt = (M + GB_BM - 1) / GB_BM;
+  p.nt = (N + GB_BN - 1) / GB_BN;
+  const int tiles = p.mt * p.nt, nk = K / GB_KT;
+  const int rem = tiles % cus;
+  int sp = rem ? cus / rem : 1;
+  if (sp > nk / 4) sp = nk / 4;
+  if (sp <= 1) {
+    p.full = tiles;
+    p.kper = nk;
+  } else {
+    p.full = tiles - rem;
+    p.kper = (nk + sp - 1) / sp;
+    p.splits = (nk + p.kper - 1) / p.kper;
+  }
+  p.units = p.full + (tiles - p.full) * p.splits;
+  return p;
+}
+size_t big_scratch_elems(const BigPlan& p) {
+  return (size_t)(p.mt * p.nt - p.full) * p.splits * GB_BM * GB_BN;
+}
+
+hipError_t launch_big(const GemmArgs& g, hipStream_t s) {
+  BigPlan p = big_plan(g.M, g.N, g.K, device_cus());
+  if (p.full < p.mt * p.nt && (!g.part || g.part_cap < big_scratch_elems(p))) {
+    p.full = p.mt * p.nt;   // no room for partials: whole tiles only
+    p.splits = 1;
+    p.kper = g.K / GB_KT;
+    p.units = p.full;
+  }
+  if (g.A_lo) hipLaunchKernelGGL(gemm_big_kernel<true>, dim3(p.units), dim3(GB_NT), 0, s, g, p);
+  else hipLaunchKernelGGL(gemm_big_kernel<false>, dim3(p.units), dim3(GB_NT), 0, s, g, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || p.full == p.mt * p.nt) return e;
+  const size_t quads = big_scratch_elems(p) / p.splits / 4;
+  size_t blocks = (quads + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  const bool vec = g.N % 4 == 0 && (!g.C || g.ldc % 4 == 0) && (!g.R || g.ldr % 4 == 0) && (!g.C_hi || g.ldch % 4 == 0);
+  if (vec) hipLaunchKernelGGL(gemm_big_fixup<true>, dim3((unsigned)blocks), dim3(256), 0, s, g, p);
+  else hipLaunchKernelGGL(gemm_big_fixup<false>, dim3((unsigned)blocks), dim3(256), 0, s, g, p);
   return hipGetLastError();
 }
 
@@ -807,14 +1166,17 @@ size_t gemm_scratch_elems(int M, int N, int K, bool a_lo, bool w_lo) {
   (void)a_lo;
   if (M <= 0 || N <= 0 || K <= 0) return 0;
   const SkPlan p = skinny_plan(M, N, K, w_lo, device_cus());
-  return p.use && p.ksplit > 1 ? (size_t)p.ksplit * M * N : 0;
+  size_t n = p.use && p.ksplit > 1 ? (size_t)p.ksplit * M * N : 0;
+  if (M >= 512 && !w_lo && K % GB_KT == 0) n = std::max(n, big_scratch_elems(big_plan(M, N, K, device_cus())));
+  return n;
 }
 
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
   if (g.W2) {
+    if (big_ok(g)) return launch_big(g, s);
     const bool dma = g.M > 64 && !g.W_lo && !g.w_packed && g.K % BK == 0 && g.N1 % 128 == 0 && g.N2 % 128 == 0;
-    if (dma) return g.A_lo ? launch_dma<2, 2, true, 3>(g, s) : launch_dma<2, 2, false, 4>(g, s);
+    if (dma) return launch_dense(g, s);
     // one launch per segment, each writing its own column range of C
     const bf16* ws[3] = {g.W_hi, g.W2, g.W3};
     const int n0s[3] = {0, g.N1, g.N1 + g.N2}, ns[3] = {g.N1, g.N2, g.N - g.N1 - g.N2};
@@ -842,8 +1204,8 @@ hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
     return g.A_lo ? launch_skinny_a<true>(g, p, s) : launch_skinny_a<false>(g, p, s);
   }
   if (g.M <= 64 && !g.w_packed) return launch_cfg<1, 4, 2, 2>(g, s);      // 64 x 256: weight streaming
-  if (!g.W_lo && g.K % BK == 0)
-    return g.A_lo ? launch_dma<2, 2, true, 3>(g, s) : launch_dma<2, 2, false, 4>(g, s);
+  if (big_ok(g)) return launch_big(g, s);
+  if (!g.W_lo && g.K % BK == 0) return launch_dense(g, s);
   if (g.M <= 128) return launch_cfg<2, 2, 2, 4>(g, s);     // 128 x 256
   return launch_cfg<2, 2, 2, 2>(g, s);                     // 128 x 128: dense
 }

@@ -10,8 +10,8 @@
 // values survive.  The 16x16 decay-weighted mixing matrix and the x tile go through LDS and
 // the intra-chunk product is done in fp32 on the VALU.  The chunk-local cumulative sum of
 // dt*A is a 16-lane shuffle scan.  When the block fits one chunk and no final state is
-// requested, the initial state is read straight from global memory into MFMA fragments;
-// otherwise the fp32 state lives in LDS between chunks.
+// requested (ssd_scan_one), the initial state is read straight from global memory into MFMA
+// fragments; otherwise (ssd_scan_kernel) the fp32 state lives in LDS between chunks.
 #include "common.h"
 #include "kernels.h"
 
@@ -22,12 +22,12 @@ namespace {
 constexpr int P = 64;
 constexpr int QMAX = 16;
 
-template <int N, bool MULTI>
+template <int N>
 struct ScanLds {
   static constexpr int XT = P * (QMAX + 1);          // x^T tile, fp32, padded rows
   static constexpr int MM = QMAX * (QMAX + 1);        // mixing matrix, fp32
-  static constexpr int BT = MULTI ? N * (QMAX + 1) : 0;   // B^T tile, fp32
-  static constexpr int ST = MULTI ? P * (N + 1) : 0;      // state, fp32, padded rows
+  static constexpr int BT = N * (QMAX + 1);           // B^T tile, fp32
+  static constexpr int ST = P * (N + 1);              // state, fp32, padded rows
   static constexpr int BYTES = 4 * (XT + MM + BT + ST);
 };
 
@@ -42,10 +42,10 @@ __device__ __forceinline__ void split8(const float* v, bf16x8& hi, bf16x8& lo) {
   }
 }
 
-template <int N, bool MULTI>
+template <int N>
 __global__ void __launch_bounds__(64) ssd_scan_kernel(ScanArgs a) {
   constexpr int NS = (N + 31) / 32;
-  using LD = ScanLds<N, MULTI>;
+  using LD = ScanLds<N>;
   extern __shared__ __align__(16) float sm[];
   float* xT = sm;                       // [P][QMAX+1]
   float* Mm = xT + LD::XT;              // [QMAX][QMAX+1]
@@ -59,19 +59,17 @@ __global__ void __launch_bounds__(64) ssd_scan_kernel(ScanArgs a) {
   const float Ah = a.A_is_log ? -__expf(a.A[h]) : a.A[h], Dh = a.Dskip[h];
   const size_t s0_off = ((size_t)b * H + h) * P * N;
 
-  if constexpr (MULTI) {
-    for (int p = 0; p < P; ++p) {
-      for (int n = lane; n < N; n += 64) {
-        float v = 0.f;
-        if (a.S0_hi) {
-          v = bf2f(a.S0_hi[s0_off + p * N + n]);
-          if (a.S0_lo) v += bf2f(a.S0_lo[s0_off + p * N + n]);
-        }
-        S[p * (N + 1) + n] = v;
+  for (int p = 0; p < P; ++p) {
+    for (int n = lane; n < N; n += 64) {
+      float v = 0.f;
+      if (a.S0_hi) {
+        v = bf2f(a.S0_hi[s0_off + p * N + n]);
+        if (a.S0_lo) v += bf2f(a.S0_lo[s0_off + p * N + n]);
       }
+      S[p * (N + 1) + n] = v;
     }
-    __syncthreads();
   }
+  __syncthreads();
 
   for (int c0 = 0; c0 < T; c0 += a.chunk) {
     const int Qc = min(a.chunk, T - c0);
@@ -115,22 +113,13 @@ __global__ void __launch_bounds__(64) ssd_scan_kernel(ScanArgs a) {
       for (int ns = 0; ns < NS; ++ns) {
         const int n = 32 * ns + 8 * g4;
         bf16x8 sh, sl;
-        bool has_lo;
-        if constexpr (MULTI) {
-          float v[8];
+        float v[8];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) v[e] = n + e < N ? S[p * (N + 1) + n + e] : 0.f;
-          split8(v, sh, sl);
-          has_lo = true;
-        } else {
-          const bool ok = a.S0_hi != nullptr && n < N;
-          sh = ld8_or0(a.S0_hi + s0_off + (size_t)p * N + n, ok);
-          has_lo = a.S0_lo != nullptr;
-          sl = has_lo ? ld8_or0(a.S0_lo + s0_off + (size_t)p * N + n, ok) : zero8();
-        }
+        for (int e = 0; e < 8; ++e) v[e] = n + e < N ? S[p * (N + 1) + n + e] : 0.f;
+        split8(v, sh, sl);
         ys[pb] = mma16(cf[ns], sh, ys[pb]);
         if (a.C_lo) ys[pb] = mma16(cfl[ns], sh, ys[pb]);
-        if (has_lo) ys[pb] = mma16(cf[ns], sl, ys[pb]);
+        ys[pb] = mma16(cf[ns], sl, ys[pb]);
       }
     }
     // C B^T: lane gets rows t = 4 g4 + i, column s = l16
@@ -151,19 +140,17 @@ __global__ void __launch_bounds__(64) ssd_scan_kernel(ScanArgs a) {
       const bool ok = l16 <= t && t < Qc;
       Mm[t * (QMAX + 1) + l16] = ok ? cb[i] * __expf(ell_t[i] - ell_s) * dt_s : 0.f;
     }
-    if constexpr (MULTI) {
-      // B^T tile for the state update: Bt[n][s]
-      for (int s = 0; s < QMAX; ++s)
-        for (int n = lane; n < N; n += 64) {
-          float v = 0.f;
-          if (s < Qc) {
-            const size_t off = (size_t)(b * T + c0 + s) * a.bc_ld + (size_t)grp * N + n;
-            v = bf2f(a.B_hi[off]);
-            if (a.B_lo) v += bf2f(a.B_lo[off]);
-          }
-          Bt[n * (QMAX + 1) + s] = v;
+    // B^T tile for the state update: Bt[n][s]
+    for (int s = 0; s < QMAX; ++s)
+      for (int n = lane; n < N; n += 64) {
+        float v = 0.f;
+        if (s < Qc) {
+          const size_t off = (size_t)(b * T + c0 + s) * a.bc_ld + (size_t)grp * N + n;
+          v = bf2f(a.B_hi[off]);
+          if (a.B_lo) v += bf2f(a.B_lo[off]);
         }
-    }
+        Bt[n * (QMAX + 1) + s] = v;
+      }
     __syncthreads();
     // y = exp(l_t) (C S^T) + M x + D x
 #pragma unroll
@@ -180,7 +167,7 @@ __global__ void __launch_bounds__(64) ssd_scan_kernel(ScanArgs a) {
         a.y[(size_t)(b * T + c0 + t) * H * P + (size_t)h * P + p] = acc;
       }
     }
-    if constexpr (MULTI) {
+    {
       // S <- exp(l_end) S + sum_s exp(l_end - l_s) dt_s x_s (outer) B_s ; lane = row p
       const float ell_end = __shfl(cum, Qc - 1);
       const float dec = __expf(ell_end);
@@ -203,9 +190,120 @@ __global__ void __launch_bounds__(64) ssd_scan_kernel(ScanArgs a) {
   }
 
   if (a.S_final) {
-    if constexpr (MULTI) {
-      for (int p = 0; p < P; ++p)
-        for (int n = lane; n < N; n += 64) a.S_final[s0_off + p * N + n] = S[p * (N + 1) + n];
+    for (int p = 0; p < P; ++p)
+      for (int n = lane; n < N; n += 64) a.S_final[s0_off + p * N + n] = S[p * (N + 1) + n];
+  }
+}
+
+// The block in one chunk and no final state (every drafting step): the same arithmetic as
+// ssd_scan_kernel<N, false>, with every global load of the wave (dt, the x tile, the B and C
+// fragments, all initial-state fragments) issued before the first is used, so that a wave
+// waits for memory once instead of once per state fragment.
+template <int N>
+__global__ void __launch_bounds__(64) ssd_scan_one(ScanArgs a) {
+  constexpr int NS = (N + 31) / 32;
+  __shared__ float xT[P * (QMAX + 1)];   // x^T tile, fp32, padded rows
+  __shared__ float Mm[QMAX * (QMAX + 1)];
+
+  const int H = a.H, T = a.T, G = a.G;
+  const int b = blockIdx.x / H, h = blockIdx.x % H;
+  const int grp = h / (H / G);
+  const int lane = threadIdx.x, g4 = lane >> 4, l16 = lane & 15;
+  const size_t s0_off = ((size_t)b * H + h) * P * N;
+
+  // ---- loads, in order of use
+  const float dtv = l16 < T ? a.dt[(size_t)(b * T + l16) * a.dt_ld + h] : 0.f;
+  // x tile: lane holds x[t = lane / 4][p = 16 (lane % 4) .. + 15]
+  const int xt = lane >> 2, xp = 16 * (lane & 3);
+  const bool xok = xt < T;
+  const size_t xoff = (size_t)(b * T + xt) * a.x_ld + (size_t)h * P + xp;
+  const bf16x8 xh0 = ld8_or0(a.x_hi + xoff, xok), xh1 = ld8_or0(a.x_hi + xoff + 8, xok);
+  const bf16x8 xl0 = a.x_lo ? ld8_or0(a.x_lo + xoff, xok) : zero8();
+  const bf16x8 xl1 = a.x_lo ? ld8_or0(a.x_lo + xoff + 8, xok) : zero8();
+  // C (A operand, rows t) and B (B operand, columns s) fragments over n
+  bf16x8 cf[NS], cfl[NS], bfr[NS], bfl[NS];
+  const size_t tok_t = (size_t)(b * T + l16) * a.bc_ld + (size_t)grp * N;
+#pragma unroll
+  for (int ns = 0; ns < NS; ++ns) {
+    const int n = 32 * ns + 8 * g4;
+    const bool ok = l16 < T && n < N;
+    cf[ns] = ld8_or0(a.C_hi + tok_t + n, ok);
+    cfl[ns] = a.C_lo ? ld8_or0(a.C_lo + tok_t + n, ok) : zero8();
+    bfr[ns] = ld8_or0(a.B_hi + tok_t + n, ok);
+    bfl[ns] = a.B_lo ? ld8_or0(a.B_lo + tok_t + n, ok) : zero8();
+  }
+  // initial state as B operand of C S^T: column p = 16 pb + l16, n = 32 ns + 8 g4 ..
+  bf16x8 sh[4][NS], sl[4][NS];
+#pragma unroll
+  for (int pb = 0; pb < 4; ++pb)
+#pragma unroll
+    for (int ns = 0; ns < NS; ++ns) {
+      const int n = 32 * ns + 8 * g4;
+      const size_t off = s0_off + (size_t)(16 * pb + l16) * N + n;
+      const bool ok = a.S0_hi != nullptr && n < N;
+      sh[pb][ns] = ld8_or0(a.S0_hi + off, ok);
+      sl[pb][ns] = a.S0_lo != nullptr ? ld8_or0(a.S0_lo + off, ok) : zero8();
+    }
+  const float Ah = a.A_is_log ? -__expf(a.A[h]) : a.A[h], Dh = a.Dskip[h];
+
+  // ---- inclusive cumulative sum of dt*A over the chunk (lanes 0..15)
+  float cum = dtv * Ah;
+#pragma unroll
+  for (int off = 1; off < 16; off <<= 1) {
+    const float v = __shfl_up(cum, off, 16);
+    if (l16 >= off) cum += v;
+  }
+  // ---- x^T tile in LDS
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    xT[(xp + e) * (QMAX + 1) + xt] = bf2f(xh0[e]) + bf2f(xl0[e]);
+    xT[(xp + 8 + e) * (QMAX + 1) + xt] = bf2f(xh1[e]) + bf2f(xl1[e]);
+  }
+  // ---- C B^T: lane gets rows t = 4 g4 + i, column s = l16
+  f32x4 cb = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ns = 0; ns < NS; ++ns) {
+    cb = mma16(cf[ns], bfr[ns], cb);
+    if (a.C_lo) cb = mma16(cfl[ns], bfr[ns], cb);
+    if (a.B_lo) cb = mma16(cf[ns], bfl[ns], cb);
+  }
+  // ---- state term C S^T: lane gets rows t = 4 g4 + i, column p = 16 pb + l16
+  f32x4 ys[4];
+#pragma unroll
+  for (int pb = 0; pb < 4; ++pb) {
+    ys[pb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ns = 0; ns < NS; ++ns) {
+      ys[pb] = mma16(cf[ns], sh[pb][ns], ys[pb]);
+      if (a.C_lo) ys[pb] = mma16(cfl[ns], sh[pb][ns], ys[pb]);
+      if (a.S0_lo) ys[pb] = mma16(cf[ns], sl[pb][ns], ys[pb]);
+    }
+  }
+  // ---- decay-weighted mixing matrix M[t][s] = (C_t . B_s) exp(l_t - l_s) dt_s for s <= t
+  const float ell_s = __shfl(cum, l16);
+  const float dt_s = __shfl(dtv, l16);
+  float ell_t[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int t = 4 * g4 + i;
+    ell_t[i] = __shfl(cum, t);
+    const bool ok = l16 <= t && t < T;
+    Mm[t * (QMAX + 1) + l16] = ok ? cb[i] * __expf(ell_t[i] - ell_s) * dt_s : 0.f;
+  }
+  __syncthreads();
+  // ---- y = exp(l_t) (C S^T) + M x + D x
+#pragma unroll
+  for (int pb = 0; pb < 4; ++pb) {
+    const int p = 16 * pb + l16;
+    const float* xr = xT + p * (QMAX + 1);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int t = 4 * g4 + i;
+      if (t >= T) continue;
+      const float* mr = Mm + t * (QMAX + 1);
+      float acc = __expf(ell_t[i]) * ys[pb][i] + Dh * xr[t];
+      for (int s2 = 0; s2 <= t; ++s2) acc += mr[s2] * xr[s2];
+      a.y[(size_t)(b * T + t) * H * P + (size_t)h * P + p] = acc;
     }
   }
 }
@@ -213,13 +311,13 @@ __global__ void __launch_bounds__(64) ssd_scan_kernel(ScanArgs a) {
 template <int N>
 hipError_t launch_n(const ScanArgs& a, hipStream_t s) {
   const bool multi = a.S_final != nullptr || a.T > a.chunk;
-  constexpr int lds_multi = ScanLds<N, true>::BYTES, lds_single = ScanLds<N, false>::BYTES;
+  constexpr int lds_multi = ScanLds<N>::BYTES;
   if (multi) {
-    auto kern = ssd_scan_kernel<N, true>;
+    auto kern = ssd_scan_kernel<N>;
     hipLaunchKernelGGL(kern, dim3(a.B * a.H), dim3(64), lds_multi, s, a);
   } else {
-    auto kern = ssd_scan_kernel<N, false>;
-    hipLaunchKernelGGL(kern, dim3(a.B * a.H), dim3(64), lds_single, s, a);
+    auto kern = ssd_scan_one<N>;
+    hipLaunchKernelGGL(kern, dim3(a.B * a.H), dim3(64), 0, s, a);
   }
   return hipGetLastError();
 }

@@ -23,6 +23,10 @@ SMALL = {
     # B*k = 160 rows: the pipelined dense GEMMs, the fused Q/K/V product with a ragged last tile
     "m160_fused_qkv": I.StepConfig(name="s", B=10, k=16, d_model=320, H=5, P=64, N=32, G=1, chunk=16, Hq=8,
                                    Hkv=2, D=128, lengths="uniform:1:700"),
+    # B*k = 640 rows: the 256 x 256 products, with k-split last tiles (in_proj, out_proj with
+    # hi/lo inputs; Q/K/V over weight segments of 4096 and 1024 rows; O projection)
+    "m640_large_tiles": I.StepConfig(name="s", B=40, k=16, d_model=512, H=8, P=64, N=16, G=1, chunk=16, Hq=32,
+                                     Hkv=8, D=128, lengths="uniform:0:300"),
 }
 
 

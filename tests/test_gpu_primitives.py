@@ -26,7 +26,10 @@ def _small_attn_cfg(**kw):
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("M,N,K", [(4, 256, 256), (64, 1000, 512), (100, 384, 264), (128, 512, 1024),
                                    (300, 700, 4096), (1, 4096, 4096), (48, 5000, 4096), (20, 3000, 1024),
-                                   (8, 300, 264), (64, 200000, 160)])
+                                   (8, 300, 264), (64, 200000, 160),
+                                   # 256 x 256 tiles: whole tiles, k-split last tiles, ragged M and N
+                                   (512, 768, 256), (1024, 2304, 1024), (777, 1000, 512), (1536, 4096, 512),
+                                   (600, 300, 4096)])
 def test_linear(dtype, M, N, K):
     print(f"[linear] dtype={dtype} M={M} N={N} K={K}", flush=True)
     A = I.normal("lin_A", (M, K), 1.0, 0, dtype)
@@ -224,6 +227,10 @@ SCAN_CASES = [
     (1, 16, 4, 16, 1, 1, "bf16", False, True),
     (3, 5, 6, 64, 3, 2, "f32", True, False),
     (2, 16, 4, 32, 1, 16, "bf16", False, False),
+    # one chunk without a final state (the drafting step's path) in fp32 planes, with T < chunk
+    (2, 16, 8, 128, 1, 16, "f32", True, False),
+    (3, 7, 4, 64, 2, 8, "bf16", True, False),
+    (1, 1, 2, 16, 1, 16, "f32", True, False),
 ]
 
 
