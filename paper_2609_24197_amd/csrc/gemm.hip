@@ -790,28 +790,37 @@ hipError_t launch_dense(const GemmArgs& g, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------------------
-// Large products (M >= 512, the block positions of many requests): 256 x 256 output tiles,
-// eight waves of 128 x 64 each (4 x 2 blocks of 32 x 32).  A wave reads 0.75 KB of LDS
-// fragments per v_mfma_f32_32x32x16_bf16 (0.625 KB with an A lo plane), so the fragment reads
-// of two waves per SIMD stay below the CU's LDS bandwidth at the full MFMA rate; with 64 x 64
-// per wave they would need all of it.  32-wide k-tiles come into LDS by DMA, 3 stages deep.
-// With few tiles (tiles mod CUs small) the last tiles are split over K: unit u < full is
-// whole tile u, the others are (tile, k-part) pairs whose fp32 partials a fix-up kernel sums
-// in k-part order, so the result does not depend on scheduling.
-constexpr int GB_BM = 256, GB_BN = 256, GB_KT = 32, GB_NT = 512, GB_ST = 3;
+// Large products (M >= 512, the block positions of many requests).  Eight waves in a 2 x 4
+// grid; a wave owns TM x TN blocks of 32 x 32 (v_mfma_f32_32x32x16_bf16) and reads 0.75 KB of
+// LDS fragments per MFMA: 128 x 64 per wave (256 x 256 tiles) for a bf16 A, 64 x 64 per wave
+// with the A lo plane (128 x 256 tiles, two products per block).  With 64 x 64 per wave and one
+// plane the fragment reads alone would need the CU's whole LDS bandwidth at the MFMA rate.
+// 32-wide k-tiles come into LDS by DMA, 4 stages deep.  The fragment reads run one k-step
+// ahead across k-tiles: a tile's second k-step is read while its first is multiplied, and the
+// next tile's first k-step while its second is, so the matrix unit has work queued across
+// every wait for LDS or for the next tile.  With few tiles (tiles mod CUs small) the last tiles are split over K: unit
+// u < full is whole tile u, the others are (tile, k-part) pairs whose fp32 partials a fix-up
+// kernel sums in k-part order, so the result does not depend on scheduling.
+#ifndef HSPEC_BIG_ST
+#define HSPEC_BIG_ST 4
+#endif
+constexpr int GB_KT = 32, GB_NT = 512, GB_ST = HSPEC_BIG_ST;
 
 template <bool ALO>
 struct BigCfg {
+  static constexpr int TM = ALO ? 2 : 4, TN = 2;
+  static constexpr int BM = 2 * TM * 32, BN = 4 * TN * 32;
   static constexpr int CPRT = GB_KT / 8;                           // 16-byte units per tile row
-  static constexpr int SA = GB_BM * GB_KT, SW = GB_BN * GB_KT;     // elements per plane per stage
-  static constexpr int A_I = GB_BM * CPRT / GB_NT, W_I = GB_BN * CPRT / GB_NT;   // DMA per wave
+  static constexpr int SA = BM * GB_KT, SW = BN * GB_KT;           // elements per plane per stage
+  static constexpr int A_I = BM * CPRT / GB_NT, W_I = BN * CPRT / GB_NT;   // DMA per wave
   static constexpr int NI = A_I * (ALO ? 2 : 1) + W_I;
-  static constexpr int VM = (GB_ST - 2) * NI;
-  static_assert(GB_BM * CPRT % GB_NT == 0 && GB_BN * CPRT % GB_NT == 0 && VM < 64, "big gemm shape");
+  static_assert(BM * CPRT % GB_NT == 0 && BN * CPRT % GB_NT == 0 && (GB_ST - 3) * NI < 64 && GB_ST >= 3 &&
+                GB_ST <= 5, "big gemm shape");
 };
 
 // Work division of a large product (host-computed, passed to the kernels).
 struct BigPlan {
+  int bm = 0, bn = 0;       // tile shape
   int mt = 0, nt = 0;       // tile grid
   int full = 0;             // units [0, full): whole tiles (virtual ids)
   int splits = 1, kper = 0; // remaining tiles: `splits` k-parts of kper k-tiles
@@ -821,21 +830,27 @@ struct BigPlan {
 template <bool ALO>
 __global__ void __launch_bounds__(GB_NT) gemm_big_kernel(GemmArgs g, BigPlan p) {
   using C = BigCfg<ALO>;
+  constexpr int TM = C::TM, TN = C::TN, BM = C::BM, BN = C::BN;
   constexpr int PA = C::SA * (ALO ? 2 : 1);
   __shared__ __align__(16) bf16 A0s[PA], W0s[C::SW];
   __shared__ __align__(16) bf16 A1s[PA], W1s[C::SW];
   __shared__ __align__(16) bf16 A2s[PA], W2s[C::SW];
+  __shared__ __align__(16) bf16 A3s[GB_ST > 3 ? PA : 8], W3s[GB_ST > 3 ? C::SW : 8];
+  __shared__ __align__(16) bf16 A4s[GB_ST > 4 ? PA : 8], W4s[GB_ST > 4 ? C::SW : 8];
   auto sa_of = [&](auto I) -> bf16* {
     if constexpr (decltype(I)::value == 0) return A0s;
     else if constexpr (decltype(I)::value == 1) return A1s;
-    else return A2s;
+    else if constexpr (decltype(I)::value == 2) return A2s;
+    else if constexpr (decltype(I)::value == 3) return A3s;
+    else return A4s;
   };
   auto sw_of = [&](auto I) -> bf16* {
     if constexpr (decltype(I)::value == 0) return W0s;
     else if constexpr (decltype(I)::value == 1) return W1s;
-    else return W2s;
+    else if constexpr (decltype(I)::value == 2) return W2s;
+    else if constexpr (decltype(I)::value == 3) return W3s;
+    else return W4s;
   };
-  constexpr int TM = 4, TN = 2;
 
   // unit -> (tile, k-tile range)
   const int nk_all = g.K / GB_KT;
@@ -854,12 +869,12 @@ __global__ void __launch_bounds__(GB_NT) gemm_big_kernel(GemmArgs g, BigPlan p) 
     ke = min(nk_all, kb + p.kper);
   }
   const int mt = v % p.mt, nt = v / p.mt;
-  const int m0 = mt * GB_BM, n0 = nt * GB_BN;
+  const int m0 = mt * BM, n0 = nt * BN;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / 4, wn = wave % 4;
 
-  const int rows_a = min(GB_BM, g.M - m0);
+  const int rows_a = min(BM, g.M - m0);
   const bf16* A0 = g.A_hi + (size_t)m0 * g.lda;
   const bf16* Al0 = (ALO ? g.A_lo : g.A_hi) + (size_t)m0 * g.lda;
   const bf16* wbase = g.W_hi;   // W row segment of this tile (tiles never straddle one)
@@ -869,7 +884,7 @@ __global__ void __launch_bounds__(GB_NT) gemm_big_kernel(GemmArgs g, BigPlan p) 
     else if (n0 >= g.N1) { wbase = g.W2; wseg0 = g.N1; wseg1 = g.N1 + g.N2; }
     else wseg1 = g.N1;
   }
-  const int rows_w = min(GB_BN, wseg1 - n0);
+  const int rows_w = min(BN, wseg1 - n0);
 
   // unit q (16 bytes) of a stage plane: row q / 4, stored chunk q % 4 = logical chunk ^ key(row).
   // Element offsets (32-bit: host-checked) from the tile's first row, at k-tile kb.
@@ -907,69 +922,75 @@ __global__ void __launch_bounds__(GB_NT) gemm_big_kernel(GemmArgs g, BigPlan p) 
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[a][b][i] = 0.f;
 
-  // fragments of k-step ks + 1 are read while the MFMAs of k-step ks run
-  auto compute = [&](const bf16* L, const bf16* LW) {
-    const bf16* sA = L;
-    const bf16* sAl = L + C::SA;
-    bf16x8 fa[2][TM], fal[2][ALO ? TM : 1], fw[2][TN];
-    auto frags = [&](int ks, int buf) {
-      const int ch = 2 * ks + (lane >> 5);
+  // fragment buffers: F0 holds k-step 0 of a tile, F1 k-step 1
+  bf16x8 fa0[TM], fl0[ALO ? TM : 1], fw0[TN], fa1[TM], fl1[ALO ? TM : 1], fw1[TN];
+  auto frags = [&](const bf16* L, const bf16* LW, int ks, bf16x8 (&fa)[TM], bf16x8 (&fl)[ALO ? TM : 1],
+                   bf16x8 (&fw)[TN]) {
+    const int ch = 2 * ks + (lane >> 5);
 #pragma unroll
-      for (int a = 0; a < TM; ++a) {
-        const int r = (wm * TM + a) * 32 + (lane & 31);
-        fa[buf][a] = *reinterpret_cast<const bf16x8*>(sA + 8 * swz_t<GB_KT>(r, ch));
-        if constexpr (ALO) fal[buf][a] = *reinterpret_cast<const bf16x8*>(sAl + 8 * swz_t<GB_KT>(r, ch));
-      }
+    for (int a = 0; a < TM; ++a) {
+      const int r = (wm * TM + a) * 32 + (lane & 31);
+      fa[a] = *reinterpret_cast<const bf16x8*>(L + 8 * swz_t<GB_KT>(r, ch));
+      if constexpr (ALO) fl[a] = *reinterpret_cast<const bf16x8*>(L + C::SA + 8 * swz_t<GB_KT>(r, ch));
+    }
+#pragma unroll
+    for (int b = 0; b < TN; ++b) {
+      const int r = (wn * TN + b) * 32 + (lane & 31);
+      fw[b] = *reinterpret_cast<const bf16x8*>(LW + 8 * swz_t<GB_KT>(r, ch));
+    }
+  };
+  auto mma = [&](const bf16x8 (&fa)[TM], const bf16x8 (&fl)[ALO ? TM : 1], const bf16x8 (&fw)[TN]) {
+#pragma unroll
+    for (int a = 0; a < TM; ++a)
 #pragma unroll
       for (int b = 0; b < TN; ++b) {
-        const int r = (wn * TN + b) * 32 + (lane & 31);
-        fw[buf][b] = *reinterpret_cast<const bf16x8*>(LW + 8 * swz_t<GB_KT>(r, ch));
+        acc[a][b] = mma32(fa[a], fw[b], acc[a][b]);
+        if constexpr (ALO) acc[a][b] = mma32(fl[a], fw[b], acc[a][b]);
       }
-    };
-    frags(0, 0);
-#pragma unroll
-    for (int ks = 0; ks < GB_KT / 16; ++ks) {
-      if (ks + 1 < GB_KT / 16) frags(ks + 1, (ks + 1) & 1);
-      __builtin_amdgcn_sched_barrier(0);
-      const int cb = ks & 1;
-#pragma unroll
-      for (int a = 0; a < TM; ++a)
-#pragma unroll
-        for (int b = 0; b < TN; ++b) {
-          acc[a][b] = mma32(fa[cb][a], fw[cb][b], acc[a][b]);
-          if constexpr (ALO) acc[a][b] = mma32(fal[cb][a], fw[cb][b], acc[a][b]);
-        }
-    }
   };
 
   const int nk = ke - kb;
+  // prologue without branches (tiles past the end re-read the last one into unused stages)
   [&]<int... I>(std::integer_sequence<int, I...>) {
     (issue(min(I, nk - 1), sa_of(Int<I>{}), sw_of(Int<I>{})), ...);
   }(std::make_integer_sequence<int, GB_ST - 1>{});
-  auto steady = [&](int t, auto S) {
-    wait_vm_lgkm0<C::VM>();
-    wg_barrier();
-    constexpr int N = (decltype(S)::value + GB_ST - 1) % GB_ST;
-    issue(t + GB_ST - 1, sa_of(Int<N>{}), sw_of(Int<N>{}));
-    compute(sa_of(S), sw_of(S));
-  };
-  auto step = [&](int t, auto S) {
-    if (t + GB_ST - 2 < nk) wait_vm_lgkm0<C::VM>();
-    else wait_vm_lgkm0<0>();
-    wg_barrier();
-    constexpr int N = (decltype(S)::value + GB_ST - 1) % GB_ST;
-    if (t + GB_ST - 1 < nk) issue(t + GB_ST - 1, sa_of(Int<N>{}), sw_of(Int<N>{}));
-    compute(sa_of(S), sw_of(S));
+  wait_vmcnt<(GB_ST - 2) * C::NI>();   // tile 0 landed for this wave
+  wg_barrier();
+  frags(A0s, W0s, 0, fa0, fl0, fw0);
+
+  // Step t (stage S = t mod ST): the MFMAs of k-step 0 of tile t are issued, then the reads of
+  // its k-step 1; tile t+1 is waited for (its DMA was issued ST-2 steps ago) and the stage of
+  // tile t-1 (whose last reads every wave completed before this step's first MFMAs) refilled
+  // with tile t+ST-1; then the MFMAs of k-step 1 and the reads of k-step 0 of tile t+1.  Every
+  // batch of reads is issued right behind a batch of MFMAs, so its wait overlaps their run.
+  auto step = [&](int t, auto S, bool tail) {
+    constexpr int s = decltype(S)::value, s1 = (s + 1) % GB_ST, sn = (s + GB_ST - 1) % GB_ST;
+    mma(fa0, fl0, fw0);
+    __builtin_amdgcn_sched_barrier(0);
+    frags(sa_of(Int<s>{}), sw_of(Int<s>{}), 1, fa1, fl1, fw1);
+    __builtin_amdgcn_sched_barrier(0);
+    if (t + 1 < nk) {
+      if (!tail) wait_vmcnt<(GB_ST - 3) * C::NI>();   // tiles t+2 .. t+ST-2 may stay in flight
+      else wait_vmcnt<0>();
+      wg_barrier();
+      if (t + GB_ST - 1 < nk) issue(t + GB_ST - 1, sa_of(Int<sn>{}), sw_of(Int<sn>{}));
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    mma(fa1, fl1, fw1);
+    __builtin_amdgcn_sched_barrier(0);
+    if (t + 1 < nk) frags(sa_of(Int<s1>{}), sw_of(Int<s1>{}), 0, fa0, fl0, fw0);
+    __builtin_amdgcn_sched_barrier(0);
   };
   int t0 = 0;
+  // steady rounds: every DMA of the round's waits is issued (t + ST - 2 < nk for all its steps)
   for (; t0 + 2 * GB_ST - 2 < nk; t0 += GB_ST) {
     [&]<int... I>(std::integer_sequence<int, I...>) {
-      (steady(t0 + I, Int<I>{}), ...);
+      (step(t0 + I, Int<I>{}, false), ...);
     }(std::make_integer_sequence<int, GB_ST>{});
   }
   for (; t0 < nk; t0 += GB_ST) {
     [&]<int... I>(std::integer_sequence<int, I...>) {
-      ((t0 + I < nk ? step(t0 + I, Int<I>{}) : void()), ...);
+      ((t0 + I < nk ? step(t0 + I, Int<I>{}, true) : void()), ...);
     }(std::make_integer_sequence<int, GB_ST>{});
   }
 
@@ -980,8 +1001,8 @@ __global__ void __launch_bounds__(GB_NT) gemm_big_kernel(GemmArgs g, BigPlan p) 
       for (int b = 0; b < TN; ++b)
         store_block32(g, acc[a][b], m0 + (wm * TM + a) * 32, n0 + (wn * TN + b) * 32, lane);
   } else {
-    // partial of k-part r % splits: [unit][256][256] fp32; lane holds rows 8(i/4)+4(l/32)+i%4
-    float* part = g.part + (size_t)(u - p.full) * GB_BM * GB_BN;
+    // partial of k-part r % splits: [unit][BM][BN] fp32; lane holds rows 8(i/4)+4(l/32)+i%4
+    float* part = g.part + (size_t)(u - p.full) * BM * BN;
 #pragma unroll
     for (int a = 0; a < TM; ++a)
 #pragma unroll
@@ -989,7 +1010,7 @@ __global__ void __launch_bounds__(GB_NT) gemm_big_kernel(GemmArgs g, BigPlan p) 
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int r = (wm * TM + a) * 32 + 8 * (i / 4) + 4 * (lane >> 5) + (i % 4);
-          part[r * GB_BN + (wn * TN + b) * 32 + (lane & 31)] = acc[a][b][i];
+          part[r * BN + (wn * TN + b) * 32 + (lane & 31)] = acc[a][b][i];
         }
   }
 }
@@ -1001,13 +1022,13 @@ template <bool VEC>
 __global__ void __launch_bounds__(256) gemm_big_fixup(GemmArgs g, BigPlan p) {
   constexpr int GROUP = 8;   // k-parts whose loads are issued together
   const int tiles = p.mt * p.nt - p.full;
-  const size_t per = (size_t)GB_BM * GB_BN;
+  const size_t per = (size_t)p.bm * p.bn;
   const size_t quads = (size_t)tiles * per / 4;
   for (size_t q = (size_t)blockIdx.x * 256 + threadIdx.x; q < quads; q += (size_t)gridDim.x * 256) {
     const int tl = (int)(q / (per / 4));
     const int rc = (int)(q % (per / 4)) * 4;
     const int v = p.full + tl;
-    const int m = (v % p.mt) * GB_BM + rc / GB_BN, n0 = (v / p.mt) * GB_BN + rc % GB_BN;
+    const int m = (v % p.mt) * p.bm + rc / p.bn, n0 = (v / p.mt) * p.bn + rc % p.bn;
     if (m >= g.M || n0 >= g.N) continue;
     const float* src = g.part + (size_t)tl * p.splits * per + rc;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -1063,20 +1084,23 @@ __global__ void __launch_bounds__(256) gemm_big_fixup(GemmArgs g, BigPlan p) {
   }
 }
 
-// Whether the 256 x 256 path serves a product, and its work division for `cus` CUs: whole
+// Whether the large-tile path serves a product, and its work division for `cus` CUs: whole
 // tiles for every full round, the tiles of a short last round split over K so that the round
 // fills the chip (at least 4 k-tiles per part).
 bool big_ok(const GemmArgs& g) {
   if (g.M < 512 || g.W_lo || g.w_packed || g.K % GB_KT) return false;
+  const int bm = g.A_lo ? BigCfg<true>::BM : BigCfg<false>::BM, bn = g.A_lo ? BigCfg<true>::BN : BigCfg<false>::BN;
   // 32-bit element offsets inside a tile's rows of A and W
-  if ((long long)GB_BM * g.lda >= (1ll << 31) || (long long)GB_BN * g.ldw >= (1ll << 31)) return false;
-  if (g.W2 && (g.N1 % GB_BN || g.N2 % GB_BN)) return false;
+  if ((long long)bm * g.lda >= (1ll << 31) || (long long)bn * g.ldw >= (1ll << 31)) return false;
+  if (g.W2 && (g.N1 % bn || g.N2 % bn)) return false;
   return true;
 }
-BigPlan big_plan(int M, int N, int K, int cus) {
+BigPlan big_plan(int M, int N, int K, bool a_lo, int cus) {
   BigPlan p;
-  p.mt = (M + GB_BM - 1) / GB_BM;
-  p.nt = (N + GB_BN - 1) / GB_BN;
+  p.bm = a_lo ? BigCfg<true>::BM : BigCfg<false>::BM;
+  p.bn = a_lo ? BigCfg<true>::BN : BigCfg<false>::BN;
+  p.mt = (M + p.bm - 1) / p.bm;
+  p.nt = (N + p.bn - 1) / p.bn;
   const int tiles = p.mt * p.nt, nk = K / GB_KT;
   const int rem = tiles % cus;
   int sp = rem ? cus / rem : 1;
@@ -1093,11 +1117,11 @@ BigPlan big_plan(int M, int N, int K, int cus) {
   return p;
 }
 size_t big_scratch_elems(const BigPlan& p) {
-  return (size_t)(p.mt * p.nt - p.full) * p.splits * GB_BM * GB_BN;
+  return (size_t)(p.mt * p.nt - p.full) * p.splits * p.bm * p.bn;
 }
 
 hipError_t launch_big(const GemmArgs& g, hipStream_t s) {
-  BigPlan p = big_plan(g.M, g.N, g.K, device_cus());
+  BigPlan p = big_plan(g.M, g.N, g.K, g.A_lo != nullptr, device_cus());
   if (p.full < p.mt * p.nt && (!g.part || g.part_cap < big_scratch_elems(p))) {
     p.full = p.mt * p.nt;   // no room for partials: whole tiles only
     p.splits = 1;
@@ -1167,7 +1191,10 @@ size_t gemm_scratch_elems(int M, int N, int K, bool a_lo, bool w_lo) {
   if (M <= 0 || N <= 0 || K <= 0) return 0;
   const SkPlan p = skinny_plan(M, N, K, w_lo, device_cus());
   size_t n = p.use && p.ksplit > 1 ? (size_t)p.ksplit * M * N : 0;
-  if (M >= 512 && !w_lo && K % GB_KT == 0) n = std::max(n, big_scratch_elems(big_plan(M, N, K, device_cus())));
+  if (M >= 512 && !w_lo && K % GB_KT == 0) {
+    n = std::max(n, big_scratch_elems(big_plan(M, N, K, false, device_cus())));
+    n = std::max(n, big_scratch_elems(big_plan(M, N, K, true, device_cus())));
+  }
   return n;
 }
 
