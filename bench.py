@@ -167,6 +167,11 @@ def main():
     ap.add_argument("--cpu-requests", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--window", type=int, default=None,
+                    help="sliding window of the drafter attention in tokens (the paper's drafters use "
+                         "2048); default: the workload's own (full context)")
+    ap.add_argument("--block-causal", action="store_true",
+                    help="causal attention inside the drafted block instead of bidirectional")
     ap.add_argument("--counters", action="store_true",
                     help="launch each measured kernel once (for rocprofv3 --pmc) and exit")
     args = ap.parse_args()
@@ -180,6 +185,10 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     cfg = I.CONFIGS[args.config]
+    if args.window is not None:
+        cfg = cfg.replace(window=args.window)
+    if args.block_causal:
+        cfg = cfg.replace(block_causal=True)
     if args.counters:
         counters(cfg, args.seed, torch)
         return
@@ -266,7 +275,8 @@ def main():
         "config": {"workload": cfg.name, "B": cfg.B, "k": cfg.k, "ctx_lens": cfg.lengths,
                    "sum_ctx_tokens": int(L.sum()), "Hq": cfg.Hq, "Hkv": cfg.Hkv, "D": cfg.D,
                    "d_model": cfg.d_model, "mamba": f"H{cfg.H} P{cfg.P} N{cfg.N} G{cfg.G} chunk{cfg.chunk}",
-                   "page_size": cfg.page_size, "W_dS_layout": "packed" if cfg.dtype == "bf16" else "row-major",
+                   "page_size": cfg.page_size, "window": cfg.window, "block_causal": cfg.block_causal,
+                   "W_dS_layout": "packed" if cfg.dtype == "bf16" else "row-major",
                    "parallelism": "single GPU"},
         "roofline": roof,
         "roofline_kv_sweep": roof_sweep,

@@ -109,8 +109,12 @@ typedef struct {
  *   slot page_table[b, i / page_size] * page_size + i % page_size.  Block position j sits at
  *   RoPE position ctx_lens[b] + j.  window > 0 hides cache position p from the query at
  *   position pos when pos - p >= window (sliding window; requires k <= window).
- *   split_tokens: context length per split of the KV sweep (multiple of 64, at most 8192,
- *   and at least max_ctx_len / 256 so that no request has more than 256 splits), 0 = automatic.
+ *   The sweep reads, for each request, the cache positions some block query can see: all
+ *   of [0, ctx_len), or [ctx_len - window + 1, ctx_len) under a window; the swept length is
+ *   at most max_ctx_len, or window - 1 with a window.
+ *   split_tokens: cache positions per split of the KV sweep (multiple of 64, at most 8192,
+ *   and at least the swept length / 256 so that no request has more than 256 splits),
+ *   0 = automatic.
  *   A setting outside these limits returns HSPEC_ERR_UNSUPPORTED.
  *   scale: softmax scale, 0 = 1/sqrt(D).  rope_theta: RoPE base (rotate-half pairing).
  */

@@ -149,9 +149,10 @@ hspec_status check_attn_cfg(const hspec_attn_cfg* c, int max_ctx_len) {
   if (c->page_size < 16 || (c->page_size & (c->page_size - 1)))
     return fail(HSPEC_ERR_UNSUPPORTED, "page_size must be a power of two >= 16, got %d", c->page_size);
   if (c->split_tokens > 8192) return fail(HSPEC_ERR_UNSUPPORTED, "split_tokens must be <= 8192");
-  const int split = c->split_tokens > 0 ? c->split_tokens : hspec::attention_default_split(c->B, c->Hkv, max_ctx_len);
-  if (max_ctx_len > 0 && (max_ctx_len + split - 1) / split > 256)
-    return fail(HSPEC_ERR_UNSUPPORTED, "max_ctx_len / split_tokens gives more than 256 splits");
+  const int swept = hspec::attention_swept_len(max_ctx_len, c->window);
+  const int split = c->split_tokens > 0 ? c->split_tokens : hspec::attention_default_split(c->B, c->Hkv, swept);
+  if (swept > 0 && (swept + split - 1) / split > 256)
+    return fail(HSPEC_ERR_UNSUPPORTED, "swept context / split_tokens gives more than 256 splits");
   return HSPEC_OK;
 }
 
@@ -319,8 +320,9 @@ struct AttnPlan {
 };
 
 void plan_sweep(Arena& ar, const hspec_attn_cfg& c, int max_ctx_len, AttnPlan& p) {
-  p.split = c.split_tokens > 0 ? c.split_tokens : hspec::attention_default_split(c.B, c.Hkv, max_ctx_len);
-  p.max_splits = max_ctx_len > 0 ? (max_ctx_len + p.split - 1) / p.split : 1;
+  const int swept = hspec::attention_swept_len(max_ctx_len, c.window);
+  p.split = c.split_tokens > 0 ? c.split_tokens : hspec::attention_default_split(c.B, c.Hkv, swept);
+  p.max_splits = swept > 0 ? (swept + p.split - 1) / p.split : 1;
   const int R = c.k * (c.Hq / c.Hkv);
   const size_t units = (size_t)c.B * c.Hkv * p.max_splits;
   p.units = ar.take<int32_t>((size_t)2 * c.B * p.max_splits);

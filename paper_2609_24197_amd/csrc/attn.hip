@@ -71,6 +71,20 @@ __device__ __forceinline__ int clamp_len(const AttnArgs& a, int b) {
   return L;
 }
 
+// First cache position a sweep reads for a request of length L.  Under a sliding window the
+// query at position L + j sees cache positions p >= L + j - window + 1, so no query of the
+// block sees p < L - window + 1; those positions are not read at all.
+__device__ __forceinline__ int swept_lo(const AttnArgs& a, int L) {
+  return a.window > 0 && L - a.window + 1 > 0 ? L - a.window + 1 : 0;
+}
+
+// Splits of one request: the swept range [swept_lo, L) cut into runs of `split` positions
+// (one split, with no cache keys, when the range is empty).
+__device__ __forceinline__ int n_splits(const AttnArgs& a, int L) {
+  const int n = L - swept_lo(a, L);
+  return n > 0 ? (n + a.split - 1) / a.split : 1;
+}
+
 // Element offset of (row, column d) in a swizzled K/V tile.  16-byte chunk c of row r lives at
 // chunk slot c ^ f(r).  For 256-byte rows f(r) = 2 (r mod 8) + (r / 8 mod 2): the 16 rows read
 // by one 16-lane K fragment load land on 16 different slots, and the 8 rows x 32 bytes read by
@@ -138,15 +152,11 @@ attn_sweep(AttnArgs a) {
   const int2 unit_e = *reinterpret_cast<const int2*>(a.units + 2 * (item / a.Hkv));
   const int b = unit_e.x >> 16, sp = unit_e.x & 0xffff, h = item % a.Hkv;
   const int L = unit_e.y;   // validated by the work-list kernel
-  const int nsplit = L > 0 ? (L + a.split - 1) / a.split : 1;
-  const int k0 = sp * a.split;
+  const int nsplit = n_splits(a, L);
+  const int k0 = swept_lo(a, L) + sp * a.split;
   const int k1 = min(L, k0 + a.split);
   const bool last = sp == nsplit - 1;
-  int kstart = k0;
-  if (a.window > 0) {
-    const int lo0 = L - a.window + 1;
-    if (lo0 > kstart) kstart = k0 + ((lo0 - k0) / KT) * KT;
-  }
+  const int kstart = k0;
   const int n_cache = kstart < k1 ? (k1 - kstart + KT - 1) / KT : 0;
   const int n_block = last ? (T + KT - 1) / KT : 0;
   const int ntiles = n_cache + n_block;
@@ -445,9 +455,9 @@ __global__ void __launch_bounds__(PLAN_THREADS) attn_plan(AttnArgs a, int clear_
     int nfull = 0, L = 0;
     if (b < a.B) {
       L = clamp_len(a, b);
-      const int ns = L > 0 ? (L + a.split - 1) / a.split : 1;
+      const int ns = n_splits(a, L);
       nfull = ns - 1;
-      if (ranked) s_rem[b] = L - nfull * a.split;
+      if (ranked) s_rem[b] = L - swept_lo(a, L) - nfull * a.split;
     }
     s_scan[tid] = nfull;
     __syncthreads();
@@ -469,7 +479,7 @@ __global__ void __launch_bounds__(PLAN_THREADS) attn_plan(AttnArgs a, int clear_
   const int full = s_base;
   for (int b = tid; b < a.B; b += PLAN_THREADS) {
     const int L = clamp_len(a, b);
-    const int ns = L > 0 ? (L + a.split - 1) / a.split : 1;
+    const int ns = n_splits(a, L);
     int rank = b;
     if (ranked) {
       const int rem = s_rem[b];
@@ -504,7 +514,7 @@ __global__ void __launch_bounds__(RED_THREADS) attn_reduce(AttnArgs a) {
   int L = a.ctx_lens[b];
   const int cap = min(a.max_pages * a.ps, a.max_ctx_len);
   L = L < 0 ? 0 : (L > cap ? cap : L);   // out-of-range lengths were flagged by the sweep
-  const int nsplit = L > 0 ? (L + a.split - 1) / a.split : 1;
+  const int nsplit = n_splits(a, L);
   if (nsplit == 1) return;
   const size_t unit0 = ((size_t)b * a.Hkv + h) * a.max_splits;
   for (int it = threadIdx.x; it < RED_COLS * nq; it += RED_THREADS) {
@@ -630,16 +640,16 @@ size_t attention_partials_bytes(int B, int Hkv, int max_splits, int R, int D) {
   return units * R * D * sizeof(float) + units * R * 2 * sizeof(float);
 }
 
-int attention_default_split(int B, int Hkv, int max_ctx_len) {
+int attention_default_split(int B, int Hkv, int swept_len) {
   // About 1024 (request, split, head) items of the longest requests: enough to fill every
   // resident workgroup slot, few enough that split partials and unit start-up stay small.
-  long long want = ((long long)max_ctx_len * B * Hkv + 1023) / 1024;
+  long long want = ((long long)swept_len * B * Hkv + 1023) / 1024;
   long long s = ((want + 63) / 64) * 64;
   if (s < 256) s = 256;
-  long long cap = ((long long)(max_ctx_len > 0 ? max_ctx_len : 1) + 63) / 64 * 64;
+  long long cap = ((long long)(swept_len > 0 ? swept_len : 1) + 63) / 64 * 64;
   if (s > cap) s = cap;
   if (s > MAX_SPLIT) s = MAX_SPLIT;
-  const long long min_for_256 = ((long long)max_ctx_len + 255) / 256;   // at most 256 splits
+  const long long min_for_256 = ((long long)swept_len + 255) / 256;   // at most 256 splits
   if (s < min_for_256) s = (min_for_256 + 63) / 64 * 64;
   return (int)s;
 }

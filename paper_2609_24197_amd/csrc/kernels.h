@@ -58,7 +58,12 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s, unsigned parts = A
 size_t attention_partials_bytes(int B, int Hkv, int max_splits, int R, int D);
 constexpr int kStatusWords = 64;   // int32 words reserved at the start of every workspace
 constexpr int kStatusClear = 4;    // cleared at the start of every call: status bits, work items, queue
-int attention_default_split(int B, int Hkv, int max_ctx_len);
+int attention_default_split(int B, int Hkv, int swept_len);
+// Longest run of cache positions the sweep reads for one request: max_ctx_len, or window - 1
+// under a sliding window (no query of the block sees an older position).
+inline int attention_swept_len(int max_ctx_len, int window) {
+  return window > 0 && window - 1 < max_ctx_len ? window - 1 : max_ctx_len;
+}
 
 hipError_t launch_gather_slots(int B, int max_pages, int ps, int num_pages, const int32_t* page_table,
                                const int32_t* ctx_lens, int max_ctx_len, int32_t* slots, int* status,

@@ -15,23 +15,34 @@ def kv_bytes_per_token(Hkv: int, D: int, elem_bytes: int) -> int:
     return 2 * Hkv * D * elem_bytes
 
 
+def visible_ctx(cfg, L: int) -> int:
+    """Cache positions at least one block query sees: all L, or the last window - 1 under a
+    sliding window (the query at L + j sees positions p > L + j - window)."""
+    w = getattr(cfg, "window", 0)
+    return min(int(L), w - 1) if w > 0 else int(L)
+
+
 def sweep_bytes(cfg, ctx_lens, elem_bytes: int = 2) -> int:
     """Algorithmic bytes of the target-KV attention (sweep and split reduction together).
 
-    Per context token: K and V rows of every KV head.  Per block position:
+    Per visible context token: K and V rows of every KV head.  Per block position:
     its query heads, the block K/V, and the fp32 output row.  Split partials are not
     algorithmic bytes.
     """
-    ctx = int(sum(int(L) for L in ctx_lens))
+    ctx = sum(visible_ctx(cfg, L) for L in ctx_lens)
     per_tok = kv_bytes_per_token(cfg.Hkv, cfg.D, elem_bytes)
     block = cfg.B * cfg.k * ((cfg.Hq + 2 * cfg.Hkv) * cfg.D * elem_bytes + cfg.Hq * cfg.D * 4)
     return ctx * per_tok + block
 
 
 def sweep_flops(cfg, ctx_lens) -> int:
-    """QK^T and PV over every visible key: 4 * D flops per (query head, key)."""
-    keys = sum(int(L) + cfg.k for L in ctx_lens)
-    return 4 * cfg.D * cfg.Hq * cfg.k * keys
+    """QK^T and PV over every key a query sees: 4 * D flops per (query head, key)."""
+    w, causal = getattr(cfg, "window", 0), getattr(cfg, "block_causal", False)
+    keys = 0
+    for L in ctx_lens:
+        for j in range(cfg.k):
+            keys += (min(int(L), w - 1 - j) if w > 0 else int(L)) + (j + 1 if causal else cfg.k)
+    return 4 * cfg.D * cfg.Hq * keys
 
 
 def state_proj_bytes(cfg, elem_bytes: int = 2, s0_bytes: int = 2) -> int:
@@ -61,7 +72,7 @@ def weight_bytes(cfg, elem_bytes: int = 2) -> int:
 def step_bytes(cfg, ctx_lens, elem_bytes: int = 2) -> int:
     """Whole step with S0 kept on chip: weights + target KV + block activations in and out."""
     act = cfg.B * cfg.d_h * elem_bytes + cfg.B * cfg.k * cfg.d_model * (elem_bytes + 4)
-    ctx = int(sum(int(L) for L in ctx_lens))
+    ctx = sum(visible_ctx(cfg, L) for L in ctx_lens)
     return weight_bytes(cfg, elem_bytes) + ctx * kv_bytes_per_token(cfg.Hkv, cfg.D, elem_bytes) + act
 
 

@@ -94,11 +94,25 @@ def test_attention_validation():
     assert call(_attn_cfg(window=-1)) == 2
     assert call(_attn_cfg(window=8)) == 2       # k > window
     assert call(_attn_cfg(split_tokens=100)) == 2
+    assert call(_attn_cfg(split_tokens=64), maxL=20000) == 4    # 313 splits of the whole context
     assert call(_attn_cfg(page_size=0)) == 2
     assert call(_attn_cfg(dtype=9)) == 3
     assert call(_attn_cfg(), maxL=-1) == 2
     c = _attn_cfg()
     assert L.hspec_paged_attn(C.byref(c), FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, 8192, FAKE, ws, n, None) == 1
+
+
+def test_window_bounds_the_swept_context():
+    """Under a sliding window the sweep's split buffers are sized by window - 1 positions,
+    not by max_ctx_len."""
+    L = _lib()
+    def ws(**kw):
+        c = _attn_cfg(split_tokens=64, **kw)
+        return L.hspec_paged_attn_workspace(C.byref(c), 20000)
+    full, win = ws(), ws(window=2048)
+    # 313 splits of 64 per (request, KV head) against 32
+    assert win < full
+    assert full - win >= 64 * 8 * (313 - 32) * 64 * 4 * 128
 
 
 def test_paged_attn_phase_validation():

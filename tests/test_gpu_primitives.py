@@ -133,6 +133,27 @@ def test_paged_attn_split_invariance():
         assert_close(o, base, f"split {s} vs whole context", max_abs=2e-3, rel_l2=3e-3)
 
 
+def test_paged_attn_window_splits():
+    """Under a sliding window the splits tile only the positions some query can see,
+    starting at ctx_len - window + 1 (not page- or tile-aligned): lengths around the window,
+    several splits inside it, and a length short of it."""
+    cfg = _small_attn_cfg(B=6, window=300, lengths="list:1000,299,300,301,5,777")
+    x = I.make_attn_inputs(cfg, seed=8)
+    ref = _ref_attn(cfg, x)
+    for split in (64, 128, 0):
+        print(f"[paged_attn window] split {split}", flush=True)
+        o, st = _run_attn(cfg, x, split=split)
+        o2, _ = _run_attn(cfg, x, split=split)
+        assert st == 0
+        assert np.array_equal(o, o2), f"split {split} not deterministic"
+        assert_close(o, ref, f"window 300, split {split}")
+    causal = cfg.replace(block_causal=True, B=2, lengths="list:4100,2049", window=2048)
+    xc = I.make_attn_inputs(causal, seed=9)
+    o, st = _run_attn(causal, xc, split=256)
+    assert st == 0
+    assert_close(o, _ref_attn(causal, xc), "window 2048 causal, split 256")
+
+
 def test_paged_attn_phases_bitwise():
     """The work list, sweep and reduction launched one call each give the one-call result."""
     cfg = _small_attn_cfg(B=3, lengths="list:1000,37,450").replace(split_tokens=256)
