@@ -494,15 +494,20 @@ struct SkPlan {
   int ntw = 4, ksplit = 1, kper = 0;
 };
 
+// Waves per workgroup: 128-row A chunks (hi and lo planes, double-buffered) leave LDS room for
+// the epilogue staging of 4 waves only.
+constexpr int sk_waves(int M) { return M > 64 ? 4 : SK_NW; }
+
 SkPlan skinny_plan(int M, int N, int K, bool w_lo, int cus) {
   SkPlan p;
-  if (M > 64 || w_lo || K % SK_STEP != 0 || N % 4 != 0) return p;
+  if (M > 128 || w_lo || K % SK_STEP != 0 || N % 4 != 0) return p;
   p.use = true;
+  const int nw = sk_waves(M);
   const int want = 2 * cus;
-  int tiles = (N + SK_NW * 64 - 1) / (SK_NW * 64);
+  int tiles = (N + nw * 64 - 1) / (nw * 64);
   if (tiles < want) {
     p.ntw = 1;
-    tiles = (N + SK_NW * 16 - 1) / (SK_NW * 16);
+    tiles = (N + nw * 16 - 1) / (nw * 16);
   }
   const int kch = (K + SK_KC - 1) / SK_KC;
   int ks = tiles >= want ? 1 : (want + tiles - 1) / tiles;
@@ -515,10 +520,11 @@ SkPlan skinny_plan(int M, int N, int K, bool w_lo, int cus) {
 
 template <int MT, int NTW, bool ALO, bool PK>
 hipError_t launch_skinny_t(const GemmArgs& g, const SkPlan& p, hipStream_t s) {
-  using S = SkCfg<MT, NTW, SK_NW, ALO>;
+  constexpr int NW = sk_waves(16 * MT);
+  using S = SkCfg<MT, NTW, NW, ALO>;
   // the residual is added by the reduction when K is split
-  auto kern = (g.R && p.ksplit == 1 && !PK) ? skinny_kernel<MT, NTW, SK_NW, ALO, PK, !PK>
-                                            : skinny_kernel<MT, NTW, SK_NW, ALO, PK, false>;
+  auto kern = (g.R && p.ksplit == 1 && !PK) ? skinny_kernel<MT, NTW, NW, ALO, PK, !PK>
+                                            : skinny_kernel<MT, NTW, NW, ALO, PK, false>;
   const int nitems = ((g.N + S::BN - 1) / S::BN) * p.ksplit;
   // one workgroup per CU walks several items when there are more items than CUs
   const int grid = p.ksplit == 1 && nitems > device_cus() ? device_cus() : nitems;
@@ -542,7 +548,8 @@ template <bool ALO>
 hipError_t launch_skinny_a(const GemmArgs& g, const SkPlan& p, hipStream_t s) {
   if (g.M <= 16) return launch_skinny_m<1, ALO>(g, p, s);
   if (g.M <= 32) return launch_skinny_m<2, ALO>(g, p, s);
-  return launch_skinny_m<4, ALO>(g, p, s);
+  if (g.M <= 64) return launch_skinny_m<4, ALO>(g, p, s);
+  return launch_skinny_m<8, ALO>(g, p, s);
 }
 
 // ------------------------------------------------------------- pipelined dense path

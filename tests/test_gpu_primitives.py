@@ -27,6 +27,8 @@ def _small_attn_cfg(**kw):
 @pytest.mark.parametrize("M,N,K", [(4, 256, 256), (64, 1000, 512), (100, 384, 264), (128, 512, 1024),
                                    (300, 700, 4096), (1, 4096, 4096), (48, 5000, 4096), (20, 3000, 1024),
                                    (8, 300, 264), (64, 200000, 160),
+                                   # 65..128 rows: 128-row weight streaming
+                                   (65, 4096, 1024), (128, 16768, 512), (96, 300, 512), (127, 1000, 2048),
                                    # 256 x 256 tiles: whole tiles, k-split last tiles, ragged M and N
                                    (512, 768, 256), (1024, 2304, 1024), (777, 1000, 512), (1536, 4096, 512),
                                    (600, 300, 4096)])
@@ -308,7 +310,7 @@ def test_pack_w_ds_layout(d_S, r):
     assert np.array_equal(got, _pack_host(W, r))
 
 
-@pytest.mark.parametrize("B", [1, 5, 40, 64, 65, 130])
+@pytest.mark.parametrize("B", [1, 5, 40, 64, 65, 100, 128, 130])
 def test_state_init_packed(B):
     """Proj_dS from the packed W_dS (the layout the benchmark streams) against the oracle."""
     cfg = _small_attn_cfg(B=B, d_model=512, H=8, N=128, lengths="fixed:16")
