@@ -16,7 +16,11 @@ written for a reader to check against the paper by eye:
   K/V, with RoPE positions continuing the prefix (Sec. 3.3.2: KV dimension,
   attention mask, positional alignment; App. B.2 for Qwen3 attention and the
   sliding window);
-* the drafting step, x1 = e + Mamba(RMSNorm(e)), out = x1 + Attn(RMSNorm(x1)).
+* the drafting step, x1 = e + Mamba(RMSNorm(e)), out = x1 + Attn(RMSNorm(x1));
+* the draft head: final RMSNorm, the LM head over the pruned vocabulary (App. B.2,
+  "Pruned drafter vocabulary"), and the first-order Markov correction of each
+  position's logits by the token chosen at the position before it (Sec. 3.3.3),
+  then greedy or Gumbel-max sampled tokens.
 
 Attention is the naive softmax over the full score row; the scan is the
 sequential per-token recurrence.  ``ssd_chunked`` is a second float64
@@ -44,7 +48,7 @@ import numpy as np
 __all__ = [
     "f64", "rmsnorm", "silu", "softplus", "state_init", "in_proj_split", "causal_conv1d",
     "ssd_sequential", "ssd_chunked", "gated_rmsnorm", "mamba_mixer", "gather_slots", "rope",
-    "paged_attention", "attention_layer", "draft_step", "compare",
+    "paged_attention", "attention_layer", "draft_step", "draft_head", "compare",
 ]
 
 
@@ -366,6 +370,42 @@ def draft_step(W, x, cfg, requests=None, return_parts: bool = False):
         return out, dict(S0=S0, F=F, x1=x1, **{"m_" + k: v for k, v in mparts.items()},
                          **{"a_" + k: v for k, v in aparts.items()})
     return out
+
+
+# ------------------------------------------- Sec. 3.3.3 and App. B.2: the draft head
+
+def draft_head(hidden, W, prev_tok, eps: float, temperature: float = 1.0, gumbel=None, forced=None):
+    """Draft tokens from the last hidden states of the block.
+
+    logits_j = RMSNorm(hidden_j) g_f W_lm^T over the pruned vocabulary (App. B.2).
+    The Markov head (Sec. 3.3.3; rank R = 256 in App. B.1) adds to position j a
+    rank-R term selected by the token t_{j-1} chosen at the position before it:
+        l'_j[v] = logits_j[v] + sum_r U_M[v, r] E_M[t_{j-1}, r],
+    with t_{-1} = prev_tok, the request's last committed token.  Then
+        t_j = argmax_v (l'_j[v] / temperature + gumbel_j[v])   (sampling), or
+        t_j = argmax_v l'_j[v]                                  (greedy, gumbel None),
+    the lowest index winning a tie.  Gumbel-max: with gumbel_j[v] = -log(-log u), u ~
+    U(0, 1) drawn independently, t_j is a draw from softmax(l'_j / temperature).
+
+    ``forced`` [B, k] replaces the chosen t_{j-1} by forced[:, j-1] in the Markov term
+    (teacher forcing), so that a second implementation's chain can be checked step by
+    step.  Returns (tokens [B, k] int64, corrected logits l' [B, k, V] float64).
+    """
+    h = f64(hidden)
+    B, k = h.shape[0], h.shape[1]
+    hn = rmsnorm(h, f64(W["norm_f_w"]), eps)
+    logits = hn @ f64(W["W_lm"]).T
+    E, U = f64(W["E_M"]), f64(W["U_M"])
+    tokens = np.zeros((B, k), dtype=np.int64)
+    out = np.empty_like(logits)
+    prev = np.asarray(prev_tok, dtype=np.int64)
+    for j in range(k):
+        lj = logits[:, j, :] + E[prev] @ U.T
+        out[:, j, :] = lj
+        score = lj if gumbel is None else lj / temperature + f64(gumbel)[:, j, :]
+        tokens[:, j] = np.argmax(score, axis=-1)
+        prev = tokens[:, j] if forced is None else np.asarray(forced, dtype=np.int64)[:, j]
+    return tokens, out
 
 
 def compare(gpu, ref) -> dict:

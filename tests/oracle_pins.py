@@ -423,4 +423,70 @@ def pin_attention_layer_dense(O):
         assert np.allclose(out[b], o.reshape(cfg.k, -1) @ W["W_o"].T, rtol=1e-11, atol=1e-12)
 
 
+def _head_weights(rng, V, d, R, lm_std=1.0, markov=None):
+    W = dict(norm_f_w=1.0 + 0.1 * rng.standard_normal(d), W_lm=lm_std * rng.standard_normal((V, d)) / np.sqrt(d))
+    if markov is None:
+        W["E_M"], W["U_M"] = np.zeros((V, R)), np.zeros((V, R))
+    else:
+        W["E_M"], W["U_M"] = markov
+    return W
+
+
+def pin_head_without_markov_is_argmax(O):
+    """With a zero Markov term the head is torch's RMSNorm, a matmul and a per-position
+    argmax (App. B.2: the LM head over the pruned vocabulary)."""
+    import torch
+    rng = rng0(41)
+    B, k, d, V = 3, 5, 24, 50
+    W = _head_weights(rng, V, d, 4)
+    h = rng.standard_normal((B, k, d))
+    tok, logits = O.draft_head(h, W, np.zeros(B, np.int64), eps=1e-6)
+    ht = torch.nn.functional.rms_norm(torch.from_numpy(h), (d,), torch.from_numpy(W["norm_f_w"]), 1e-6)
+    ref = (ht @ torch.from_numpy(W["W_lm"]).T).numpy()
+    assert np.allclose(logits, ref, rtol=1e-12, atol=1e-12)
+    assert np.array_equal(tok, np.argmax(ref, axis=-1))
+
+
+def pin_head_markov_chain_follows_bigram(O):
+    """A Markov term that is a strong bigram t -> pi(t) (E_M one-hot, U_M = alpha * the
+    permutation matrix) makes the drafted chain t_j = pi^(j+1)(prev) whatever the base
+    logits say (Sec. 3.3.3: first-order dependency on the preceding position's token).
+    pi is a 7-cycle, so pi != pi^-1 and a transposed term would walk the other way."""
+    rng = rng0(42)
+    V, k, d = 7, 6, 16
+    pi = (np.arange(V) + 3) % V   # t -> t + 3 (mod 7): one cycle through all 7 tokens
+    cur, seen = 0, []
+    for _ in range(V):
+        seen.append(cur)
+        cur = pi[cur]
+    assert sorted(seen) == list(range(V)) and cur == 0   # a single cycle through all tokens
+    E = np.eye(V)
+    U = np.zeros((V, V))
+    U[pi, np.arange(V)] = 50.0                       # U[pi(t), t]: the term for prev t peaks at pi(t)
+    W = _head_weights(rng, V, d, V, lm_std=0.5, markov=(E, U))
+    prev = np.array([0, 4])
+    h = rng.standard_normal((2, k, d))
+    tok, _ = O.draft_head(h, W, prev, eps=1e-6)
+    for b in range(2):
+        t = prev[b]
+        for j in range(k):
+            t = pi[t]
+            assert tok[b, j] == t, (b, j, tok[b], t)
+
+
+def pin_head_gumbel_max_samples_softmax(O):
+    """Gumbel-max: argmax(l / T + G) with G = -log(-log U) is a draw from softmax(l / T).
+    40,000 requests share one hidden state, so their tokens are 40,000 draws; each token's
+    frequency must lie within 5 binomial standard deviations of scipy's softmax."""
+    rng = rng0(43)
+    V, d, n, T = 5, 8, 40000, 0.7
+    W = _head_weights(rng, V, d, 2, lm_std=1.0)
+    h = np.broadcast_to(rng.standard_normal((1, 1, d)), (n, 1, d))
+    g = -np.log(-np.log(rng.uniform(size=(n, 1, V))))
+    tok, logits = O.draft_head(h, W, np.zeros(n, np.int64), eps=1e-6, temperature=T, gumbel=g)
+    p = scipy.special.softmax(logits[0, 0] / T)
+    freq = np.bincount(tok[:, 0], minlength=V) / n
+    assert np.all(np.abs(freq - p) < 5 * np.sqrt(p * (1 - p) / n) + 1e-12), (freq, p)
+
+
 PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -45,6 +45,11 @@ MUTATIONS = {
     "block_keys_dropped": ("K = np.concatenate([Kc[lo:L], kb[b, :nb]], axis=0)", "K = np.concatenate([Kc[lo:L], kb[b, :0]], axis=0)"),
     "missing_mamba_residual": ("x1 = e + m_out", "x1 = m_out"),
     "missing_attn_residual": ("out_sub = x1 + a_out", "out_sub = a_out"),
+    "head_no_final_norm": ('hn = rmsnorm(h, f64(W["norm_f_w"]), eps)', "hn = h"),
+    "markov_prev_never_advances": ("prev = tokens[:, j] if forced is None", "prev = prev if forced is None"),
+    "markov_factors_swapped": ("lj = logits[:, j, :] + E[prev] @ U.T", "lj = logits[:, j, :] + U[prev] @ E.T"),
+    "gumbel_sign": ("lj / temperature + f64(gumbel)[:, j, :]", "lj / temperature - f64(gumbel)[:, j, :]"),
+    "temperature_multiplies": ("lj / temperature + f64(gumbel)[:, j, :]", "lj * temperature + f64(gumbel)[:, j, :]"),
     "chunk_decay_sign": ("decay = np.exp(lt[:, :, :, None] - lt[:, :, None, :])", "decay = np.exp(lt[:, :, None, :] - lt[:, :, :, None])"),
 }
 
