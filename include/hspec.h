@@ -63,7 +63,7 @@ enum {
 };
 
 /* Device status bits (first int32 of the workspace). */
-enum { HSPEC_DEV_BAD_PAGE = 1, HSPEC_DEV_BAD_CTX_LEN = 2 };
+enum { HSPEC_DEV_BAD_PAGE = 1, HSPEC_DEV_BAD_CTX_LEN = 2, HSPEC_DEV_BAD_TOKEN = 4, HSPEC_DEV_NONFINITE = 8 };
 
 /*
  * Mamba layer configuration (Sec. 3.3.1; sizes of App. B.1 "Mamba").
@@ -179,6 +179,40 @@ hspec_status hspec_draft_step(const hspec_mamba_cfg* mcfg, const hspec_mamba_w* 
                               const void* v_cache, const int32_t* page_table, const int32_t* ctx_lens,
                               int max_ctx_len, float* out, void* workspace, size_t ws_bytes, void* stream);
 size_t hspec_draft_step_workspace(const hspec_mamba_cfg* mcfg, const hspec_attn_cfg* acfg, int max_ctx_len);
+
+/*
+ * Draft head (Sec. 3.3.3 "Causal correction"; App. B.1 "Markov rank"; App. B.2 "Pruned drafter
+ * vocabulary"): from the block's last hidden states to k draft tokens per request.
+ *   logits_j = RMSNorm(hidden_j) norm_f_w W_lm^T                 (V pruned-vocabulary columns)
+ *   l'_j[v]  = logits_j[v] + sum_r U_M[v, r] E_M[t_{j-1}, r]     (first-order Markov term, rank R)
+ *   t_j      = argmax_v l'_j[v]                                   (gumbel == NULL: greedy)
+ *            = argmax_v (l'_j[v] / temperature + gumbel[b, j, v])  (Gumbel-max sampling)
+ * with t_{-1} = prev_tok[b], the request's last committed token; a tie goes to the lowest index.
+ *   hidden [B, k, d_model] fp32 (e.g. the drafting step's output); norm_f_w [d_model] fp32;
+ *   W_lm [V, d_model], E_M [V, R], U_M [V, R] bf16 (V = vocab, R = rank);
+ *   prev_tok [B] int32 in [0, V); gumbel [B, k, V] fp32 or NULL (the caller draws the noise);
+ *   forced [B, k] int32 or NULL: when given, the Markov term of position j uses forced[b, j-1]
+ *   as t_{j-1} (teacher forcing, to score a given continuation) and tokens still receive each
+ *   position's argmax; tokens [B, k] int32 out; logits [B, k, V] fp32 out (the corrected l') or
+ *   NULL.  The normalised hidden state enters the LM head as one bf16 plane.
+ * d_model % 8 == 0 and R % 32 == 0, else HSPEC_ERR_UNSUPPORTED; temperature > 0 when gumbel is
+ * given, else HSPEC_ERR_SHAPE.  Token ids outside [0, V) in prev_tok or forced are read as 0 and
+ * set HSPEC_DEV_BAD_TOKEN; a NaN score counts as -inf and sets HSPEC_DEV_NONFINITE.
+ */
+typedef struct {
+  int B, k, d_model, vocab, rank;
+  float eps, temperature;
+} hspec_head_cfg;
+
+typedef struct {
+  const float* norm_f_w;
+  const void *W_lm, *E_M, *U_M;
+} hspec_head_w;
+
+hspec_status hspec_draft_head(const hspec_head_cfg* cfg, const hspec_head_w* w, const float* hidden,
+                              const int32_t* prev_tok, const float* gumbel, const int32_t* forced,
+                              int32_t* tokens, float* logits, void* workspace, size_t ws_bytes, void* stream);
+size_t hspec_draft_head_workspace(const hspec_head_cfg* cfg);
 
 /* ------------------------------------------------------------- weight preparation */
 

@@ -750,6 +750,81 @@ HSPEC_API hspec_status hspec_linear(hspec_dtype dtype, int M, int N, int K, cons
   return HSPEC_OK;
 }
 
+// ------------------------------------------------------------------------- draft head
+
+hspec_status check_head(const hspec_head_cfg* c) {
+  if (!c) return fail(HSPEC_ERR_NULL, "head config is NULL");
+  if (c->B <= 0 || c->k <= 0 || c->d_model <= 0 || c->vocab <= 0 || c->rank <= 0)
+    return fail(HSPEC_ERR_SHAPE, "non-positive head dimension");
+  if (c->d_model % 8) return fail(HSPEC_ERR_UNSUPPORTED, "d_model must be a multiple of 8");
+  if (c->rank % 32) return fail(HSPEC_ERR_UNSUPPORTED, "the Markov rank must be a multiple of 32");
+  if ((long long)c->B * c->k > (1LL << 30) || (long long)c->vocab * c->rank > (1LL << 40))
+    return fail(HSPEC_ERR_UNSUPPORTED, "head too large");
+  return HSPEC_OK;
+}
+
+struct HeadPlan {
+  int* status = nullptr;
+  bf16* hn = nullptr;
+  float* base = nullptr;
+  unsigned long long* keys = nullptr;
+  GemmScratch gs;
+};
+
+void plan_head(Arena& ar, const hspec_head_cfg& c, HeadPlan& p) {
+  p.status = status_word(ar);
+  const size_t M = (size_t)c.B * c.k;
+  p.hn = ar.take<bf16>(M * c.d_model);
+  p.base = ar.take<float>(M * c.vocab);
+  p.keys = ar.take<unsigned long long>(M);
+  p.gs = reserve_gemm(ar, HSPEC_BF16, {{(int)M, c.vocab, c.d_model}});
+}
+
+HSPEC_API size_t hspec_draft_head_workspace(const hspec_head_cfg* cfg) {
+  if (!cfg || cfg->B <= 0 || cfg->k <= 0 || cfg->d_model <= 0 || cfg->vocab <= 0) return 0;
+  Arena ar;
+  HeadPlan p;
+  plan_head(ar, *cfg, p);
+  return ar.size();
+}
+
+HSPEC_API hspec_status hspec_draft_head(const hspec_head_cfg* cfg, const hspec_head_w* w, const float* hidden,
+                                        const int32_t* prev_tok, const float* gumbel, const int32_t* forced,
+                                        int32_t* tokens, float* logits, void* workspace, size_t ws_bytes,
+                                        void* stream) {
+  g_err.clear();
+  if (hspec_status s = check_head(cfg)) return s;
+  if (!w || !w->norm_f_w || !w->W_lm || !w->E_M || !w->U_M) return fail(HSPEC_ERR_NULL, "head weight is NULL");
+  if (!hidden || !prev_tok || !tokens) return fail(HSPEC_ERR_NULL, "hidden, prev_tok or tokens is NULL");
+  if (gumbel && !(cfg->temperature > 0.f)) return fail(HSPEC_ERR_SHAPE, "sampling needs temperature > 0");
+  if (hspec_status s = check_ws(workspace, ws_bytes, hspec_draft_head_workspace(cfg))) return s;
+  hipStream_t st = (hipStream_t)stream;
+  const hspec_head_cfg& c = *cfg;
+  Arena ar{(char*)workspace};
+  HeadPlan p;
+  plan_head(ar, c, p);
+  HIP_TRY(hspec::launch_zero_words(p.status, hspec::kStatusClear, st));
+  const int M = c.B * c.k;
+  HIP_TRY(hspec::launch_rmsnorm_planes(hidden, 0, w->norm_f_w, M, c.d_model, c.eps, p.hn, nullptr, st));
+  // LM head over the pruned vocabulary; written straight into the caller's logits when given
+  float* base = logits ? logits : p.base;
+  hspec::GemmArgs g;
+  g.A_hi = p.hn; g.lda = c.d_model;
+  g.W_hi = static_cast<const bf16*>(w->W_lm); g.ldw = c.d_model;
+  g.M = M; g.N = c.vocab; g.K = c.d_model;
+  g.C = base; g.ldc = c.vocab;
+  use_scratch(g, p.gs);
+  HIP_TRY(hspec::launch_gemm(g, st));
+  hspec::HeadArgs h;
+  h.B = c.B; h.k = c.k; h.V = c.vocab; h.R = c.rank;
+  h.E = static_cast<const bf16*>(w->E_M); h.U = static_cast<const bf16*>(w->U_M);
+  h.base = base; h.logits = logits; h.gumbel = gumbel;
+  h.inv_temp = gumbel ? 1.f / c.temperature : 1.f;
+  h.prev = prev_tok; h.forced = forced; h.keys = p.keys; h.tokens = tokens; h.status = p.status;
+  HIP_TRY(hspec::launch_markov_head(h, st));
+  return HSPEC_OK;
+}
+
 HSPEC_API size_t hspec_pack_w_ds_bytes(int d_S, int r) {
   if (d_S <= 0 || r <= 0 || d_S % 16 || r % 64) return 0;
   return (size_t)d_S * r * sizeof(bf16);

@@ -1,0 +1,158 @@
+// Draft head: the Markov correction of the block's logits and the choice of draft tokens
+// (Sec. 3.3.3 causal correction; App. B.1 "Markov rank"; App. B.2 "Pruned drafter vocabulary").
+//
+// Position j of request b gets the logits of the LM head plus a rank-R term picked by the token
+// chosen at position j - 1:
+//   l'[b, j, v] = base[b, j, v] + sum_r E[t_{b, j-1}, r] U[v, r],   t_{b, -1} = prev[b],
+// and its token is the argmax over v of l' (greedy) or of l' / T + G (Gumbel-max sampling with
+// the caller's noise G).  The chain is sequential in j, so each position is one launch:
+//   * a workgroup owns 128 vocabulary columns and all requests (in tiles of 64);
+//   * the rank-R product is one MFMA tile per (16 requests, 16 columns), its operands read
+//     straight from L2 (E rows gathered by token, U rows of the workgroup's columns);
+//   * the argmax across workgroups is a 64-bit atomicMax on (orderable score << 32 | ~column),
+//     which picks the largest score and, among equal scores, the lowest column;
+//   * the next launch decodes the previous position's token from that key.
+#include "common.h"
+#include "kernels.h"
+
+namespace hspec {
+namespace {
+
+constexpr int MK_COLS = 128;   // vocabulary columns per workgroup (4 waves x 2 MFMA column blocks)
+constexpr int MK_ROWS = 64;    // requests per tile (4 MFMA row blocks)
+constexpr int ST_BAD_TOKEN = 4;
+constexpr int ST_NONFINITE = 8;
+
+// Order-preserving map of a float to uint32 (larger float, larger key); NaN is mapped as -inf.
+__device__ __forceinline__ unsigned long long score_key(float s, int col) {
+  unsigned u = __float_as_uint(s);
+  const unsigned ord = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((unsigned long long)ord << 32) | (0xffffffffu - (unsigned)col);
+}
+__device__ __forceinline__ int key_token(unsigned long long key) {
+  return (int)(0xffffffffu - (unsigned)(key & 0xffffffffu));
+}
+__device__ __forceinline__ unsigned long long shfl_xor_u64(unsigned long long v, int m) {
+  const unsigned lo = __shfl_xor((unsigned)(v & 0xffffffffu), m);
+  const unsigned hi = __shfl_xor((unsigned)(v >> 32), m);
+  return ((unsigned long long)hi << 32) | lo;
+}
+
+__global__ void __launch_bounds__(256) markov_step_kernel(HeadArgs a, int j) {
+  __shared__ int s_prev[MK_ROWS];
+  __shared__ unsigned long long s_best[4][MK_ROWS];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int vw = blockIdx.x * MK_COLS + wave * 32;   // first column of this wave
+  const int l16 = lane & 15, g4 = lane >> 4;
+
+  for (int b0 = 0; b0 < a.B; b0 += MK_ROWS) {
+    if (tid < MK_ROWS) {
+      const int b = b0 + tid;
+      int t = 0;
+      if (b < a.B) {
+        if (j == 0) t = a.prev[b];
+        else if (a.forced) t = a.forced[(size_t)b * a.k + j - 1];
+        else t = key_token(a.keys[(size_t)b * a.k + j - 1]);
+        if (t < 0 || t >= a.V) {
+          if (blockIdx.x == 0) set_status(a.status, ST_BAD_TOKEN);
+          t = 0;
+        }
+      }
+      s_prev[tid] = t;
+    }
+    __syncthreads();
+
+    // adj[b][v] = E[prev_b] . U[v] over the rank, 32 at a time
+    f32x4 acc[4][2];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const bf16* erow[4];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) erow[rb] = a.E + (size_t)s_prev[rb * 16 + l16] * a.R + 8 * g4;
+    const bf16* urow[2];
+    bool ucol[2];
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb) {
+      const int col = vw + cb * 16 + l16;
+      ucol[cb] = col < a.V;
+      urow[cb] = a.U + (size_t)(ucol[cb] ? col : 0) * a.R + 8 * g4;
+    }
+    for (int ks = 0; ks < a.R; ks += 32) {
+      bf16x8 ef[4], uf[2];
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb) ef[rb] = ld8(erow[rb] + ks);
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb) uf[cb] = ucol[cb] ? ld8(urow[cb] + ks) : zero8();
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb) acc[rb][cb] = mma16(ef[rb], uf[cb], acc[rb][cb]);
+    }
+
+    // corrected logits, scores, and the best (score, column) of each request in this wave
+    bool bad = false;
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = rb * 16 + 4 * g4 + i;
+        const int b = b0 + r;
+        unsigned long long best = 0;
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb) {
+          const int col = vw + cb * 16 + l16;
+          if (b < a.B && col < a.V) {
+            const size_t off = ((size_t)b * a.k + j) * a.V + col;
+            const float l = a.base[off] + acc[rb][cb][i];
+            if (a.logits) a.logits[off] = l;
+            float sc = a.gumbel ? l * a.inv_temp + a.gumbel[off] : l;
+            if (!(sc == sc)) {
+              bad = true;
+              sc = -INFINITY;
+            }
+            const unsigned long long key = score_key(sc, col);
+            best = key > best ? key : best;
+          }
+        }
+#pragma unroll
+        for (int m = 1; m < 16; m <<= 1) {
+          const unsigned long long o = shfl_xor_u64(best, m);
+          best = o > best ? o : best;
+        }
+        if (l16 == 0) s_best[wave][r] = best;
+      }
+    if (bad) set_status(a.status, ST_NONFINITE);
+    __syncthreads();
+    if (tid < MK_ROWS && b0 + tid < a.B) {
+      unsigned long long best = s_best[0][tid];
+#pragma unroll
+      for (int w = 1; w < 4; ++w) best = s_best[w][tid] > best ? s_best[w][tid] : best;
+      if (best) atomicMax(a.keys + (size_t)(b0 + tid) * a.k + j, best);
+    }
+    __syncthreads();   // s_prev and s_best are reused by the next request tile
+  }
+}
+
+__global__ void head_tokens_kernel(const unsigned long long* keys, int n, int32_t* tokens) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) tokens[i] = key_token(keys[i]);
+}
+
+}  // namespace
+
+hipError_t launch_markov_head(const HeadArgs& a, hipStream_t s) {
+  if (a.B <= 0 || a.k <= 0) return hipSuccess;
+  const int n = a.B * a.k;
+  if (hipError_t e = launch_zero_words(reinterpret_cast<int*>(a.keys), 2 * n, s)) return e;
+  const int grid = (a.V + MK_COLS - 1) / MK_COLS;
+  for (int j = 0; j < a.k; ++j) {
+    hipLaunchKernelGGL(markov_step_kernel, dim3(grid), dim3(256), 0, s, a, j);
+    if (hipError_t e = hipGetLastError()) return e;
+  }
+  hipLaunchKernelGGL(head_tokens_kernel, dim3((n + 255) / 256), dim3(256), 0, s, a.keys, n, a.tokens);
+  return hipGetLastError();
+}
+
+}  // namespace hspec

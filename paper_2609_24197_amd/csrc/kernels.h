@@ -120,4 +120,21 @@ hipError_t launch_split_planes(const float* x, size_t n, bf16* hi, bf16* lo, hip
 // Zero n int32 words (device status, counters) with a kernel, graph-capture safe.
 hipError_t launch_zero_words(int* p, int n, hipStream_t s);
 
+// Markov correction and token choice of the draft head (one launch per block position).
+struct HeadArgs {
+  int B = 0, k = 0, V = 0, R = 0;
+  const bf16* E = nullptr;            // [V, R] rank-R code of the preceding token
+  const bf16* U = nullptr;            // [V, R] rank-R output factor
+  const float* base = nullptr;        // [B*k, V] LM-head logits
+  float* logits = nullptr;            // [B*k, V] corrected logits, or null (may equal base)
+  const float* gumbel = nullptr;      // [B*k, V] sampling noise, or null (greedy)
+  float inv_temp = 1.f;               // 1 / temperature, with gumbel
+  const int32_t* prev = nullptr;      // [B] last committed token
+  const int32_t* forced = nullptr;    // [B, k] tokens used as t_{j-1} instead of the chosen ones, or null
+  unsigned long long* keys = nullptr; // [B*k] argmax keys (workspace)
+  int32_t* tokens = nullptr;          // [B*k] out
+  int* status = nullptr;
+};
+hipError_t launch_markov_head(const HeadArgs& a, hipStream_t s);
+
 }  // namespace hspec

@@ -20,7 +20,7 @@ _lib = None
 BF16, F32 = 0, 1
 BLOCK_CAUSAL = 1
 W_DS_PACKED = 1
-DEV_BAD_PAGE, DEV_BAD_CTX_LEN = 1, 2
+DEV_BAD_PAGE, DEV_BAD_CTX_LEN, DEV_BAD_TOKEN, DEV_NONFINITE = 1, 2, 4, 8
 STATUS = {0: "HSPEC_OK", 1: "HSPEC_ERR_NULL", 2: "HSPEC_ERR_SHAPE", 3: "HSPEC_ERR_DTYPE",
           4: "HSPEC_ERR_UNSUPPORTED", 5: "HSPEC_ERR_WORKSPACE", 6: "HSPEC_ERR_LAUNCH"}
 
@@ -44,6 +44,15 @@ class AttnCfg(C.Structure):
 
 class AttnW(C.Structure):
     _fields_ = [(n, C.c_void_p) for n in ("W_q", "W_k", "W_v", "W_o", "q_norm_w", "k_norm_w")]
+
+
+class HeadCfg(C.Structure):
+    _fields_ = [(n, C.c_int) for n in ("B", "k", "d_model", "vocab", "rank")] + [
+        ("eps", C.c_float), ("temperature", C.c_float)]
+
+
+class HeadW(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in ("norm_f_w", "W_lm", "E_M", "U_M")]
 
 
 class HspecError(RuntimeError):
@@ -78,6 +87,9 @@ EXPORTS = {
                                                       C.c_void_p]),
     "hspec_linear": (C.c_int, [C.c_int] * 4 + [C.c_void_p] * 5 + [C.c_size_t, C.c_void_p]),
     "hspec_linear_workspace": (C.c_size_t, [C.c_int] * 4),
+    "hspec_draft_head": (C.c_int, [C.POINTER(HeadCfg), C.POINTER(HeadW)] + [C.c_void_p] * 7 + [C.c_size_t,
+                                                                                          C.c_void_p]),
+    "hspec_draft_head_workspace": (C.c_size_t, [C.POINTER(HeadCfg)]),
     "hspec_pack_w_ds_bytes": (C.c_size_t, [C.c_int, C.c_int]),
     "hspec_pack_w_ds": (C.c_int, [C.c_int, C.c_int, C.c_void_p, C.c_void_p, C.c_void_p]),
     "hspec_read_status": (C.c_int, [C.c_void_p, C.POINTER(C.c_int32), C.c_void_p]),
@@ -283,3 +295,18 @@ def linear(dtype, A, W, C_out, ws, R=None):
     N = W.shape[0]
     _check(lib().hspec_linear(dtype, M, N, K, ptr(A), ptr(W), ptr(R), ptr(C_out), ptr(ws), ws.numel(),
                               stream_ptr()))
+
+
+def head_cfg(cfg, vocab: int, rank: int, temperature: float = 1.0) -> HeadCfg:
+    return HeadCfg(cfg.B, cfg.k, cfg.d_model, int(vocab), int(rank), cfg.eps, float(temperature))
+
+
+def draft_head_workspace(hc: HeadCfg) -> int:
+    return lib().hspec_draft_head_workspace(C.byref(hc))
+
+
+def draft_head(hc: HeadCfg, W: dict, hidden, prev_tok, tokens, ws, logits=None, gumbel=None, forced=None):
+    """tokens [B, k] int32 (and the corrected logits [B, k, V] if given) = hspec_draft_head."""
+    hw = HeadW(*(ptr(W[n]) for n in ("norm_f_w", "W_lm", "E_M", "U_M")))
+    _check(lib().hspec_draft_head(C.byref(hc), C.byref(hw), ptr(hidden), ptr(prev_tok), ptr(gumbel), ptr(forced),
+                                  ptr(tokens), ptr(logits), ptr(ws), ws.numel(), stream_ptr()))

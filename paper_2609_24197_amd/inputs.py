@@ -275,3 +275,37 @@ def make_attn_inputs(cfg: StepConfig, seed=0, extra_pages=0, pad_pages=0):
     x["k_blk"] = normal("attn_kblk", (cfg.B, cfg.k, cfg.Hkv, cfg.D), 1.0, seed, cfg.dtype)
     x["v_blk"] = normal("attn_vblk", (cfg.B, cfg.k, cfg.Hkv, cfg.D), 1.0, seed, cfg.dtype)
     return x
+
+
+HEAD_VOCAB = 32000   # pruned drafter vocabulary (App. B.2)
+HEAD_RANK = 256      # Markov rank (App. B.1)
+
+
+def make_head_weights(cfg: StepConfig, seed: int = 0, vocab: int = HEAD_VOCAB, rank: int = HEAD_RANK) -> dict:
+    """Draft-head weights: final norm gain, LM head [V, d_model] ~ N(0, 1/d_model), and the two
+    rank-R Markov factors E_M, U_M [V, R] ~ N(0, 1/R) (bf16)."""
+    return {
+        "norm_f_w": normal("norm_f_w", (cfg.d_model,), 0.1, seed, "f32", 1.0),
+        "W_lm": normal("W_lm", (vocab, cfg.d_model), cfg.d_model ** -0.5, seed, "bf16"),
+        "E_M": normal("E_M", (vocab, rank), 1.0, seed, "bf16"),
+        "U_M": normal("U_M", (vocab, rank), rank ** -0.5, seed, "bf16"),
+    }
+
+
+def make_head_inputs(cfg: StepConfig, seed: int = 0, vocab: int = HEAD_VOCAB, sample: bool = False) -> dict:
+    """Hidden states [B, k, d_model] fp32 ~ N(0, 1), the last committed token of each request, and
+    (sample=True) Gumbel noise -log(-log u), u ~ U(0, 1), for every (request, position, token)."""
+    x = {
+        "hidden": normal("head_hidden", (cfg.B, cfg.k, cfg.d_model), 1.0, seed, "f32"),
+        "prev_tok": _stream(seed, "prev_tok").integers(0, vocab, size=cfg.B).astype(np.int32),
+    }
+    if sample:
+        n = cfg.B * cfg.k * vocab
+        u = np.empty(n, dtype=np.float64)
+        nblk = (n + BLOCK - 1) // BLOCK
+        for i in range(nblk):
+            lo, hi = i * BLOCK, min(n, (i + 1) * BLOCK)
+            u[lo:hi] = _stream(seed, "gumbel_u", i).random(hi - lo)
+        u = np.clip(u, 1e-300, None)
+        x["gumbel"] = (-np.log(-np.log(u))).astype(np.float32).reshape(cfg.B, cfg.k, vocab)
+    return x

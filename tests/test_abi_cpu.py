@@ -115,6 +115,27 @@ def test_window_bounds_the_swept_context():
     assert full - win >= 64 * 8 * (313 - 32) * 64 * 4 * 128
 
 
+def test_draft_head_validation():
+    L = _lib()
+    ws, n = _ws_big()
+    cfg = I.CONFIGS[3]
+    w = hspec.HeadW(FAKE.value, FAKE.value, FAKE.value, FAKE.value)
+    def call(ptrs=None, **kw):
+        c = hspec.head_cfg(cfg, 32000, 256, kw.pop("temperature", 1.0))
+        for k, v in kw.items():
+            setattr(c, k, v)
+        p = ptrs or [FAKE] * 6
+        return L.hspec_draft_head(C.byref(c), C.byref(w), *p, ws, n, None)
+    assert call(rank=48) == 4
+    assert call(d_model=100) == 4
+    assert call(vocab=0) == 2
+    assert call(ptrs=[FAKE, FAKE, FAKE, None, FAKE, None], temperature=0.0) == 2   # sampling at T = 0
+    assert call(ptrs=[None] + [FAKE] * 5) == 1
+    assert call(ptrs=[FAKE, FAKE, None, None, None, None]) == 1                    # tokens NULL
+    c = hspec.head_cfg(cfg, 32000, 256)
+    assert L.hspec_draft_head_workspace(C.byref(c)) > 64 * 16 * 32000 * 4
+
+
 def test_paged_attn_phase_validation():
     L = _lib()
     ws, n = _ws_big()
