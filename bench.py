@@ -101,6 +101,29 @@ def time_attention(cfg, Ad, o, aws, maxL, n: int, warmup: int, context, torch):
     return t_sweep, t_core
 
 
+def head_figures(cfg, out, step, args, torch):
+    """Timing of hspec_draft_head on the drafting step's output, each call after one step, and
+    of its LM-head product ([B*k, d_model] x [d_model, V], bf16) launched alone."""
+    V, R = I.HEAD_VOCAB, I.HEAD_RANK
+    HW = {k: hspec.to_device(v) for k, v in I.make_head_weights(cfg, args.seed).items()}
+    prev = hspec.to_device(I.make_head_inputs(cfg, args.seed)["prev_tok"])
+    hc = hspec.head_cfg(cfg, V, R)
+    hws = hspec.workspace(hspec.draft_head_workspace(hc))
+    tok = torch.empty((cfg.B, cfg.k), dtype=torch.int32, device="cuda")
+    t_head = time_in_step(lambda: hspec.draft_head(hc, HW, out, prev, tok, hws), args.steps, args.warmup, step, torch)
+    assert hspec.read_status(hws) == 0
+    M = cfg.B * cfg.k
+    A = torch.randn(M, cfg.d_model, device="cuda").to(torch.bfloat16)
+    C = torch.empty(M, V, device="cuda")
+    lws = hspec.workspace(hspec.linear_workspace(hspec.BF16, M, V, cfg.d_model))
+    t_lm = time_in_step(lambda: hspec.linear(hspec.BF16, A, HW["W_lm"], C, lws), args.steps, args.warmup, step, torch)
+    flops = 2 * M * V * cfg.d_model
+    log(f"draft head: {t_head * 1e6:.1f} us (LM-head GEMM alone {t_lm * 1e6:.1f} us, {flops / t_lm / 1e12:.0f} TFLOP/s)")
+    return {"avg_us": round(t_head * 1e6, 2), "vocab": V, "markov_rank": R, "tokens": "greedy",
+            "lm_head_gemm_us": round(t_lm * 1e6, 2), "lm_head_tflops": round(flops / t_lm / 1e12, 1),
+            "lm_head_frac_of_bf16_peak": round(flops / t_lm / 1e12 / RL.MFMA_BF16_PEAK_TFLOPS, 4)}
+
+
 def cpu_baseline(cfg, W, x, n_req: int):
     """The float64 oracle on the first n_req requests of the same workload (all positions)."""
     import oracle.hspec_oracle as O
@@ -260,6 +283,10 @@ def main():
                                                   "achieved": round(b_sweep / t_core / 1e9, 1)}}
     del Ad, aws, o
 
+    # the draft head after the step (final norm, LM head over the pruned vocabulary, Markov
+    # correction, greedy tokens) on the step's own output, and its LM-head GEMM alone
+    head = head_figures(cfg, out, step, args, torch)
+
     cpu = None
     if not args.no_cpu_baseline:
         del Wd, Xd, ws, out
@@ -281,6 +308,7 @@ def main():
         "roofline": roof,
         "roofline_kv_sweep": roof_sweep,
         "cpu_baseline": cpu,
+        "draft_head": dict(head, drafted_tok_s_with_head=round(cfg.B * cfg.k / (ms / 1e3 + head["avg_us"] / 1e6), 1)),
         "step_bytes_ideal": int(RL.step_bytes(cfg, L)),
     }
     print(json.dumps(rec), flush=True)

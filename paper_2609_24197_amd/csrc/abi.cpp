@@ -803,7 +803,10 @@ HSPEC_API hspec_status hspec_draft_head(const hspec_head_cfg* cfg, const hspec_h
   Arena ar{(char*)workspace};
   HeadPlan p;
   plan_head(ar, c, p);
-  HIP_TRY(hspec::launch_zero_words(p.status, hspec::kStatusClear, st));
+  hspec::HeadArgs h;
+  h.B = c.B; h.k = c.k; h.V = c.vocab; h.R = c.rank;
+  h.keys = p.keys; h.status = p.status;
+  HIP_TRY(hspec::launch_head_clear(h, hspec::kStatusClear, st));
   const int M = c.B * c.k;
   HIP_TRY(hspec::launch_rmsnorm_planes(hidden, 0, w->norm_f_w, M, c.d_model, c.eps, p.hn, nullptr, st));
   // LM head over the pruned vocabulary; written straight into the caller's logits when given
@@ -815,12 +818,10 @@ HSPEC_API hspec_status hspec_draft_head(const hspec_head_cfg* cfg, const hspec_h
   g.C = base; g.ldc = c.vocab;
   use_scratch(g, p.gs);
   HIP_TRY(hspec::launch_gemm(g, st));
-  hspec::HeadArgs h;
-  h.B = c.B; h.k = c.k; h.V = c.vocab; h.R = c.rank;
   h.E = static_cast<const bf16*>(w->E_M); h.U = static_cast<const bf16*>(w->U_M);
   h.base = base; h.logits = logits; h.gumbel = gumbel;
   h.inv_temp = gumbel ? 1.f / c.temperature : 1.f;
-  h.prev = prev_tok; h.forced = forced; h.keys = p.keys; h.tokens = tokens; h.status = p.status;
+  h.prev = prev_tok; h.forced = forced; h.tokens = tokens;
   HIP_TRY(hspec::launch_markov_head(h, st));
   return HSPEC_OK;
 }

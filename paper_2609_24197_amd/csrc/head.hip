@@ -38,12 +38,18 @@ __device__ __forceinline__ unsigned long long shfl_xor_u64(unsigned long long v,
   return ((unsigned long long)hi << 32) | lo;
 }
 
+// RK: rank / 32 when known at compile time (every fragment load is issued before the first
+// MFMA), 0 for any rank that is a multiple of 32 (one round of loads per 32).
+template <int RK>
 __global__ void __launch_bounds__(256) markov_step_kernel(HeadArgs a, int j) {
   __shared__ int s_prev[MK_ROWS];
   __shared__ unsigned long long s_best[4][MK_ROWS];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int vw = blockIdx.x * MK_COLS + wave * 32;   // first column of this wave
   const int l16 = lane & 15, g4 = lane >> 4;
+  // the next position's keys start at zero; they are first updated by the next launch
+  if (blockIdx.x == 0 && j + 1 < a.k)
+    for (int b = tid; b < a.B; b += 256) a.keys[(size_t)b * a.k + j + 1] = 0;
 
   for (int b0 = 0; b0 < a.B; b0 += MK_ROWS) {
     if (tid < MK_ROWS) {
@@ -62,7 +68,19 @@ __global__ void __launch_bounds__(256) markov_step_kernel(HeadArgs a, int j) {
     }
     __syncthreads();
 
-    // adj[b][v] = E[prev_b] . U[v] over the rank, 32 at a time
+    // this tile's LM-head logits, loaded while the rank product runs
+    float base[4][4][2];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb) {
+          const int b = b0 + rb * 16 + 4 * g4 + i, col = vw + cb * 16 + l16;
+          base[rb][i][cb] = (b < a.B && col < a.V) ? a.base[((size_t)b * a.k + j) * a.V + col] : 0.f;
+        }
+
+    // adj[b][v] = E[prev_b] . U[v] over the rank
     f32x4 acc[4][2];
 #pragma unroll
     for (int rb = 0; rb < 4; ++rb)
@@ -79,16 +97,27 @@ __global__ void __launch_bounds__(256) markov_step_kernel(HeadArgs a, int j) {
       ucol[cb] = col < a.V;
       urow[cb] = a.U + (size_t)(ucol[cb] ? col : 0) * a.R + 8 * g4;
     }
-    for (int ks = 0; ks < a.R; ks += 32) {
-      bf16x8 ef[4], uf[2];
+    auto rank_steps = [&](int ks0, auto nsteps) {
+      constexpr int NS = decltype(nsteps)::value;
+      bf16x8 ef[NS][4], uf[NS][2];
 #pragma unroll
-      for (int rb = 0; rb < 4; ++rb) ef[rb] = ld8(erow[rb] + ks);
+      for (int s = 0; s < NS; ++s) {
 #pragma unroll
-      for (int cb = 0; cb < 2; ++cb) uf[cb] = ucol[cb] ? ld8(urow[cb] + ks) : zero8();
+        for (int rb = 0; rb < 4; ++rb) ef[s][rb] = ld8(erow[rb] + ks0 + 32 * s);
 #pragma unroll
-      for (int rb = 0; rb < 4; ++rb)
+        for (int cb = 0; cb < 2; ++cb) uf[s][cb] = ucol[cb] ? ld8(urow[cb] + ks0 + 32 * s) : zero8();
+      }
 #pragma unroll
-        for (int cb = 0; cb < 2; ++cb) acc[rb][cb] = mma16(ef[rb], uf[cb], acc[rb][cb]);
+      for (int s = 0; s < NS; ++s)
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+          for (int cb = 0; cb < 2; ++cb) acc[rb][cb] = mma16(ef[s][rb], uf[s][cb], acc[rb][cb]);
+    };
+    if constexpr (RK > 0) {
+      rank_steps(0, Int<RK>{});
+    } else {
+      for (int ks = 0; ks < a.R; ks += 32) rank_steps(ks, Int<1>{});
     }
 
     // corrected logits, scores, and the best (score, column) of each request in this wave
@@ -105,7 +134,7 @@ __global__ void __launch_bounds__(256) markov_step_kernel(HeadArgs a, int j) {
           const int col = vw + cb * 16 + l16;
           if (b < a.B && col < a.V) {
             const size_t off = ((size_t)b * a.k + j) * a.V + col;
-            const float l = a.base[off] + acc[rb][cb][i];
+            const float l = base[rb][i][cb] + acc[rb][cb][i];
             if (a.logits) a.logits[off] = l;
             float sc = a.gumbel ? l * a.inv_temp + a.gumbel[off] : l;
             if (!(sc == sc)) {
@@ -135,6 +164,12 @@ __global__ void __launch_bounds__(256) markov_step_kernel(HeadArgs a, int j) {
   }
 }
 
+// The call's first kernel: status words and the keys of position 0.
+__global__ void head_clear_kernel(int* status, int nwords, unsigned long long* keys, int B, int k) {
+  for (int i = threadIdx.x; i < nwords; i += blockDim.x) status[i] = 0;
+  for (int b = threadIdx.x; b < B; b += blockDim.x) keys[(size_t)b * k] = 0;
+}
+
 __global__ void head_tokens_kernel(const unsigned long long* keys, int n, int32_t* tokens) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) tokens[i] = key_token(keys[i]);
@@ -145,13 +180,18 @@ __global__ void head_tokens_kernel(const unsigned long long* keys, int n, int32_
 hipError_t launch_markov_head(const HeadArgs& a, hipStream_t s) {
   if (a.B <= 0 || a.k <= 0) return hipSuccess;
   const int n = a.B * a.k;
-  if (hipError_t e = launch_zero_words(reinterpret_cast<int*>(a.keys), 2 * n, s)) return e;
   const int grid = (a.V + MK_COLS - 1) / MK_COLS;
+  auto kern = a.R == 256 ? markov_step_kernel<8> : markov_step_kernel<0>;
   for (int j = 0; j < a.k; ++j) {
-    hipLaunchKernelGGL(markov_step_kernel, dim3(grid), dim3(256), 0, s, a, j);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, a, j);
     if (hipError_t e = hipGetLastError()) return e;
   }
   hipLaunchKernelGGL(head_tokens_kernel, dim3((n + 255) / 256), dim3(256), 0, s, a.keys, n, a.tokens);
+  return hipGetLastError();
+}
+
+hipError_t launch_head_clear(const HeadArgs& a, int status_words, hipStream_t s) {
+  hipLaunchKernelGGL(head_clear_kernel, dim3(1), dim3(256), 0, s, a.status, status_words, a.keys, a.B, a.k);
   return hipGetLastError();
 }
 

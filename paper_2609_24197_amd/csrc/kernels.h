@@ -135,6 +135,10 @@ struct HeadArgs {
   int32_t* tokens = nullptr;          // [B*k] out
   int* status = nullptr;
 };
+// Clears the status words and the keys of position 0: the first kernel of a head call.
+hipError_t launch_head_clear(const HeadArgs& a, int status_words, hipStream_t s);
+// One Markov-correction launch per block position (each clears the next position's keys),
+// then the tokens.
 hipError_t launch_markov_head(const HeadArgs& a, hipStream_t s);
 
 }  // namespace hspec
