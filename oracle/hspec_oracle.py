@@ -17,6 +17,10 @@ written for a reader to check against the paper by eye:
   attention mask, positional alignment; App. B.2 for Qwen3 attention and the
   sliding window);
 * the drafting step, x1 = e + Mamba(RMSNorm(e)), out = x1 + Attn(RMSNorm(x1));
+* the whole drafter (Sec. 3.3; App. B.1 "Number of drafter layers" and "Target-layer
+  mapping"): one S_init shared by every layer's Mamba, then layers of Mamba, attention
+  over that layer's own target cache (absent in the partial layer) and a SwiGLU MLP,
+  each pre-normed with a residual;
 * the draft head: final RMSNorm, the LM head over the pruned vocabulary (App. B.2,
   "Pruned drafter vocabulary"), and the first-order Markov correction of each
   position's logits by the token chosen at the position before it (Sec. 3.3.3),
@@ -48,7 +52,7 @@ import numpy as np
 __all__ = [
     "f64", "rmsnorm", "silu", "softplus", "state_init", "in_proj_split", "causal_conv1d",
     "ssd_sequential", "ssd_chunked", "gated_rmsnorm", "mamba_mixer", "gather_slots", "rope",
-    "paged_attention", "attention_layer", "draft_step", "draft_head", "compare",
+    "paged_attention", "attention_layer", "draft_step", "mlp", "drafter_forward", "draft_head", "compare",
 ]
 
 
@@ -369,6 +373,44 @@ def draft_step(W, x, cfg, requests=None, return_parts: bool = False):
     if return_parts:
         return out, dict(S0=S0, F=F, x1=x1, **{"m_" + k: v for k, v in mparts.items()},
                          **{"a_" + k: v for k, v in aparts.items()})
+    return out
+
+
+# ---------------------------------------- Sec. 3.3 and App. B.1: the whole drafter
+
+def mlp(x: np.ndarray, W) -> np.ndarray:
+    """SwiGLU MLP of the drafter layers (hidden size = the target's, App. B.1 "MLP"):
+    (SiLU(x W_gate^T) * (x W_up^T)) W_down^T."""
+    return (silu(x @ f64(W["W_gate"]).T) * (x @ f64(W["W_up"]).T)) @ f64(W["W_down"]).T
+
+
+def drafter_forward(layers, shared, x, caches, cfg, requests=None):
+    """The drafter's block forward (Sec. 3.3; App. B.1).
+
+    S_init = state_init(h_last) is computed once, from the |M| fused target layers, and given
+    to the Mamba module of every layer.  Then, from x = e (the block embeddings), for each
+    layer W in ``layers``:
+        x = x + Mamba(RMSNorm(x) norm1_w; S_init)
+        x = x + Attn(RMSNorm(x) norm2_w) over caches[W["cache"]]   (layers with attention)
+        x = x + MLP(RMSNorm(x) norm3_w)
+    ``shared`` holds W_r and W_dS; ``caches`` is a list of dicts with k_cache and v_cache
+    (one per target layer an attention reads); x holds h_last, block_emb, page_table and
+    ctx_lens, the page table and lengths being shared by all target layers.  ``requests``
+    restricts the work to some rows; the others are NaN.
+    """
+    idx = np.arange(cfg.B) if requests is None else np.asarray(requests)
+    S0, _ = state_init(np.asarray(x["h_last"])[idx], shared["W_r"], shared["W_dS"], cfg.H, cfg.P, cfg.N)
+    h = f64(np.asarray(x["block_emb"])[idx])
+    for W in layers:
+        h = h + mamba_mixer(rmsnorm(h, f64(W["norm1_w"]), cfg.eps), S0, W, cfg)
+        if W.get("cache") is not None:
+            c = caches[W["cache"]]
+            cache = dict(k_cache=c["k_cache"], v_cache=c["v_cache"], page_table=np.asarray(x["page_table"])[idx],
+                         ctx_lens=np.asarray(x["ctx_lens"])[idx])
+            h = h + attention_layer(rmsnorm(h, f64(W["norm2_w"]), cfg.eps), W, cache, cfg)
+        h = h + mlp(rmsnorm(h, f64(W["norm3_w"]), cfg.eps), W)
+    out = np.full((cfg.B,) + h.shape[1:], np.nan)
+    out[idx] = h
     return out
 
 

@@ -59,12 +59,17 @@ class StepConfig:
     eps: float = 1e-6
     rope_theta: float = 1e6
     n_fuse: int = 1   # |M|, number of fused target layers
+    ff: int = 0       # MLP hidden size of the full drafter, 0 = 3 * d_model
     r: int = 0        # fusion rank, 0 = d_model
     split_tokens: int = 0  # split-K size for the KV sweep, 0 = automatic
 
     @property
     def d_h(self) -> int:
         return self.n_fuse * self.d_model
+
+    @property
+    def d_ff(self) -> int:
+        return self.ff or 3 * self.d_model
 
     @property
     def rank(self) -> int:
@@ -201,15 +206,16 @@ def make_page_table(cfg: StepConfig, lengths: np.ndarray, seed: int = 0, extra_p
     return table, max(num_pages, 1)
 
 
-def make_weights(cfg: StepConfig, seed: int = 0, skip=()) -> dict:
-    """Synthetic drafter weights: W ~ N(0, 1/fan_in), stored as [out, in]."""
+def make_weights(cfg: StepConfig, seed: int = 0, skip=(), prefix: str = "") -> dict:
+    """Synthetic drafter weights: W ~ N(0, 1/fan_in), stored as [out, in].  ``prefix`` keys the
+    random streams (one set of weights per drafter layer); the dict keys stay the same."""
     dt = cfg.dtype
     H, dm, di = cfg.H, cfg.d_model, cfg.d_inner
     w = {}
 
     def add(name, shape, std, store=dt, mean=0.0):
         if name not in skip:
-            w[name] = normal(name, shape, std, seed, store, mean)
+            w[name] = normal(prefix + name, shape, std, seed, store, mean)
 
     add("W_r", (cfg.rank, cfg.d_h), cfg.d_h ** -0.5)
     add("W_dS", (cfg.d_S, cfg.rank), cfg.rank ** -0.5)
@@ -217,10 +223,10 @@ def make_weights(cfg: StepConfig, seed: int = 0, skip=()) -> dict:
     add("conv_w", (cfg.conv_dim, cfg.conv_w), cfg.conv_w ** -0.5)
     add("conv_b", (cfg.conv_dim,), cfg.conv_w ** -0.5)
     # dt bias: inverse softplus of dt0, log-uniform in [1e-3, 1e-1] (Mamba-2 initialisation)
-    u = _stream(seed, "dt_bias").uniform(math.log(1e-3), math.log(1e-1), size=H)
+    u = _stream(seed, prefix + "dt_bias").uniform(math.log(1e-3), math.log(1e-1), size=H)
     dt0 = np.exp(u)
     w["dt_bias"] = (dt0 + np.log(-np.expm1(-dt0))).astype(np.float32)
-    w["A_log"] = _stream(seed, "A_log").uniform(-2.0, 1.0, size=H).astype(np.float32)
+    w["A_log"] = _stream(seed, prefix + "A_log").uniform(-2.0, 1.0, size=H).astype(np.float32)
     add("D", (H,), 1.0, "f32")
     add("gnorm_w", (di,), 0.1, "f32", 1.0)
     add("W_out", (dm, di), di ** -0.5)
@@ -274,6 +280,48 @@ def make_attn_inputs(cfg: StepConfig, seed=0, extra_pages=0, pad_pages=0):
     x["q"] = normal("attn_q", (cfg.B, cfg.k, cfg.Hq, cfg.D), 1.0, seed, cfg.dtype)
     x["k_blk"] = normal("attn_kblk", (cfg.B, cfg.k, cfg.Hkv, cfg.D), 1.0, seed, cfg.dtype)
     x["v_blk"] = normal("attn_vblk", (cfg.B, cfg.k, cfg.Hkv, cfg.D), 1.0, seed, cfg.dtype)
+    return x
+
+
+DRAFTER_LAYERS = ("MAF", "MAF", "MAF", "MF")   # App. B.1: 3 x (Mamba, attention, MLP) + 1 x (Mamba, MLP)
+DRAFTER_FUSE = 5                                # |M|: five target layers fused into the state
+
+
+def make_drafter_weights(cfg: StepConfig, seed: int = 0, layers=DRAFTER_LAYERS, skip_state: bool = False):
+    """Weights of the whole drafter: ``shared`` (W_r [r, |M| d_model], W_dS) and one dict per
+    layer with its Mamba, attention (layers spelled with "A"; key "cache" = the index of the
+    target cache it reads, in order) and SwiGLU MLP weights ([ff, d_model] gate and up,
+    [d_model, ff] down) and the three pre-norm gains."""
+    shared = {} if skip_state else make_weights(cfg, seed, skip=("W_in", "conv_w", "conv_b", "D", "gnorm_w", "W_out",
+                                                                 "norm1_w", "norm2_w", "W_q", "W_k", "W_v", "W_o",
+                                                                 "q_norm_w", "k_norm_w"))
+    shared.pop("dt_bias", None)
+    shared.pop("A_log", None)
+    out, n_attn = [], 0
+    for l, spec in enumerate(layers):
+        pre = f"L{l}."
+        attn = () if "A" in spec else ("W_q", "W_k", "W_v", "W_o", "q_norm_w", "k_norm_w", "norm2_w")
+        W = make_weights(cfg, seed, skip=("W_r", "W_dS") + attn, prefix=pre)
+        W["norm3_w"] = normal(pre + "norm3_w", (cfg.d_model,), 0.1, seed, "f32", 1.0)
+        W["W_gate"] = normal(pre + "W_gate", (cfg.d_ff, cfg.d_model), cfg.d_model ** -0.5, seed, cfg.dtype)
+        W["W_up"] = normal(pre + "W_up", (cfg.d_ff, cfg.d_model), cfg.d_model ** -0.5, seed, cfg.dtype)
+        W["W_down"] = normal(pre + "W_down", (cfg.d_model, cfg.d_ff), cfg.d_ff ** -0.5, seed, cfg.dtype)
+        W["cache"] = n_attn if "A" in spec else None
+        n_attn += "A" in spec
+        out.append(W)
+    return shared, out
+
+
+def make_drafter_inputs(cfg: StepConfig, seed: int = 0, n_caches: int = 3, extra_pages: int = 0) -> dict:
+    """make_inputs plus the K/V caches of further target layers (``caches``: one dict per target
+    layer an attention reads), all on the one page table."""
+    x = make_inputs(cfg, seed, extra_pages)
+    caches = [dict(k_cache=x.pop("k_cache"), v_cache=x.pop("v_cache"))]
+    shape = caches[0]["k_cache"].shape
+    for c in range(1, n_caches):
+        caches.append(dict(k_cache=normal(f"k_cache{c}", shape, 1.0, seed, cfg.dtype),
+                           v_cache=normal(f"v_cache{c}", shape, 1.0, seed, cfg.dtype)))
+    x["caches"] = caches
     return x
 
 

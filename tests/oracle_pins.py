@@ -489,4 +489,76 @@ def pin_head_gumbel_max_samples_softmax(O):
     assert np.all(np.abs(freq - p) < 5 * np.sqrt(p * (1 - p) / n) + 1e-12), (freq, p)
 
 
+def pin_mlp_is_swiglu(O):
+    """The drafter MLP against torch's SiLU, matmul and elementwise product (SwiGLU)."""
+    import torch
+    rng = rng0(51)
+    x = rng.standard_normal((2, 3, 12))
+    W = dict(W_gate=rng.standard_normal((20, 12)), W_up=rng.standard_normal((20, 12)),
+             W_down=rng.standard_normal((12, 20)))
+    t = {k: torch.from_numpy(v) for k, v in W.items()}
+    xt = torch.from_numpy(x)
+    ref = (torch.nn.functional.silu(xt @ t["W_gate"].T) * (xt @ t["W_up"].T)) @ t["W_down"].T
+    assert np.allclose(O.mlp(x, W), ref.numpy(), rtol=1e-12, atol=1e-12)
+
+
+def _drafter_case(seed=52, layers=("MAF", "MF"), n_caches=1):
+    cfg = _tiny_cfg(n_fuse=3, ff=24, lengths="list:21,6")
+    shared, L = I.make_drafter_weights(cfg, seed, layers=layers)
+    x = I.make_drafter_inputs(cfg, seed, n_caches=n_caches)
+    return cfg, shared, L, x
+
+
+def pin_drafter_residual_stream(O):
+    """With every sublayer's output projection zero (W_out, W_o, W_down), each residual adds
+    nothing and the forward returns the block embeddings exactly (Sec. 3.3: pre-norm residual
+    sublayers)."""
+    cfg, shared, L, x = _drafter_case()
+    for W in L:
+        for k in ("W_out", "W_o", "W_down"):
+            if k in W:
+                W[k] = np.zeros_like(W[k])
+    out = O.drafter_forward(L, shared, x, x["caches"], cfg)
+    assert np.array_equal(out, O.f64(x["block_emb"]))
+
+
+def pin_drafter_one_layer_is_draft_step(O):
+    """One Mamba-attention layer with a zero MLP is the drafting step (same S_init, same
+    sublayers, same residuals)."""
+    cfg, shared, L, x = _drafter_case(layers=("MAF",))
+    L[0]["W_down"] = np.zeros_like(L[0]["W_down"])
+    out = O.drafter_forward(L, shared, x, x["caches"], cfg)
+    W = dict(L[0], **shared)
+    xs = dict(x, k_cache=x["caches"][0]["k_cache"], v_cache=x["caches"][0]["v_cache"])
+    assert np.allclose(out, O.draft_step(W, xs, cfg), rtol=1e-12, atol=1e-12)
+
+
+def pin_drafter_state_shared_by_layers(O):
+    """App. B.1 / Sec. 3.3.1: S_init is computed once and every Mamba module starts from it.
+    Two Mamba-MLP layers with zero MLPs: the output is e + m1 + m2 with m2 the (separately
+    pinned) mixer of RMSNorm(e + m1) from the same S_init."""
+    cfg, shared, L, x = _drafter_case(layers=("MF", "MF"))
+    for W in L:
+        W["W_down"] = np.zeros_like(W["W_down"])
+    out = O.drafter_forward(L, shared, x, x["caches"], cfg)
+    S0, _ = O.state_init(x["h_last"], shared["W_r"], shared["W_dS"], cfg.H, cfg.P, cfg.N)
+    e = O.f64(x["block_emb"])
+    h1 = e + O.mamba_mixer(O.rmsnorm(e, O.f64(L[0]["norm1_w"]), cfg.eps), S0, L[0], cfg)
+    h2 = h1 + O.mamba_mixer(O.rmsnorm(h1, O.f64(L[1]["norm1_w"]), cfg.eps), S0, L[1], cfg)
+    assert np.allclose(out, h2, rtol=1e-12, atol=1e-12)
+
+
+def pin_drafter_layer_reads_its_cache(O):
+    """Layer-wise KV mapping (Sec. 3.3.2; App. B.1): attention layer i reads target cache i.
+    With layer 0's output projection zero, changing cache 0 leaves the output unchanged and
+    changing cache 1 does not."""
+    cfg, shared, L, x = _drafter_case(layers=("MAF", "MAF"), n_caches=2)
+    L[0]["W_o"] = np.zeros_like(L[0]["W_o"])
+    base = O.drafter_forward(L, shared, x, x["caches"], cfg)
+    c0 = [dict(k_cache=-x["caches"][0]["k_cache"], v_cache=x["caches"][0]["v_cache"] * 2), x["caches"][1]]
+    c1 = [x["caches"][0], dict(k_cache=x["caches"][1]["k_cache"], v_cache=x["caches"][1]["v_cache"] * 2)]
+    assert np.array_equal(O.drafter_forward(L, shared, x, c0, cfg), base)
+    assert not np.allclose(O.drafter_forward(L, shared, x, c1, cfg), base)
+
+
 PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

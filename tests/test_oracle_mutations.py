@@ -45,6 +45,13 @@ MUTATIONS = {
     "block_keys_dropped": ("K = np.concatenate([Kc[lo:L], kb[b, :nb]], axis=0)", "K = np.concatenate([Kc[lo:L], kb[b, :0]], axis=0)"),
     "missing_mamba_residual": ("x1 = e + m_out", "x1 = m_out"),
     "missing_attn_residual": ("out_sub = x1 + a_out", "out_sub = a_out"),
+    "mlp_gate_up_swapped": ('return (silu(x @ f64(W["W_gate"]).T) * (x @ f64(W["W_up"]).T))',
+                            'return (silu(x @ f64(W["W_up"]).T) * (x @ f64(W["W_gate"]).T))'),
+    "drafter_mlp_no_residual": ("h = h + mlp(rmsnorm(h, f64(W[\"norm3_w\"]), cfg.eps), W)",
+                                "h = mlp(rmsnorm(h, f64(W[\"norm3_w\"]), cfg.eps), W)"),
+    "drafter_state_zeroed_after_first": ("h = h + mamba_mixer(rmsnorm(h, f64(W[\"norm1_w\"]), cfg.eps), S0, W, cfg)",
+                                         "h = h + mamba_mixer(rmsnorm(h, f64(W[\"norm1_w\"]), cfg.eps), S0, W, cfg); S0 = 0 * S0"),
+    "drafter_all_layers_cache0": ('c = caches[W["cache"]]', "c = caches[0]"),
     "head_no_final_norm": ('hn = rmsnorm(h, f64(W["norm_f_w"]), eps)', "hn = h"),
     "markov_prev_never_advances": ("prev = tokens[:, j] if forced is None", "prev = prev if forced is None"),
     "markov_factors_swapped": ("lj = logits[:, j, :] + E[prev] @ U.T", "lj = logits[:, j, :] + U[prev] @ E.T"),
