@@ -58,8 +58,12 @@ typedef enum { HSPEC_BF16 = 0, HSPEC_F32 = 1 } hspec_dtype;
 
 /* hspec_attn_cfg.flags */
 enum {
-  HSPEC_BLOCK_CAUSAL = 1u << 0 /* block keys s visible to block query j only if s <= j
-                                  (default: the whole block is visible to every query) */
+  HSPEC_BLOCK_CAUSAL = 1u << 0, /* block keys s visible to block query j only if s <= j
+                                   (default: the whole block is visible to every query) */
+  HSPEC_ATTN_PRECISE_IO = 1u << 1 /* the layer's normalised input enters W_q/W_k/W_v, and its
+                                     attention output enters W_o, as bf16 hi/lo planes (two
+                                     products each) instead of one bf16 plane: for stacks of
+                                     attention layers (hspec_drafter_forward sets it) */
 };
 
 /* Device status bits (first int32 of the workspace). */
@@ -179,6 +183,40 @@ hspec_status hspec_draft_step(const hspec_mamba_cfg* mcfg, const hspec_mamba_w* 
                               const void* v_cache, const int32_t* page_table, const int32_t* ctx_lens,
                               int max_ctx_len, float* out, void* workspace, size_t ws_bytes, void* stream);
 size_t hspec_draft_step_workspace(const hspec_mamba_cfg* mcfg, const hspec_attn_cfg* acfg, int max_ctx_len);
+
+/*
+ * Whole drafter forward over the block (Sec. 3.3; App. B.1 "Number of drafter layers", "MLP",
+ * "Target-layer mapping"):
+ *   S0 = reshape(W_dS (W_r h_last)), once, given to every layer's Mamba (h_last [B, d_h]: the
+ *   |M| fused target layers' last hidden states, d_h = |M| * target hidden size);
+ *   x = block_emb;  for each layer:
+ *     x += Mamba(RMSNorm(x) norm1_w; S0)
+ *     x += Attn(RMSNorm(x) norm2_w) over the layer's own target cache   (layers with attention)
+ *     x += W_down (SiLU(W_gate RMSNorm(x) norm3_w) * (W_up RMSNorm(x) norm3_w))
+ *   out [B, k, d_model] fp32 = x.
+ * mcfg.d_h and mcfg.r size W_r [r, d_h] and W_dS [d_S, r] (packed with HSPEC_W_DS_PACKED); the
+ * layers' mamba weights (their W_r and W_dS are not read) and attention weights are as in the
+ * layer calls; all attention layers share acfg, page_table and ctx_lens and read their own
+ * k_cache/v_cache.  ff: MLP hidden size (multiple of 8); W_gate, W_up [ff, d_model] and W_down
+ * [d_model, ff] in the storage dtype.  layers: host array of n_layers (>= 1) entries.
+ */
+typedef struct {
+  const hspec_mamba_w* mamba; /* W_in .. W_out of this layer */
+  const float* norm1_w;       /* pre-Mamba RMSNorm gain [d_model] */
+  const hspec_attn_w* attn;   /* NULL: the layer has no attention */
+  const float* norm2_w;       /* pre-attention gain (layers with attention) */
+  const void *k_cache, *v_cache; /* the target layer this attention reads */
+  const float* norm3_w;       /* pre-MLP gain */
+  const void *W_gate, *W_up, *W_down;
+} hspec_layer_w;
+
+hspec_status hspec_drafter_forward(const hspec_mamba_cfg* mcfg, const hspec_attn_cfg* acfg, int ff, int n_layers,
+                                   const void* W_r, const void* W_dS, const hspec_layer_w* layers,
+                                   const void* h_last, const void* block_emb, const int32_t* page_table,
+                                   const int32_t* ctx_lens, int max_ctx_len, float* out, void* workspace,
+                                   size_t ws_bytes, void* stream);
+size_t hspec_drafter_forward_workspace(const hspec_mamba_cfg* mcfg, const hspec_attn_cfg* acfg, int ff,
+                                       int max_ctx_len);
 
 /*
  * Draft head (Sec. 3.3.3 "Causal correction"; App. B.1 "Markov rank"; App. B.2 "Pruned drafter

@@ -86,6 +86,13 @@ hipError_t as_planes(const void* src, hspec_dtype d, const SplitSlot& slot, Plan
   return hspec::launch_split_planes(static_cast<const float*>(src), slot.n, slot.hi, slot.lo, st);
 }
 
+// The planes as_planes gave for src on an earlier call with the same workspace, without
+// splitting again: src itself for bf16 storage, the workspace slot for fp32.
+Planes planes_in_place(const void* src, hspec_dtype d, const SplitSlot& slot) {
+  if (!is_f32(d)) return Planes{static_cast<const bf16*>(src), nullptr};
+  return Planes{slot.hi, slot.lo};
+}
+
 // Split-K scratch shared by a sequence of GEMMs on one stream, sized for the largest.
 struct GemmScratch {
   float* p = nullptr;
@@ -138,6 +145,8 @@ hspec_status check_attn_cfg(const hspec_attn_cfg* c, int max_ctx_len) {
     return fail(HSPEC_ERR_SHAPE, "non-positive attention dimension");
   if (c->Hq % c->Hkv) return fail(HSPEC_ERR_SHAPE, "Hq %% Hkv != 0 (Hq=%d, Hkv=%d)", c->Hq, c->Hkv);
   if (c->D != 64 && c->D != 128) return fail(HSPEC_ERR_UNSUPPORTED, "D must be 64 or 128, got %d", c->D);
+  if (c->flags & ~(unsigned)(HSPEC_BLOCK_CAUSAL | HSPEC_ATTN_PRECISE_IO))
+    return fail(HSPEC_ERR_UNSUPPORTED, "unknown attention flags 0x%x", c->flags);
   if (c->k * (c->Hq / c->Hkv) > 128)
     return fail(HSPEC_ERR_UNSUPPORTED, "k * Hq/Hkv must be <= 128, got %d", c->k * (c->Hq / c->Hkv));
   if (c->window < 0) return fail(HSPEC_ERR_SHAPE, "window < 0");
@@ -326,10 +335,8 @@ void plan_sweep(Arena& ar, const hspec_attn_cfg& c, int max_ctx_len, AttnPlan& p
   const int R = c.k * (c.Hq / c.Hkv);
   const size_t units = (size_t)c.B * c.Hkv * p.max_splits;
   p.units = ar.take<int32_t>((size_t)2 * c.B * p.max_splits);
-  if (p.max_splits > 1) {
-    p.part_o = ar.take<float>(units * R * c.D);
-    p.part_ml = ar.take<float>(units * R * 2);
-  }
+  p.part_o = ar.take<float>(units * R * c.D);   // every split writes partials
+  p.part_ml = ar.take<float>(units * R * 2);
   const size_t cache = (size_t)c.num_pages * c.page_size * c.Hkv * c.D;
   p.kc = reserve_split(ar, c.dtype, cache);
   p.vc = reserve_split(ar, c.dtype, cache);
@@ -338,9 +345,10 @@ void plan_sweep(Arena& ar, const hspec_attn_cfg& c, int max_ctx_len, AttnPlan& p
 void plan_attn(Arena& ar, const hspec_attn_cfg& c, int max_ctx_len, bool x_norm, AttnPlan& p) {
   const size_t M = (size_t)c.B * c.k;
   const bool f32 = is_f32(c.dtype);
+  const bool io_lo = f32 || (c.flags & HSPEC_ATTN_PRECISE_IO);   // hi/lo planes into W_q/k/v and W_o
   if (x_norm) {
     p.xn_hi = ar.take<bf16>(M * c.d_model);
-    if (f32) p.xn_lo = ar.take<bf16>(M * c.d_model);
+    if (io_lo) p.xn_lo = ar.take<bf16>(M * c.d_model);
   } else {
     p.x_in = reserve_split(ar, c.dtype, M * c.d_model);
   }
@@ -349,16 +357,17 @@ void plan_attn(Arena& ar, const hspec_attn_cfg& c, int max_ctx_len, bool x_norm,
   p.wv = reserve_split(ar, c.dtype, (size_t)c.Hkv * c.D * c.d_model);
   p.wo = reserve_split(ar, c.dtype, (size_t)c.d_model * c.Hq * c.D);
   p.qkv = ar.take<float>(M * (c.Hq + 2 * c.Hkv) * c.D);
+  // q, k and v as hi/lo planes: the sweep multiplies q_hi with the cache (q_lo too for fp32
+  // storage); the block keys are taken in fp32 from both planes
   p.q_hi = ar.take<bf16>(M * c.Hq * c.D);
   p.k_hi = ar.take<bf16>(M * c.Hkv * c.D);
   p.v_hi = ar.take<bf16>(M * c.Hkv * c.D);
-  if (f32) {
-    p.q_lo = ar.take<bf16>(M * c.Hq * c.D);
-    p.k_lo = ar.take<bf16>(M * c.Hkv * c.D);
-    p.v_lo = ar.take<bf16>(M * c.Hkv * c.D);
-  }
+  p.q_lo = ar.take<bf16>(M * c.Hq * c.D);
+  p.k_lo = ar.take<bf16>(M * c.Hkv * c.D);
+  p.v_lo = ar.take<bf16>(M * c.Hkv * c.D);
   plan_sweep(ar, c, max_ctx_len, p);
   p.o_hi = ar.take<bf16>(M * c.Hq * c.D);
+  if (io_lo) p.o_lo = ar.take<bf16>(M * c.Hq * c.D);
   p.gs = reserve_gemm(ar, c.dtype, {{(int)M, c.Hq * c.D, c.d_model}, {(int)M, c.Hkv * c.D, c.d_model},
                                     {(int)M, c.d_model, c.Hq * c.D}});
 }
@@ -420,9 +429,10 @@ hspec_status run_attn_core(const hspec_attn_cfg& c, const hspec_attn_w& w, Plane
   a.q_hi = p.q_hi; a.q_lo = p.q_lo; a.kb_hi = p.k_hi; a.kb_lo = p.k_lo; a.vb_hi = p.v_hi; a.vb_lo = p.v_lo;
   a.kc_hi = kc.hi; a.kc_lo = kc.lo; a.vc_hi = vc.hi; a.vc_lo = vc.lo;
   a.o_bf16 = p.o_hi;
+  a.o_bf16_lo = p.o_lo;
   HIP_TRY(hspec::launch_attention(a, st));
   hspec::GemmArgs g;
-  g.A_hi = p.o_hi; g.lda = c.Hq * c.D;
+  g.A_hi = p.o_hi; g.A_lo = p.o_lo; g.lda = c.Hq * c.D;
   g.W_hi = wo.hi; g.W_lo = wo.lo; g.ldw = c.Hq * c.D;
   g.M = M; g.N = c.d_model; g.K = c.Hq * c.D;
   g.C = out; g.ldc = c.d_model;
@@ -680,6 +690,12 @@ HSPEC_API hspec_status hspec_paged_attn_phase(const hspec_attn_cfg* cfg, const v
     HIP_TRY(as_planes(v_blk, cfg->dtype, p.vbin, pv, st));
     HIP_TRY(as_planes(k_cache, cfg->dtype, p.kc, kc, st));
     HIP_TRY(as_planes(v_cache, cfg->dtype, p.vc, vc, st));
+  } else {
+    // the reduction alone still reads the block q, k and v: the caller's bf16 tensors, or the
+    // planes the sweep phase of this attention wrote into the workspace (fp32 storage)
+    pq = planes_in_place(q, cfg->dtype, p.qin);
+    pk = planes_in_place(k_blk, cfg->dtype, p.kbin);
+    pv = planes_in_place(v_blk, cfg->dtype, p.vbin);
   }
   hspec::AttnArgs a = sweep_args(*cfg, p, page_table, ctx_lens, max_ctx_len, status);
   a.q_hi = pq.hi; a.q_lo = pq.lo; a.kb_hi = pk.hi; a.kb_lo = pk.lo; a.vb_hi = pv.hi; a.vb_lo = pv.lo;
@@ -747,6 +763,172 @@ HSPEC_API hspec_status hspec_linear(hspec_dtype dtype, int M, int N, int K, cons
   g.C = C; g.ldc = N; g.R = R; g.ldr = N; g.r_bf16 = 0;
   use_scratch(g, gs);
   HIP_TRY(hspec::launch_gemm(g, st));
+  return HSPEC_OK;
+}
+
+// ---------------------------------------------------------------- whole drafter forward
+
+struct ForwardPlan {
+  MambaPlan m;                              // with the state plan; its u planes also feed the MLP
+  AttnPlan at;
+  float *xa = nullptr, *xb = nullptr;       // residual stream, alternating
+  SplitSlot wg, wu, wd;
+  float* gu = nullptr;                      // [M, 2 ff]: gate | up
+  bf16 *h_hi = nullptr, *h_lo = nullptr;    // [M, ff]
+  GemmScratch gs;
+};
+
+void plan_forward(Arena& ar, const hspec_mamba_cfg& mc, const hspec_attn_cfg& ac, int ff, int max_ctx_len,
+                  ForwardPlan& p) {
+  plan_mamba(ar, mc, true, p.m);
+  plan_attn(ar, ac, max_ctx_len, true, p.at);
+  const size_t M = (size_t)mc.B * mc.k;
+  p.xa = ar.take<float>(M * mc.d_model);
+  p.xb = ar.take<float>(M * mc.d_model);
+  p.wg = reserve_split(ar, mc.dtype, (size_t)ff * mc.d_model);
+  p.wu = reserve_split(ar, mc.dtype, (size_t)ff * mc.d_model);
+  p.wd = reserve_split(ar, mc.dtype, (size_t)mc.d_model * ff);
+  p.gu = ar.take<float>(M * 2 * ff);
+  p.h_hi = ar.take<bf16>(M * ff);
+  p.h_lo = ar.take<bf16>(M * ff);
+  p.gs = reserve_gemm(ar, mc.dtype, {{(int)M, 2 * ff, mc.d_model}, {(int)M, ff, mc.d_model}, {(int)M, mc.d_model, ff}});
+}
+
+// x_out = x + W_down (SiLU(W_gate u) * (W_up u)), u already normalised (planes).
+hspec_status run_mlp(const hspec_mamba_cfg& c, const hspec_layer_w& L, int ff, Planes u, const ForwardPlan& p,
+                     const float* x, float* x_out, hipStream_t st) {
+  const int M = c.B * c.k;
+  Planes wg, wu, wd;
+  HIP_TRY(as_planes(L.W_gate, c.dtype, p.wg, wg, st));
+  HIP_TRY(as_planes(L.W_up, c.dtype, p.wu, wu, st));
+  HIP_TRY(as_planes(L.W_down, c.dtype, p.wd, wd, st));
+  if (!wg.lo) {
+    // one product over the two row segments [W_gate; W_up]
+    hspec::GemmArgs g;
+    g.A_hi = u.hi; g.A_lo = u.lo; g.lda = c.d_model;
+    g.W_hi = wg.hi; g.W2 = wu.hi; g.N1 = ff; g.N2 = ff; g.ldw = c.d_model;
+    g.M = M; g.N = 2 * ff; g.K = c.d_model;
+    g.C = p.gu; g.ldc = 2 * ff;
+    use_scratch(g, p.gs);
+    HIP_TRY(hspec::launch_gemm(g, st));
+  } else {
+    const Planes* w2[2] = {&wg, &wu};
+    for (int i = 0; i < 2; ++i) {
+      hspec::GemmArgs g;
+      g.A_hi = u.hi; g.A_lo = u.lo; g.lda = c.d_model;
+      g.W_hi = w2[i]->hi; g.W_lo = w2[i]->lo; g.ldw = c.d_model;
+      g.M = M; g.N = ff; g.K = c.d_model;
+      g.C = p.gu + (size_t)i * ff; g.ldc = 2 * ff;
+      use_scratch(g, p.gs);
+      HIP_TRY(hspec::launch_gemm(g, st));
+    }
+  }
+  HIP_TRY(hspec::launch_silu_mul(p.gu, M, ff, p.h_hi, p.h_lo, st));
+  hspec::GemmArgs g;
+  g.A_hi = p.h_hi; g.A_lo = p.h_lo; g.lda = ff;
+  g.W_hi = wd.hi; g.W_lo = wd.lo; g.ldw = ff;
+  g.M = M; g.N = c.d_model; g.K = ff;
+  g.C = x_out; g.ldc = c.d_model;
+  g.R = x; g.ldr = c.d_model; g.r_bf16 = 0;
+  use_scratch(g, p.gs);
+  HIP_TRY(hspec::launch_gemm(g, st));
+  return HSPEC_OK;
+}
+
+HSPEC_API size_t hspec_drafter_forward_workspace(const hspec_mamba_cfg* mcfg, const hspec_attn_cfg* acfg, int ff,
+                                                 int max_ctx_len) {
+  if (!mcfg || !acfg || ff <= 0) return 0;
+  hspec_attn_cfg ac = *acfg;
+  ac.flags |= HSPEC_ATTN_PRECISE_IO;
+  Arena ar;
+  status_word(ar);
+  ForwardPlan p;
+  plan_forward(ar, *mcfg, ac, ff, max_ctx_len < 0 ? 0 : max_ctx_len, p);
+  return ar.size();
+}
+
+HSPEC_API hspec_status hspec_drafter_forward(const hspec_mamba_cfg* mcfg, const hspec_attn_cfg* acfg, int ff,
+                                             int n_layers, const void* W_r, const void* W_dS,
+                                             const hspec_layer_w* layers, const void* h_last, const void* block_emb,
+                                             const int32_t* page_table, const int32_t* ctx_lens, int max_ctx_len,
+                                             float* out, void* workspace, size_t ws_bytes, void* stream) {
+  g_err.clear();
+  if (!mcfg || !acfg) return fail(HSPEC_ERR_NULL, "mamba or attention config is NULL");
+  if (n_layers < 1) return fail(HSPEC_ERR_SHAPE, "n_layers must be >= 1");
+  if (!layers) return fail(HSPEC_ERR_NULL, "layers is NULL");
+  if (ff <= 0) return fail(HSPEC_ERR_SHAPE, "ff must be positive");
+  if (ff % 8) return fail(HSPEC_ERR_UNSUPPORTED, "ff must be a multiple of 8");
+  bool any_attn = false;
+  for (int l = 0; l < n_layers; ++l) {
+    const hspec_layer_w& L = layers[l];
+    hspec_mamba_w mw = L.mamba ? *L.mamba : hspec_mamba_w{};
+    mw.W_r = W_r;
+    mw.W_dS = W_dS;
+    if (hspec_status s = check_mamba(mcfg, L.mamba ? &mw : nullptr, true)) return s;
+    if (!L.norm1_w || !L.norm3_w || !L.W_gate || !L.W_up || !L.W_down)
+      return fail(HSPEC_ERR_NULL, "layer %d: a norm or MLP weight is NULL", l);
+    if (L.attn) {
+      any_attn = true;
+      if (hspec_status s = check_attn_w(acfg, L.attn)) return s;
+      if (!L.norm2_w || !L.k_cache || !L.v_cache) return fail(HSPEC_ERR_NULL, "layer %d: attention input is NULL", l);
+    }
+  }
+  if (hspec_status s = check_attn_cfg(acfg, max_ctx_len)) return s;
+  if (mcfg->B != acfg->B || mcfg->k != acfg->k || mcfg->d_model != acfg->d_model)
+    return fail(HSPEC_ERR_SHAPE, "mamba and attention configs disagree on B, k or d_model");
+  if (mcfg->dtype != acfg->dtype) return fail(HSPEC_ERR_DTYPE, "mamba and attention dtypes differ");
+  if (!h_last || !block_emb || !out || (any_attn && (!page_table || !ctx_lens)))
+    return fail(HSPEC_ERR_NULL, "an input or output pointer is NULL");
+  if (hspec_status s = check_ws(workspace, ws_bytes, hspec_drafter_forward_workspace(mcfg, acfg, ff, max_ctx_len)))
+    return s;
+  hipStream_t st = (hipStream_t)stream;
+  const hspec_mamba_cfg& mc = *mcfg;
+  hspec_attn_cfg ac = *acfg;
+  ac.flags |= HSPEC_ATTN_PRECISE_IO;   // the layers' attention errors add up over the stack
+  Arena ar{(char*)workspace};
+  int* status = status_word(ar);
+  ForwardPlan p;
+  plan_forward(ar, mc, ac, ff, max_ctx_len, p);
+  const int M = mc.B * mc.k;
+  const bool f32 = is_f32(mc.dtype);
+  HIP_TRY(hspec::launch_zero_words(status, hspec::kStatusClear, st));
+  hspec_mamba_w sw{};
+  sw.W_r = W_r;
+  sw.W_dS = W_dS;
+  if (hspec_status s = run_state(mc, sw, h_last, p.m.st, nullptr, st)) return s;
+
+  // the residual stream: block_emb (storage dtype), then fp32 buffers; the last sublayer
+  // writes straight into out
+  int total = 0;
+  for (int l = 0; l < n_layers; ++l) total += layers[l].attn ? 3 : 2;
+  int done = 0;
+  const void* x = block_emb;
+  int x_bf16 = !f32;
+  auto dst = [&]() -> float* { return ++done == total ? out : (x == p.xa ? p.xb : p.xa); };
+  Planes u{p.m.u_hi, p.m.u_lo};
+  for (int l = 0; l < n_layers; ++l) {
+    const hspec_layer_w& L = layers[l];
+    HIP_TRY(hspec::launch_rmsnorm_planes(x, x_bf16, L.norm1_w, M, mc.d_model, mc.eps, p.m.u_hi, p.m.u_lo, st));
+    float* y = dst();
+    if (hspec_status s = run_mamba_core(mc, *L.mamba, u, p.m, x, x_bf16, y, nullptr, st)) return s;
+    x = y;
+    x_bf16 = 0;
+    if (L.attn) {
+      // the work list (the same for every layer) and a fresh item queue for this sweep
+      HIP_TRY(hspec::launch_attention_plan(sweep_args(ac, p.at, page_table, ctx_lens, max_ctx_len, status), 0, st));
+      HIP_TRY(hspec::launch_rmsnorm_planes(x, 0, L.norm2_w, M, ac.d_model, ac.eps, p.at.xn_hi, p.at.xn_lo, st));
+      Planes xn{p.at.xn_hi, p.at.xn_lo};
+      y = dst();
+      if (hspec_status s = run_attn_core(ac, *L.attn, xn, L.k_cache, L.v_cache, page_table, ctx_lens, max_ctx_len,
+                                         p.at, static_cast<const float*>(x), y, status, st))
+        return s;
+      x = y;
+    }
+    HIP_TRY(hspec::launch_rmsnorm_planes(x, 0, L.norm3_w, M, mc.d_model, mc.eps, p.m.u_hi, p.m.u_lo, st));
+    y = dst();
+    if (hspec_status s = run_mlp(mc, L, ff, u, p, static_cast<const float*>(x), y, st)) return s;
+    x = y;
+  }
   return HSPEC_OK;
 }
 

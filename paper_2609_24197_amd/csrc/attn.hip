@@ -1,21 +1,24 @@
 // Block queries over one target layer's paged K/V cache, reused in place, plus the block's
-// own K/V (H-Spec Sec. 3.3.2): the KV sweep, split along the context, and the cross-split
-// softmax reduction.
+// own K/V (H-Spec Sec. 3.3.2): the KV sweep over the cache, split along the context, and the
+// reduction that adds the block keys and combines the splits.
 //
-// Work unit = (request b, KV head h, split s).  Its query tile is the k*g rows of the block
-// positions j and the g query heads of the group, stored as columns c = j*g + i.  Each wave
-// owns 32 of those columns; the waves of a workgroup share 64-key K/V tiles staged in LDS:
-//   * K tiles are read back as MFMA A-fragments (16 keys x 32 dims, 16-byte reads), giving
-//     S^T = K Q^T with v_mfma_f32_16x16x32_bf16, so each lane holds 4 keys of one column;
-//   * the online softmax reduces a column over its 4 lanes with two cross-lane shuffles;
+// Work unit = (request b, split s, KV head h).  Its query tile is the k*g rows of the block
+// positions j and the g query heads of the group, stored as columns c = j*g + i; each wave
+// owns 16 of those columns.  A persistent grid takes units from a device queue (the work list
+// puts full splits first, then the last splits by decreasing length).  Per unit, 32-key K/V
+// tiles of the cache stream into LDS by direct DMA in a 3-stage pipeline:
+//   * K tiles are read back as MFMA fragments, giving S^T = K Q^T with
+//     v_mfma_f32_16x16x32_bf16, so each lane holds 4 keys of one column;
+//   * the online softmax (base 2, lazily rescaled) reduces a column over its 4 lanes;
 //   * the probabilities already sit in the B-fragment layout of O^T = V^T P^T, and V is read
-//     transposed from LDS (one bf16 per read) as the A-fragment.
-// Global loads of the next tile are issued before the current tile is multiplied.  A split
-// that covers a whole request writes the normalised output directly; otherwise it writes
-// (unnormalised O, running max, running sum) and the reduction kernel combines the splits
-// in a fixed order, so results are bitwise reproducible and independent of where pages
-// live in the pool.  Cache slots at or past ctx_len and pages the table does not reference
-// are never read; page ids outside the pool raise a device status bit and read as zeros.
+//     transposed from LDS (ds_read_b64_tr_b16) as the A-fragment.
+// Every split writes (unnormalised O, running max, running sum).  The reduction kernel then
+// computes, in fp32 from the hi/lo planes of q, k and v, the softmax terms of the k block keys
+// (few keys with large weights, where bf16 rounding would not average out) and combines them
+// with the splits in a fixed order, so results are bitwise reproducible and independent of
+// where pages live in the pool.  Cache slots at or past ctx_len and pages the table does not
+// reference are never read; page ids outside the pool raise a device status bit and read as
+// zeros.
 #include <climits>
 #include <type_traits>
 
@@ -152,19 +155,15 @@ attn_sweep(AttnArgs a) {
   const int2 unit_e = *reinterpret_cast<const int2*>(a.units + 2 * (item / a.Hkv));
   const int b = unit_e.x >> 16, sp = unit_e.x & 0xffff, h = item % a.Hkv;
   const int L = unit_e.y;   // validated by the work-list kernel
-  const int nsplit = n_splits(a, L);
   const int k0 = swept_lo(a, L) + sp * a.split;
   const int k1 = min(L, k0 + a.split);
-  const bool last = sp == nsplit - 1;
   const int kstart = k0;
-  const int n_cache = kstart < k1 ? (k1 - kstart + KT - 1) / KT : 0;
-  const int n_block = last ? (T + KT - 1) / KT : 0;
-  const int ntiles = n_cache + n_block;
+  const int ntiles = kstart < k1 ? (k1 - kstart + KT - 1) / KT : 0;   // cache keys only
 
   // query fragments: B operand of S^T = K Q^T (lane: column l16, dims 32 s + 8 g4 ..) and the
-  // key window [lo, hi) of each column for cache keys and for block keys
+  // key window [lo, hi) of each column
   bf16x8 qf[QB][NS], qfl[QB][LO ? NS : 1];
-  int c_lo[QB], c_hi[QB], b_hi[QB];
+  int c_lo[QB], c_hi[QB];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const int c = wave * C::COLS + qb * 16 + l16;
@@ -179,11 +178,10 @@ attn_sweep(AttnArgs a) {
     }
     c_lo[qb] = a.window > 0 ? L + j - a.window + 1 : INT_MIN;
     c_hi[qb] = real ? k1 : INT_MIN;
-    b_hi[qb] = real ? (a.causal ? j + 1 : T) : INT_MIN;
   }
   // page ids of this split, validated once
   const int pg0 = k0 >> lps;
-  if (n_cache > 0) {
+  if (ntiles > 0) {
     const int npg = ((k1 - 1) >> lps) - pg0 + 1;
     const int32_t* ptab = a.page_table + (size_t)b * a.max_pages + pg0;
     for (int e = tid; e < npg; e += C::NT) {
@@ -202,33 +200,26 @@ attn_sweep(AttnArgs a) {
   // every tensor-plane; each lane picks the global chunk that belongs at its slot.  Keys past
   // the valid range load a valid row instead (finite values; masked out of the softmax).
   auto issue = [&](int ti, bf16* sb) {
-    const bool cache = ti < n_cache;
-    const int base = cache ? kstart + ti * KT : (ti - n_cache) * KT;
+    const int base = kstart + ti * KT;
 #pragma unroll
     for (int i = 0; i < C::DMA; ++i) {
       const int slot = (wave * C::DMA + i) * 64 + lane;
       const int row = slot / C::CPR;
       const int cl = (tile_off<C::CPR>(row, 8 * (slot % C::CPR)) / 8 - row * C::CPR);   // chunk stored here
-      size_t off;
       int key = base + row;
-      if (cache) {
-        key = key < k1 ? key : k0;
-        const int slot_id = pids[(key >> lps) - pg0] + (key & (a.ps - 1));
-        off = (size_t)slot_id * (a.Hkv * D) + (h * D + 8 * cl);
-      } else {
-        key = key < T ? key : 0;
-        off = ((size_t)(b * T + key) * a.Hkv + h) * D + 8 * cl;
-      }
-      const bf16* Kp = cache ? a.kc_hi : a.kb_hi;
-      const bf16* Vp = cache ? a.vc_hi : a.vb_hi;
+      key = key < k1 ? key : k0;
+      const int slot_id = pids[(key >> lps) - pg0] + (key & (a.ps - 1));
+      const size_t off = (size_t)slot_id * (a.Hkv * D) + (h * D + 8 * cl);
+      const bf16* Kp = a.kc_hi;
+      const bf16* Vp = a.vc_hi;
       bf16* dst = sb + (wave * C::DMA + i) * 64 * 8;
       // the cache is read once per step: non-temporal loads (HSPEC_SWEEP_AUX cache-policy bits)
       __builtin_amdgcn_global_load_lds((const GLB_AS void*)(Kp + off), (LDS_AS void*)dst, 16, 0, HSPEC_SWEEP_AUX);
       __builtin_amdgcn_global_load_lds((const GLB_AS void*)(Vp + off), (LDS_AS void*)(dst + C::PLANES * C::TILE),
                                        16, 0, HSPEC_SWEEP_AUX);
       if constexpr (LO) {
-        const bf16* Kl = cache ? a.kc_lo : a.kb_lo;
-        const bf16* Vl = cache ? a.vc_lo : a.vb_lo;
+        const bf16* Kl = a.kc_lo;
+        const bf16* Vl = a.vc_lo;
         __builtin_amdgcn_global_load_lds((const GLB_AS void*)(Kl + off), (LDS_AS void*)(dst + C::TILE), 16, 0, 0);
         __builtin_amdgcn_global_load_lds((const GLB_AS void*)(Vl + off),
                                          (LDS_AS void*)(dst + C::PLANES * C::TILE + C::TILE), 16, 0, 0);
@@ -252,8 +243,7 @@ attn_sweep(AttnArgs a) {
   auto compute = [&](int ti, const bf16* sb) {
     const bf16* sK = sb;
     const bf16* sV = sb + C::PLANES * C::TILE;
-    const bool cache = ti < n_cache;
-    const int base = cache ? kstart + ti * KT : (ti - n_cache) * KT;
+    const int base = kstart + ti * KT;
 
     // all K fragments first, then the QK^T chains interleaved across key tiles
     bf16x8 kf[NKT][NS], kfl[NKT][LO ? NS : 1];
@@ -304,7 +294,7 @@ attn_sweep(AttnArgs a) {
         }
     }
 
-    const bool full = cache && base + KT <= k1 && (a.window <= 0 || base >= lo_last);
+    const bool full = base + KT <= k1 && (a.window <= 0 || base >= lo_last);
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
       float mx = -INFINITY;
@@ -317,8 +307,8 @@ attn_sweep(AttnArgs a) {
             mx = fmaxf(mx, st[kt][qb][i]);
           }
       } else {
-        const int lo = cache ? c_lo[qb] : INT_MIN;
-        const int hi = cache ? c_hi[qb] : b_hi[qb];
+        const int lo = c_lo[qb];
+        const int hi = c_hi[qb];
 #pragma unroll
         for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
@@ -399,33 +389,18 @@ attn_sweep(AttnArgs a) {
     round(t0, std::make_integer_sequence<int, ST>{});
   }
 
-  // write: lane holds O[column l16][d = 16 d + 4 g4 + i]
+  // write the split's unnormalised (O, m, l): lane holds O[column l16][d = 16 d + 4 g4 + i]
   const size_t unit = ((size_t)b * a.Hkv + h) * a.max_splits + sp;
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const int c = wave * C::COLS + qb * 16 + l16;
     if (c >= R) continue;
-    if (nsplit == 1) {
-      const float inv = 1.f / l_run[qb];
-      const int j = c / g, hq = h * g + c % g;
-      const size_t off = ((size_t)(b * T + j) * a.Hq + hq) * D + 4 * g4;
+    float* po = a.part_o + (unit * R + c) * D + 4 * g4;
 #pragma unroll
-      for (int d = 0; d < NDB; ++d) {
-        f32x4 v = o[d][qb] * inv;
-        if (a.o_f32) *reinterpret_cast<f32x4*>(a.o_f32 + off + 16 * d) = v;
-        if (a.o_bf16) {
-          bf16x4 hv = {f2bf(v[0]), f2bf(v[1]), f2bf(v[2]), f2bf(v[3])};
-          *reinterpret_cast<bf16x4*>(a.o_bf16 + off + 16 * d) = hv;
-        }
-      }
-    } else {
-      float* po = a.part_o + (unit * R + c) * D + 4 * g4;
-#pragma unroll
-      for (int d = 0; d < NDB; ++d) *reinterpret_cast<f32x4*>(po + 16 * d) = o[d][qb];
-      if (g4 == 0) {
-        a.part_ml[(unit * R + c) * 2 + 0] = m_run[qb];
-        a.part_ml[(unit * R + c) * 2 + 1] = l_run[qb];
-      }
+    for (int d = 0; d < NDB; ++d) *reinterpret_cast<f32x4*>(po + 16 * d) = o[d][qb];
+    if (g4 == 0) {
+      a.part_ml[(unit * R + c) * 2 + 0] = m_run[qb];
+      a.part_ml[(unit * R + c) * 2 + 1] = l_run[qb];
     }
   }
   }   // item loop
@@ -498,16 +473,38 @@ __global__ void __launch_bounds__(PLAN_THREADS) attn_plan(AttnArgs a, int clear_
   }
 }
 
-// Split reduction.  One workgroup per (request, KV head, 16 query columns), one thread per
-// (column, 4 dims) and 2 per thread: every thread loads the running max, sum and partial
-// output of each split for its column at once, then o = sum_s O_s 2^(m_s - m*) / sum_s l_s
-// 2^(m_s - m*) in split order.
+// Split reduction and block keys.  One workgroup per (request, KV head, 16 query columns);
+// thread t serves column t / 16.  The block keys are taken in fp32 (q, k and v rebuilt from
+// their hi/lo planes), 16 at a time, staged once per workgroup in LDS: lane t % 16 scores key
+// t % 16 against its column, the column's 16 lanes keep an online softmax, then each lane
+// accumulates D/16 dims of P V.  The same lanes then add sum_s O_s 2^(m_s - m*) and
+// sum_s l_s 2^(m_s - m*) over the splits in split order; o = (O_blk + sum) / (l_blk + sum).
 constexpr int RED_COLS = 16;
 constexpr int RED_THREADS = 256;
 constexpr int RED_NS = 4;   // splits whose loads are all issued together; more take further rounds
 
+__device__ __forceinline__ f32x4 ld4_planes(const bf16* hi, const bf16* lo, size_t off) {
+  const bf16x4 hv = *reinterpret_cast<const bf16x4*>(hi + off);
+  f32x4 v = {bf2f(hv[0]), bf2f(hv[1]), bf2f(hv[2]), bf2f(hv[3])};
+  if (lo) {
+    const bf16x4 lv = *reinterpret_cast<const bf16x4*>(lo + off);
+    v += f32x4{bf2f(lv[0]), bf2f(lv[1]), bf2f(lv[2]), bf2f(lv[3])};
+  }
+  return v;
+}
+
+template <int D>
 __global__ void __launch_bounds__(RED_THREADS) attn_reduce(AttnArgs a) {
-  const int g = a.Hq / a.Hkv, T = a.T, R = T * g, D = a.D, nq = D / 4;
+  constexpr int DP = D + 4;      // padded fp32 row: float4 reads of 16 different rows hit distinct banks
+  constexpr int DPL = D / 16;    // dims per lane in P V and the merge
+  constexpr int KC = 16;         // block keys per chunk
+  constexpr int P4 = D / 4;      // float4 pieces per row
+  static_assert(RED_COLS == 16 && RED_THREADS == 256, "16 columns x 16 lanes");
+  __shared__ __align__(16) float sQ[RED_COLS * DP];
+  __shared__ __align__(16) float sK[KC * DP];
+  __shared__ __align__(16) float sV[KC * DP];
+  __shared__ float sP[RED_COLS][KC + 1];
+  const int g = a.Hq / a.Hkv, T = a.T, R = T * g;
   const int cblocks = (R + RED_COLS - 1) / RED_COLS;
   const int bh = blockIdx.x / cblocks, c0 = (blockIdx.x % cblocks) * RED_COLS;
   const int b = bh / a.Hkv, h = bh % a.Hkv;
@@ -515,52 +512,120 @@ __global__ void __launch_bounds__(RED_THREADS) attn_reduce(AttnArgs a) {
   const int cap = min(a.max_pages * a.ps, a.max_ctx_len);
   L = L < 0 ? 0 : (L > cap ? cap : L);   // out-of-range lengths were flagged by the sweep
   const int nsplit = n_splits(a, L);
-  if (nsplit == 1) return;
   const size_t unit0 = ((size_t)b * a.Hkv + h) * a.max_splits;
-  for (int it = threadIdx.x; it < RED_COLS * nq; it += RED_THREADS) {
-    const int c = c0 + it / nq, d4 = (it % nq) * 4;
-    if (c >= R) continue;
-    // per round of RED_NS splits: running maxima, sums and partial outputs, all loads in flight
-    // together; with at most RED_NS splits the maxima are known after the one round
-    float m[RED_NS], l[RED_NS];
-    f32x4 o[RED_NS];
-    auto fetch = [&](int s0) {
+  const int tid = threadIdx.x, ci = tid >> 4, ln = tid & 15;
+  const bool live = c0 + ci < R;
+  const int c = live ? c0 + ci : c0;
+  const int j = c / g, hq = h * g + c % g;
+  const int nb = a.causal ? j + 1 : T;   // block keys this column sees
+  const int d0 = ln * DPL;
+
+  // the splits' running maxima, sums and partial outputs for this lane's dims (all loads in
+  // flight together when there are at most RED_NS splits), issued before the block keys
+  float m[RED_NS], l[RED_NS];
+  f32x4 o[RED_NS][DPL / 4];
+  auto fetch = [&](int s0) {
 #pragma unroll
-      for (int i = 0; i < RED_NS; ++i) {
-        const bool in = s0 + i < nsplit;
-        const size_t u = (unit0 + s0 + (in ? i : 0)) * R + c;
-        m[i] = in ? a.part_ml[u * 2] : -INFINITY;
-        l[i] = in ? a.part_ml[u * 2 + 1] : 0.f;
-        o[i] = in ? *reinterpret_cast<const f32x4*>(a.part_o + u * D + d4) : f32x4{0.f, 0.f, 0.f, 0.f};
-      }
-    };
-    float mstar = -INFINITY;
-    if (nsplit <= RED_NS) {
-      fetch(0);
+    for (int i = 0; i < RED_NS; ++i) {
+      const bool in = s0 + i < nsplit;
+      const size_t u = (unit0 + s0 + (in ? i : 0)) * R + c;
+      m[i] = in ? a.part_ml[u * 2] : -INFINITY;
+      l[i] = in ? a.part_ml[u * 2 + 1] : 0.f;
 #pragma unroll
-      for (int i = 0; i < RED_NS; ++i) mstar = fmaxf(mstar, m[i]);
-    } else {
-      for (int sp = 0; sp < nsplit; ++sp) mstar = fmaxf(mstar, a.part_ml[((unit0 + sp) * R + c) * 2]);
+      for (int e = 0; e < DPL / 4; ++e)
+        o[i][e] = in ? *reinterpret_cast<const f32x4*>(a.part_o + u * D + d0 + 4 * e) : f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    const float m_use = mstar == -INFINITY ? 0.f : mstar;
-    float lsum = 0.f;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int s0 = 0; s0 < nsplit; s0 += RED_NS) {
-      if (nsplit > RED_NS) fetch(s0);
+  };
+  if (nsplit <= RED_NS) fetch(0);
+
+  // q of the workgroup's columns (the last column repeated past R)
+  for (int p = tid; p < RED_COLS * P4; p += RED_THREADS) {
+    const int r = p / P4, d4 = (p % P4) * 4;
+    const int cr = min(c0 + r, R - 1);
+    const size_t qoff = ((size_t)(b * T + cr / g) * a.Hq + h * g + cr % g) * D + d4;
+    *reinterpret_cast<f32x4*>(sQ + r * DP + d4) = ld4_planes(a.q_hi, a.q_lo, qoff);
+  }
+  float mb = -INFINITY, lb = 0.f;
+  f32x4 ob[DPL / 4];
 #pragma unroll
-      for (int i = 0; i < RED_NS; ++i) {
-        const float e = exp2f(m[i] - m_use);
-        lsum += l[i] * e;
-        acc += o[i] * e;
-      }
+  for (int e = 0; e < DPL / 4; ++e) ob[e] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int s0 = 0; s0 < T; s0 += KC) {
+    __syncthreads();   // q staged; the previous chunk's tiles are no longer read
+    for (int p = tid; p < KC * P4; p += RED_THREADS) {
+      const int r = p / P4, d4 = (p % P4) * 4;
+      const size_t koff = ((size_t)(b * T + min(s0 + r, T - 1)) * a.Hkv + h) * D + d4;
+      *reinterpret_cast<f32x4*>(sK + r * DP + d4) = ld4_planes(a.kb_hi, a.kb_lo, koff);
+      *reinterpret_cast<f32x4*>(sV + r * DP + d4) = ld4_planes(a.vb_hi, a.vb_lo, koff);
     }
-    acc *= 1.f / lsum;
-    const int j = c / g, hq = h * g + c % g;
-    const size_t off = ((size_t)(b * T + j) * a.Hq + hq) * D + d4;
-    if (a.o_f32) *reinterpret_cast<f32x4*>(a.o_f32 + off) = acc;
+    __syncthreads();
+    float sc = 0.f;
+#pragma unroll 8
+    for (int d = 0; d < D; d += 4) {
+      const f32x4 qv = *reinterpret_cast<const f32x4*>(sQ + ci * DP + d);
+      const f32x4 kv = *reinterpret_cast<const f32x4*>(sK + ln * DP + d);
+      sc += qv[0] * kv[0] + qv[1] * kv[1] + qv[2] * kv[2] + qv[3] * kv[3];
+    }
+    sc = s0 + ln < nb ? sc * a.scale_log2 : -INFINITY;
+    float cm = sc;
+#pragma unroll
+    for (int msk = 1; msk < 16; msk <<= 1) cm = fmaxf(cm, __shfl_xor(cm, msk));
+    const float mn = fmaxf(mb, cm);   // finite: key 0 is seen by every column
+    const float alpha = exp2f(mb - mn), pr = exp2f(sc - mn);
+    float ps = pr;
+#pragma unroll
+    for (int msk = 1; msk < 16; msk <<= 1) ps += __shfl_xor(ps, msk);
+    lb = lb * alpha + ps;
+    mb = mn;
+    sP[ci][ln] = pr;
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < DPL / 4; ++e) ob[e] *= alpha;
+#pragma unroll 4
+    for (int s = 0; s < KC; ++s) {
+      const float pv = sP[ci][s];
+#pragma unroll
+      for (int e = 0; e < DPL / 4; ++e) ob[e] += *reinterpret_cast<const f32x4*>(sV + s * DP + d0 + 4 * e) * pv;
+    }
+  }
+
+  float mstar = mb;
+  if (nsplit <= RED_NS) {
+#pragma unroll
+    for (int i = 0; i < RED_NS; ++i) mstar = fmaxf(mstar, m[i]);
+  } else {
+    for (int sp = 0; sp < nsplit; ++sp) mstar = fmaxf(mstar, a.part_ml[((unit0 + sp) * R + c) * 2]);
+  }
+  const float eb = exp2f(mb - mstar);
+  float lsum = lb * eb;
+  f32x4 acc[DPL / 4];
+#pragma unroll
+  for (int e = 0; e < DPL / 4; ++e) acc[e] = ob[e] * eb;
+  for (int s0 = 0; s0 < nsplit; s0 += RED_NS) {
+    if (nsplit > RED_NS) fetch(s0);
+#pragma unroll
+    for (int i = 0; i < RED_NS; ++i) {
+      const float w = exp2f(m[i] - mstar);
+      lsum += l[i] * w;
+#pragma unroll
+      for (int e = 0; e < DPL / 4; ++e) acc[e] += o[i][e] * w;
+    }
+  }
+  if (!live) return;
+  const float inv = 1.f / lsum;
+  const size_t off = ((size_t)(b * T + j) * a.Hq + hq) * D + d0;
+#pragma unroll
+  for (int e = 0; e < DPL / 4; ++e) {
+    const f32x4 v = acc[e] * inv;
+    if (a.o_f32) *reinterpret_cast<f32x4*>(a.o_f32 + off + 4 * e) = v;
     if (a.o_bf16) {
-      bf16x4 hv = {f2bf(acc[0]), f2bf(acc[1]), f2bf(acc[2]), f2bf(acc[3])};
-      *reinterpret_cast<bf16x4*>(a.o_bf16 + off) = hv;
+      bf16x4 hv = {f2bf(v[0]), f2bf(v[1]), f2bf(v[2]), f2bf(v[3])};
+      *reinterpret_cast<bf16x4*>(a.o_bf16 + off + 4 * e) = hv;
+      if (a.o_bf16_lo) {
+        bf16x4 lv;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) lv[q] = f2bf(v[q] - bf2f(hv[q]));
+        *reinterpret_cast<bf16x4*>(a.o_bf16_lo + off + 4 * e) = lv;
+      }
     }
   }
 }
@@ -660,18 +725,21 @@ hipError_t launch_attention_plan(const AttnArgs& a, int clear_words, hipStream_t
 }
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s, unsigned parts) {
-  const bool lo = a.q_lo != nullptr;
+  const bool lo = a.kc_lo != nullptr;   // fp32 storage: the cache comes as hi/lo planes
   hipError_t e = hipSuccess;
   if (parts & ATTN_SWEEP) {
+    if (!a.q_hi || !a.kc_hi || !a.vc_hi || !a.part_o || !a.part_ml) return hipErrorInvalidValue;
     if (a.D == 128) e = lo ? launch_sweep_nw<128, true>(a, s) : launch_sweep_nw<128, false>(a, s);
     else if (a.D == 64) e = lo ? launch_sweep_nw<64, true>(a, s) : launch_sweep_nw<64, false>(a, s);
     else return hipErrorInvalidValue;
     if (e != hipSuccess) return e;
   }
-  if ((parts & ATTN_REDUCE) && a.max_splits > 1) {
+  if (parts & ATTN_REDUCE) {
+    if (!a.q_hi || !a.kb_hi || !a.vb_hi || !a.part_o || !a.part_ml) return hipErrorInvalidValue;   // block q/k/v, partials
     const int R = a.T * (a.Hq / a.Hkv);
     const int cblocks = (R + RED_COLS - 1) / RED_COLS;
-    hipLaunchKernelGGL(attn_reduce, dim3(a.B * a.Hkv * cblocks), dim3(256), 0, s, a);
+    if (a.D == 128) hipLaunchKernelGGL(attn_reduce<128>, dim3(a.B * a.Hkv * cblocks), dim3(RED_THREADS), 0, s, a);
+    else hipLaunchKernelGGL(attn_reduce<64>, dim3(a.B * a.Hkv * cblocks), dim3(RED_THREADS), 0, s, a);
     e = hipGetLastError();
   }
   return e;

@@ -270,6 +270,18 @@ __global__ void split_kernel(const float* x, size_t n, bf16* hi, bf16* lo) {
     put_planes(hi, lo, i, x[i]);
 }
 
+// h = SiLU(gate) * up for rows [gate | up] of width 2 ff, as bf16 hi/lo planes [rows, ff].
+__global__ void __launch_bounds__(256) silu_mul_kernel(const float* gu, int ff, bf16* hi, bf16* lo) {
+  const size_t row = blockIdx.y;
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= ff) return;
+  const float g = gu[row * 2 * ff + i], u = gu[row * 2 * ff + ff + i];
+  const float v = silu(g) * u;
+  const bf16 h = f2bf(v);
+  hi[row * ff + i] = h;
+  if (lo) lo[row * ff + i] = f2bf(v - bf2f(h));
+}
+
 __global__ void zero_kernel(int* p, int n) {
   for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = 0;
 }
@@ -326,6 +338,12 @@ hipError_t launch_split_planes(const float* x, size_t n, bf16* hi, bf16* lo, hip
   size_t blocks = (n + 255) / 256;
   if (blocks > 65536) blocks = 65536;
   hipLaunchKernelGGL(split_kernel, dim3((unsigned)blocks), dim3(256), 0, s, x, n, hi, lo);
+  return hipGetLastError();
+}
+
+hipError_t launch_silu_mul(const float* gu, int rows, int ff, bf16* hi, bf16* lo, hipStream_t s) {
+  if (rows <= 0 || ff <= 0) return hipSuccess;
+  hipLaunchKernelGGL(silu_mul_kernel, dim3((ff + 255) / 256, rows), dim3(256), 0, s, gu, ff, hi, lo);
   return hipGetLastError();
 }
 

@@ -47,6 +47,7 @@ struct AttnArgs {
   float* part_ml = nullptr;   // [B*Hkv*max_splits, R, 2]
   float* o_f32 = nullptr;     // [B, T, Hq, D] (one of o_f32 / o_bf16)
   bf16* o_bf16 = nullptr;
+  bf16* o_bf16_lo = nullptr;  // with o_bf16: the lo plane of o, or null
   int* status = nullptr;      // device status word; status[1] = work items, status[2] = queue (zero at launch)
   int32_t* units = nullptr;   // [B * max_splits][2] work list (request << 16 | split, length)
 };
@@ -117,6 +118,8 @@ hipError_t launch_qk_norm_rope(const float* qkv, const float* qw, const float* k
                                hipStream_t s);
 // fp32 -> bf16 hi/lo planes (lo optional).
 hipError_t launch_split_planes(const float* x, size_t n, bf16* hi, bf16* lo, hipStream_t s);
+// SwiGLU: h = SiLU(gate) * up from rows [gate | up] (fp32, width 2 ff) -> bf16 planes [rows, ff].
+hipError_t launch_silu_mul(const float* gu, int rows, int ff, bf16* hi, bf16* lo, hipStream_t s);
 // Zero n int32 words (device status, counters) with a kernel, graph-capture safe.
 hipError_t launch_zero_words(int* p, int n, hipStream_t s);
 

@@ -19,6 +19,7 @@ _lib = None
 
 BF16, F32 = 0, 1
 BLOCK_CAUSAL = 1
+ATTN_PRECISE_IO = 2
 W_DS_PACKED = 1
 DEV_BAD_PAGE, DEV_BAD_CTX_LEN, DEV_BAD_TOKEN, DEV_NONFINITE = 1, 2, 4, 8
 STATUS = {0: "HSPEC_OK", 1: "HSPEC_ERR_NULL", 2: "HSPEC_ERR_SHAPE", 3: "HSPEC_ERR_DTYPE",
@@ -44,6 +45,12 @@ class AttnCfg(C.Structure):
 
 class AttnW(C.Structure):
     _fields_ = [(n, C.c_void_p) for n in ("W_q", "W_k", "W_v", "W_o", "q_norm_w", "k_norm_w")]
+
+
+class LayerW(C.Structure):
+    _fields_ = [("mamba", C.POINTER(MambaW)), ("norm1_w", C.c_void_p), ("attn", C.POINTER(AttnW)),
+                ("norm2_w", C.c_void_p), ("k_cache", C.c_void_p), ("v_cache", C.c_void_p), ("norm3_w", C.c_void_p),
+                ("W_gate", C.c_void_p), ("W_up", C.c_void_p), ("W_down", C.c_void_p)]
 
 
 class HeadCfg(C.Structure):
@@ -87,6 +94,11 @@ EXPORTS = {
                                                       C.c_void_p]),
     "hspec_linear": (C.c_int, [C.c_int] * 4 + [C.c_void_p] * 5 + [C.c_size_t, C.c_void_p]),
     "hspec_linear_workspace": (C.c_size_t, [C.c_int] * 4),
+    "hspec_drafter_forward": (C.c_int, [C.POINTER(MambaCfg), C.POINTER(AttnCfg), C.c_int, C.c_int, C.c_void_p,
+                                        C.c_void_p, C.POINTER(LayerW)] + [C.c_void_p] * 4 + [C.c_int, C.c_void_p,
+                                                                                             C.c_void_p, C.c_size_t,
+                                                                                             C.c_void_p]),
+    "hspec_drafter_forward_workspace": (C.c_size_t, [C.POINTER(MambaCfg), C.POINTER(AttnCfg), C.c_int, C.c_int]),
     "hspec_draft_head": (C.c_int, [C.POINTER(HeadCfg), C.POINTER(HeadW)] + [C.c_void_p] * 7 + [C.c_size_t,
                                                                                           C.c_void_p]),
     "hspec_draft_head_workspace": (C.c_size_t, [C.POINTER(HeadCfg)]),
@@ -310,3 +322,36 @@ def draft_head(hc: HeadCfg, W: dict, hidden, prev_tok, tokens, ws, logits=None, 
     hw = HeadW(*(ptr(W[n]) for n in ("norm_f_w", "W_lm", "E_M", "U_M")))
     _check(lib().hspec_draft_head(C.byref(hc), C.byref(hw), ptr(hidden), ptr(prev_tok), ptr(gumbel), ptr(forced),
                                   ptr(tokens), ptr(logits), ptr(ws), ws.numel(), stream_ptr()))
+
+
+def drafter_forward_workspace(cfg, max_pages, num_pages, max_ctx_len) -> int:
+    mc, ac = mamba_cfg(cfg), attn_cfg(cfg, max_pages, num_pages)
+    return lib().hspec_drafter_forward_workspace(C.byref(mc), C.byref(ac), cfg.d_ff, int(max_ctx_len))
+
+
+def drafter_forward(cfg, shared: dict, layers: list, X: dict, out, ws, max_ctx_len: int):
+    """out [B, k, d_model] fp32 = the whole drafter over the block (hspec_drafter_forward).
+    ``shared``: W_r, W_dS (or W_dS_packed); ``layers``: per-layer weight dicts of device tensors
+    with "cache" = index into X["caches"] (None: no attention)."""
+    mc = mamba_cfg(cfg, shared)
+    ac = attn_cfg(cfg, X["page_table"].shape[1], X["caches"][0]["k_cache"].shape[0])
+    keep = []
+    arr = (LayerW * len(layers))()
+    for i, W in enumerate(layers):
+        mw = mamba_w(W)
+        keep.append(mw)
+        aw = None
+        c = None
+        if W.get("cache") is not None:
+            aw = attn_w(W)
+            keep.append(aw)
+            c = X["caches"][W["cache"]]
+        arr[i] = LayerW(C.pointer(mw), ptr(W["norm1_w"]), C.pointer(aw) if aw is not None else None,
+                        ptr(W.get("norm2_w")) if aw is not None else None, ptr(c["k_cache"]) if c else None,
+                        ptr(c["v_cache"]) if c else None, ptr(W["norm3_w"]), ptr(W["W_gate"]), ptr(W["W_up"]),
+                        ptr(W["W_down"]))
+    W_dS = shared.get("W_dS_packed", shared.get("W_dS"))
+    _check(lib().hspec_drafter_forward(C.byref(mc), C.byref(ac), cfg.d_ff, len(layers), ptr(shared["W_r"]), ptr(W_dS),
+                                       arr, ptr(X["h_last"]), ptr(X["block_emb"]), ptr(X["page_table"]),
+                                       ptr(X["ctx_lens"]), int(max_ctx_len), ptr(out), ptr(ws), ws.numel(),
+                                       stream_ptr()))
