@@ -124,6 +124,42 @@ def head_figures(cfg, out, step, args, torch):
             "lm_head_frac_of_bf16_peak": round(flops / t_lm / 1e12 / RL.MFMA_BF16_PEAK_TFLOPS, 4)}
 
 
+def forward_figures(cfg, Wd, Xd, x, args, torch):
+    """Timing of hspec_drafter_forward (3 x (Mamba, attention, MLP) + 1 x (Mamba, MLP), |M| = 5,
+    MLP hidden 3 d_model) on the same batch: the step's packed W_dS (the same seeded values), a
+    W_r over the five fused layers, and two more target caches on the same page table."""
+    fc = cfg.replace(n_fuse=I.DRAFTER_FUSE, ff=3 * cfg.d_model)
+    _, L = I.make_drafter_weights(fc, args.seed, skip_state=True)
+    shared = {"W_r": hspec.to_device(I.make_weights(fc, args.seed, skip=tuple(
+        k for k in ("W_dS", "W_in", "conv_w", "conv_b", "D", "gnorm_w", "W_out", "norm1_w", "norm2_w", "W_q", "W_k",
+                    "W_v", "W_o", "q_norm_w", "k_norm_w")))["W_r"]), "W_dS_packed": Wd["W_dS_packed"]}
+    Ld = [{k: (hspec.to_device(v) if isinstance(v, np.ndarray) else v) for k, v in W.items()} for W in L]
+    shape = x["k_cache"].shape
+    X = dict(Xd, h_last=hspec.to_device(I.normal("h_last", (cfg.B, fc.d_h), 1.0, args.seed, cfg.dtype)),
+             caches=[dict(k_cache=Xd["k_cache"], v_cache=Xd["v_cache"])] + [
+                 dict(k_cache=hspec.to_device(I.normal(f"k_cache{c}", shape, 1.0, args.seed, cfg.dtype)),
+                      v_cache=hspec.to_device(I.normal(f"v_cache{c}", shape, 1.0, args.seed, cfg.dtype)))
+                 for c in (1, 2)])
+    maxL = int(x["ctx_lens"].max())
+    fws = hspec.workspace(hspec.drafter_forward_workspace(fc, x["page_table"].shape[1], x["num_pages"], maxL))
+    out = torch.empty((cfg.B, cfg.k, cfg.d_model), dtype=torch.float32, device="cuda")
+    fwd = lambda: hspec.drafter_forward(fc, shared, Ld, X, out, fws, maxL)  # noqa: E731
+    for _ in range(args.warmup):
+        fwd()
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(args.steps):
+        fwd()
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / args.steps
+    assert hspec.read_status(fws) == 0 and bool(torch.isfinite(out).all())
+    log(f"drafter forward (4 layers): {ms:.3f} ms, {cfg.B * cfg.k / ms * 1e3:,.0f} drafted tok/s")
+    return {"ms": round(ms, 4), "drafted_tok_s": round(cfg.B * cfg.k / ms * 1e3, 1), "layers": "3 x MAF + 1 x MF",
+            "fused_target_layers": I.DRAFTER_FUSE, "mlp_hidden": fc.d_ff, "target_caches": 3}
+
+
 def cpu_baseline(cfg, W, x, n_req: int):
     """The float64 oracle on the first n_req requests of the same workload (all positions)."""
     import oracle.hspec_oracle as O
@@ -286,6 +322,7 @@ def main():
     # the draft head after the step (final norm, LM head over the pruned vocabulary, Markov
     # correction, greedy tokens) on the step's own output, and its LM-head GEMM alone
     head = head_figures(cfg, out, step, args, torch)
+    fwd = forward_figures(cfg, Wd, Xd, x, args, torch) if cfg.dtype == "bf16" else None
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -309,6 +346,8 @@ def main():
         "roofline_kv_sweep": roof_sweep,
         "cpu_baseline": cpu,
         "draft_head": dict(head, drafted_tok_s_with_head=round(cfg.B * cfg.k / (ms / 1e3 + head["avg_us"] / 1e6), 1)),
+        "drafter_forward": None if fwd is None else dict(
+            fwd, with_head_drafted_tok_s=round(cfg.B * cfg.k / (fwd["ms"] / 1e3 + head["avg_us"] / 1e6), 1)),
         "step_bytes_ideal": int(RL.step_bytes(cfg, L)),
     }
     print(json.dumps(rec), flush=True)

@@ -335,8 +335,10 @@ void plan_sweep(Arena& ar, const hspec_attn_cfg& c, int max_ctx_len, AttnPlan& p
   const int R = c.k * (c.Hq / c.Hkv);
   const size_t units = (size_t)c.B * c.Hkv * p.max_splits;
   p.units = ar.take<int32_t>((size_t)2 * c.B * p.max_splits);
-  p.part_o = ar.take<float>(units * R * c.D);   // every split writes partials
-  p.part_ml = ar.take<float>(units * R * 2);
+  if (p.max_splits > 1 || (c.flags & HSPEC_ATTN_PRECISE_IO)) {   // split partials
+    p.part_o = ar.take<float>(units * R * c.D);
+    p.part_ml = ar.take<float>(units * R * 2);
+  }
   const size_t cache = (size_t)c.num_pages * c.page_size * c.Hkv * c.D;
   p.kc = reserve_split(ar, c.dtype, cache);
   p.vc = reserve_split(ar, c.dtype, cache);
@@ -357,14 +359,16 @@ void plan_attn(Arena& ar, const hspec_attn_cfg& c, int max_ctx_len, bool x_norm,
   p.wv = reserve_split(ar, c.dtype, (size_t)c.Hkv * c.D * c.d_model);
   p.wo = reserve_split(ar, c.dtype, (size_t)c.d_model * c.Hq * c.D);
   p.qkv = ar.take<float>(M * (c.Hq + 2 * c.Hkv) * c.D);
-  // q, k and v as hi/lo planes: the sweep multiplies q_hi with the cache (q_lo too for fp32
-  // storage); the block keys are taken in fp32 from both planes
+  // q, k and v: hi/lo planes for fp32 storage (the sweep's hi/lo products) and for precise
+  // attention I/O (the reduction rebuilds the block keys in fp32 from both planes)
   p.q_hi = ar.take<bf16>(M * c.Hq * c.D);
   p.k_hi = ar.take<bf16>(M * c.Hkv * c.D);
   p.v_hi = ar.take<bf16>(M * c.Hkv * c.D);
-  p.q_lo = ar.take<bf16>(M * c.Hq * c.D);
-  p.k_lo = ar.take<bf16>(M * c.Hkv * c.D);
-  p.v_lo = ar.take<bf16>(M * c.Hkv * c.D);
+  if (io_lo) {
+    p.q_lo = ar.take<bf16>(M * c.Hq * c.D);
+    p.k_lo = ar.take<bf16>(M * c.Hkv * c.D);
+    p.v_lo = ar.take<bf16>(M * c.Hkv * c.D);
+  }
   plan_sweep(ar, c, max_ctx_len, p);
   p.o_hi = ar.take<bf16>(M * c.Hq * c.D);
   if (io_lo) p.o_lo = ar.take<bf16>(M * c.Hq * c.D);
@@ -379,6 +383,7 @@ hspec::AttnArgs sweep_args(const hspec_attn_cfg& c, const AttnPlan& p, const int
   a.B = c.B; a.T = c.k; a.Hq = c.Hq; a.Hkv = c.Hkv; a.D = c.D; a.ps = c.page_size;
   a.max_pages = c.max_pages; a.num_pages = c.num_pages; a.window = c.window;
   a.causal = (c.flags & HSPEC_BLOCK_CAUSAL) ? 1 : 0;
+  a.block_in_sweep = (c.flags & HSPEC_ATTN_PRECISE_IO) ? 0 : 1;
   a.max_ctx_len = max_ctx_len; a.split = p.split; a.max_splits = p.max_splits;
   const float scale = c.scale > 0.f ? c.scale : 1.f / std::sqrt((float)c.D);
   a.scale_log2 = scale * 1.4426950408889634f;

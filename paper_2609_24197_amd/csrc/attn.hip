@@ -12,11 +12,14 @@
 //   * the online softmax (base 2, lazily rescaled) reduces a column over its 4 lanes;
 //   * the probabilities already sit in the B-fragment layout of O^T = V^T P^T, and V is read
 //     transposed from LDS (ds_read_b64_tr_b16) as the A-fragment.
-// Every split writes (unnormalised O, running max, running sum).  The reduction kernel then
-// computes, in fp32 from the hi/lo planes of q, k and v, the softmax terms of the k block keys
-// (few keys with large weights, where bf16 rounding would not average out) and combines them
-// with the splits in a fixed order, so results are bitwise reproducible and independent of
-// where pages live in the pool.  Cache slots at or past ctx_len and pages the table does not
+// The k block keys are taken one of two ways.  By default the last split of each request
+// streams them after its cache keys, in bf16 like the cache, and a request with one split
+// writes its output directly.  With block_in_sweep off (HSPEC_ATTN_PRECISE_IO) every split
+// writes (unnormalised O, running max, running sum) and the reduction computes the block keys'
+// softmax terms in fp32 from the hi/lo planes of q, k and v: few keys with large weights, where
+// bf16 rounding does not average out over a stack of layers.  Either way the splits are combined
+// in a fixed order, so results are bitwise reproducible and independent of where pages live in
+// the pool.  Cache slots at or past ctx_len and pages the table does not
 // reference are never read; page ids outside the pool raise a device status bit and read as
 // zeros.
 #include <climits>
@@ -155,15 +158,19 @@ attn_sweep(AttnArgs a) {
   const int2 unit_e = *reinterpret_cast<const int2*>(a.units + 2 * (item / a.Hkv));
   const int b = unit_e.x >> 16, sp = unit_e.x & 0xffff, h = item % a.Hkv;
   const int L = unit_e.y;   // validated by the work-list kernel
+  const int nsplit = n_splits(a, L);
   const int k0 = swept_lo(a, L) + sp * a.split;
   const int k1 = min(L, k0 + a.split);
   const int kstart = k0;
-  const int ntiles = kstart < k1 ? (k1 - kstart + KT - 1) / KT : 0;   // cache keys only
+  const int n_cache = kstart < k1 ? (k1 - kstart + KT - 1) / KT : 0;
+  // the block keys follow the cache keys of a request's last split, unless the reduction takes them
+  const int n_block = (a.block_in_sweep && sp == nsplit - 1) ? (T + KT - 1) / KT : 0;
+  const int ntiles = n_cache + n_block;
 
   // query fragments: B operand of S^T = K Q^T (lane: column l16, dims 32 s + 8 g4 ..) and the
-  // key window [lo, hi) of each column
+  // key window [lo, hi) of each column for cache keys and for block keys
   bf16x8 qf[QB][NS], qfl[QB][LO ? NS : 1];
-  int c_lo[QB], c_hi[QB];
+  int c_lo[QB], c_hi[QB], b_hi[QB];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const int c = wave * C::COLS + qb * 16 + l16;
@@ -178,10 +185,11 @@ attn_sweep(AttnArgs a) {
     }
     c_lo[qb] = a.window > 0 ? L + j - a.window + 1 : INT_MIN;
     c_hi[qb] = real ? k1 : INT_MIN;
+    b_hi[qb] = real ? (a.causal ? j + 1 : T) : INT_MIN;
   }
   // page ids of this split, validated once
   const int pg0 = k0 >> lps;
-  if (ntiles > 0) {
+  if (n_cache > 0) {
     const int npg = ((k1 - 1) >> lps) - pg0 + 1;
     const int32_t* ptab = a.page_table + (size_t)b * a.max_pages + pg0;
     for (int e = tid; e < npg; e += C::NT) {
@@ -200,26 +208,33 @@ attn_sweep(AttnArgs a) {
   // every tensor-plane; each lane picks the global chunk that belongs at its slot.  Keys past
   // the valid range load a valid row instead (finite values; masked out of the softmax).
   auto issue = [&](int ti, bf16* sb) {
-    const int base = kstart + ti * KT;
+    const bool cache = ti < n_cache;
+    const int base = cache ? kstart + ti * KT : (ti - n_cache) * KT;
 #pragma unroll
     for (int i = 0; i < C::DMA; ++i) {
       const int slot = (wave * C::DMA + i) * 64 + lane;
       const int row = slot / C::CPR;
       const int cl = (tile_off<C::CPR>(row, 8 * (slot % C::CPR)) / 8 - row * C::CPR);   // chunk stored here
+      size_t off;
       int key = base + row;
-      key = key < k1 ? key : k0;
-      const int slot_id = pids[(key >> lps) - pg0] + (key & (a.ps - 1));
-      const size_t off = (size_t)slot_id * (a.Hkv * D) + (h * D + 8 * cl);
-      const bf16* Kp = a.kc_hi;
-      const bf16* Vp = a.vc_hi;
+      if (cache) {
+        key = key < k1 ? key : k0;
+        const int slot_id = pids[(key >> lps) - pg0] + (key & (a.ps - 1));
+        off = (size_t)slot_id * (a.Hkv * D) + (h * D + 8 * cl);
+      } else {
+        key = key < T ? key : 0;
+        off = ((size_t)(b * T + key) * a.Hkv + h) * D + 8 * cl;
+      }
+      const bf16* Kp = cache ? a.kc_hi : a.kb_hi;
+      const bf16* Vp = cache ? a.vc_hi : a.vb_hi;
       bf16* dst = sb + (wave * C::DMA + i) * 64 * 8;
       // the cache is read once per step: non-temporal loads (HSPEC_SWEEP_AUX cache-policy bits)
       __builtin_amdgcn_global_load_lds((const GLB_AS void*)(Kp + off), (LDS_AS void*)dst, 16, 0, HSPEC_SWEEP_AUX);
       __builtin_amdgcn_global_load_lds((const GLB_AS void*)(Vp + off), (LDS_AS void*)(dst + C::PLANES * C::TILE),
                                        16, 0, HSPEC_SWEEP_AUX);
       if constexpr (LO) {
-        const bf16* Kl = a.kc_lo;
-        const bf16* Vl = a.vc_lo;
+        const bf16* Kl = cache ? a.kc_lo : a.kb_lo;
+        const bf16* Vl = cache ? a.vc_lo : a.vb_lo;
         __builtin_amdgcn_global_load_lds((const GLB_AS void*)(Kl + off), (LDS_AS void*)(dst + C::TILE), 16, 0, 0);
         __builtin_amdgcn_global_load_lds((const GLB_AS void*)(Vl + off),
                                          (LDS_AS void*)(dst + C::PLANES * C::TILE + C::TILE), 16, 0, 0);
@@ -243,7 +258,8 @@ attn_sweep(AttnArgs a) {
   auto compute = [&](int ti, const bf16* sb) {
     const bf16* sK = sb;
     const bf16* sV = sb + C::PLANES * C::TILE;
-    const int base = kstart + ti * KT;
+    const bool cache = ti < n_cache;
+    const int base = cache ? kstart + ti * KT : (ti - n_cache) * KT;
 
     // all K fragments first, then the QK^T chains interleaved across key tiles
     bf16x8 kf[NKT][NS], kfl[NKT][LO ? NS : 1];
@@ -294,7 +310,7 @@ attn_sweep(AttnArgs a) {
         }
     }
 
-    const bool full = base + KT <= k1 && (a.window <= 0 || base >= lo_last);
+    const bool full = cache && base + KT <= k1 && (a.window <= 0 || base >= lo_last);
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
       float mx = -INFINITY;
@@ -307,8 +323,8 @@ attn_sweep(AttnArgs a) {
             mx = fmaxf(mx, st[kt][qb][i]);
           }
       } else {
-        const int lo = c_lo[qb];
-        const int hi = c_hi[qb];
+        const int lo = cache ? c_lo[qb] : INT_MIN;
+        const int hi = cache ? c_hi[qb] : b_hi[qb];
 #pragma unroll
         for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
@@ -389,18 +405,40 @@ attn_sweep(AttnArgs a) {
     round(t0, std::make_integer_sequence<int, ST>{});
   }
 
-  // write the split's unnormalised (O, m, l): lane holds O[column l16][d = 16 d + 4 g4 + i]
+  // write: lane holds O[column l16][d = 16 d + 4 g4 + i].  A request whose one split already
+  // holds every key writes its output; otherwise the split's unnormalised (O, m, l).
   const size_t unit = ((size_t)b * a.Hkv + h) * a.max_splits + sp;
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const int c = wave * C::COLS + qb * 16 + l16;
     if (c >= R) continue;
-    float* po = a.part_o + (unit * R + c) * D + 4 * g4;
+    if (a.block_in_sweep && nsplit == 1) {
+      const float inv = 1.f / l_run[qb];
+      const int j = c / g, hq = h * g + c % g;
+      const size_t off = ((size_t)(b * T + j) * a.Hq + hq) * D + 4 * g4;
 #pragma unroll
-    for (int d = 0; d < NDB; ++d) *reinterpret_cast<f32x4*>(po + 16 * d) = o[d][qb];
-    if (g4 == 0) {
-      a.part_ml[(unit * R + c) * 2 + 0] = m_run[qb];
-      a.part_ml[(unit * R + c) * 2 + 1] = l_run[qb];
+      for (int d = 0; d < NDB; ++d) {
+        f32x4 v = o[d][qb] * inv;
+        if (a.o_f32) *reinterpret_cast<f32x4*>(a.o_f32 + off + 16 * d) = v;
+        if (a.o_bf16) {
+          bf16x4 hv = {f2bf(v[0]), f2bf(v[1]), f2bf(v[2]), f2bf(v[3])};
+          *reinterpret_cast<bf16x4*>(a.o_bf16 + off + 16 * d) = hv;
+          if (a.o_bf16_lo) {
+            bf16x4 lv;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) lv[e] = f2bf(v[e] - bf2f(hv[e]));
+            *reinterpret_cast<bf16x4*>(a.o_bf16_lo + off + 16 * d) = lv;
+          }
+        }
+      }
+    } else {
+      float* po = a.part_o + (unit * R + c) * D + 4 * g4;
+#pragma unroll
+      for (int d = 0; d < NDB; ++d) *reinterpret_cast<f32x4*>(po + 16 * d) = o[d][qb];
+      if (g4 == 0) {
+        a.part_ml[(unit * R + c) * 2 + 0] = m_run[qb];
+        a.part_ml[(unit * R + c) * 2 + 1] = l_run[qb];
+      }
     }
   }
   }   // item loop
@@ -491,6 +529,72 @@ __device__ __forceinline__ f32x4 ld4_planes(const bf16* hi, const bf16* lo, size
     v += f32x4{bf2f(lv[0]), bf2f(lv[1]), bf2f(lv[2]), bf2f(lv[3])};
   }
   return v;
+}
+
+// Split reduction when the sweep took the block keys: one thread per (column, 4 dims) and 2 per
+// thread; o = sum_s O_s 2^(m_s - m*) / sum_s l_s 2^(m_s - m*) in split order.  Requests with one
+// split were written by the sweep.
+__global__ void __launch_bounds__(RED_THREADS) attn_merge(AttnArgs a) {
+  const int g = a.Hq / a.Hkv, T = a.T, R = T * g, D = a.D, nq = D / 4;
+  const int cblocks = (R + RED_COLS - 1) / RED_COLS;
+  const int bh = blockIdx.x / cblocks, c0 = (blockIdx.x % cblocks) * RED_COLS;
+  const int b = bh / a.Hkv, h = bh % a.Hkv;
+  int L = a.ctx_lens[b];
+  const int cap = min(a.max_pages * a.ps, a.max_ctx_len);
+  L = L < 0 ? 0 : (L > cap ? cap : L);   // out-of-range lengths were flagged by the sweep
+  const int nsplit = n_splits(a, L);
+  if (nsplit == 1) return;
+  const size_t unit0 = ((size_t)b * a.Hkv + h) * a.max_splits;
+  for (int it = threadIdx.x; it < RED_COLS * nq; it += RED_THREADS) {
+    const int c = c0 + it / nq, d4 = (it % nq) * 4;
+    if (c >= R) continue;
+    float m[RED_NS], l[RED_NS];
+    f32x4 o[RED_NS];
+    auto fetch = [&](int s0) {
+#pragma unroll
+      for (int i = 0; i < RED_NS; ++i) {
+        const bool in = s0 + i < nsplit;
+        const size_t u = (unit0 + s0 + (in ? i : 0)) * R + c;
+        m[i] = in ? a.part_ml[u * 2] : -INFINITY;
+        l[i] = in ? a.part_ml[u * 2 + 1] : 0.f;
+        o[i] = in ? *reinterpret_cast<const f32x4*>(a.part_o + u * D + d4) : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    };
+    float mstar = -INFINITY;
+    if (nsplit <= RED_NS) {
+      fetch(0);
+#pragma unroll
+      for (int i = 0; i < RED_NS; ++i) mstar = fmaxf(mstar, m[i]);
+    } else {
+      for (int sp = 0; sp < nsplit; ++sp) mstar = fmaxf(mstar, a.part_ml[((unit0 + sp) * R + c) * 2]);
+    }
+    const float m_use = mstar == -INFINITY ? 0.f : mstar;
+    float lsum = 0.f;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int s0 = 0; s0 < nsplit; s0 += RED_NS) {
+      if (nsplit > RED_NS) fetch(s0);
+#pragma unroll
+      for (int i = 0; i < RED_NS; ++i) {
+        const float e = exp2f(m[i] - m_use);
+        lsum += l[i] * e;
+        acc += o[i] * e;
+      }
+    }
+    acc *= 1.f / lsum;
+    const int j = c / g, hq = h * g + c % g;
+    const size_t off = ((size_t)(b * T + j) * a.Hq + hq) * D + d4;
+    if (a.o_f32) *reinterpret_cast<f32x4*>(a.o_f32 + off) = acc;
+    if (a.o_bf16) {
+      bf16x4 hv = {f2bf(acc[0]), f2bf(acc[1]), f2bf(acc[2]), f2bf(acc[3])};
+      *reinterpret_cast<bf16x4*>(a.o_bf16 + off) = hv;
+      if (a.o_bf16_lo) {
+        bf16x4 lv;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) lv[e] = f2bf(acc[e] - bf2f(hv[e]));
+        *reinterpret_cast<bf16x4*>(a.o_bf16_lo + off) = lv;
+      }
+    }
+  }
 }
 
 template <int D>
@@ -728,16 +832,24 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s, unsigned parts) {
   const bool lo = a.kc_lo != nullptr;   // fp32 storage: the cache comes as hi/lo planes
   hipError_t e = hipSuccess;
   if (parts & ATTN_SWEEP) {
-    if (!a.q_hi || !a.kc_hi || !a.vc_hi || !a.part_o || !a.part_ml) return hipErrorInvalidValue;
+    if (!a.q_hi || !a.kc_hi || !a.vc_hi) return hipErrorInvalidValue;
+    if (a.block_in_sweep ? (!a.kb_hi || !a.vb_hi) : (!a.part_o || !a.part_ml)) return hipErrorInvalidValue;
     if (a.D == 128) e = lo ? launch_sweep_nw<128, true>(a, s) : launch_sweep_nw<128, false>(a, s);
     else if (a.D == 64) e = lo ? launch_sweep_nw<64, true>(a, s) : launch_sweep_nw<64, false>(a, s);
     else return hipErrorInvalidValue;
     if (e != hipSuccess) return e;
   }
   if (parts & ATTN_REDUCE) {
-    if (!a.q_hi || !a.kb_hi || !a.vb_hi || !a.part_o || !a.part_ml) return hipErrorInvalidValue;   // block q/k/v, partials
     const int R = a.T * (a.Hq / a.Hkv);
     const int cblocks = (R + RED_COLS - 1) / RED_COLS;
+    if (a.block_in_sweep) {
+      if (a.max_splits > 1) {
+        if (!a.part_o || !a.part_ml) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(attn_merge, dim3(a.B * a.Hkv * cblocks), dim3(RED_THREADS), 0, s, a);
+      }
+      return hipGetLastError();
+    }
+    if (!a.q_hi || !a.kb_hi || !a.vb_hi || !a.part_o || !a.part_ml) return hipErrorInvalidValue;   // block q/k/v, partials
     if (a.D == 128) hipLaunchKernelGGL(attn_reduce<128>, dim3(a.B * a.Hkv * cblocks), dim3(RED_THREADS), 0, s, a);
     else hipLaunchKernelGGL(attn_reduce<64>, dim3(a.B * a.Hkv * cblocks), dim3(RED_THREADS), 0, s, a);
     e = hipGetLastError();

@@ -42,6 +42,7 @@ struct AttnArgs {
   const int32_t* ctx_lens = nullptr;                  // [B]
   int B = 0, T = 0, Hq = 0, Hkv = 0, D = 0, ps = 0, max_pages = 0, num_pages = 0;
   int window = 0, causal = 0, max_ctx_len = 0, split = 0, max_splits = 0;
+  int block_in_sweep = 1;     // 1: the sweep takes the block keys (bf16); 0: the reduction, in fp32
   float scale_log2 = 0.f;
   float* part_o = nullptr;    // [B*Hkv*max_splits, R, D]
   float* part_ml = nullptr;   // [B*Hkv*max_splits, R, 2]

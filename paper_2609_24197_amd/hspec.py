@@ -180,7 +180,8 @@ def mamba_cfg(cfg: I.StepConfig, W: dict | None = None) -> MambaCfg:
 
 def attn_cfg(cfg: I.StepConfig, max_pages: int, num_pages: int) -> AttnCfg:
     return AttnCfg(cfg.B, cfg.k, cfg.d_model, cfg.Hq, cfg.Hkv, cfg.D, cfg.page_size, max_pages, num_pages,
-                   cfg.window, cfg.split_tokens, BLOCK_CAUSAL if cfg.block_causal else 0, dtype_code(cfg),
+                   cfg.window, cfg.split_tokens,
+                   (BLOCK_CAUSAL if cfg.block_causal else 0) | (ATTN_PRECISE_IO if cfg.precise_io else 0), dtype_code(cfg),
                    cfg.eps, 0.0, cfg.rope_theta)
 
 

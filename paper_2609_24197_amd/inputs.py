@@ -56,6 +56,7 @@ class StepConfig:
     page_size: int = 16
     window: int = 0   # sliding window in tokens, 0 = full context
     block_causal: bool = False
+    precise_io: bool = False   # attention I/O as hi/lo planes, block keys in fp32 (stacked layers)
     eps: float = 1e-6
     rope_theta: float = 1e6
     n_fuse: int = 1   # |M|, number of fused target layers

@@ -27,6 +27,9 @@ SMALL = {
     # hi/lo inputs; Q/K/V over weight segments of 4096 and 1024 rows; O projection)
     "m640_large_tiles": I.StepConfig(name="s", B=40, k=16, d_model=512, H=8, P=64, N=16, G=1, chunk=16, Hq=32,
                                      Hkv=8, D=128, lengths="uniform:0:300"),
+    # hi/lo attention I/O, block keys in fp32 in the reduction (as in the whole drafter)
+    "precise_io": I.StepConfig(name="s", B=3, k=16, d_model=512, H=8, P=64, N=128, G=1, chunk=16, Hq=32, Hkv=8,
+                               D=128, lengths="list:300,0,77", precise_io=True),
 }
 
 

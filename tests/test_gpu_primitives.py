@@ -103,6 +103,12 @@ ATTN_CASES = {
     "causal": _small_attn_cfg(block_causal=True),
     "causal_window": _small_attn_cfg(block_causal=True, window=64, lengths="list:700,64,65"),
     "empty_ctx": _small_attn_cfg(B=2, lengths="list:0,0"),
+    # block keys in fp32 inside the reduction, every split through partials
+    "precise_ragged": _small_attn_cfg(precise_io=True),
+    "precise_causal_window": _small_attn_cfg(block_causal=True, window=64, lengths="list:700,64,65", precise_io=True),
+    "precise_empty_ctx": _small_attn_cfg(B=2, lengths="list:0,0", precise_io=True),
+    "precise_d64_k7": _small_attn_cfg(Hq=4, Hkv=4, D=64, k=7, lengths="list:33,64,200", precise_io=True),
+    "precise_f32": I.CONFIGS[1].replace(precise_io=True),
 }
 
 
@@ -156,9 +162,10 @@ def test_paged_attn_window_splits():
     assert_close(o, _ref_attn(causal, xc), "window 2048 causal, split 256")
 
 
-def test_paged_attn_phases_bitwise():
+@pytest.mark.parametrize("precise", [False, True], ids=["block_in_sweep", "block_in_reduction"])
+def test_paged_attn_phases_bitwise(precise):
     """The work list, sweep and reduction launched one call each give the one-call result."""
-    cfg = _small_attn_cfg(B=3, lengths="list:1000,37,450").replace(split_tokens=256)
+    cfg = _small_attn_cfg(B=3, lengths="list:1000,37,450", precise_io=precise).replace(split_tokens=256)
     x = I.make_attn_inputs(cfg, seed=6)
     whole, _ = _run_attn(cfg, x, split=256)
     d = dev(x)
