@@ -21,6 +21,8 @@ written for a reader to check against the paper by eye:
   mapping"): one S_init shared by every layer's Mamba, then layers of Mamba, attention
   over that layer's own target cache (absent in the partial layer) and a SwiGLU MLP,
   each pre-normed with a residual;
+* drafter-side KV injection (Sec. 2), the per-step cost of block-diffusion drafters that the
+  method removes, as a comparison stand-in;
 * the draft head: final RMSNorm, the LM head over the pruned vocabulary (App. B.2,
   "Pruned drafter vocabulary"), and the first-order Markov correction of each
   position's logits by the token chosen at the position before it (Sec. 3.3.3),
@@ -52,7 +54,8 @@ import numpy as np
 __all__ = [
     "f64", "rmsnorm", "silu", "softplus", "state_init", "in_proj_split", "causal_conv1d",
     "ssd_sequential", "ssd_chunked", "gated_rmsnorm", "mamba_mixer", "gather_slots", "rope",
-    "paged_attention", "attention_layer", "draft_step", "mlp", "drafter_forward", "draft_head", "compare",
+    "paged_attention", "attention_layer", "draft_step", "mlp", "drafter_forward", "kv_inject", "draft_head",
+    "compare",
 ]
 
 
@@ -399,10 +402,13 @@ def drafter_forward(layers, shared, x, caches, cfg, requests=None):
     restricts the work to some rows; the others are NaN.
     """
     idx = np.arange(cfg.B) if requests is None else np.asarray(requests)
-    S0, _ = state_init(np.asarray(x["h_last"])[idx], shared["W_r"], shared["W_dS"], cfg.H, cfg.P, cfg.N)
+    S0 = None
+    if any(W.get("W_in") is not None for W in layers):
+        S0, _ = state_init(np.asarray(x["h_last"])[idx], shared["W_r"], shared["W_dS"], cfg.H, cfg.P, cfg.N)
     h = f64(np.asarray(x["block_emb"])[idx])
     for W in layers:
-        h = h + mamba_mixer(rmsnorm(h, f64(W["norm1_w"]), cfg.eps), S0, W, cfg)
+        if W.get("W_in") is not None:   # layers without a Mamba module skip it (block-diffusion backbone)
+            h = h + mamba_mixer(rmsnorm(h, f64(W["norm1_w"]), cfg.eps), S0, W, cfg)
         if W.get("cache") is not None:
             c = caches[W["cache"]]
             cache = dict(k_cache=c["k_cache"], v_cache=c["v_cache"], page_table=np.asarray(x["page_table"])[idx],
@@ -411,6 +417,37 @@ def drafter_forward(layers, shared, x, caches, cfg, requests=None):
         h = h + mlp(rmsnorm(h, f64(W["norm3_w"]), cfg.eps), W)
     out = np.full((cfg.B,) + h.shape[1:], np.nan)
     out[idx] = h
+    return out
+
+
+def kv_inject(h_new, W_fc, layers, caches, page_table, ctx_lens, cfg):
+    """Drafter-side KV injection of a block-diffusion drafter (Sec. 2, "KV injection in block
+    drafting"), the cost H-Spec removes: every new input position's fused target hidden state
+    f = W_fc h_new (h_new: the |M| selected target layers, concatenated) is projected, for each
+    drafter layer, into k = RoPE(RMSNorm_D(W_k f) k_norm_w) and v = W_v f at its position
+    ctx_len + i, and appended to that layer's paged drafter cache.
+
+    h_new [B, n, |M| d_model]; layers: dicts with W_k, W_v, k_norm_w; caches: one dict of
+    k_cache/v_cache [num_pages, page_size, Hkv, D] per layer.  Returns the updated caches in
+    float64 (copies); slots other than the appended ones keep their values.
+    """
+    f = f64(h_new) @ f64(W_fc).T
+    Bsz, n = f.shape[0], f.shape[1]
+    L = np.asarray(ctx_lens, dtype=np.int64)
+    pos = L[:, None] + np.arange(n)[None, :]
+    out = []
+    for W, c in zip(layers, caches):
+        k = (f @ f64(W["W_k"]).T).reshape(Bsz, n, cfg.Hkv, cfg.D)
+        v = (f @ f64(W["W_v"]).T).reshape(Bsz, n, cfg.Hkv, cfg.D)
+        k = rope(rmsnorm(k, f64(W["k_norm_w"]), cfg.eps), pos, cfg.rope_theta)
+        kc, vc = f64(c["k_cache"]).copy(), f64(c["v_cache"]).copy()
+        for b in range(Bsz):
+            for i in range(n):
+                p = int(pos[b, i])
+                slot = int(page_table[b, p // cfg.page_size]) * cfg.page_size + p % cfg.page_size
+                kc.reshape(-1, cfg.Hkv, cfg.D)[slot] = k[b, i]
+                vc.reshape(-1, cfg.Hkv, cfg.D)[slot] = v[b, i]
+        out.append(dict(k_cache=kc, v_cache=vc))
     return out
 
 

@@ -561,4 +561,65 @@ def pin_drafter_layer_reads_its_cache(O):
     assert not np.allclose(O.drafter_forward(L, shared, x, c1, cfg), base)
 
 
+def pin_drafter_without_mamba(O):
+    """A block-diffusion layer (attention and MLP, no Mamba) needs no state projection: with its
+    attention output zero it is e + MLP(RMSNorm(e)) (the MLP pinned against torch above)."""
+    cfg, shared, L, x = _drafter_case(layers=("AF",))
+    for k in ("W_in", "conv_w", "conv_b", "D", "gnorm_w", "W_out", "dt_bias", "A_log", "norm1_w"):
+        L[0].pop(k, None)
+    L[0]["W_o"] = np.zeros_like(L[0]["W_o"])
+    out = O.drafter_forward(L, {}, x, x["caches"], cfg)
+    e = O.f64(x["block_emb"])
+    assert np.allclose(out, e + O.mlp(O.rmsnorm(e, O.f64(L[0]["norm3_w"]), cfg.eps), L[0]), rtol=1e-12, atol=1e-12)
+
+
+def _inject_case(seed=61):
+    cfg = _tiny_cfg(n_fuse=3, lengths="list:9,0")
+    rng = rng0(seed)
+    n = 3
+    x = I.make_drafter_inputs(cfg, seed, n_caches=2, extra_pages=4)
+    # room for n more positions: extend each request's pages from the spare pool
+    pt = x["page_table"].copy()
+    spare = [p for p in range(x["num_pages"]) if p not in set(pt[pt >= 0].tolist())]
+    need = [(int(Lb) + n + cfg.page_size - 1) // cfg.page_size for Lb in x["ctx_lens"]]
+    pt = np.concatenate([pt, np.full((cfg.B, max(need)), -1, np.int32)], axis=1)
+    for b in range(cfg.B):
+        for pg in range(need[b]):
+            if pt[b, pg] < 0:
+                pt[b, pg] = spare.pop()
+    h = rng.standard_normal((cfg.B, n, cfg.d_h))
+    W_fc = rng.standard_normal((cfg.d_model, cfg.d_h)) / np.sqrt(cfg.d_h)
+    layers = [dict(W_k=rng.standard_normal((cfg.Hkv * cfg.D, cfg.d_model)) / np.sqrt(cfg.d_model),
+                   W_v=rng.standard_normal((cfg.Hkv * cfg.D, cfg.d_model)) / np.sqrt(cfg.d_model),
+                   k_norm_w=1 + 0.1 * rng.standard_normal(cfg.D)) for _ in range(2)]
+    return cfg, h, W_fc, layers, x["caches"], pt, x["ctx_lens"], n
+
+
+def pin_kv_inject_placement(O):
+    """KV injection (Sec. 2) appends each new position's K/V at slot(ctx_len + i) of every
+    layer's cache and leaves every other slot as it was; read back through the (separately
+    pinned) slot map, the rows are the projections of the fused hidden state, RoPE'd keys at
+    the continued positions."""
+    cfg, h, W_fc, layers, caches, pt, L, n = _inject_case()
+    new = O.kv_inject(h, W_fc, layers, caches, pt, L, cfg)
+    slots = O.gather_slots(pt, L + n, cfg.page_size, int(max(L)) + n)
+    f = h @ W_fc.T
+    for W, c0, c1 in zip(layers, caches, new):
+        touched = np.zeros(c0["k_cache"].reshape(-1, cfg.Hkv, cfg.D).shape[0], bool)
+        for b in range(cfg.B):
+            pos = int(L[b]) + np.arange(n)
+            k = O.rope(O.rmsnorm((f[b] @ W["W_k"].T).reshape(n, cfg.Hkv, cfg.D), W["k_norm_w"], cfg.eps)[None],
+                       pos[None], cfg.rope_theta)[0]
+            v = (f[b] @ W["W_v"].T).reshape(n, cfg.Hkv, cfg.D)
+            sl = slots[b, pos]
+            assert np.all(sl >= 0)
+            touched[sl] = True
+            assert np.allclose(c1["k_cache"].reshape(-1, cfg.Hkv, cfg.D)[sl], k, rtol=1e-12, atol=1e-12)
+            assert np.allclose(c1["v_cache"].reshape(-1, cfg.Hkv, cfg.D)[sl], v, rtol=1e-12, atol=1e-12)
+        for name in ("k_cache", "v_cache"):
+            a0 = O.f64(c0[name]).reshape(touched.size, -1)
+            a1 = c1[name].reshape(touched.size, -1)
+            assert np.array_equal(a0[~touched], a1[~touched])
+
+
 PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

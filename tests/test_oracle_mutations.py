@@ -52,6 +52,12 @@ MUTATIONS = {
     "drafter_state_zeroed_after_first": ("h = h + mamba_mixer(rmsnorm(h, f64(W[\"norm1_w\"]), cfg.eps), S0, W, cfg)",
                                          "h = h + mamba_mixer(rmsnorm(h, f64(W[\"norm1_w\"]), cfg.eps), S0, W, cfg); S0 = 0 * S0"),
     "drafter_all_layers_cache0": ('c = caches[W["cache"]]', "c = caches[0]"),
+    "inject_positions_from_zero": ("pos = L[:, None] + np.arange(n)[None, :]\n    out = []",
+                                   "pos = 0 * L[:, None] + np.arange(n)[None, :]\n    out = []"),
+    "inject_v_rotated": ("v = (f @ f64(W[\"W_v\"]).T).reshape(Bsz, n, cfg.Hkv, cfg.D)",
+                         "v = rope((f @ f64(W[\"W_v\"]).T).reshape(Bsz, n, cfg.Hkv, cfg.D), pos, cfg.rope_theta)"),
+    "inject_slot_wrong_page": ("slot = int(page_table[b, p // cfg.page_size]) * cfg.page_size + p % cfg.page_size",
+                               "slot = int(page_table[b, p // cfg.page_size]) * cfg.page_size + (p + 1) % cfg.page_size"),
     "head_no_final_norm": ('hn = rmsnorm(h, f64(W["norm_f_w"]), eps)', "hn = h"),
     "markov_prev_never_advances": ("prev = tokens[:, j] if forced is None", "prev = prev if forced is None"),
     "markov_factors_swapped": ("lj = logits[:, j, :] + E[prev] @ U.T", "lj = logits[:, j, :] + U[prev] @ E.T"),
