@@ -201,7 +201,8 @@ size_t hspec_draft_step_workspace(const hspec_mamba_cfg* mcfg, const hspec_attn_
  * [d_model, ff] in the storage dtype.  layers: host array of n_layers (>= 1) entries.
  */
 typedef struct {
-  const hspec_mamba_w* mamba; /* W_in .. W_out of this layer */
+  const hspec_mamba_w* mamba; /* W_in .. W_out of this layer; NULL: no Mamba (a block-diffusion
+                                 layer; with no Mamba in any layer, W_r and W_dS are not read) */
   const float* norm1_w;       /* pre-Mamba RMSNorm gain [d_model] */
   const hspec_attn_w* attn;   /* NULL: the layer has no attention */
   const float* norm2_w;       /* pre-attention gain (layers with attention) */
@@ -217,6 +218,25 @@ hspec_status hspec_drafter_forward(const hspec_mamba_cfg* mcfg, const hspec_attn
                                    size_t ws_bytes, void* stream);
 size_t hspec_drafter_forward_workspace(const hspec_mamba_cfg* mcfg, const hspec_attn_cfg* acfg, int ff,
                                        int max_ctx_len);
+
+/*
+ * Drafter-side KV injection, the per-step cost of block-diffusion drafters that H-Spec removes
+ * (Sec. 2, "KV injection in block drafting"; Fig. 3), for comparison: the n = cfg->k new
+ * positions of every request (h_new [B, n, d_h], the |M| target layers' hidden states,
+ * storage dtype) are fused, f = h_new W_fc^T (W_fc [d_model, d_h]), and for each drafter layer
+ * l projected into k = RoPE(RMSNorm_D(f W_k[l]^T) k_norm_w[l]) and v = f W_v[l]^T
+ * (W_k[l], W_v[l] [Hkv*D, d_model]), which are written at slot(ctx_lens[b] + i) of that
+ * layer's paged cache k_cache[l], v_cache[l] [num_pages, page_size, Hkv, D] (storage dtype,
+ * updated in place).  W_k, W_v, k_norm_w, k_cache, v_cache are host arrays of n_layers device
+ * pointers.  The page table must map positions up to ctx_len + n - 1; unmapped positions set
+ * HSPEC_DEV_BAD_CTX_LEN and page ids outside the pool HSPEC_DEV_BAD_PAGE, and are skipped.
+ * Uses cfg B, k, d_model, Hkv, D, page_size, max_pages, num_pages, dtype, eps, rope_theta.
+ */
+hspec_status hspec_kv_inject(const hspec_attn_cfg* cfg, int d_h, int n_layers, const void* h_new, const void* W_fc,
+                             const void* const* W_k, const void* const* W_v, const float* const* k_norm_w,
+                             void* const* k_cache, void* const* v_cache, const int32_t* page_table,
+                             const int32_t* ctx_lens, void* workspace, size_t ws_bytes, void* stream);
+size_t hspec_kv_inject_workspace(const hspec_attn_cfg* cfg, int d_h);
 
 /*
  * Draft head (Sec. 3.3.3 "Causal correction"; App. B.1 "Markov rank"; App. B.2 "Pruned drafter

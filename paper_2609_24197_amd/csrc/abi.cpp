@@ -394,7 +394,8 @@ hspec::AttnArgs sweep_args(const hspec_attn_cfg& c, const AttnPlan& p, const int
 // QKV projections -> q/k norm + RoPE -> sweep + reduce -> O projection (+ residual R).
 hspec_status run_attn_core(const hspec_attn_cfg& c, const hspec_attn_w& w, Planes xn, const void* k_cache,
                            const void* v_cache, const int32_t* pt, const int32_t* lens, int max_ctx_len,
-                           const AttnPlan& p, const float* R, float* out, int* status, hipStream_t st) {
+                           const AttnPlan& p, const void* R, int r_bf16, float* out, int* status,
+                           hipStream_t st) {
   const int M = c.B * c.k;
   const int ldq = (c.Hq + 2 * c.Hkv) * c.D;
   Planes wq, wk, wv, wo, kc, vc;
@@ -441,7 +442,7 @@ hspec_status run_attn_core(const hspec_attn_cfg& c, const hspec_attn_w& w, Plane
   g.W_hi = wo.hi; g.W_lo = wo.lo; g.ldw = c.Hq * c.D;
   g.M = M; g.N = c.d_model; g.K = c.Hq * c.D;
   g.C = out; g.ldc = c.d_model;
-  g.R = R; g.ldr = c.d_model; g.r_bf16 = 0;
+  g.R = R; g.ldr = c.d_model; g.r_bf16 = r_bf16;
   use_scratch(g, p.gs);
   HIP_TRY(hspec::launch_gemm(g, st));
   return HSPEC_OK;
@@ -548,7 +549,7 @@ HSPEC_API hspec_status hspec_target_kv_block_attn(const hspec_attn_cfg* cfg, con
                                        hspec::kStatusClear, st));
   Planes xn;
   HIP_TRY(as_planes(x, cfg->dtype, p.x_in, xn, st));
-  return run_attn_core(*cfg, *w, xn, k_cache, v_cache, page_table, ctx_lens, max_ctx_len, p, nullptr, out, status, st);
+  return run_attn_core(*cfg, *w, xn, k_cache, v_cache, page_table, ctx_lens, max_ctx_len, p, nullptr, 0, out, status, st);
 }
 
 HSPEC_API size_t hspec_draft_step_workspace(const hspec_mamba_cfg* mcfg, const hspec_attn_cfg* acfg,
@@ -592,7 +593,7 @@ HSPEC_API hspec_status hspec_draft_step(const hspec_mamba_cfg* mcfg, const hspec
   if (hspec_status s = run_mamba_core(*mcfg, *mw, u, p.m, block_emb, !f32, p.x1, nullptr, st)) return s;
   HIP_TRY(hspec::launch_rmsnorm_planes(p.x1, 0, norm2_w, M, acfg->d_model, acfg->eps, p.at.xn_hi, p.at.xn_lo, st));
   Planes xn{p.at.xn_hi, p.at.xn_lo};
-  return run_attn_core(*acfg, *aw, xn, k_cache, v_cache, page_table, ctx_lens, max_ctx_len, p.at, p.x1, out, status,
+  return run_attn_core(*acfg, *aw, xn, k_cache, v_cache, page_table, ctx_lens, max_ctx_len, p.at, p.x1, 0, out, status,
                        st);
 }
 
@@ -801,7 +802,7 @@ void plan_forward(Arena& ar, const hspec_mamba_cfg& mc, const hspec_attn_cfg& ac
 
 // x_out = x + W_down (SiLU(W_gate u) * (W_up u)), u already normalised (planes).
 hspec_status run_mlp(const hspec_mamba_cfg& c, const hspec_layer_w& L, int ff, Planes u, const ForwardPlan& p,
-                     const float* x, float* x_out, hipStream_t st) {
+                     const void* x, int x_bf16, float* x_out, hipStream_t st) {
   const int M = c.B * c.k;
   Planes wg, wu, wd;
   HIP_TRY(as_planes(L.W_gate, c.dtype, p.wg, wg, st));
@@ -834,7 +835,7 @@ hspec_status run_mlp(const hspec_mamba_cfg& c, const hspec_layer_w& L, int ff, P
   g.W_hi = wd.hi; g.W_lo = wd.lo; g.ldw = ff;
   g.M = M; g.N = c.d_model; g.K = ff;
   g.C = x_out; g.ldc = c.d_model;
-  g.R = x; g.ldr = c.d_model; g.r_bf16 = 0;
+  g.R = x; g.ldr = c.d_model; g.r_bf16 = x_bf16;
   use_scratch(g, p.gs);
   HIP_TRY(hspec::launch_gemm(g, st));
   return HSPEC_OK;
@@ -863,14 +864,18 @@ HSPEC_API hspec_status hspec_drafter_forward(const hspec_mamba_cfg* mcfg, const 
   if (!layers) return fail(HSPEC_ERR_NULL, "layers is NULL");
   if (ff <= 0) return fail(HSPEC_ERR_SHAPE, "ff must be positive");
   if (ff % 8) return fail(HSPEC_ERR_UNSUPPORTED, "ff must be a multiple of 8");
-  bool any_attn = false;
+  bool any_attn = false, any_mamba = false;
   for (int l = 0; l < n_layers; ++l) {
     const hspec_layer_w& L = layers[l];
-    hspec_mamba_w mw = L.mamba ? *L.mamba : hspec_mamba_w{};
-    mw.W_r = W_r;
-    mw.W_dS = W_dS;
-    if (hspec_status s = check_mamba(mcfg, L.mamba ? &mw : nullptr, true)) return s;
-    if (!L.norm1_w || !L.norm3_w || !L.W_gate || !L.W_up || !L.W_down)
+    if (L.mamba) {
+      any_mamba = true;
+      hspec_mamba_w mw = *L.mamba;
+      mw.W_r = W_r;
+      mw.W_dS = W_dS;
+      if (hspec_status s = check_mamba(mcfg, &mw, true)) return s;
+      if (!L.norm1_w) return fail(HSPEC_ERR_NULL, "layer %d: norm1_w is NULL", l);
+    }
+    if (!L.norm3_w || !L.W_gate || !L.W_up || !L.W_down)
       return fail(HSPEC_ERR_NULL, "layer %d: a norm or MLP weight is NULL", l);
     if (L.attn) {
       any_attn = true;
@@ -882,7 +887,9 @@ HSPEC_API hspec_status hspec_drafter_forward(const hspec_mamba_cfg* mcfg, const 
   if (mcfg->B != acfg->B || mcfg->k != acfg->k || mcfg->d_model != acfg->d_model)
     return fail(HSPEC_ERR_SHAPE, "mamba and attention configs disagree on B, k or d_model");
   if (mcfg->dtype != acfg->dtype) return fail(HSPEC_ERR_DTYPE, "mamba and attention dtypes differ");
-  if (!h_last || !block_emb || !out || (any_attn && (!page_table || !ctx_lens)))
+  if (!any_mamba && (mcfg->B <= 0 || mcfg->k <= 0 || mcfg->d_model <= 0 || mcfg->d_model % 8 || !dtype_ok(mcfg->dtype)))
+    return fail(HSPEC_ERR_SHAPE, "bad B, k, d_model or dtype");
+  if (!block_emb || !out || (any_mamba && !h_last) || (any_attn && (!page_table || !ctx_lens)))
     return fail(HSPEC_ERR_NULL, "an input or output pointer is NULL");
   if (hspec_status s = check_ws(workspace, ws_bytes, hspec_drafter_forward_workspace(mcfg, acfg, ff, max_ctx_len)))
     return s;
@@ -897,15 +904,17 @@ HSPEC_API hspec_status hspec_drafter_forward(const hspec_mamba_cfg* mcfg, const 
   const int M = mc.B * mc.k;
   const bool f32 = is_f32(mc.dtype);
   HIP_TRY(hspec::launch_zero_words(status, hspec::kStatusClear, st));
-  hspec_mamba_w sw{};
-  sw.W_r = W_r;
-  sw.W_dS = W_dS;
-  if (hspec_status s = run_state(mc, sw, h_last, p.m.st, nullptr, st)) return s;
+  if (any_mamba) {
+    hspec_mamba_w sw{};
+    sw.W_r = W_r;
+    sw.W_dS = W_dS;
+    if (hspec_status s = run_state(mc, sw, h_last, p.m.st, nullptr, st)) return s;
+  }
 
   // the residual stream: block_emb (storage dtype), then fp32 buffers; the last sublayer
   // writes straight into out
   int total = 0;
-  for (int l = 0; l < n_layers; ++l) total += layers[l].attn ? 3 : 2;
+  for (int l = 0; l < n_layers; ++l) total += 1 + (layers[l].mamba ? 1 : 0) + (layers[l].attn ? 1 : 0);
   int done = 0;
   const void* x = block_emb;
   int x_bf16 = !f32;
@@ -913,26 +922,137 @@ HSPEC_API hspec_status hspec_drafter_forward(const hspec_mamba_cfg* mcfg, const 
   Planes u{p.m.u_hi, p.m.u_lo};
   for (int l = 0; l < n_layers; ++l) {
     const hspec_layer_w& L = layers[l];
-    HIP_TRY(hspec::launch_rmsnorm_planes(x, x_bf16, L.norm1_w, M, mc.d_model, mc.eps, p.m.u_hi, p.m.u_lo, st));
-    float* y = dst();
-    if (hspec_status s = run_mamba_core(mc, *L.mamba, u, p.m, x, x_bf16, y, nullptr, st)) return s;
-    x = y;
-    x_bf16 = 0;
+    float* y = nullptr;
+    if (L.mamba) {
+      HIP_TRY(hspec::launch_rmsnorm_planes(x, x_bf16, L.norm1_w, M, mc.d_model, mc.eps, p.m.u_hi, p.m.u_lo, st));
+      y = dst();
+      if (hspec_status s = run_mamba_core(mc, *L.mamba, u, p.m, x, x_bf16, y, nullptr, st)) return s;
+      x = y;
+      x_bf16 = 0;
+    }
     if (L.attn) {
       // the work list (the same for every layer) and a fresh item queue for this sweep
       HIP_TRY(hspec::launch_attention_plan(sweep_args(ac, p.at, page_table, ctx_lens, max_ctx_len, status), 0, st));
-      HIP_TRY(hspec::launch_rmsnorm_planes(x, 0, L.norm2_w, M, ac.d_model, ac.eps, p.at.xn_hi, p.at.xn_lo, st));
+      HIP_TRY(hspec::launch_rmsnorm_planes(x, x_bf16, L.norm2_w, M, ac.d_model, ac.eps, p.at.xn_hi, p.at.xn_lo, st));
       Planes xn{p.at.xn_hi, p.at.xn_lo};
       y = dst();
       if (hspec_status s = run_attn_core(ac, *L.attn, xn, L.k_cache, L.v_cache, page_table, ctx_lens, max_ctx_len,
-                                         p.at, static_cast<const float*>(x), y, status, st))
+                                         p.at, x, x_bf16, y, status, st))
         return s;
       x = y;
+      x_bf16 = 0;
     }
-    HIP_TRY(hspec::launch_rmsnorm_planes(x, 0, L.norm3_w, M, mc.d_model, mc.eps, p.m.u_hi, p.m.u_lo, st));
+    HIP_TRY(hspec::launch_rmsnorm_planes(x, x_bf16, L.norm3_w, M, mc.d_model, mc.eps, p.m.u_hi, p.m.u_lo, st));
     y = dst();
-    if (hspec_status s = run_mlp(mc, L, ff, u, p, static_cast<const float*>(x), y, st)) return s;
+    if (hspec_status s = run_mlp(mc, L, ff, u, p, x, x_bf16, y, st)) return s;
     x = y;
+    x_bf16 = 0;
+  }
+  return HSPEC_OK;
+}
+
+// ------------------------------------------------ drafter-side KV injection (comparison)
+
+struct InjectPlan {
+  int* status = nullptr;
+  SplitSlot h, wfc, wk, wv;
+  float* f = nullptr;                        // fused [M, d_model]
+  bf16 *f_hi = nullptr, *f_lo = nullptr;
+  float* kv = nullptr;                       // [M, 2 Hkv D]: k | v of one layer
+  bf16 *k_hi = nullptr, *k_lo = nullptr, *v_hi = nullptr, *v_lo = nullptr;
+  GemmScratch gs;
+};
+
+void plan_inject(Arena& ar, const hspec_attn_cfg& c, int d_h, InjectPlan& p) {
+  p.status = status_word(ar);
+  const size_t M = (size_t)c.B * c.k, kvw = (size_t)c.Hkv * c.D;
+  p.h = reserve_split(ar, c.dtype, M * d_h);
+  p.wfc = reserve_split(ar, c.dtype, (size_t)c.d_model * d_h);
+  p.wk = reserve_split(ar, c.dtype, kvw * c.d_model);
+  p.wv = reserve_split(ar, c.dtype, kvw * c.d_model);
+  p.f = ar.take<float>(M * c.d_model);
+  p.f_hi = ar.take<bf16>(M * c.d_model);
+  p.f_lo = ar.take<bf16>(M * c.d_model);
+  p.kv = ar.take<float>(M * 2 * kvw);
+  p.k_hi = ar.take<bf16>(M * kvw);
+  p.k_lo = ar.take<bf16>(M * kvw);
+  p.v_hi = ar.take<bf16>(M * kvw);
+  p.v_lo = ar.take<bf16>(M * kvw);
+  p.gs = reserve_gemm(ar, c.dtype, {{(int)M, c.d_model, d_h}, {(int)M, 2 * (int)kvw, c.d_model}, {(int)M, (int)kvw, c.d_model}});
+}
+
+HSPEC_API size_t hspec_kv_inject_workspace(const hspec_attn_cfg* cfg, int d_h) {
+  if (!cfg || d_h <= 0 || cfg->B <= 0 || cfg->k <= 0) return 0;
+  Arena ar;
+  InjectPlan p;
+  plan_inject(ar, *cfg, d_h, p);
+  return ar.size();
+}
+
+HSPEC_API hspec_status hspec_kv_inject(const hspec_attn_cfg* cfg, int d_h, int n_layers, const void* h_new,
+                                       const void* W_fc, const void* const* W_k, const void* const* W_v,
+                                       const float* const* k_norm_w, void* const* k_cache, void* const* v_cache,
+                                       const int32_t* page_table, const int32_t* ctx_lens, void* workspace,
+                                       size_t ws_bytes, void* stream) {
+  g_err.clear();
+  if (hspec_status s = check_attn_cfg(cfg, 0)) return s;
+  if (d_h <= 0 || n_layers < 1) return fail(HSPEC_ERR_SHAPE, "d_h and n_layers must be positive");
+  if (d_h % 8) return fail(HSPEC_ERR_UNSUPPORTED, "d_h must be a multiple of 8");
+  if (cfg->d_model <= 0 || cfg->d_model % 8) return fail(HSPEC_ERR_UNSUPPORTED, "d_model must be a positive multiple of 8");
+  if (!h_new || !W_fc || !W_k || !W_v || !k_norm_w || !k_cache || !v_cache || !page_table || !ctx_lens)
+    return fail(HSPEC_ERR_NULL, "an input or output pointer is NULL");
+  for (int l = 0; l < n_layers; ++l)
+    if (!W_k[l] || !W_v[l] || !k_norm_w[l] || !k_cache[l] || !v_cache[l])
+      return fail(HSPEC_ERR_NULL, "layer %d: a weight or cache pointer is NULL", l);
+  if (hspec_status s = check_ws(workspace, ws_bytes, hspec_kv_inject_workspace(cfg, d_h))) return s;
+  hipStream_t st = (hipStream_t)stream;
+  const hspec_attn_cfg& c = *cfg;
+  Arena ar{(char*)workspace};
+  InjectPlan p;
+  plan_inject(ar, c, d_h, p);
+  HIP_TRY(hspec::launch_zero_words(p.status, hspec::kStatusClear, st));
+  const int M = c.B * c.k, kvw = c.Hkv * c.D;
+  Planes h, wfc;
+  HIP_TRY(as_planes(h_new, c.dtype, p.h, h, st));
+  HIP_TRY(as_planes(W_fc, c.dtype, p.wfc, wfc, st));
+  hspec::GemmArgs g;
+  g.A_hi = h.hi; g.A_lo = h.lo; g.lda = d_h;
+  g.W_hi = wfc.hi; g.W_lo = wfc.lo; g.ldw = d_h;
+  g.M = M; g.N = c.d_model; g.K = d_h;
+  g.C = p.f; g.ldc = c.d_model;
+  use_scratch(g, p.gs);
+  HIP_TRY(hspec::launch_gemm(g, st));
+  HIP_TRY(hspec::launch_split_planes(p.f, (size_t)M * c.d_model, p.f_hi, p.f_lo, st));
+  for (int l = 0; l < n_layers; ++l) {
+    Planes wk, wv;
+    HIP_TRY(as_planes(W_k[l], c.dtype, p.wk, wk, st));
+    HIP_TRY(as_planes(W_v[l], c.dtype, p.wv, wv, st));
+    if (!wk.lo) {   // one product over the two row segments [W_k; W_v]
+      hspec::GemmArgs gk;
+      gk.A_hi = p.f_hi; gk.A_lo = p.f_lo; gk.lda = c.d_model;
+      gk.W_hi = wk.hi; gk.W2 = wv.hi; gk.N1 = kvw; gk.N2 = kvw; gk.ldw = c.d_model;
+      gk.M = M; gk.N = 2 * kvw; gk.K = c.d_model;
+      gk.C = p.kv; gk.ldc = 2 * kvw;
+      use_scratch(gk, p.gs);
+      HIP_TRY(hspec::launch_gemm(gk, st));
+    } else {
+      const Planes* w2[2] = {&wk, &wv};
+      for (int i = 0; i < 2; ++i) {
+        hspec::GemmArgs gk;
+        gk.A_hi = p.f_hi; gk.A_lo = p.f_lo; gk.lda = c.d_model;
+        gk.W_hi = w2[i]->hi; gk.W_lo = w2[i]->lo; gk.ldw = c.d_model;
+        gk.M = M; gk.N = kvw; gk.K = c.d_model;
+        gk.C = p.kv + (size_t)i * kvw; gk.ldc = 2 * kvw;
+        use_scratch(gk, p.gs);
+        HIP_TRY(hspec::launch_gemm(gk, st));
+      }
+    }
+    // k: per-head RMSNorm + RoPE at ctx_len + i (no query heads); v: copied
+    HIP_TRY(hspec::launch_qk_norm_rope(p.kv, nullptr, k_norm_w[l], ctx_lens, c.B, c.k, 0, c.Hkv, c.D, c.eps,
+                                       c.rope_theta, nullptr, nullptr, p.k_hi, p.k_lo, p.v_hi, p.v_lo, st));
+    HIP_TRY(hspec::launch_kv_append(p.k_hi, p.k_lo, p.v_hi, p.v_lo, c.B, c.k, c.Hkv, c.D, page_table, c.max_pages,
+                                    c.num_pages, c.page_size, ctx_lens, k_cache[l], v_cache[l], !is_f32(c.dtype),
+                                    p.status, st));
   }
   return HSPEC_OK;
 }

@@ -282,6 +282,42 @@ __global__ void __launch_bounds__(256) silu_mul_kernel(const float* gu, int ff, 
   if (lo) lo[row * ff + i] = f2bf(v - bf2f(h));
 }
 
+// Appends the new rows [B*n, Hkv*D] (bf16 planes) of K and V at slot(ctx_len + i) of a paged
+// cache.  Positions the table does not map, or page ids outside the pool, set a status bit and
+// are skipped.
+template <typename T>
+__global__ void __launch_bounds__(256) kv_append_kernel(const bf16* k_hi, const bf16* k_lo, const bf16* v_hi,
+                                                        const bf16* v_lo, int n, int row, const int32_t* pt,
+                                                        int max_pages, int num_pages, int ps, const int32_t* lens,
+                                                        T* kc, T* vc, int* status) {
+  const int tok = blockIdx.x, b = tok / n, i = tok % n;
+  const int L = lens[b];
+  const int pos = L + i;
+  const int pg = pos / ps;
+  if (L < 0 || pg >= max_pages) {
+    if (threadIdx.x == 0 && status) atomicOr(status, 2);
+    return;
+  }
+  const int pid = pt[(size_t)b * max_pages + pg];
+  if (pid < 0 || pid >= num_pages) {
+    if (threadIdx.x == 0 && status) atomicOr(status, 1);
+    return;
+  }
+  const size_t dst = ((size_t)pid * ps + pos % ps) * row, src = (size_t)tok * row;
+  for (int e = threadIdx.x; e < row; e += blockDim.x) {
+    float kv = bf2f(k_hi[src + e]), vv = bf2f(v_hi[src + e]);
+    if (k_lo) kv += bf2f(k_lo[src + e]);
+    if (v_lo) vv += bf2f(v_lo[src + e]);
+    if constexpr (sizeof(T) == 2) {
+      kc[dst + e] = f2bf(kv);
+      vc[dst + e] = f2bf(vv);
+    } else {
+      kc[dst + e] = kv;
+      vc[dst + e] = vv;
+    }
+  }
+}
+
 __global__ void zero_kernel(int* p, int n) {
   for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = 0;
 }
@@ -344,6 +380,20 @@ hipError_t launch_split_planes(const float* x, size_t n, bf16* hi, bf16* lo, hip
 hipError_t launch_silu_mul(const float* gu, int rows, int ff, bf16* hi, bf16* lo, hipStream_t s) {
   if (rows <= 0 || ff <= 0) return hipSuccess;
   hipLaunchKernelGGL(silu_mul_kernel, dim3((ff + 255) / 256, rows), dim3(256), 0, s, gu, ff, hi, lo);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_append(const bf16* k_hi, const bf16* k_lo, const bf16* v_hi, const bf16* v_lo, int B, int n,
+                            int Hkv, int D, const int32_t* page_table, int max_pages, int num_pages, int ps,
+                            const int32_t* ctx_lens, void* k_cache, void* v_cache, int cache_bf16, int* status,
+                            hipStream_t s) {
+  if (B * n <= 0) return hipSuccess;
+  if (cache_bf16)
+    hipLaunchKernelGGL(kv_append_kernel<bf16>, dim3(B * n), dim3(256), 0, s, k_hi, k_lo, v_hi, v_lo, n, Hkv * D,
+                       page_table, max_pages, num_pages, ps, ctx_lens, (bf16*)k_cache, (bf16*)v_cache, status);
+  else
+    hipLaunchKernelGGL(kv_append_kernel<float>, dim3(B * n), dim3(256), 0, s, k_hi, k_lo, v_hi, v_lo, n, Hkv * D,
+                       page_table, max_pages, num_pages, ps, ctx_lens, (float*)k_cache, (float*)v_cache, status);
   return hipGetLastError();
 }
 

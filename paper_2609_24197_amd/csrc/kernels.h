@@ -121,6 +121,12 @@ hipError_t launch_qk_norm_rope(const float* qkv, const float* qw, const float* k
 hipError_t launch_split_planes(const float* x, size_t n, bf16* hi, bf16* lo, hipStream_t s);
 // SwiGLU: h = SiLU(gate) * up from rows [gate | up] (fp32, width 2 ff) -> bf16 planes [rows, ff].
 hipError_t launch_silu_mul(const float* gu, int rows, int ff, bf16* hi, bf16* lo, hipStream_t s);
+// Appends K/V rows [B*n, Hkv*D] (bf16 planes, lo optional) at slot(ctx_len + i) of a paged cache
+// (bf16 or fp32 storage); unmapped positions set status bit 2, bad page ids bit 1.
+hipError_t launch_kv_append(const bf16* k_hi, const bf16* k_lo, const bf16* v_hi, const bf16* v_lo, int B, int n,
+                            int Hkv, int D, const int32_t* page_table, int max_pages, int num_pages, int ps,
+                            const int32_t* ctx_lens, void* k_cache, void* v_cache, int cache_bf16, int* status,
+                            hipStream_t s);
 // Zero n int32 words (device status, counters) with a kernel, graph-capture safe.
 hipError_t launch_zero_words(int* p, int n, hipStream_t s);
 

@@ -99,6 +99,9 @@ EXPORTS = {
                                                                                              C.c_void_p, C.c_size_t,
                                                                                              C.c_void_p]),
     "hspec_drafter_forward_workspace": (C.c_size_t, [C.POINTER(MambaCfg), C.POINTER(AttnCfg), C.c_int, C.c_int]),
+    "hspec_kv_inject": (C.c_int, [C.POINTER(AttnCfg), C.c_int, C.c_int, C.c_void_p, C.c_void_p] +
+                        [C.POINTER(C.c_void_p)] * 5 + [C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
+    "hspec_kv_inject_workspace": (C.c_size_t, [C.POINTER(AttnCfg), C.c_int]),
     "hspec_draft_head": (C.c_int, [C.POINTER(HeadCfg), C.POINTER(HeadW)] + [C.c_void_p] * 7 + [C.c_size_t,
                                                                                           C.c_void_p]),
     "hspec_draft_head_workspace": (C.c_size_t, [C.POINTER(HeadCfg)]),
@@ -339,7 +342,7 @@ def drafter_forward(cfg, shared: dict, layers: list, X: dict, out, ws, max_ctx_l
     keep = []
     arr = (LayerW * len(layers))()
     for i, W in enumerate(layers):
-        mw = mamba_w(W)
+        mw = mamba_w(W) if W.get("W_in") is not None else None
         keep.append(mw)
         aw = None
         c = None
@@ -347,12 +350,33 @@ def drafter_forward(cfg, shared: dict, layers: list, X: dict, out, ws, max_ctx_l
             aw = attn_w(W)
             keep.append(aw)
             c = X["caches"][W["cache"]]
-        arr[i] = LayerW(C.pointer(mw), ptr(W["norm1_w"]), C.pointer(aw) if aw is not None else None,
+        arr[i] = LayerW(C.pointer(mw) if mw is not None else None, ptr(W.get("norm1_w")),
+                        C.pointer(aw) if aw is not None else None,
                         ptr(W.get("norm2_w")) if aw is not None else None, ptr(c["k_cache"]) if c else None,
                         ptr(c["v_cache"]) if c else None, ptr(W["norm3_w"]), ptr(W["W_gate"]), ptr(W["W_up"]),
                         ptr(W["W_down"]))
     W_dS = shared.get("W_dS_packed", shared.get("W_dS"))
+    if "W_r" not in shared:
+        shared = dict(shared, W_r=None)
     _check(lib().hspec_drafter_forward(C.byref(mc), C.byref(ac), cfg.d_ff, len(layers), ptr(shared["W_r"]), ptr(W_dS),
-                                       arr, ptr(X["h_last"]), ptr(X["block_emb"]), ptr(X["page_table"]),
+                                       arr, ptr(X.get("h_last")), ptr(X["block_emb"]), ptr(X["page_table"]),
                                        ptr(X["ctx_lens"]), int(max_ctx_len), ptr(out), ptr(ws), ws.numel(),
                                        stream_ptr()))
+
+
+def kv_inject_workspace(cfg, max_pages, num_pages) -> int:
+    ac = attn_cfg(cfg, max_pages, num_pages)
+    return lib().hspec_kv_inject_workspace(C.byref(ac), cfg.d_h)
+
+
+def kv_inject(cfg, IW: dict, h_new, caches: list, page_table, ctx_lens, ws):
+    """Drafter-side KV injection (hspec_kv_inject): appends cfg.k new positions per request to
+    each layer's cache in ``caches`` (dicts of k_cache/v_cache device tensors, in place)."""
+    n = len(IW["layers"])
+    ac = attn_cfg(cfg, page_table.shape[1], caches[0]["k_cache"].shape[0])
+    arr = lambda xs: (C.c_void_p * n)(*[x.data_ptr() for x in xs])  # noqa: E731
+    L = IW["layers"]
+    _check(lib().hspec_kv_inject(C.byref(ac), cfg.d_h, n, ptr(h_new), ptr(IW["W_fc"]), arr([w["W_k"] for w in L]),
+                                 arr([w["W_v"] for w in L]), arr([w["k_norm_w"] for w in L]),
+                                 arr([c["k_cache"] for c in caches]), arr([c["v_cache"] for c in caches]),
+                                 ptr(page_table), ptr(ctx_lens), ptr(ws), ws.numel(), stream_ptr()))

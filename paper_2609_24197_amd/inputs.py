@@ -302,7 +302,11 @@ def make_drafter_weights(cfg: StepConfig, seed: int = 0, layers=DRAFTER_LAYERS, 
     for l, spec in enumerate(layers):
         pre = f"L{l}."
         attn = () if "A" in spec else ("W_q", "W_k", "W_v", "W_o", "q_norm_w", "k_norm_w", "norm2_w")
-        W = make_weights(cfg, seed, skip=("W_r", "W_dS") + attn, prefix=pre)
+        mamba = () if "M" in spec else ("W_in", "conv_w", "conv_b", "D", "gnorm_w", "W_out", "norm1_w")
+        W = make_weights(cfg, seed, skip=("W_r", "W_dS") + attn + mamba, prefix=pre)
+        if "M" not in spec:
+            W.pop("dt_bias")
+            W.pop("A_log")
         W["norm3_w"] = normal(pre + "norm3_w", (cfg.d_model,), 0.1, seed, "f32", 1.0)
         W["W_gate"] = normal(pre + "W_gate", (cfg.d_ff, cfg.d_model), cfg.d_model ** -0.5, seed, cfg.dtype)
         W["W_up"] = normal(pre + "W_up", (cfg.d_ff, cfg.d_model), cfg.d_model ** -0.5, seed, cfg.dtype)
@@ -324,6 +328,19 @@ def make_drafter_inputs(cfg: StepConfig, seed: int = 0, n_caches: int = 3, extra
                            v_cache=normal(f"v_cache{c}", shape, 1.0, seed, cfg.dtype)))
     x["caches"] = caches
     return x
+
+
+def make_inject_weights(cfg: StepConfig, seed: int = 0, n_layers: int = 5) -> dict:
+    """Weights of the drafter-side KV-injection stand-in: the fusion W_fc [d_model, |M| d_model]
+    and, per drafter layer, W_k, W_v [Hkv D, d_model] and the key norm gain."""
+    dm, kv = cfg.d_model, cfg.Hkv * cfg.D
+    return {
+        "W_fc": normal("inj.W_fc", (dm, cfg.d_h), cfg.d_h ** -0.5, seed, cfg.dtype),
+        "layers": [{"W_k": normal(f"inj{l}.W_k", (kv, dm), dm ** -0.5, seed, cfg.dtype),
+                    "W_v": normal(f"inj{l}.W_v", (kv, dm), dm ** -0.5, seed, cfg.dtype),
+                    "k_norm_w": normal(f"inj{l}.k_norm_w", (cfg.D,), 0.1, seed, "f32", 1.0)}
+                   for l in range(n_layers)],
+    }
 
 
 HEAD_VOCAB = 32000   # pruned drafter vocabulary (App. B.2)

@@ -67,3 +67,52 @@ def test_drafter_forward_full_size():
     idx = [0, cfg.B - 1]
     ref = O.drafter_forward(L, shared, x, x["caches"], cfg, requests=idx)
     assert_close(out[idx], ref[idx], "full-size drafter")
+
+
+# ------------------------------------------------- block-diffusion comparison stand-in
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_kv_inject(dtype):
+    """Drafter-side KV injection: the k new positions of every request land at slot(ctx_len + i)
+    of each layer's cache (values to the tolerance); every other slot is bit-identical."""
+    n = 5
+    cfg = I.StepConfig(name="inj", B=3, k=n, d_model=256, H=4, P=64, N=16, G=1, chunk=8, Hq=8, Hkv=2, D=128,
+                       lengths="list:45,5,17", n_fuse=3, dtype=dtype)
+    x = I.make_drafter_inputs(cfg, seed=31, n_caches=2, extra_pages=3)   # pages mapped up to ctx_len
+    ctx = (x["ctx_lens"] - n).astype(np.int32)                           # ... the last n are the new ones
+    IW = I.make_inject_weights(cfg, seed=31, n_layers=2)
+    h_new = I.normal("inj_h", (cfg.B, n, cfg.d_h), 1.0, 31, dtype)
+    caches = [dev(c) for c in x["caches"]]
+    d = dev(dict(page_table=x["page_table"], ctx_lens=ctx, h_new=h_new))
+    IWd = {"W_fc": hspec.to_device(IW["W_fc"]), "layers": [dev(w) for w in IW["layers"]]}
+    ws = hspec.workspace(hspec.kv_inject_workspace(cfg, x["page_table"].shape[1], x["num_pages"]))
+    hspec.kv_inject(cfg, IWd, d["h_new"], caches, d["page_table"], d["ctx_lens"], ws)
+    assert hspec.read_status(ws) == 0
+    ref = O.kv_inject(h_new, IW["W_fc"], IW["layers"], x["caches"], x["page_table"], ctx, cfg)
+    slots = O.gather_slots(x["page_table"], x["ctx_lens"], cfg.page_size, int(x["ctx_lens"].max()))
+    new = np.concatenate([slots[b, int(ctx[b]):int(x["ctx_lens"][b])] for b in range(cfg.B)])
+    for l in range(2):
+        for name in ("k_cache", "v_cache"):
+            g = host(caches[l][name]).reshape(-1, cfg.Hkv * cfg.D)
+            r = ref[l][name].reshape(-1, cfg.Hkv * cfg.D)
+            orig = x["caches"][l][name].reshape(-1, cfg.Hkv * cfg.D)
+            keep = np.ones(g.shape[0], bool)
+            keep[new] = False
+            assert np.array_equal(g[keep], orig[keep]), f"layer {l} {name}: a slot outside the new ones changed"
+            assert_close(O.f64(g[new]), r[new], f"layer {l} {name}")
+
+
+def test_block_diffusion_forward():
+    """The comparison backbone: attention-MLP layers without Mamba over their own caches."""
+    cfg = I.StepConfig(name="bd", B=3, k=16, d_model=256, H=4, P=64, N=16, G=1, chunk=16, Hq=32, Hkv=8, D=128,
+                       lengths="list:300,0,77", ff=512)
+    shared, L = I.make_drafter_weights(cfg, seed=32, layers=("AF",) * 3, skip_state=True)
+    x = I.make_drafter_inputs(cfg, seed=32, n_caches=3)
+    X = dev({k: v for k, v in x.items() if k not in ("caches", "h_last")})
+    X["caches"] = [dev(c) for c in x["caches"]]
+    maxL = int(x["ctx_lens"].max())
+    ws = hspec.workspace(hspec.drafter_forward_workspace(cfg, x["page_table"].shape[1], x["num_pages"], maxL))
+    out = empty((cfg.B, cfg.k, cfg.d_model))
+    hspec.drafter_forward(cfg, {}, _dev_layers(L), X, out, ws, maxL)
+    assert hspec.read_status(ws) == 0
+    assert_close(host(out), O.drafter_forward(L, {}, x, x["caches"], cfg), "block-diffusion backbone")
