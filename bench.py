@@ -160,6 +160,98 @@ def forward_figures(cfg, Wd, Xd, x, args, torch):
             "fused_target_layers": I.DRAFTER_FUSE, "mlp_hidden": fc.d_ff, "target_caches": 3}
 
 
+def compare_systems(args, torch):
+    """The hybrid drafter against a block-diffusion drafter with drafter-side KV injection, per
+    draft step (the runtime-scaling study of Sec. 4 and the injection cost of Fig. 3), on
+    synthetic random weights and caches drawn on the device (timing only; parity is tested
+    separately):
+      hybrid: hspec_drafter_forward, 3 x (Mamba, attention, MLP) + 1 x (Mamba, MLP), the Mamba
+              state projected from |M| = 5 fused target layers;
+      block diffusion: hspec_kv_inject of the k new positions into 5 drafter-side caches, then
+              5 x (attention, MLP) over those caches (hspec_drafter_forward without Mamba).
+    Shapes: the App. B.1 drafter for an 8B target (48 Mamba heads of 64, 4 groups, r = 4096,
+    d_state 16: the smallest the scan takes, App. B.1 uses 4), Qwen3-8B attention (32 / 8 / 128),
+    MLP hidden 12,288, k = 16, the 2,048-token window of App. B.2."""
+    dev = "cuda"
+    bf = torch.bfloat16
+
+    def rnd(*shape, std=1.0, dtype=bf):
+        return (torch.randn(*shape, device=dev) * std).to(dtype)
+
+    base = I.StepConfig(name="cmp", B=8, k=16, d_model=4096, H=48, P=64, N=16, G=4, chunk=16, Hq=32, Hkv=8, D=128,
+                        lengths="fixed:1040", n_fuse=I.DRAFTER_FUSE, ff=12288, window=2048)
+    dm, di, ff, kv = base.d_model, base.d_inner, base.d_ff, base.Hkv * base.D
+
+    def attn_w():
+        return dict(W_q=rnd(base.Hq * base.D, dm, std=dm ** -0.5), W_k=rnd(kv, dm, std=dm ** -0.5),
+                    W_v=rnd(kv, dm, std=dm ** -0.5), W_o=rnd(dm, base.Hq * base.D, std=(base.Hq * base.D) ** -0.5),
+                    q_norm_w=torch.ones(base.D, device=dev), k_norm_w=torch.ones(base.D, device=dev),
+                    norm2_w=torch.ones(dm, device=dev))
+
+    def mlp_w():
+        return dict(W_gate=rnd(ff, dm, std=dm ** -0.5), W_up=rnd(ff, dm, std=dm ** -0.5),
+                    W_down=rnd(dm, ff, std=ff ** -0.5), norm3_w=torch.ones(dm, device=dev))
+
+    def mamba_w():
+        return dict(W_in=rnd(base.d_in_proj, dm, std=dm ** -0.5), conv_w=rnd(base.conv_dim, base.conv_w, std=0.5),
+                    conv_b=rnd(base.conv_dim, std=0.5), dt_bias=torch.full((base.H,), -4.0, device=dev),
+                    A_log=torch.zeros(base.H, device=dev), D=torch.ones(base.H, device=dev),
+                    gnorm_w=torch.ones(di, device=dev), W_out=rnd(dm, di, std=di ** -0.5),
+                    norm1_w=torch.ones(dm, device=dev))
+
+    hyb = [dict(mamba_w(), **attn_w(), **mlp_w(), cache=i) for i in range(3)] + [dict(mamba_w(), **mlp_w(), cache=None)]
+    shared = {"W_r": rnd(base.rank, base.d_h, std=base.d_h ** -0.5),
+              "W_dS_packed": hspec.pack_w_ds(rnd(base.d_S, base.rank, std=base.rank ** -0.5), base.d_S, base.rank)}
+    bd = [dict(attn_w(), **mlp_w(), cache=i) for i in range(5)]
+    IW = {"W_fc": rnd(dm, base.d_h, std=base.d_h ** -0.5),
+          "layers": [dict(W_k=rnd(kv, dm, std=dm ** -0.5), W_v=rnd(kv, dm, std=dm ** -0.5),
+                          k_norm_w=torch.ones(base.D, device=dev)) for _ in range(5)]}
+
+    def timed(fn, n=10, warm=3):
+        for _ in range(warm):
+            fn()
+        torch.cuda.synchronize()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        for _ in range(n):
+            fn()
+        e.record()
+        torch.cuda.synchronize()
+        return s.elapsed_time(e) / n
+
+    def point(C, L):
+        cfg = base.replace(B=C, lengths=f"fixed:{L}")
+        table, num_pages = I.make_page_table(cfg.replace(lengths=f"fixed:{L + cfg.k}"),
+                                             np.full(C, L + cfg.k, np.int32), seed=0)
+        pt = torch.from_numpy(table).to(dev)
+        lens = torch.full((C,), L, dtype=torch.int32, device=dev)
+        caches = [dict(k_cache=rnd(num_pages, 16, base.Hkv, base.D), v_cache=rnd(num_pages, 16, base.Hkv, base.D))
+                  for _ in range(5)]
+        X = dict(page_table=pt, ctx_lens=lens, block_emb=rnd(C, cfg.k, dm), h_last=rnd(C, base.d_h), caches=caches)
+        h_new = rnd(C, cfg.k, base.d_h)
+        ws_h = hspec.workspace(hspec.drafter_forward_workspace(cfg, table.shape[1], num_pages, L))
+        ws_i = hspec.workspace(hspec.kv_inject_workspace(cfg, table.shape[1], num_pages))
+        out = torch.empty((C, cfg.k, dm), dtype=torch.float32, device=dev)
+        t_h = timed(lambda: hspec.drafter_forward(cfg, shared, hyb, X, out, ws_h, L))
+        t_i = timed(lambda: hspec.kv_inject(cfg, IW, h_new, caches, pt, lens, ws_i))
+        t_b = timed(lambda: hspec.drafter_forward(cfg, {}, bd, X, out, ws_h, L))
+        assert hspec.read_status(ws_h) == 0 and hspec.read_status(ws_i) == 0
+        row = {"C": C, "ctx": L, "hybrid_ms": round(t_h, 4), "inject_ms": round(t_i, 4),
+               "block_diffusion_ms": round(t_b, 4), "block_diffusion_with_inject_ms": round(t_i + t_b, 4),
+               "hybrid_speedup": round((t_i + t_b) / t_h - 1.0, 4)}
+        log(f"C={C:4d} ctx={L:5d}: hybrid {t_h:.3f} ms; block diffusion {t_b:.3f} + injection {t_i:.3f} ms; "
+            f"hybrid faster by {row['hybrid_speedup'] * 100:+.1f} %")
+        return row
+
+    conc = [point(C, 1040) for C in (4, 8, 16, 32, 64, 128)]
+    ctx = [point(128, L) for L in (256, 512, 768, 1024, 1536, 2048, 3072, 4096)]
+    print(json.dumps({"metric": "draft-step forward time, hybrid vs block diffusion with KV injection",
+                      "unit": "ms", "data": "synthetic", "dtype": "bf16",
+                      "shapes": {"d_model": dm, "mamba": "H48 P64 N16 G4", "Hq": base.Hq, "Hkv": base.Hkv,
+                                 "D": base.D, "ff": ff, "k": base.k, "fused_layers": base.n_fuse, "window": 2048},
+                      "concurrency": conc, "context_at_C128": ctx}), flush=True)
+
+
 def cpu_baseline(cfg, W, x, n_req: int):
     """The float64 oracle on the first n_req requests of the same workload (all positions)."""
     import oracle.hspec_oracle as O
@@ -231,6 +323,9 @@ def main():
                          "2048); default: the workload's own (full context)")
     ap.add_argument("--block-causal", action="store_true",
                     help="causal attention inside the drafted block instead of bidirectional")
+    ap.add_argument("--compare", action="store_true",
+                    help="time the hybrid drafter against a block-diffusion drafter with KV injection "
+                         "across concurrency and context length, print one JSON line and exit")
     ap.add_argument("--counters", action="store_true",
                     help="launch each measured kernel once (for rocprofv3 --pmc) and exit")
     args = ap.parse_args()
@@ -250,6 +345,9 @@ def main():
         cfg = cfg.replace(block_causal=True)
     if args.counters:
         counters(cfg, args.seed, torch)
+        return
+    if args.compare:
+        compare_systems(args, torch)
         return
     t0 = time.perf_counter()
     W = I.make_weights(cfg, args.seed)

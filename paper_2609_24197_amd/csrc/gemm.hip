@@ -797,7 +797,7 @@ hipError_t launch_dense(const GemmArgs& g, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------------------
-// Large products (M >= 512, the block positions of many requests).  Eight waves in a 2 x 4
+// Large products (M >= 256, the block positions of many requests).  Eight waves in a 2 x 4
 // grid; a wave owns TM x TN blocks of 32 x 32 (v_mfma_f32_32x32x16_bf16) and reads 0.75 KB of
 // LDS fragments per MFMA: 128 x 64 per wave (256 x 256 tiles) for a bf16 A, 64 x 64 per wave
 // with the A lo plane (128 x 256 tiles, two products per block).  With 64 x 64 per wave and one
@@ -810,6 +810,9 @@ hipError_t launch_dense(const GemmArgs& g, hipStream_t s) {
 // kernel sums in k-part order, so the result does not depend on scheduling.
 #ifndef HSPEC_BIG_ST
 #define HSPEC_BIG_ST 4
+#endif
+#ifndef HSPEC_BIG_MIN_M
+#define HSPEC_BIG_MIN_M 256   // rows from which products take the large tiles
 #endif
 constexpr int GB_KT = 32, GB_NT = 512, GB_ST = HSPEC_BIG_ST;
 
@@ -1095,7 +1098,7 @@ __global__ void __launch_bounds__(256) gemm_big_fixup(GemmArgs g, BigPlan p) {
 // tiles for every full round, the tiles of a short last round split over K so that the round
 // fills the chip (at least 4 k-tiles per part).
 bool big_ok(const GemmArgs& g) {
-  if (g.M < 512 || g.W_lo || g.w_packed || g.K % GB_KT) return false;
+  if (g.M < HSPEC_BIG_MIN_M || g.W_lo || g.w_packed || g.K % GB_KT) return false;
   const int bm = g.A_lo ? BigCfg<true>::BM : BigCfg<false>::BM, bn = g.A_lo ? BigCfg<true>::BN : BigCfg<false>::BN;
   // 32-bit element offsets inside a tile's rows of A and W
   if ((long long)bm * g.lda >= (1ll << 31) || (long long)bn * g.ldw >= (1ll << 31)) return false;
@@ -1198,7 +1201,7 @@ size_t gemm_scratch_elems(int M, int N, int K, bool a_lo, bool w_lo) {
   if (M <= 0 || N <= 0 || K <= 0) return 0;
   const SkPlan p = skinny_plan(M, N, K, w_lo, device_cus());
   size_t n = p.use && p.ksplit > 1 ? (size_t)p.ksplit * M * N : 0;
-  if (M >= 512 && !w_lo && K % GB_KT == 0) {
+  if (M >= HSPEC_BIG_MIN_M && !w_lo && K % GB_KT == 0) {
     n = std::max(n, big_scratch_elems(big_plan(M, N, K, false, device_cus())));
     n = std::max(n, big_scratch_elems(big_plan(M, N, K, true, device_cus())));
   }

@@ -31,7 +31,9 @@ def _small_attn_cfg(**kw):
                                    (65, 4096, 1024), (128, 16768, 512), (96, 300, 512), (127, 1000, 2048),
                                    # 256 x 256 tiles: whole tiles, k-split last tiles, ragged M and N
                                    (512, 768, 256), (1024, 2304, 1024), (777, 1000, 512), (1536, 4096, 512),
-                                   (600, 300, 4096)])
+                                   (600, 300, 4096),
+                                   # 256..511 rows: one or two row tiles, most columns k-split
+                                   (256, 16768, 512), (384, 4096, 1024), (257, 1000, 2048)])
 def test_linear(dtype, M, N, K):
     print(f"[linear] dtype={dtype} M={M} N={N} K={K}", flush=True)
     A = I.normal("lin_A", (M, K), 1.0, 0, dtype)
