@@ -36,9 +36,12 @@ sequential one against an independent derivation.
 Pins: every primitive here (state projection layout, conv, pointwise functions,
 RoPE, slot map, naive attention, the recurrence) is checked against textbook
 special cases, closed forms and library routines.  The composed functions
-``mamba_mixer``, ``attention_layer`` and ``draft_step`` are pinned only through
-their parts and whole-function properties (zero input, causality, decay rate,
-residual structure, dense-cache attention); beyond those they are parity unpinned.
+``mamba_mixer``, ``attention_layer``, ``draft_step`` and ``drafter_forward`` are pinned
+only through their parts and whole-function properties (zero input, causality, decay
+rate, residual structure, dense-cache attention, the shared initial state, the
+layer-to-cache mapping); beyond those they are parity unpinned.  ``draft_head`` and
+``kv_inject`` are pinned by special cases (no Markov term, a bigram chain, Gumbel-max
+frequencies; slot placement and untouched slots).
 
 Inputs are storage arrays: bf16 as uint16 bit patterns, or float32/float64.
 They are widened to float64 here, block by block for the large state

@@ -136,6 +136,51 @@ def test_draft_head_validation():
     assert L.hspec_draft_head_workspace(C.byref(c)) > 64 * 16 * 32000 * 4
 
 
+def test_drafter_forward_validation():
+    L = _lib()
+    ws, n = _ws_big()
+    cfg = I.CONFIGS[3].replace(n_fuse=5, ff=12288)
+    mc, ac = hspec.mamba_cfg(cfg), hspec.attn_cfg(cfg, 512, 20000)
+    mw = hspec.MambaW(*([FAKE.value] * 10))
+    aw = hspec.AttnW(*([FAKE.value] * 6))
+    def layer(**kw):
+        d = dict(mamba=C.pointer(mw), norm1_w=FAKE.value, attn=C.pointer(aw), norm2_w=FAKE.value,
+                 k_cache=FAKE.value, v_cache=FAKE.value, norm3_w=FAKE.value, W_gate=FAKE.value, W_up=FAKE.value,
+                 W_down=FAKE.value)
+        d.update(kw)
+        return hspec.LayerW(**d)
+    def call(layers, ff=12288, nl=None, W_r=FAKE, mcfg=mc):
+        arr = (hspec.LayerW * len(layers))(*layers)
+        return L.hspec_drafter_forward(C.byref(mcfg), C.byref(ac), ff, len(layers) if nl is None else nl, W_r, FAKE,
+                                       arr, FAKE, FAKE, FAKE, FAKE, 8192, FAKE, ws, n, None)
+    assert call([layer()], nl=0) == 2
+    assert call([layer()], ff=100) == 4                      # ff % 8
+    assert call([layer()], ff=0) == 2
+    assert call([layer(W_down=None)]) == 1
+    assert call([layer(norm2_w=None)]) == 1                  # attention layer without its norm
+    assert call([layer()], W_r=None) == 1                    # a Mamba layer needs W_r / W_dS
+    bad = hspec.mamba_cfg(cfg.replace(P=32))
+    assert call([layer()], mcfg=bad) == 4
+    assert L.hspec_drafter_forward_workspace(C.byref(mc), C.byref(ac), 12288, 8192) > 0
+
+
+def test_kv_inject_validation():
+    L = _lib()
+    ws, n = _ws_big()
+    cfg = I.CONFIGS[3].replace(n_fuse=5)
+    ac = hspec.attn_cfg(cfg, 512, 20000)
+    arr = (C.c_void_p * 5)(*([FAKE.value] * 5))
+    nul = (C.c_void_p * 5)(*([FAKE.value] * 4 + [None]))
+    def call(d_h=cfg.d_h, nl=5, w_k=arr, h=FAKE):
+        return L.hspec_kv_inject(C.byref(ac), d_h, nl, h, FAKE, w_k, arr, arr, arr, arr, FAKE, FAKE, ws, n, None)
+    assert call(d_h=0) == 2
+    assert call(nl=0) == 2
+    assert call(d_h=100) == 4
+    assert call(h=None) == 1
+    assert call(w_k=nul) == 1                                # layer 4's W_k is NULL
+    assert L.hspec_kv_inject_workspace(C.byref(ac), cfg.d_h) > 0
+
+
 def test_paged_attn_phase_validation():
     L = _lib()
     ws, n = _ws_big()
