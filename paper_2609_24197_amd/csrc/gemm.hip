@@ -816,9 +816,10 @@ hipError_t launch_dense(const GemmArgs& g, hipStream_t s) {
 #endif
 constexpr int GB_KT = 32, GB_NT = 512, GB_ST = HSPEC_BIG_ST;
 
-template <bool ALO>
+// TMV: 32-row MFMA tiles per wave (block tiles of 64 TMV rows); hi/lo A takes 2 to fit registers.
+template <bool ALO, int TMV = (ALO ? 2 : 4)>
 struct BigCfg {
-  static constexpr int TM = ALO ? 2 : 4, TN = 2;
+  static constexpr int TM = TMV, TN = 2;
   static constexpr int BM = 2 * TM * 32, BN = 4 * TN * 32;
   static constexpr int CPRT = GB_KT / 8;                           // 16-byte units per tile row
   static constexpr int SA = BM * GB_KT, SW = BN * GB_KT;           // elements per plane per stage
@@ -837,9 +838,9 @@ struct BigPlan {
   int units = 0;
 };
 
-template <bool ALO>
+template <bool ALO, int TMV>
 __global__ void __launch_bounds__(GB_NT) gemm_big_kernel(GemmArgs g, BigPlan p) {
-  using C = BigCfg<ALO>;
+  using C = BigCfg<ALO, TMV>;
   constexpr int TM = C::TM, TN = C::TN, BM = C::BM, BN = C::BN;
   constexpr int PA = C::SA * (ALO ? 2 : 1);
   __shared__ __align__(16) bf16 A0s[PA], W0s[C::SW];
@@ -1105,10 +1106,18 @@ bool big_ok(const GemmArgs& g) {
   if (g.W2 && (g.N1 % bn || g.N2 % bn)) return false;
   return true;
 }
+// Row-tile height: 128 for hi/lo A; for one A plane 256, or 128 when 256-row tiles would not
+// fill one round of CUs (then more whole tiles, fewer k-split ones).
+int big_tm(int M, int N, bool a_lo, int cus) {
+  if (a_lo) return 2;
+  const int tiles256 = ((M + 255) / 256) * ((N + BigCfg<false>::BN - 1) / BigCfg<false>::BN);
+  return tiles256 < cus ? 2 : 4;
+}
+
 BigPlan big_plan(int M, int N, int K, bool a_lo, int cus) {
   BigPlan p;
-  p.bm = a_lo ? BigCfg<true>::BM : BigCfg<false>::BM;
-  p.bn = a_lo ? BigCfg<true>::BN : BigCfg<false>::BN;
+  p.bm = 64 * big_tm(M, N, a_lo, cus);
+  p.bn = BigCfg<false>::BN;
   p.mt = (M + p.bm - 1) / p.bm;
   p.nt = (N + p.bn - 1) / p.bn;
   const int tiles = p.mt * p.nt, nk = K / GB_KT;
@@ -1138,8 +1147,9 @@ hipError_t launch_big(const GemmArgs& g, hipStream_t s) {
     p.kper = g.K / GB_KT;
     p.units = p.full;
   }
-  if (g.A_lo) hipLaunchKernelGGL(gemm_big_kernel<true>, dim3(p.units), dim3(GB_NT), 0, s, g, p);
-  else hipLaunchKernelGGL(gemm_big_kernel<false>, dim3(p.units), dim3(GB_NT), 0, s, g, p);
+  if (g.A_lo) hipLaunchKernelGGL((gemm_big_kernel<true, 2>), dim3(p.units), dim3(GB_NT), 0, s, g, p);
+  else if (p.bm == 128) hipLaunchKernelGGL((gemm_big_kernel<false, 2>), dim3(p.units), dim3(GB_NT), 0, s, g, p);
+  else hipLaunchKernelGGL((gemm_big_kernel<false, 4>), dim3(p.units), dim3(GB_NT), 0, s, g, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.full == p.mt * p.nt) return e;
   const size_t quads = big_scratch_elems(p) / p.splits / 4;
