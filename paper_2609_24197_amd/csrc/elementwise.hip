@@ -56,14 +56,43 @@ __device__ __forceinline__ void put8(bf16* hi, bf16* lo, size_t i, const float (
   if (lo) *reinterpret_cast<bf16x8*>(lo + i) = l;
 }
 
-// One workgroup per row, 8 elements per thread and step (n % 8 == 0); the second pass re-reads
-// the row from cache.
-template <typename T>
+// One workgroup per row, 8 elements per thread and step (n % 8 == 0).  NR > 0: the row fits in
+// NR chunks of 8 per thread (n <= 2048 NR); every chunk is loaded before the sum of squares and
+// kept in registers for the scaling pass (chunks past the row end load the row's first chunk and
+// count as zero).  NR == 0: any n, the second pass re-reads the row from cache.
+template <typename T, int NR>
 __global__ void __launch_bounds__(256) rmsnorm_kernel(const T* x, const float* w, int n, float eps,
                                                       bf16* hi, bf16* lo) {
   __shared__ float red[4];
   const size_t row = blockIdx.x;
   const T* xr = x + row * n;
+  if constexpr (NR > 0) {
+    float v[NR][8];
+    float ss = 0.f;
+#pragma unroll
+    for (int c = 0; c < NR; ++c) {
+      const int i = (threadIdx.x + c * 256) * 8;
+      load8(xr + (i < n ? i : 0), v[c]);
+    }
+#pragma unroll
+    for (int c = 0; c < NR; ++c)
+      if ((threadIdx.x + c * 256) * 8 < n)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) ss += v[c][e] * v[c][e];
+    ss = block_sum(ss, red);
+    const float r = rsqrtf(ss / n + eps);
+#pragma unroll
+    for (int c = 0; c < NR; ++c) {
+      const int i = (threadIdx.x + c * 256) * 8;
+      if (i >= n) break;
+      float g[8];
+      load8(w + i, g);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[c][e] = v[c][e] * r * g[e];
+      put8(hi, lo, row * n + i, v[c]);
+    }
+    return;
+  }
   float ss = 0.f;
   for (int i = threadIdx.x * 8; i < n; i += blockDim.x * 8) {
     float v[8];
@@ -106,6 +135,92 @@ __global__ void __launch_bounds__(256) conv_split_kernel(ConvArgs a) {
       const int hh = c - cdim;
       a.dt[(size_t)tok * a.H + hh] = softplus(a.zxbcdt[(size_t)tok * dproj + 2 * di + 2 * gn + hh] + a.dt_bias[hh]);
     }
+  }
+}
+
+// Causal conv with the paper's width of 4 taps: a thread owns 4 consecutive channels of
+// CONV_TT consecutive tokens of one request and reads the CONV_TT + 3 inputs they need (tokens
+// before the block's first are zero) straight from zx, all loads in flight together.  Weights of
+// the 4 channels are 16 consecutive values, read as vectors.  Same alignment needs as the serial
+// kernel below.
+constexpr int CONV_TT = 4;
+
+template <typename T>
+__global__ void __launch_bounds__(256) conv4_tok_kernel(ConvArgs a) {
+  const int di = a.H * a.P, gn = a.G * a.N, cdim = di + 2 * gn;
+  const int dproj = 2 * di + 2 * gn + a.H;
+  const int nq = (a.T + CONV_TT - 1) / CONV_TT;
+  const int b = blockIdx.y / nq, t0 = (blockIdx.y % nq) * CONV_TT;
+  const int c = (blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (c >= cdim + a.H) return;
+  const float* zb = a.zxbcdt + (size_t)b * a.T * dproj;
+  if (c >= cdim) {                                   // dt = softplus(dt_raw + dt_bias), 4 heads
+    const int hh = c - cdim;
+    f32x4 v[CONV_TT];
+#pragma unroll
+    for (int u = 0; u < CONV_TT; ++u)
+      v[u] = t0 + u < a.T ? *reinterpret_cast<const f32x4*>(zb + (size_t)(t0 + u) * dproj + 2 * di + 2 * gn + hh)
+                          : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int u = 0; u < CONV_TT; ++u) {
+      if (t0 + u >= a.T) break;
+      f32x4 o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = softplus(v[u][e] + a.dt_bias[hh + e]);
+      *reinterpret_cast<f32x4*>(a.dt + ((size_t)b * a.T + t0 + u) * a.H + hh) = o;
+    }
+    return;
+  }
+  // in[j] is token t0 - 3 + j
+  f32x4 in[CONV_TT + 3];
+#pragma unroll
+  for (int j = 0; j < CONV_TT + 3; ++j) {
+    const int tau = t0 - 3 + j;
+    in[j] = tau >= 0 && tau < a.T ? *reinterpret_cast<const f32x4*>(zb + (size_t)tau * dproj + di + c)
+                                  : f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  float w[16], bias[4];
+  if constexpr (sizeof(T) == 2) {
+    const bf16x8 w0 = ld8(reinterpret_cast<const bf16*>(a.conv_w) + (size_t)c * 4);
+    const bf16x8 w1 = ld8(reinterpret_cast<const bf16*>(a.conv_w) + (size_t)c * 4 + 8);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      w[e] = bf2f(w0[e]);
+      w[8 + e] = bf2f(w1[e]);
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(reinterpret_cast<const float*>(a.conv_w) + (size_t)c * 4 + 4 * q);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) w[4 * q + e] = v[e];
+    }
+  }
+  const T* cb = reinterpret_cast<const T*>(a.conv_b);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) bias[e] = to_f32(cb[c + e]);
+  bf16* ohi;
+  bf16* olo;
+  int ld, col;
+  if (c < di) { ohi = a.x_hi; olo = a.x_lo; ld = di; col = c; }
+  else if (c < di + gn) { ohi = a.B_hi; olo = a.B_lo; ld = gn; col = c - di; }
+  else { ohi = a.C_hi; olo = a.C_lo; ld = gn; col = c - di - gn; }
+#pragma unroll
+  for (int u = 0; u < CONV_TT; ++u) {
+    if (t0 + u >= a.T) break;
+    bf16x4 h, l;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float v = bias[e];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v += w[4 * e + j] * in[u + j][e];
+      v = silu(v);
+      h[e] = f2bf(v);
+      l[e] = f2bf(v - bf2f(h[e]));
+    }
+    const size_t o = ((size_t)b * a.T + t0 + u) * ld + col;
+    *reinterpret_cast<bf16x4*>(ohi + o) = h;
+    if (olo) *reinterpret_cast<bf16x4*>(olo + o) = l;
   }
 }
 
@@ -171,8 +286,10 @@ __global__ void __launch_bounds__(256) conv_split4_kernel(ConvArgs a) {
 }
 
 // One workgroup per (row, group); 8 elements per thread and step.  VEC: y and z rows can be
-// read as 16-byte vectors.
-template <bool VEC>
+// read as 16-byte vectors.  NR > 0 (with VEC): the group fits in NR chunks of 8 per thread and is
+// gated once, kept in registers between the sum of squares and the scaling pass (chunks past the
+// group's end load its first chunk and count as zero); NR == 0: the second pass re-reads y and z.
+template <bool VEC, int NR>
 __global__ void __launch_bounds__(256) gated_rmsnorm_kernel(const float* y, const float* z, int z_ld,
                                                             const float* w, int n, int G, float eps,
                                                             bf16* hi, bf16* lo) {
@@ -196,6 +313,38 @@ __global__ void __launch_bounds__(256) gated_rmsnorm_kernel(const float* y, cons
 #pragma unroll
     for (int e = 0; e < 8; ++e) v[e] *= silu(zz[e]);
   };
+  if constexpr (NR > 0) {
+    float v[NR][8], zz[NR][8];
+#pragma unroll
+    for (int c = 0; c < NR; ++c) {
+      const int i = (threadIdx.x + c * 256) * 8, ic = i < gs ? i : 0;
+      load8(yr + ic, v[c]);
+      load8(zr + ic, zz[c]);
+    }
+    float ss = 0.f;
+#pragma unroll
+    for (int c = 0; c < NR; ++c) {
+      const bool in = (threadIdx.x + c * 256) * 8 < gs;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        v[c][e] *= silu(zz[c][e]);
+        ss += in ? v[c][e] * v[c][e] : 0.f;
+      }
+    }
+    ss = block_sum(ss, red);
+    const float r = rsqrtf(ss / gs + eps);
+#pragma unroll
+    for (int c = 0; c < NR; ++c) {
+      const int i = (threadIdx.x + c * 256) * 8;
+      if (i >= gs) break;
+      float g[8];
+      load8(w + (size_t)gi * gs + i, g);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[c][e] = v[c][e] * r * g[e];
+      put8(hi, lo, row * n + (size_t)gi * gs + i, v[c]);
+    }
+    return;
+  }
   float ss = 0.f;
   for (int i = threadIdx.x * 8; i < gs; i += blockDim.x * 8) {
     float v[8];
@@ -215,53 +364,112 @@ __global__ void __launch_bounds__(256) gated_rmsnorm_kernel(const float* y, cons
   }
 }
 
-// One workgroup (4 waves) per token.  A head's D/2 rotate-half pairs (i, i + D/2) sit on D/2
-// consecutive lanes, so a wave holds 64 / (D/2) heads at a time; the rotation angle of pair i
-// is the same for every head of the token and is computed once per thread (in fp64, reduced
-// modulo 2 pi, then fp32 sin/cos).
-__global__ void __launch_bounds__(256) qk_norm_rope_kernel(const float* qkv, const float* qw, const float* kw,
-                                                           const int32_t* ctx_lens, int T, int Hq, int Hkv,
-                                                           int D, float eps, double theta, bf16* q_hi,
-                                                           bf16* q_lo, bf16* k_hi, bf16* k_lo, bf16* v_hi,
-                                                           bf16* v_lo) {
+// Per-head RMSNorm of q and k, then rotate-half RoPE at position ctx_len + j; v heads are copied.
+// One workgroup (4 waves) per token, for D a multiple of 8 with D/8 dividing 64 (D = 8 .. 512):
+// a lane owns elements i0..i0+3 and i0 + D/2 .. i0 + D/2 + 3 of a head (16-byte loads, 8-byte
+// plane stores), D/8 lanes per head.  The D/2 rotation angles of the token are computed once
+// (in fp64, reduced modulo 2 pi, then fp32 sin/cos) by the first D/2 threads into LDS while the
+// first heads load.
+constexpr int QKR4_U = 4;
+
+__global__ void __launch_bounds__(256) qk_norm_rope4_kernel(const float* qkv, const float* qw, const float* kw,
+                                                            const int32_t* ctx_lens, int T, int Hq, int Hkv,
+                                                            int D, float eps, double theta, bf16* q_hi,
+                                                            bf16* q_lo, bf16* k_hi, bf16* k_lo, bf16* v_hi,
+                                                            bf16* v_lo) {
+  __shared__ float s_cs[256], s_sn[256];
   const int nh = Hq + 2 * Hkv;
   const int tok = blockIdx.x;
   const int b = tok / T, j = tok % T;
-  const int half = D / 2, hpw = 64 / half;
+  const int half = D / 2, lph = D / 8, hpw = 64 / lph;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int i = lane % half, hsub = lane / half;
-  const double pos = (double)ctx_lens[b] + j;
-  double phi = pos * pow(theta, -2.0 * (double)i / (double)D);
-  const double two_pi = 6.283185307179586476925286766559;
-  phi -= two_pi * rint(phi / two_pi);
-  float sn, cs;
-  sincosf((float)phi, &sn, &cs);
+  const int i0 = 4 * (lane % lph), hsub = lane / lph;
+  const int hstep = 4 * hpw;                 // heads per workgroup pass
   const float* src_tok = qkv + (size_t)tok * nh * D;
-  for (int h0 = wave * hpw; h0 < nh; h0 += 4 * hpw) {
-    const int head = h0 + hsub;
-    const bool act = head < nh;
-    const float* src = src_tok + (size_t)(act ? head : 0) * D;
-    const float x1 = act ? src[i] : 0.f, x2 = act ? src[i + half] : 0.f;
-    // sum of squares over the head's D/2 lanes (every lane takes part in the exchange)
-    float ss = x1 * x1 + x2 * x2;
-    for (int off = half / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
-    if (!act) continue;
-    if (head >= Hq + Hkv) {                    // v heads: copy
-      const size_t o = ((size_t)tok * Hkv + (head - Hq - Hkv)) * D;
-      put_planes(v_hi, v_lo, o + i, x1);
-      put_planes(v_hi, v_lo, o + i + half, x2);
-      continue;
+  f32x4 x1[QKR4_U], x2[QKR4_U];
+  auto load_heads = [&](int h0) {
+#pragma unroll
+    for (int u = 0; u < QKR4_U; ++u) {
+      const int head = h0 + u * hstep + wave * hpw + hsub;
+      const float* src = src_tok + (size_t)(head < nh ? head : 0) * D + i0;
+      x1[u] = *reinterpret_cast<const f32x4*>(src);
+      x2[u] = *reinterpret_cast<const f32x4*>(src + half);
     }
-    const bool isq = head < Hq;
-    const float* g = isq ? qw : kw;
-    const float r = rsqrtf(ss / D + eps);
-    const float a1 = x1 * r * g[i], a2 = x2 * r * g[i + half];
-    const float o1 = a1 * cs - a2 * sn, o2 = a2 * cs + a1 * sn;
-    bf16* hi = isq ? q_hi : k_hi;
-    bf16* lo = isq ? q_lo : k_lo;
-    const size_t o = isq ? ((size_t)tok * Hq + head) * D : ((size_t)tok * Hkv + (head - Hq)) * D;
-    put_planes(hi, lo, o + i, o1);
-    put_planes(hi, lo, o + i + half, o2);
+  };
+  load_heads(0);
+  for (int p = threadIdx.x; p < half; p += blockDim.x) {
+    double phi = ((double)ctx_lens[b] + j) * pow(theta, -2.0 * (double)p / (double)D);
+    const double two_pi = 6.283185307179586476925286766559;
+    phi -= two_pi * rint(phi / two_pi);
+    float sn, cs;
+    sincosf((float)phi, &sn, &cs);
+    s_cs[p] = cs;
+    s_sn[p] = sn;
+  }
+  f32x4 gq1 = {0.f, 0.f, 0.f, 0.f}, gq2 = gq1;
+  if (Hq > 0) {
+    gq1 = *reinterpret_cast<const f32x4*>(qw + i0);
+    gq2 = *reinterpret_cast<const f32x4*>(qw + half + i0);
+  }
+  const f32x4 gk1 = *reinterpret_cast<const f32x4*>(kw + i0), gk2 = *reinterpret_cast<const f32x4*>(kw + half + i0);
+  __syncthreads();
+  float cs[4], sn[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    cs[e] = s_cs[i0 + e];
+    sn[e] = s_sn[i0 + e];
+  }
+  for (int h0 = 0; h0 < nh; h0 += QKR4_U * hstep) {
+    if (h0) load_heads(h0);
+#pragma unroll
+    for (int u = 0; u < QKR4_U; ++u) {
+      const int head = h0 + u * hstep + wave * hpw + hsub;
+      // sum of squares over the head's D/8 lanes (every lane takes part in the exchange)
+      float ss = 0.f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) ss += x1[u][e] * x1[u][e] + x2[u][e] * x2[u][e];
+      for (int off = lph / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+      if (head >= nh) continue;
+      float o1[4], o2[4];
+      bf16 *hi, *lo;
+      size_t o;
+      if (head >= Hq + Hkv) {                  // v heads: copy
+        o = ((size_t)tok * Hkv + (head - Hq - Hkv)) * D;
+        hi = v_hi;
+        lo = v_lo;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          o1[e] = x1[u][e];
+          o2[e] = x2[u][e];
+        }
+      } else {
+        const bool isq = head < Hq;
+        const float r = rsqrtf(ss / D + eps);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float a1 = x1[u][e] * r * (isq ? gq1[e] : gk1[e]), a2 = x2[u][e] * r * (isq ? gq2[e] : gk2[e]);
+          o1[e] = a1 * cs[e] - a2 * sn[e];
+          o2[e] = a2 * cs[e] + a1 * sn[e];
+        }
+        hi = isq ? q_hi : k_hi;
+        lo = isq ? q_lo : k_lo;
+        o = isq ? ((size_t)tok * Hq + head) * D : ((size_t)tok * Hkv + (head - Hq)) * D;
+      }
+      bf16x4 h1, l1, h2, l2;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        h1[e] = f2bf(o1[e]);
+        l1[e] = f2bf(o1[e] - bf2f(h1[e]));
+        h2[e] = f2bf(o2[e]);
+        l2[e] = f2bf(o2[e] - bf2f(h2[e]));
+      }
+      *reinterpret_cast<bf16x4*>(hi + o + i0) = h1;
+      *reinterpret_cast<bf16x4*>(hi + o + half + i0) = h2;
+      if (lo) {
+        *reinterpret_cast<bf16x4*>(lo + o + i0) = l1;
+        *reinterpret_cast<bf16x4*>(lo + o + half + i0) = l2;
+      }
+    }
   }
 }
 
@@ -327,10 +535,23 @@ __global__ void zero_kernel(int* p, int n) {
 hipError_t launch_rmsnorm_planes(const void* x, int x_bf16, const float* w, int rows, int n, float eps,
                                  bf16* out_hi, bf16* out_lo, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  if (x_bf16)
-    hipLaunchKernelGGL(rmsnorm_kernel<bf16>, dim3(rows), dim3(256), 0, s, (const bf16*)x, w, n, eps, out_hi, out_lo);
-  else
-    hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(rows), dim3(256), 0, s, (const float*)x, w, n, eps, out_hi, out_lo);
+  // chunks of 8 per thread when the row is held in registers (0: two passes over the row)
+  const int nr = n <= 2048 ? 1 : n <= 4096 ? 2 : n <= 8192 ? 4 : 0;
+  auto launch = [&](auto xt, auto nrc) {
+    using T = decltype(xt);
+    hipLaunchKernelGGL((rmsnorm_kernel<T, decltype(nrc)::value>), dim3(rows), dim3(256), 0, s,
+                       (const T*)x, w, n, eps, out_hi, out_lo);
+  };
+  auto by_type = [&](auto nrc) {
+    if (x_bf16) launch(bf16{}, nrc);
+    else launch(0.f, nrc);
+  };
+  switch (nr) {
+    case 1: by_type(Int<1>{}); break;
+    case 2: by_type(Int<2>{}); break;
+    case 4: by_type(Int<4>{}); break;
+    default: by_type(Int<0>{}); break;
+  }
   return hipGetLastError();
 }
 
@@ -338,6 +559,12 @@ hipError_t launch_conv_split(const ConvArgs& a, hipStream_t s) {
   const int di = a.H * a.P, gn = a.G * a.N;
   const int dproj = 2 * di + 2 * gn + a.H;
   const int total = di + 2 * gn + a.H;
+  if (dproj % 4 == 0 && di % 4 == 0 && gn % 4 == 0 && a.H % 4 == 0 && a.K == 4) {
+    dim3 grid((total / 4 + 255) / 256, a.B * ((a.T + CONV_TT - 1) / CONV_TT));
+    if (a.w_bf16) hipLaunchKernelGGL(conv4_tok_kernel<bf16>, grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(conv4_tok_kernel<float>, grid, dim3(256), 0, s, a);
+    return hipGetLastError();
+  }
   if (dproj % 4 == 0 && di % 4 == 0 && gn % 4 == 0 && a.H % 4 == 0 && a.K <= 8) {
     dim3 grid((total / 4 + 255) / 256, a.B);
     if (a.w_bf16) hipLaunchKernelGGL(conv_split4_kernel<bf16>, grid, dim3(256), 0, s, a);
@@ -353,10 +580,15 @@ hipError_t launch_conv_split(const ConvArgs& a, hipStream_t s) {
 hipError_t launch_gated_rmsnorm(const float* y, const float* z, int z_ld, const float* w, int rows, int n, int G,
                                 float eps, bf16* out_hi, bf16* out_lo, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  if (z_ld % 4 == 0 && (n / G) % 4 == 0)
-    hipLaunchKernelGGL(gated_rmsnorm_kernel<true>, dim3(rows * G), dim3(256), 0, s, y, z, z_ld, w, n, G, eps, out_hi, out_lo);
+  const int gs = n / G;
+  if (z_ld % 4 == 0 && gs % 4 == 0 && gs % 8 == 0 && gs <= 4096)
+    hipLaunchKernelGGL((gated_rmsnorm_kernel<true, 2>), dim3(rows * G), dim3(256), 0, s, y, z, z_ld, w, n, G, eps, out_hi, out_lo);
+  else if (z_ld % 4 == 0 && gs % 4 == 0 && gs % 8 == 0 && gs <= 8192)
+    hipLaunchKernelGGL((gated_rmsnorm_kernel<true, 4>), dim3(rows * G), dim3(256), 0, s, y, z, z_ld, w, n, G, eps, out_hi, out_lo);
+  else if (z_ld % 4 == 0 && gs % 4 == 0)
+    hipLaunchKernelGGL((gated_rmsnorm_kernel<true, 0>), dim3(rows * G), dim3(256), 0, s, y, z, z_ld, w, n, G, eps, out_hi, out_lo);
   else
-    hipLaunchKernelGGL(gated_rmsnorm_kernel<false>, dim3(rows * G), dim3(256), 0, s, y, z, z_ld, w, n, G, eps, out_hi, out_lo);
+    hipLaunchKernelGGL((gated_rmsnorm_kernel<false, 0>), dim3(rows * G), dim3(256), 0, s, y, z, z_ld, w, n, G, eps, out_hi, out_lo);
   return hipGetLastError();
 }
 
@@ -364,7 +596,8 @@ hipError_t launch_qk_norm_rope(const float* qkv, const float* qw, const float* k
                                int T, int Hq, int Hkv, int D, float eps, double theta, bf16* q_hi, bf16* q_lo,
                                bf16* k_hi, bf16* k_lo, bf16* v_hi, bf16* v_lo, hipStream_t s) {
   if (B * T <= 0) return hipSuccess;
-  hipLaunchKernelGGL(qk_norm_rope_kernel, dim3(B * T), dim3(256), 0, s, qkv, qw, kw, ctx_lens, T,
+  if (D < 8 || D % 8 || D > 512 || 64 % (D / 8)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(qk_norm_rope4_kernel, dim3(B * T), dim3(256), 0, s, qkv, qw, kw, ctx_lens, T,
                      Hq, Hkv, D, eps, theta, q_hi, q_lo, k_hi, k_lo, v_hi, v_lo);
   return hipGetLastError();
 }

@@ -27,6 +27,15 @@ SMALL = {
     # hi/lo inputs; Q/K/V over weight segments of 4096 and 1024 rows; O projection)
     "m640_large_tiles": I.StepConfig(name="s", B=40, k=16, d_model=512, H=8, P=64, N=16, G=1, chunk=16, Hq=32,
                                      Hkv=8, D=128, lengths="uniform:0:300"),
+    # fp32 storage with the 4-tap conv (token-parallel conv kernel, fp32 weights), ragged k
+    "f32_conv4": I.StepConfig(name="s", B=2, k=5, d_model=256, H=4, P=64, N=16, G=1, chunk=4, Hq=8, Hkv=2,
+                              D=128, lengths="list:33,150", dtype="f32"),
+    # head dim 64 (8 lanes per head in the q/k norm and rotation)
+    "d64_k7": I.StepConfig(name="s", B=2, k=7, d_model=256, H=4, P=64, N=16, G=1, chunk=4, Hq=4, Hkv=2,
+                           D=64, lengths="list:10,90"),
+    # a 3-tap conv (the serial conv kernel)
+    "conv3_k5": I.StepConfig(name="s", B=2, k=5, d_model=256, H=4, P=64, N=32, G=2, chunk=5, Hq=8, Hkv=2,
+                             D=128, lengths="list:0,60", conv_w=3),
     # hi/lo attention I/O, block keys in fp32 in the reduction (as in the whole drafter)
     "precise_io": I.StepConfig(name="s", B=3, k=16, d_model=512, H=8, P=64, N=128, G=1, chunk=16, Hq=32, Hkv=8,
                                D=128, lengths="list:300,0,77", precise_io=True),
