@@ -7,8 +7,9 @@
 // and its token is the argmax over v of l' (greedy) or of l' / T + G (Gumbel-max sampling with
 // the caller's noise G).  The chain is sequential in j, so each position is one launch:
 //   * a workgroup owns 128 vocabulary columns and all requests (in tiles of 64);
-//   * the rank-R product is one MFMA tile per (16 requests, 16 columns), its operands read
-//     straight from L2 (E rows gathered by token, U rows of the workgroup's columns);
+//   * the rank-R product is one MFMA tile per (16 requests, 16 columns); the E rows of the
+//     previous tokens are gathered into LDS once per workgroup, the U rows of a wave's columns
+//     read from L2;
 //   * the argmax across workgroups is a 64-bit atomicMax on (orderable score << 32 | ~column),
 //     which picks the largest score and, among equal scores, the lowest column;
 //   * the next launch decodes the previous position's token from that key.
@@ -38,12 +39,15 @@ __device__ __forceinline__ unsigned long long shfl_xor_u64(unsigned long long v,
   return ((unsigned long long)hi << 32) | lo;
 }
 
-// RK: rank / 32 when known at compile time (every fragment load is issued before the first
-// MFMA), 0 for any rank that is a multiple of 32 (one round of loads per 32).
+// RK: rank / 32 when known at compile time (the request tile's E rows gathered once per
+// workgroup into LDS, every fragment load issued before the first MFMA), 0 for any rank that is
+// a multiple of 32 (E and U fragments read from L2, one round of loads per 32).
 template <int RK>
 __global__ void __launch_bounds__(256) markov_step_kernel(HeadArgs a, int j) {
+  constexpr int RR = RK * 32, LDE = RR + 8;   // E rows in LDS, padded by 16 bytes
   __shared__ int s_prev[MK_ROWS];
   __shared__ unsigned long long s_best[4][MK_ROWS];
+  __shared__ __align__(16) bf16 s_e[RK > 0 ? MK_ROWS * LDE : 8];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int vw = blockIdx.x * MK_COLS + wave * 32;   // first column of this wave
   const int l16 = lane & 15, g4 = lane >> 4;
@@ -86,9 +90,6 @@ __global__ void __launch_bounds__(256) markov_step_kernel(HeadArgs a, int j) {
     for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
       for (int cb = 0; cb < 2; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const bf16* erow[4];
-#pragma unroll
-    for (int rb = 0; rb < 4; ++rb) erow[rb] = a.E + (size_t)s_prev[rb * 16 + l16] * a.R + 8 * g4;
     const bf16* urow[2];
     bool ucol[2];
 #pragma unroll
@@ -97,6 +98,9 @@ __global__ void __launch_bounds__(256) markov_step_kernel(HeadArgs a, int j) {
       ucol[cb] = col < a.V;
       urow[cb] = a.U + (size_t)(ucol[cb] ? col : 0) * a.R + 8 * g4;
     }
+    const bf16* erow[4];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) erow[rb] = a.E + (size_t)s_prev[rb * 16 + l16] * a.R + 8 * g4;
     auto rank_steps = [&](int ks0, auto nsteps) {
       constexpr int NS = decltype(nsteps)::value;
       bf16x8 ef[NS][4], uf[NS][2];
@@ -115,7 +119,33 @@ __global__ void __launch_bounds__(256) markov_step_kernel(HeadArgs a, int j) {
           for (int cb = 0; cb < 2; ++cb) acc[rb][cb] = mma16(ef[s][rb], uf[s][cb], acc[rb][cb]);
     };
     if constexpr (RK > 0) {
-      rank_steps(0, Int<RK>{});
+      // the tile's E rows are gathered once per workgroup into LDS; the four waves read their
+      // fragments from there
+      constexpr int CPR = RR / 8;                    // 16-byte chunks per E row
+      static_assert((MK_ROWS * CPR) % 256 == 0, "E tile chunks must divide over the workgroup");
+      bf16x8 uf[RK][2];
+#pragma unroll
+      for (int s = 0; s < RK; ++s)
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb) uf[s][cb] = ucol[cb] ? ld8(urow[cb] + 32 * s) : zero8();
+#pragma unroll
+      for (int q = 0; q < MK_ROWS * CPR / 256; ++q) {
+        const int c = tid + 256 * q, row = c / CPR, col = (c % CPR) * 8;
+        *reinterpret_cast<bf16x8*>(s_e + row * LDE + col) = ld8(a.E + (size_t)s_prev[row] * RR + col);
+      }
+      __syncthreads();
+      bf16x8 ef[RK][4];
+#pragma unroll
+      for (int s = 0; s < RK; ++s)
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb)
+          ef[s][rb] = *reinterpret_cast<const bf16x8*>(s_e + (rb * 16 + l16) * LDE + 32 * s + 8 * g4);
+#pragma unroll
+      for (int s = 0; s < RK; ++s)
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+          for (int cb = 0; cb < 2; ++cb) acc[rb][cb] = mma16(ef[s][rb], uf[s][cb], acc[rb][cb]);
     } else {
       for (int ks = 0; ks < a.R; ks += 32) rank_steps(ks, Int<1>{});
     }
