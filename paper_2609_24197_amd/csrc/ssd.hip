@@ -291,19 +291,29 @@ __global__ void __launch_bounds__(64) ssd_scan_one(ScanArgs a) {
     Mm[t * (QMAX + 1) + l16] = ok ? cb[i] * __expf(ell_t[i] - ell_s) * dt_s : 0.f;
   }
   __syncthreads();
-  // ---- y = exp(l_t) (C S^T) + M x + D x
+  // ---- y = exp(l_t) (C S^T) + M x + D x.  The lane's four rows of M and, per p, the row of
+  // x^T are read into registers with independent LDS reads (every entry of both tiles is
+  // written above); terms with s > t are selected away, so the sum is the one over s <= t in
+  // order.
+  float mrow[4][QMAX];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int s2 = 0; s2 < QMAX; ++s2) mrow[i][s2] = Mm[(4 * g4 + i) * (QMAX + 1) + s2];
 #pragma unroll
   for (int pb = 0; pb < 4; ++pb) {
     const int p = 16 * pb + l16;
     const float* xr = xT + p * (QMAX + 1);
+    float xv[QMAX];
+#pragma unroll
+    for (int s2 = 0; s2 < QMAX; ++s2) xv[s2] = xr[s2];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int t = 4 * g4 + i;
-      if (t >= T) continue;
-      const float* mr = Mm + t * (QMAX + 1);
       float acc = __expf(ell_t[i]) * ys[pb][i] + Dh * xr[t];
-      for (int s2 = 0; s2 <= t; ++s2) acc += mr[s2] * xr[s2];
-      a.y[(size_t)(b * T + t) * H * P + (size_t)h * P + p] = acc;
+#pragma unroll
+      for (int s2 = 0; s2 < QMAX; ++s2) acc += s2 <= t ? mrow[i][s2] * xv[s2] : 0.f;
+      if (t < T) a.y[(size_t)(b * T + t) * H * P + (size_t)h * P + p] = acc;
     }
   }
 }
