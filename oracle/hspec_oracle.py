@@ -39,7 +39,9 @@ special cases, closed forms and library routines.  The composed functions
 ``mamba_mixer``, ``attention_layer``, ``draft_step`` and ``drafter_forward`` are pinned
 only through their parts and whole-function properties (zero input, causality, decay
 rate, residual structure, dense-cache attention, the shared initial state, the
-layer-to-cache mapping); beyond those they are parity unpinned.  ``draft_head`` and
+layer-to-cache mapping); the mixer's wiring (the order of the in_proj split, the SiLU after
+the conv, the gated-norm gain) is pinned by one-channel and one-hot-selector cases with
+closed forms; beyond those they are parity unpinned.  ``draft_head`` and
 ``kv_inject`` are pinned by special cases (no Markov term, a bigram chain, Gumbel-max
 frequencies; slot placement and untouched slots).
 

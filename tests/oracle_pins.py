@@ -320,6 +320,100 @@ def pin_mixer_zero_and_causal(O):
     assert not np.allclose(a[:, 0], c[:, 0])
 
 
+def pin_mixer_scalar_wiring(O):
+    """Mixer wiring, one channel of everything (H = P = N = G = 1, d_model = 5).
+
+    W_in = I makes the in_proj outputs the coordinates of u, so the stated order
+    [z, x, B, C, dt_raw] puts u_0 in the gate, u_1 in x, u_2 in B, u_3 in C and u_4 in
+    dt_raw.  A one-tap conv of weight 1 and bias 0 is the identity, so after it x, B and C
+    are exactly SiLU of their coordinates.  With one channel the gated RMSNorm is
+    w g / sqrt(g^2 + eps), and W_out = e_0 writes it to output coordinate 0 only.  The
+    output then follows the scalar recurrence s_t = a_t s_{t-1} + dt_t x_t B_t,
+    y_t = s_t C_t + D x_t, written out below position by position.  Each coordinate
+    enters through a different function (SiLU of a product, a softplus, the gate), so a
+    swapped split, a missing SiLU, or a dropped gain changes the value."""
+    import types
+    cfg = types.SimpleNamespace(H=1, P=1, N=1, G=1, eps=0.7)
+    r = rng0(30)
+    T = 3
+    u = r.standard_normal((2, T, 5)) * 1.5
+    s0 = r.standard_normal(2)
+    dtb, alog, Dk, wg = 0.4, -0.3, 0.8, -1.7
+    Wout = np.zeros((5, 1))
+    Wout[0, 0] = 1.0
+    W = dict(W_in=np.eye(5), conv_w=np.ones((3, 1)), conv_b=np.zeros(3), dt_bias=np.array([dtb]),
+             A_log=np.array([alog]), D=np.array([Dk]), gnorm_w=np.array([wg]), W_out=Wout)
+    out = O.mamba_mixer(u, s0.reshape(2, 1, 1, 1), W, cfg)
+    sg = lambda v: v / (1.0 + np.exp(-v))              # noqa: E731
+    A = -np.exp(alog)
+    for b in range(2):
+        s = s0[b]
+        for t in range(T):
+            z, x, Bv, Cv = sg(u[b, t, 0]), sg(u[b, t, 1]), sg(u[b, t, 2]), sg(u[b, t, 3])
+            dt = np.log1p(np.exp(u[b, t, 4] + dtb))
+            s = np.exp(dt * A) * s + dt * x * Bv
+            g = (s * Cv + Dk * x) * z
+            ref = wg * g / np.sqrt(g * g + cfg.eps)
+            assert np.isclose(out[b, t, 0], ref, rtol=1e-12, atol=1e-14), (b, t)
+            assert not np.any(out[b, t, 1:])
+
+
+def pin_mixer_split_selectors(O):
+    """Split order at H = 2, P = 2, N = 3, G = 1 through one-hot W_in rows.
+
+    Rows of W_in pick single coordinates of u, so each in_proj output block reads a known
+    coordinate: the stated order [z (4), x (4), B (3), C (3), dt (2)].  With u = 0 except at
+    one coordinate, only the blocks that read it are non-zero, and the mixer's parts
+    (z, x, Bm, Cm, dt) must show exactly that pattern; the conv bias is 0 so SiLU(0) = 0 keeps
+    the untouched blocks at zero (dt takes softplus(dt_bias) there)."""
+    import types
+    H, P, N = 2, 2, 3
+    cfg = types.SimpleNamespace(H=H, P=P, N=N, G=1, eps=1e-6)
+    di = H * P
+    rows = 2 * di + 2 * N + H                     # 16 in_proj outputs
+    d_model = rows
+    r = rng0(31)
+    W = dict(W_in=np.eye(rows), conv_w=np.tile(np.array([[0.0, 0.0, 0.0, 1.0]]), (di + 2 * N, 1)),
+             conv_b=np.zeros(di + 2 * N), dt_bias=r.standard_normal(H), A_log=r.standard_normal(H),
+             D=r.standard_normal(H), gnorm_w=1.0 + r.random(di), W_out=r.standard_normal((d_model, di)))
+    blocks = dict(z=(0, di), x=(di, 2 * di), Bm=(2 * di, 2 * di + N), Cm=(2 * di + N, 2 * di + 2 * N),
+                  dt=(2 * di + 2 * N, rows))
+    S0 = np.zeros((1, H, P, N))
+    for name, (c0, c1) in blocks.items():
+        for c in range(c0, c1):
+            u = np.zeros((1, 1, d_model))
+            u[0, 0, c] = 2.0
+            _, parts = O.mamba_mixer(u, S0, W, cfg, return_parts=True)
+            for other, (o0, o1) in blocks.items():
+                v = np.asarray(parts[other]).reshape(-1)
+                if other == "dt":
+                    v = v - np.log1p(np.exp(W["dt_bias"]))
+                if other == name:
+                    hot = np.zeros(o1 - o0)
+                    hot[c - c0] = 1.0
+                    if name == "z":           # the gate is returned before its SiLU
+                        want = 2.0
+                    elif name == "dt":        # softplus(2 + b) - softplus(b) at the hot head only
+                        want = np.log1p(np.exp(2.0 + W["dt_bias"][c - c0])) - np.log1p(np.exp(W["dt_bias"][c - c0]))
+                    else:                     # conv identity, then SiLU
+                        want = 2.0 / (1.0 + np.exp(-2.0))
+                    assert np.allclose(v, hot * want, rtol=1e-13, atol=1e-15), (name, c, other)
+                else:
+                    assert np.allclose(v, 0.0, atol=1e-15), (name, c, other)
+
+
+def pin_gated_norm_gain(O):
+    """Gated RMSNorm with a non-unit gain: at eps = 0 each group of RMSNorm(y SiLU(z)) / w has
+    unit mean square and is a positive multiple of y SiLU(z) (group-wise closed form)."""
+    r = rng0(32)
+    y, z = r.standard_normal((3, 12)), r.standard_normal((3, 12))
+    w = r.standard_normal(12) * 2.0
+    out = (O.gated_rmsnorm(y, z, w, 3, 0.0) / w).reshape(3, 3, 4)
+    assert np.allclose(np.mean(out ** 2, -1), 1.0, rtol=1e-13)
+    ratio = out / (y * z / (1 + np.exp(-z))).reshape(3, 3, 4)
+    assert np.all(ratio > 0) and np.allclose(ratio, ratio[..., :1], rtol=1e-12)
+
+
 def pin_draft_step_zero_input(O):
     """Step with e = 0, h_last = 0: x1 = 0 so q = k = v_blk = 0; out = W_o mean(V over cache and block)."""
     cfg = _tiny_cfg()

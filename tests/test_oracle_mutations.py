@@ -63,6 +63,15 @@ MUTATIONS = {
     "markov_factors_swapped": ("lj = logits[:, j, :] + E[prev] @ U.T", "lj = logits[:, j, :] + U[prev] @ E.T"),
     "gumbel_sign": ("lj / temperature + f64(gumbel)[:, j, :]", "lj / temperature - f64(gumbel)[:, j, :]"),
     "temperature_multiplies": ("lj / temperature + f64(gumbel)[:, j, :]", "lj * temperature + f64(gumbel)[:, j, :]"),
+    "conv_no_silu": ('xBC = silu(causal_conv1d(xBC, f64(W["conv_w"]), f64(W["conv_b"])))',
+                     'xBC = causal_conv1d(xBC, f64(W["conv_w"]), f64(W["conv_b"]))'),
+    "gnorm_no_gain": ("return gg.reshape(shp) * w", "return gg.reshape(shp)"),
+    "in_proj_z_x_swapped": ("z = zxbcdt[..., :di]\n    xBC = zxbcdt[..., di:2 * di + 2 * G * N]",
+                            "z = zxbcdt[..., di:2 * di]\n    xBC = np.concatenate([zxbcdt[..., :di], "
+                            "zxbcdt[..., 2 * di:2 * di + 2 * G * N]], axis=-1)"),
+    "xBC_B_C_swapped": ("Bm = xBC[..., di:di + G * N].reshape(Bsz, T, G, N)\n    Cm = xBC[..., di + G * N:].reshape(Bsz, T, G, N)",
+                        "Cm = xBC[..., di:di + G * N].reshape(Bsz, T, G, N)\n    Bm = xBC[..., di + G * N:].reshape(Bsz, T, G, N)"),
+    "dt_before_xBC": ("dt = zxbcdt[..., 2 * di + 2 * G * N:]", "dt = zxbcdt[..., di:di + H]"),
     "chunk_decay_sign": ("decay = np.exp(lt[:, :, :, None] - lt[:, :, None, :])", "decay = np.exp(lt[:, :, None, :] - lt[:, :, :, None])"),
 }
 
