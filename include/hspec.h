@@ -313,6 +313,14 @@ size_t hspec_ssd_scan_workspace(int B, int T, int H, int P, int N, int G, hspec_
 /*
  * Attention core (the KV sweep and its split reduction) on given post-norm, post-RoPE
  * q [B, k, Hq, D], k_blk, v_blk [B, k, Hkv, D] (storage dtype): o [B, k, Hq, D] fp32.
+ * Sec. 3.3.2 ("KV dimension", "Attention mask", "Positional alignment"): block query j of
+ * request b attends, with softmax scale 1/sqrt(D), to the target's cached keys of positions
+ * [lo_j, ctx_lens[b]) read in place through page_table (lo_j = 0, or ctx_len + j - window + 1
+ * under a sliding window, App. B.2), plus the block's own keys (all k of them, or s <= j under
+ * HSPEC_BLOCK_CAUSAL); query head hq reads KV head hq / (Hq / Hkv).  The caches and the page
+ * table are those of hspec_target_kv_block_attn.  All pointers are caller-owned device memory;
+ * host-checkable errors return before any launch; out-of-pool page ids and out-of-range
+ * lengths set bits of the workspace status word (hspec_read_status).
  */
 hspec_status hspec_paged_attn(const hspec_attn_cfg* cfg, const void* q, const void* k_blk, const void* v_blk,
                               const void* k_cache, const void* v_cache, const int32_t* page_table,
@@ -338,7 +346,12 @@ hspec_status hspec_paged_attn_phase(const hspec_attn_cfg* cfg, const void* q, co
 /*
  * Physical slot of every logical cache position: slots [B, max_ctx_len] int32, -1 at and past
  * ctx_lens[b] (and for out-of-pool page ids, which also set HSPEC_DEV_BAD_PAGE in *status).
- * status: device int32 or NULL.
+ * slot(b, i) = page_table[b, i / page_size] * page_size + i % page_size: the paged layout
+ * through which the target's cache is reused in place (Sec. 3.3.2, "Layer-wise KV mapping" and
+ * in-place reuse; Sec. 4.2 serves through vLLM's paged cache).  The KV sweep addresses the
+ * cache with the same device functions.  page_table [B, max_pages] and ctx_lens [B] are device
+ * int32; page_size must be a power of two >= 16 (else HSPEC_ERR_UNSUPPORTED); status: device
+ * int32 or NULL.  Caller-owned device memory; asynchronous on `stream`.
  */
 hspec_status hspec_gather_slots(int B, int max_pages, int page_size, int num_pages, const int32_t* page_table,
                                 const int32_t* ctx_lens, int max_ctx_len, int32_t* slots, int32_t* status,
@@ -346,7 +359,11 @@ hspec_status hspec_gather_slots(int B, int max_pages, int page_size, int num_pag
 
 /*
  * Plain projection C [M, N] fp32 = A [M, K] W [N, K]^T (+ R [M, N] fp32 if R != NULL), A and W
- * in the storage dtype (the GEMM used by every projection above).  K must be a multiple of 8.
+ * in the storage dtype (the GEMM used by every projection above: Proj_r and Proj_dS of the
+ * Sec. 3.3.1 fusion equation, and the bias-free linear maps of the Mamba and attention modules
+ * of Sec. 3.3.1-3.3.2).  Row-major, caller-owned device memory; K must be a multiple of 8
+ * (else HSPEC_ERR_UNSUPPORTED); the workspace comes from hspec_linear_workspace and must be
+ * 256-byte aligned (else HSPEC_ERR_WORKSPACE).
  */
 hspec_status hspec_linear(hspec_dtype dtype, int M, int N, int K, const void* A, const void* W,
                           const float* R, float* C, void* workspace, size_t ws_bytes, void* stream);

@@ -162,6 +162,9 @@ hspec_status check_attn_cfg(const hspec_attn_cfg* c, int max_ctx_len) {
   const int split = c->split_tokens > 0 ? c->split_tokens : hspec::attention_default_split(c->B, c->Hkv, swept);
   if (swept > 0 && (swept + split - 1) / split > 256)
     return fail(HSPEC_ERR_UNSUPPORTED, "swept context / split_tokens gives more than 256 splits");
+  if (split > 8192)   // the sweep holds one split's page ids in a fixed LDS array
+    return fail(HSPEC_ERR_UNSUPPORTED, "swept context of %d keys needs splits above 8192 keys (at most 256 x 8192)",
+                swept);
   return HSPEC_OK;
 }
 
@@ -729,6 +732,8 @@ HSPEC_API hspec_status hspec_gather_slots(int B, int max_pages, int page_size, i
   if (B <= 0 || max_pages <= 0 || page_size <= 0 || num_pages <= 0 || max_ctx_len < 0)
     return fail(HSPEC_ERR_SHAPE, "non-positive gather dimension");
   if (!page_table || !ctx_lens || (!slots && max_ctx_len > 0)) return fail(HSPEC_ERR_NULL, "a gather pointer is NULL");
+  if (page_size < 16 || (page_size & (page_size - 1)))
+    return fail(HSPEC_ERR_UNSUPPORTED, "page_size must be a power of two >= 16, got %d", page_size);
   HIP_TRY(hspec::launch_gather_slots(B, max_pages, page_size, num_pages, page_table, ctx_lens, max_ctx_len, slots,
                                      status, (hipStream_t)stream));
   return HSPEC_OK;

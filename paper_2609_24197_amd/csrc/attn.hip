@@ -45,9 +45,17 @@ typedef short s16x8 __attribute__((ext_vector_type(8)));
 #define LDS_AS __attribute__((address_space(3)))
 #define GLB_AS __attribute__((address_space(1)))
 
-constexpr int MAX_SPLIT = 8192;                 // keys per split (host-enforced)
+constexpr int MAX_SPLIT = 8192;                 // keys per split (host-enforced by the config check)
 constexpr int MIN_PAGE = 16;                    // smallest supported page size
 constexpr int MAX_PIDS = MAX_SPLIT / MIN_PAGE + 1;
+
+// Logical cache position i of a request lives in page page_table[b, i / ps], at offset i mod ps
+// within it: the target's paged cache is read in place (Sec. 3.3.2, in-place KV reuse).  The
+// sweep and the slot-map kernel both address the cache through these three functions, so the
+// bit-exact slot-map test covers the sweep's own index path.  ps is a power of two, 2^lps.
+__device__ __forceinline__ int page_of(int i, int lps) { return i >> lps; }
+__device__ __forceinline__ int page_first_slot(int pid, int lps) { return pid << lps; }
+__device__ __forceinline__ int slot_in_page(int first_slot, int i, int lps) { return first_slot + (i & ((1 << lps) - 1)); }
 
 // Tile shape of the sweep.  QB: 16-column query blocks per wave; NW waves per workgroup;
 // KT keys per tile; ST LDS stages (ST - 1 tiles in flight while one is multiplied).
@@ -188,9 +196,9 @@ attn_sweep(AttnArgs a) {
     b_hi[qb] = real ? (a.causal ? j + 1 : T) : INT_MIN;
   }
   // page ids of this split, validated once
-  const int pg0 = k0 >> lps;
+  const int pg0 = page_of(k0, lps);
   if (n_cache > 0) {
-    const int npg = ((k1 - 1) >> lps) - pg0 + 1;
+    const int npg = page_of(k1 - 1, lps) - pg0 + 1;
     const int32_t* ptab = a.page_table + (size_t)b * a.max_pages + pg0;
     for (int e = tid; e < npg; e += C::NT) {
       int pid = ptab[e];
@@ -198,7 +206,7 @@ attn_sweep(AttnArgs a) {
         set_status(a.status, ST_BAD_PAGE);
         pid = 0;
       }
-      pids[e] = pid * a.ps;        // first slot of the page
+      pids[e] = page_first_slot(pid, lps);
     }
   }
 
@@ -219,7 +227,7 @@ attn_sweep(AttnArgs a) {
       int key = base + row;
       if (cache) {
         key = key < k1 ? key : k0;
-        const int slot_id = pids[(key >> lps) - pg0] + (key & (a.ps - 1));
+        const int slot_id = slot_in_page(pids[page_of(key, lps) - pg0], key, lps);
         off = (size_t)slot_id * (a.Hkv * D) + (h * D + 8 * cl);
       } else {
         key = key < T ? key : 0;
@@ -737,6 +745,7 @@ __global__ void __launch_bounds__(RED_THREADS) attn_reduce(AttnArgs a) {
 __global__ void gather_slots_kernel(int B, int max_pages, int ps, int num_pages, const int32_t* pt,
                                     const int32_t* lens, int max_ctx_len, int32_t* slots, int* status) {
   const int b = blockIdx.y;
+  const int lps = 31 - __builtin_clz(ps);
   int L = lens[b];
   int cap = max_pages * ps < max_ctx_len ? max_pages * ps : max_ctx_len;
   if (L < 0 || L > cap) {
@@ -746,9 +755,9 @@ __global__ void gather_slots_kernel(int B, int max_pages, int ps, int num_pages,
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < max_ctx_len; i += gridDim.x * blockDim.x) {
     int v = -1;
     if (i < L) {
-      int pid = pt[(size_t)b * max_pages + i / ps];
+      int pid = pt[(size_t)b * max_pages + page_of(i, lps)];
       if (pid < 0 || pid >= num_pages) set_status(status, ST_BAD_PAGE);
-      else v = pid * ps + i % ps;
+      else v = slot_in_page(page_first_slot(pid, lps), i, lps);
     }
     slots[(size_t)b * max_ctx_len + i] = v;
   }

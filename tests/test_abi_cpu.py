@@ -95,6 +95,9 @@ def test_attention_validation():
     assert call(_attn_cfg(window=8)) == 2       # k > window
     assert call(_attn_cfg(split_tokens=100)) == 2
     assert call(_attn_cfg(split_tokens=64), maxL=20000) == 4    # 313 splits of the whole context
+    # the automatic split of a context above 256 x 8192 keys would exceed the 8192-key split
+    assert call(_attn_cfg(max_pages=131073), maxL=2097153) == 4
+    assert b"8192" in L.hspec_last_error()
     assert call(_attn_cfg(page_size=0)) == 2
     assert call(_attn_cfg(dtype=9)) == 3
     assert call(_attn_cfg(), maxL=-1) == 2
