@@ -8,7 +8,6 @@
 #include <cstdarg>
 #include <initializer_list>
 #include <cstdio>
-#include <string>
 
 #include "hspec.h"
 #include "kernels.h"
@@ -19,15 +18,17 @@ using hspec::bf16;
 
 namespace {
 
-thread_local std::string g_err;
+// Message of the last failing call on this thread.  A plain array: nothing in the library
+// runs a destructor at thread or process exit.
+thread_local char g_err[512];
+
+void clear_err() { g_err[0] = 0; }
 
 hspec_status fail(hspec_status s, const char* fmt, ...) {
-  char buf[512];
   va_list ap;
   va_start(ap, fmt);
-  vsnprintf(buf, sizeof buf, fmt, ap);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
   va_end(ap);
-  g_err = buf;
   return s;
 }
 
@@ -480,7 +481,7 @@ HSPEC_API size_t hspec_state_init_workspace(const hspec_mamba_cfg* cfg) {
 
 HSPEC_API hspec_status hspec_state_init(const hspec_mamba_cfg* cfg, const hspec_mamba_w* w, const void* h_last,
                                         float* S0, void* workspace, size_t ws_bytes, void* stream) {
-  g_err.clear();
+  clear_err();
   if (hspec_status s = check_mamba(cfg, w, false)) return s;
   if (!h_last || !S0) return fail(HSPEC_ERR_NULL, "h_last or S0 is NULL");
   if (hspec_status s = check_ws(workspace, ws_bytes, hspec_state_init_workspace(cfg))) return s;
@@ -505,7 +506,7 @@ HSPEC_API size_t hspec_mamba_block_scan_workspace(const hspec_mamba_cfg* cfg) {
 HSPEC_API hspec_status hspec_mamba_block_scan(const hspec_mamba_cfg* cfg, const hspec_mamba_w* w,
                                               const void* h_last, const void* block_hidden, float* out,
                                               float* S_final, void* workspace, size_t ws_bytes, void* stream) {
-  g_err.clear();
+  clear_err();
   if (hspec_status s = check_mamba(cfg, w, true)) return s;
   if (!h_last || !block_hidden || !out) return fail(HSPEC_ERR_NULL, "h_last, block_hidden or out is NULL");
   if (hspec_status s = check_ws(workspace, ws_bytes, hspec_mamba_block_scan_workspace(cfg))) return s;
@@ -535,7 +536,7 @@ HSPEC_API hspec_status hspec_target_kv_block_attn(const hspec_attn_cfg* cfg, con
                                                   const int32_t* page_table, const int32_t* ctx_lens,
                                                   int max_ctx_len, float* out, void* workspace, size_t ws_bytes,
                                                   void* stream) {
-  g_err.clear();
+  clear_err();
   if (hspec_status s = check_attn_cfg(cfg, max_ctx_len)) return s;
   if (hspec_status s = check_attn_w(cfg, w)) return s;
   if (!x || !k_cache || !v_cache || !page_table || !ctx_lens || !out)
@@ -570,7 +571,7 @@ HSPEC_API hspec_status hspec_draft_step(const hspec_mamba_cfg* mcfg, const hspec
                                         const void* h_last, const void* block_emb, const void* k_cache,
                                         const void* v_cache, const int32_t* page_table, const int32_t* ctx_lens,
                                         int max_ctx_len, float* out, void* workspace, size_t ws_bytes, void* stream) {
-  g_err.clear();
+  clear_err();
   if (hspec_status s = check_mamba(mcfg, mw, true)) return s;
   if (hspec_status s = check_attn_cfg(acfg, max_ctx_len)) return s;
   if (hspec_status s = check_attn_w(acfg, aw)) return s;
@@ -616,7 +617,7 @@ HSPEC_API hspec_status hspec_ssd_scan(int B, int T, int H, int P, int N, int G, 
                                       const void* x, const float* dt, const float* A, const void* Bm, const void* Cm,
                                       const float* Dskip, const void* S0, float* y, float* S_final, void* workspace,
                                       size_t ws_bytes, void* stream) {
-  g_err.clear();
+  clear_err();
   if (!dtype_ok(dtype)) return fail(HSPEC_ERR_DTYPE, "unknown dtype %d", (int)dtype);
   if (B <= 0 || T <= 0 || H <= 0 || P <= 0 || N <= 0 || G <= 0 || chunk <= 0)
     return fail(HSPEC_ERR_SHAPE, "non-positive scan dimension");
@@ -671,7 +672,7 @@ HSPEC_API hspec_status hspec_paged_attn_phase(const hspec_attn_cfg* cfg, const v
                                               const int32_t* page_table, const int32_t* ctx_lens, int max_ctx_len,
                                               float* o, void* workspace, size_t ws_bytes, unsigned phases,
                                               void* stream) {
-  g_err.clear();
+  clear_err();
   if (hspec_status s = check_attn_cfg(cfg, max_ctx_len)) return s;
   if (!q || !k_blk || !v_blk || !k_cache || !v_cache || !page_table || !ctx_lens || !o)
     return fail(HSPEC_ERR_NULL, "an input or output pointer is NULL");
@@ -728,7 +729,7 @@ HSPEC_API hspec_status hspec_paged_attn(const hspec_attn_cfg* cfg, const void* q
 HSPEC_API hspec_status hspec_gather_slots(int B, int max_pages, int page_size, int num_pages,
                                           const int32_t* page_table, const int32_t* ctx_lens, int max_ctx_len,
                                           int32_t* slots, int32_t* status, void* stream) {
-  g_err.clear();
+  clear_err();
   if (B <= 0 || max_pages <= 0 || page_size <= 0 || num_pages <= 0 || max_ctx_len < 0)
     return fail(HSPEC_ERR_SHAPE, "non-positive gather dimension");
   if (!page_table || !ctx_lens || (!slots && max_ctx_len > 0)) return fail(HSPEC_ERR_NULL, "a gather pointer is NULL");
@@ -752,7 +753,7 @@ HSPEC_API size_t hspec_linear_workspace(hspec_dtype dtype, int M, int N, int K) 
 
 HSPEC_API hspec_status hspec_linear(hspec_dtype dtype, int M, int N, int K, const void* A, const void* W,
                                     const float* R, float* C, void* workspace, size_t ws_bytes, void* stream) {
-  g_err.clear();
+  clear_err();
   if (!dtype_ok(dtype)) return fail(HSPEC_ERR_DTYPE, "unknown dtype %d", (int)dtype);
   if (M <= 0 || N <= 0 || K <= 0) return fail(HSPEC_ERR_SHAPE, "non-positive GEMM dimension");
   if (K % 8) return fail(HSPEC_ERR_UNSUPPORTED, "K must be a multiple of 8");
@@ -863,7 +864,7 @@ HSPEC_API hspec_status hspec_drafter_forward(const hspec_mamba_cfg* mcfg, const 
                                              const hspec_layer_w* layers, const void* h_last, const void* block_emb,
                                              const int32_t* page_table, const int32_t* ctx_lens, int max_ctx_len,
                                              float* out, void* workspace, size_t ws_bytes, void* stream) {
-  g_err.clear();
+  clear_err();
   if (!mcfg || !acfg) return fail(HSPEC_ERR_NULL, "mamba or attention config is NULL");
   if (n_layers < 1) return fail(HSPEC_ERR_SHAPE, "n_layers must be >= 1");
   if (!layers) return fail(HSPEC_ERR_NULL, "layers is NULL");
@@ -999,7 +1000,7 @@ HSPEC_API hspec_status hspec_kv_inject(const hspec_attn_cfg* cfg, int d_h, int n
                                        const float* const* k_norm_w, void* const* k_cache, void* const* v_cache,
                                        const int32_t* page_table, const int32_t* ctx_lens, void* workspace,
                                        size_t ws_bytes, void* stream) {
-  g_err.clear();
+  clear_err();
   if (hspec_status s = check_attn_cfg(cfg, 0)) return s;
   if (d_h <= 0 || n_layers < 1) return fail(HSPEC_ERR_SHAPE, "d_h and n_layers must be positive");
   if (d_h % 8) return fail(HSPEC_ERR_UNSUPPORTED, "d_h must be a multiple of 8");
@@ -1104,7 +1105,7 @@ HSPEC_API hspec_status hspec_draft_head(const hspec_head_cfg* cfg, const hspec_h
                                         const int32_t* prev_tok, const float* gumbel, const int32_t* forced,
                                         int32_t* tokens, float* logits, void* workspace, size_t ws_bytes,
                                         void* stream) {
-  g_err.clear();
+  clear_err();
   if (hspec_status s = check_head(cfg)) return s;
   if (!w || !w->norm_f_w || !w->W_lm || !w->E_M || !w->U_M) return fail(HSPEC_ERR_NULL, "head weight is NULL");
   if (!hidden || !prev_tok || !tokens) return fail(HSPEC_ERR_NULL, "hidden, prev_tok or tokens is NULL");
@@ -1144,7 +1145,7 @@ HSPEC_API size_t hspec_pack_w_ds_bytes(int d_S, int r) {
 }
 
 HSPEC_API hspec_status hspec_pack_w_ds(int d_S, int r, const void* W_dS, void* W_packed, void* stream) {
-  g_err.clear();
+  clear_err();
   if (d_S <= 0 || r <= 0) return fail(HSPEC_ERR_SHAPE, "non-positive W_dS dimension");
   if (d_S % 16 || r % 64) return fail(HSPEC_ERR_UNSUPPORTED, "packing needs d_S %% 16 == 0 and r %% 64 == 0");
   if (!W_dS || !W_packed) return fail(HSPEC_ERR_NULL, "W_dS or W_packed is NULL");
@@ -1154,7 +1155,7 @@ HSPEC_API hspec_status hspec_pack_w_ds(int d_S, int r, const void* W_dS, void* W
 }
 
 HSPEC_API hspec_status hspec_read_status(const void* workspace, int32_t* status, void* stream) {
-  g_err.clear();
+  clear_err();
   if (!workspace || !status) return fail(HSPEC_ERR_NULL, "workspace or status is NULL");
   hipStream_t st = (hipStream_t)stream;
   HIP_TRY(hipMemcpyAsync(status, workspace, sizeof(int32_t), hipMemcpyDeviceToHost, st));
@@ -1175,4 +1176,4 @@ HSPEC_API const char* hspec_status_string(hspec_status s) {
   return "unknown status";
 }
 
-HSPEC_API const char* hspec_last_error(void) { return g_err.c_str(); }
+HSPEC_API const char* hspec_last_error(void) { return g_err; }

@@ -92,11 +92,22 @@ __device__ __forceinline__ int swept_lo(const AttnArgs& a, int L) {
   return a.window > 0 && L - a.window + 1 > 0 ? L - a.window + 1 : 0;
 }
 
-// Splits of one request: the swept range [swept_lo, L) cut into runs of `split` positions
-// (one split, with no cache keys, when the range is empty).
+// Splits of one request: the swept range [swept_lo, L) cut into the fewest runs of at most
+// `split` positions (one split, with no cache keys, when the range is empty) ...
 __device__ __forceinline__ int n_splits(const AttnArgs& a, int L) {
   const int n = L - swept_lo(a, L);
   return n > 0 ? (n + a.split - 1) / a.split : 1;
+}
+
+// ... of near-equal length: every run but the last holds q = ceil(n / ns) positions rounded up
+// to a whole 32-key tile, the last one the rest.  q <= split (a multiple of 64), so
+// (ns - 1) q <= (ns - 1) split < n and the last run is never empty; no run is longer than
+// split, which bounds the page ids one split reads.
+__device__ __forceinline__ int split_len(const AttnArgs& a, int L) {
+  const int n = L - swept_lo(a, L);
+  if (n <= 0) return 0;
+  const int ns = (n + a.split - 1) / a.split;
+  return ((n + ns - 1) / ns + 31) & ~31;
 }
 
 // Element offset of (row, column d) in a swizzled K/V tile.  16-byte chunk c of row r lives at
@@ -167,8 +178,9 @@ attn_sweep(AttnArgs a) {
   const int b = unit_e.x >> 16, sp = unit_e.x & 0xffff, h = item % a.Hkv;
   const int L = unit_e.y;   // validated by the work-list kernel
   const int nsplit = n_splits(a, L);
-  const int k0 = swept_lo(a, L) + sp * a.split;
-  const int k1 = min(L, k0 + a.split);
+  const int qlen = split_len(a, L);
+  const int k0 = swept_lo(a, L) + sp * qlen;
+  const int k1 = min(L, k0 + qlen);
   const int kstart = k0;
   const int n_cache = kstart < k1 ? (k1 - kstart + KT - 1) / KT : 0;
   // the block keys follow the cache keys of a request's last split, unless the reduction takes them
@@ -453,34 +465,55 @@ attn_sweep(AttnArgs a) {
 }
 
 // Work list of the sweep: every (request, split) once, as (request << 16 | split, context
-// length), the full splits first and then the last splits by decreasing length, so the
-// persistent workgroups finish close together.
-// One workgroup of PLAN_THREADS: the full splits are placed by a block-wide prefix sum over
-// requests, the last splits by rank (requests beyond PLAN_RANK_MAX keep their own order).
-// Also resets the item queue and, as the first kernel of a call, its status words.
+// length), requests ordered by decreasing split length (all splits of a request together), so
+// that the persistent workgroups, taking items longest first, finish close together.
+// One workgroup of PLAN_THREADS.  Requests are ranked by split length (ties by index) and their
+// splits placed by a block-wide prefix sum over the ranks; beyond PLAN_RANK_MAX requests they
+// keep their own order.  Also resets the item queue and, as the first kernel of a call, its
+// status words.
 constexpr int PLAN_THREADS = 1024;
 constexpr int PLAN_RANK_MAX = 4096;
 
 __global__ void __launch_bounds__(PLAN_THREADS) attn_plan(AttnArgs a, int clear_words) {
-  __shared__ int s_rem[PLAN_RANK_MAX];
+  __shared__ int s_key[PLAN_RANK_MAX];    // split length of request b
+  __shared__ int s_rank[PLAN_RANK_MAX];   // rank of request b
+  __shared__ int s_off[PLAN_RANK_MAX];    // splits of the request at rank r, then its first item
   __shared__ int s_scan[PLAN_THREADS];
   __shared__ int s_base;
   const int tid = threadIdx.x;
   if (tid < clear_words) a.status[tid] = 0;   // a call's first kernel clears its status words
-  __syncthreads();
-  const bool ranked = a.B <= PLAN_RANK_MAX;
   if (tid == 0) s_base = 0;
   __syncthreads();
-  for (int b0 = 0; b0 < a.B; b0 += PLAN_THREADS) {
-    const int b = b0 + tid;
-    int nfull = 0, L = 0;
-    if (b < a.B) {
-      L = clamp_len(a, b);
-      const int ns = n_splits(a, L);
-      nfull = ns - 1;
-      if (ranked) s_rem[b] = L - swept_lo(a, L) - nfull * a.split;
+  const bool ranked = a.B <= PLAN_RANK_MAX;
+  if (ranked) {
+    for (int b = tid; b < a.B; b += PLAN_THREADS) s_key[b] = split_len(a, clamp_len(a, b));
+    __syncthreads();
+    for (int b = tid; b < a.B; b += PLAN_THREADS) {
+      const int key = s_key[b];
+      int rank = 0;
+      for (int o = 0; o < a.B; ++o) {
+        const int ko = s_key[o];
+        rank += (ko > key) || (ko == key && o < b);
+      }
+      s_rank[b] = rank;
+      s_off[rank] = n_splits(a, clamp_len(a, b));
     }
-    s_scan[tid] = nfull;
+    __syncthreads();
+  }
+  // exclusive prefix sum of the split counts, in rank order (request order past PLAN_RANK_MAX),
+  // one block of PLAN_THREADS entries at a time
+  for (int r0 = 0; r0 < a.B; r0 += PLAN_THREADS) {
+    const int r = r0 + tid;
+    int cnt = 0, L = 0;
+    if (r < a.B) {
+      if (ranked) {
+        cnt = s_off[r];
+      } else {
+        L = clamp_len(a, r);
+        cnt = n_splits(a, L);
+      }
+    }
+    s_scan[tid] = cnt;
     __syncthreads();
     for (int o = 1; o < PLAN_THREADS; o <<= 1) {
       const int v = tid >= o ? s_scan[tid - o] : 0;
@@ -488,33 +521,34 @@ __global__ void __launch_bounds__(PLAN_THREADS) attn_plan(AttnArgs a, int clear_
       s_scan[tid] += v;
       __syncthreads();
     }
-    const int first = s_base + s_scan[tid] - nfull;
-    for (int sp = 0; sp < nfull; ++sp) {
-      a.units[2 * (first + sp)] = (b << 16) | sp;
-      a.units[2 * (first + sp) + 1] = L;
+    const int first = s_base + s_scan[tid] - cnt;
+    if (r < a.B) {
+      if (ranked) {
+        s_off[r] = first;
+      } else {
+        for (int sp = 0; sp < cnt; ++sp) {
+          a.units[2 * (first + sp)] = (r << 16) | sp;
+          a.units[2 * (first + sp) + 1] = L;
+        }
+      }
     }
     __syncthreads();
     if (tid == PLAN_THREADS - 1) s_base += s_scan[tid];
     __syncthreads();
   }
-  const int full = s_base;
-  for (int b = tid; b < a.B; b += PLAN_THREADS) {
-    const int L = clamp_len(a, b);
-    const int ns = n_splits(a, L);
-    int rank = b;
-    if (ranked) {
-      const int rem = s_rem[b];
-      rank = 0;
-      for (int o = 0; o < a.B; ++o) {
-        const int ro = s_rem[o];
-        rank += (ro > rem) || (ro == rem && o < b);
+  if (ranked) {
+    for (int b = tid; b < a.B; b += PLAN_THREADS) {
+      const int L = clamp_len(a, b);
+      const int ns = n_splits(a, L);
+      const int first = s_off[s_rank[b]];
+      for (int sp = 0; sp < ns; ++sp) {
+        a.units[2 * (first + sp)] = (b << 16) | sp;
+        a.units[2 * (first + sp) + 1] = L;
       }
     }
-    a.units[2 * (full + rank)] = (b << 16) | (ns - 1);
-    a.units[2 * (full + rank) + 1] = L;
   }
   if (tid == 0) {
-    a.status[1] = (full + a.B) * a.Hkv;
+    a.status[1] = s_base * a.Hkv;
     a.status[2] = 0;
   }
 }
