@@ -177,7 +177,7 @@ def ssd_sequential(x, dt, A, Bm, Cm, Dskip, S0=None):
         Bt = Bm[:, t, grp, :]                                       # [B, H, N]
         Ct = Cm[:, t, grp, :]
         S = a[:, :, None, None] * S + (dt[:, t, :, None] * x[:, t])[:, :, :, None] * Bt[:, :, None, :]
-        y[:, t] = np.einsum("bhpn,bhn->bhp", S, Ct) + Dskip[None, :, None] * x[:, t]
+        y[:, t] = (S @ Ct[:, :, :, None])[..., 0] + Dskip[None, :, None] * x[:, t]    # S_t C_t + D x_t
     return y, S
 
 
@@ -314,17 +314,21 @@ def paged_attention(q, k_blk, v_blk, k_cache, v_cache, page_table, ctx_lens, *,
         L = int(ctx_lens[b])
         slots = gather_slots(page_table[b:b + 1], [L], page_size, L)[0]
         Kc, Vc = f64(kc[slots]), f64(vc[slots])                     # [L, Hkv, D]
-        for j in range(T):
-            pos = L + j
-            lo = max(0, pos - window + 1) if window > 0 else 0
-            nb = j + 1 if block_causal else T
-            K = np.concatenate([Kc[lo:L], kb[b, :nb]], axis=0)      # [n, Hkv, D]
-            V = np.concatenate([Vc[lo:L], vb[b, :nb]], axis=0)
-            for hq in range(Hq):
-                h = hq // g
-                s = (K[:, h, :] @ q[b, j, hq]) * scale
-                w = np.exp(s - s.max())
-                o[b, j, hq] = (w / w.sum()) @ V[:, h, :]
+        for h in range(Hkv):
+            heads = np.arange(h * g, (h + 1) * g)                   # the query heads of KV head h
+            Kh = np.ascontiguousarray(Kc[:, h, :])                  # [L, D]
+            Vh = np.ascontiguousarray(Vc[:, h, :])
+            for j in range(T):
+                pos = L + j
+                lo = max(0, pos - window + 1) if window > 0 else 0
+                nb = j + 1 if block_causal else T
+                Q = q[b, j, heads]                                  # [g, D]
+                # the full score row of each head: visible cache keys, then the block keys
+                s = np.concatenate([Kh[lo:L] @ Q.T, kb[b, :nb, h] @ Q.T], axis=0) * scale   # [n, g]
+                w = np.exp(s - s.max(axis=0))
+                w = w / w.sum(axis=0)
+                nc = L - lo
+                o[b, j, heads] = w[:nc].T @ Vh[lo:L] + w[nc:].T @ vb[b, :nb, h]
     return o
 
 
@@ -357,24 +361,29 @@ def attention_layer(v, W, cache, cfg, return_parts: bool = False, requests=None)
 
 # ------------------------------------------------------------------- the drafting step
 
-def draft_step(W, x, cfg, requests=None, return_parts: bool = False):
+def draft_step(W, x, cfg, requests=None, return_parts: bool = False, progress=None):
     """x1 = e + Mamba(RMSNorm(e) g1; S_init);  out = x1 + Attn(RMSNorm(x1) g2).
 
     Sec. 3.3 (architecture: Mamba, then attention, in each drafter layer) with
     S_init from ``state_init`` (Sec. 3.3.1).  ``requests`` restricts the work
     to a subset of requests (rows of the batch); the outputs of the other rows
-    are left as NaN.
+    are left as NaN.  ``progress``, if given, is called with the name of each
+    finished stage (for long runs).
     """
+    note = progress or (lambda stage: None)
     idx = np.arange(cfg.B) if requests is None else np.asarray(requests)
     S0, F = state_init(np.asarray(x["h_last"])[idx], W["W_r"], W["W_dS"], cfg.H, cfg.P, cfg.N)
+    note("state projection")
     e = f64(np.asarray(x["block_emb"])[idx])
     u = rmsnorm(e, f64(W["norm1_w"]), cfg.eps)
     m_out, mparts = mamba_mixer(u, S0, W, cfg, return_parts=True)
+    note("mamba")
     x1 = e + m_out
     v = rmsnorm(x1, f64(W["norm2_w"]), cfg.eps)
     cache = dict(k_cache=x["k_cache"], v_cache=x["v_cache"],
                  page_table=np.asarray(x["page_table"])[idx], ctx_lens=np.asarray(x["ctx_lens"])[idx])
     a_out, aparts = attention_layer(v, W, cache, cfg, return_parts=True)
+    note("attention")
     out_sub = x1 + a_out
     out = np.full((cfg.B,) + out_sub.shape[1:], np.nan)
     out[idx] = out_sub
@@ -392,7 +401,7 @@ def mlp(x: np.ndarray, W) -> np.ndarray:
     return (silu(x @ f64(W["W_gate"]).T) * (x @ f64(W["W_up"]).T)) @ f64(W["W_down"]).T
 
 
-def drafter_forward(layers, shared, x, caches, cfg, requests=None):
+def drafter_forward(layers, shared, x, caches, cfg, requests=None, progress=None):
     """The drafter's block forward (Sec. 3.3; App. B.1).
 
     S_init = state_init(h_last) is computed once, from the |M| fused target layers, and given
@@ -404,14 +413,17 @@ def drafter_forward(layers, shared, x, caches, cfg, requests=None):
     ``shared`` holds W_r and W_dS; ``caches`` is a list of dicts with k_cache and v_cache
     (one per target layer an attention reads); x holds h_last, block_emb, page_table and
     ctx_lens, the page table and lengths being shared by all target layers.  ``requests``
-    restricts the work to some rows; the others are NaN.
+    restricts the work to some rows; the others are NaN.  ``progress``, if given, is called
+    with the name of each finished stage.
     """
+    note = progress or (lambda stage: None)
     idx = np.arange(cfg.B) if requests is None else np.asarray(requests)
     S0 = None
     if any(W.get("W_in") is not None for W in layers):
         S0, _ = state_init(np.asarray(x["h_last"])[idx], shared["W_r"], shared["W_dS"], cfg.H, cfg.P, cfg.N)
+        note("state projection")
     h = f64(np.asarray(x["block_emb"])[idx])
-    for W in layers:
+    for li, W in enumerate(layers):
         if W.get("W_in") is not None:   # layers without a Mamba module skip it (block-diffusion backbone)
             h = h + mamba_mixer(rmsnorm(h, f64(W["norm1_w"]), cfg.eps), S0, W, cfg)
         if W.get("cache") is not None:
@@ -420,6 +432,7 @@ def drafter_forward(layers, shared, x, caches, cfg, requests=None):
                          ctx_lens=np.asarray(x["ctx_lens"])[idx])
             h = h + attention_layer(rmsnorm(h, f64(W["norm2_w"]), cfg.eps), W, cache, cfg)
         h = h + mlp(rmsnorm(h, f64(W["norm3_w"]), cfg.eps), W)
+        note(f"layer {li}")
     out = np.full((cfg.B,) + h.shape[1:], np.nan)
     out[idx] = h
     return out

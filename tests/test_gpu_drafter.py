@@ -56,17 +56,19 @@ def test_drafter_forward(name):
     assert_close(out, O.drafter_forward(L, shared, x, x["caches"], cfg), name)
 
 
+@pytest.mark.slow
+@pytest.mark.timeout(900)
 def test_drafter_forward_full_size():
     """8b-serving-b64 shapes (B 64, k 16, d_model 4096, Mamba H 128 x 64 x 128, Hq 32 / Hkv 8,
-    ff 12288, |M| = 5, packed W_dS); the oracle checks requests 0 and 63."""
+    ff 12288, |M| = 5, packed W_dS); the oracle checks every request."""
     cfg = I.CONFIGS[3].replace(n_fuse=I.DRAFTER_FUSE, ff=12288)
     shared, L = I.make_drafter_weights(cfg, seed=22)
     x = I.make_drafter_inputs(cfg, seed=22, n_caches=3)
     out, st = _run(cfg, shared, L, x, pack=True)
     assert st == 0
-    idx = [0, cfg.B - 1]
-    ref = O.drafter_forward(L, shared, x, x["caches"], cfg, requests=idx)
-    assert_close(out[idx], ref[idx], "full-size drafter")
+    ref = O.drafter_forward(L, shared, x, x["caches"], cfg,
+                            progress=lambda s: print(f"  oracle: {s} done", flush=True))
+    assert_close(out, ref, "full-size drafter")
 
 
 # ------------------------------------------------- block-diffusion comparison stand-in

@@ -38,11 +38,14 @@ MUTATIONS = {
     "rope_sign": ("x1 * c - x2 * s, x2 * c + x1 * s", "x1 * c + x2 * s, x2 * c - x1 * s"),
     "rope_positions_from_zero": ("pos = L[:, None] + np.arange(T)[None, :]", "pos = 0 * L[:, None] + np.arange(T)[None, :]"),
     "qk_norm_missing": ('q = rmsnorm(q, f64(W["q_norm_w"]), cfg.eps)', "q = q"),
-    "gqa_modulo": ("h = hq // g", "h = hq % Hkv"),
+    "gqa_interleaved": ("heads = np.arange(h * g, (h + 1) * g)", "heads = np.arange(h, Hq, Hkv)"),
     "scale_by_D": ("scale = D ** -0.5 if scale is None else scale", "scale = 1.0 / D if scale is None else scale"),
     "window_off_by_one": ("lo = max(0, pos - window + 1) if window > 0 else 0", "lo = max(0, pos - window) if window > 0 else 0"),
     "causal_flipped": ("nb = j + 1 if block_causal else T", "nb = T if block_causal else j + 1"),
-    "block_keys_dropped": ("K = np.concatenate([Kc[lo:L], kb[b, :nb]], axis=0)", "K = np.concatenate([Kc[lo:L], kb[b, :0]], axis=0)"),
+    "block_keys_dropped": ("s = np.concatenate([Kh[lo:L] @ Q.T, kb[b, :nb, h] @ Q.T], axis=0) * scale",
+                           "s = np.concatenate([Kh[lo:L] @ Q.T, kb[b, :0, h] @ Q.T], axis=0) * scale"),
+    "block_values_shifted": ("w[nc:].T @ vb[b, :nb, h]", "w[nc:].T @ np.roll(vb[b, :nb, h], 1, axis=0)"),
+    "softmax_normalised_across_heads": ("w = w / w.sum(axis=0)", "w = w / w.sum()"),
     "missing_mamba_residual": ("x1 = e + m_out", "x1 = m_out"),
     "missing_attn_residual": ("out_sub = x1 + a_out", "out_sub = a_out"),
     "mlp_gate_up_swapped": ('return (silu(x @ f64(W["W_gate"]).T) * (x @ f64(W["W_up"]).T))',
