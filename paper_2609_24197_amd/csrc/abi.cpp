@@ -327,18 +327,24 @@ struct AttnPlan {
   float* part_o = nullptr;
   float* part_ml = nullptr;
   int32_t* units = nullptr;
+  int32_t* req = nullptr;
   bf16 *o_hi = nullptr, *o_lo = nullptr;
-  int split = 0, max_splits = 0;
+  int split = 0, max_splits = 0, auto_split = 0, min_split = 0;
   GemmScratch gs;
 };
 
 void plan_sweep(Arena& ar, const hspec_attn_cfg& c, int max_ctx_len, AttnPlan& p) {
   const int swept = hspec::attention_swept_len(max_ctx_len, c.window);
   p.split = c.split_tokens > 0 ? c.split_tokens : hspec::attention_default_split(c.B, c.Hkv, swept);
-  p.max_splits = swept > 0 ? (swept + p.split - 1) / p.split : 1;
+  // automatic splitting: the work-list kernel may cut requests finer than p.split (down to
+  // attention_min_auto_split), so the buffers are sized for that many splits
+  p.auto_split = c.split_tokens > 0 ? 0 : 1;
+  p.min_split = p.auto_split ? hspec::attention_min_auto_split(p.split, swept) : p.split;
+  p.max_splits = swept > 0 ? (swept + p.min_split - 1) / p.min_split : 1;
   const int R = c.k * (c.Hq / c.Hkv);
   const size_t units = (size_t)c.B * c.Hkv * p.max_splits;
-  p.units = ar.take<int32_t>((size_t)2 * c.B * p.max_splits);
+  p.units = ar.take<int32_t>((size_t)4 * c.B * p.max_splits);
+  p.req = ar.take<int32_t>((size_t)2 * c.B);
   if (p.max_splits > 1 || (c.flags & HSPEC_ATTN_PRECISE_IO)) {   // split partials
     p.part_o = ar.take<float>(units * R * c.D);
     p.part_ml = ar.take<float>(units * R * 2);
@@ -391,16 +397,23 @@ hspec::AttnArgs sweep_args(const hspec_attn_cfg& c, const AttnPlan& p, const int
   a.max_ctx_len = max_ctx_len; a.split = p.split; a.max_splits = p.max_splits;
   const float scale = c.scale > 0.f ? c.scale : 1.f / std::sqrt((float)c.D);
   a.scale_log2 = scale * 1.4426950408889634f;
-  a.part_o = p.part_o; a.part_ml = p.part_ml; a.status = status; a.units = p.units;
+  a.part_o = p.part_o; a.part_ml = p.part_ml; a.status = status; a.units = p.units; a.req = p.req;
+  a.auto_split = p.auto_split; a.min_split = p.min_split;
+  a.grid = a.auto_split ? hspec::attention_sweep_grid(c.D, c.k * (c.Hq / c.Hkv), is_f32(c.dtype)) : 0;
   return a;
 }
 
-// QKV projections -> q/k norm + RoPE -> sweep + reduce -> O projection (+ residual R).
+// QKV projections -> q/k norm + RoPE -> sweep + reduce -> O projection (+ residual R).  The
+// sweep's work list is built inside the q/k-norm + RoPE launch (its own launch, ahead of the
+// projections, past kWorklistFusedMax requests), clearing the first plan_clear status words.
 hspec_status run_attn_core(const hspec_attn_cfg& c, const hspec_attn_w& w, Planes xn, const void* k_cache,
                            const void* v_cache, const int32_t* pt, const int32_t* lens, int max_ctx_len,
-                           const AttnPlan& p, const void* R, int r_bf16, float* out, int* status,
+                           const AttnPlan& p, const void* R, int r_bf16, float* out, int* status, int plan_clear,
                            hipStream_t st) {
   const int M = c.B * c.k;
+  const hspec::AttnArgs plan = sweep_args(c, p, pt, lens, max_ctx_len, status);
+  const bool plan_fused = c.B <= hspec::kWorklistFusedMax;
+  if (!plan_fused) HIP_TRY(hspec::launch_attention_plan(plan, plan_clear, st));
   const int ldq = (c.Hq + 2 * c.Hkv) * c.D;
   Planes wq, wk, wv, wo, kc, vc;
   HIP_TRY(as_planes(w.W_q, c.dtype, p.wq, wq, st));
@@ -434,8 +447,9 @@ hspec_status run_attn_core(const hspec_attn_cfg& c, const hspec_attn_w& w, Plane
     }
   }
   HIP_TRY(hspec::launch_qk_norm_rope(p.qkv, w.q_norm_w, w.k_norm_w, lens, c.B, c.k, c.Hq, c.Hkv, c.D, c.eps,
-                                     c.rope_theta, p.q_hi, p.q_lo, p.k_hi, p.k_lo, p.v_hi, p.v_lo, st));
-  hspec::AttnArgs a = sweep_args(c, p, pt, lens, max_ctx_len, status);
+                                     c.rope_theta, p.q_hi, p.q_lo, p.k_hi, p.k_lo, p.v_hi, p.v_lo, st,
+                                     plan_fused ? &plan : nullptr, plan_clear));
+  hspec::AttnArgs a = plan;
   a.q_hi = p.q_hi; a.q_lo = p.q_lo; a.kb_hi = p.k_hi; a.kb_lo = p.k_lo; a.vb_hi = p.v_hi; a.vb_lo = p.v_lo;
   a.kc_hi = kc.hi; a.kc_lo = kc.lo; a.vc_hi = vc.hi; a.vc_lo = vc.lo;
   a.o_bf16 = p.o_hi;
@@ -548,12 +562,11 @@ HSPEC_API hspec_status hspec_target_kv_block_attn(const hspec_attn_cfg* cfg, con
   int* status = status_word(ar);
   AttnPlan p;
   plan_attn(ar, *cfg, max_ctx_len, false, p);
-  // the sweep's work list is the call's first kernel and clears the status words
-  HIP_TRY(hspec::launch_attention_plan(sweep_args(*cfg, p, page_table, ctx_lens, max_ctx_len, status),
-                                       hspec::kStatusClear, st));
+  // no kernel before the work list sets a status bit: the work list clears the status words
   Planes xn;
   HIP_TRY(as_planes(x, cfg->dtype, p.x_in, xn, st));
-  return run_attn_core(*cfg, *w, xn, k_cache, v_cache, page_table, ctx_lens, max_ctx_len, p, nullptr, 0, out, status, st);
+  return run_attn_core(*cfg, *w, xn, k_cache, v_cache, page_table, ctx_lens, max_ctx_len, p, nullptr, 0, out, status,
+                       hspec::kStatusClear, st);
 }
 
 HSPEC_API size_t hspec_draft_step_workspace(const hspec_mamba_cfg* mcfg, const hspec_attn_cfg* acfg,
@@ -588,9 +601,7 @@ HSPEC_API hspec_status hspec_draft_step(const hspec_mamba_cfg* mcfg, const hspec
   plan_draft(ar, *mcfg, *acfg, max_ctx_len, p);
   const int M = mcfg->B * mcfg->k;
   const bool f32 = is_f32(mcfg->dtype);
-  // the sweep's work list is the call's first kernel and clears the status words
-  HIP_TRY(hspec::launch_attention_plan(sweep_args(*acfg, p.at, page_table, ctx_lens, max_ctx_len, status),
-                                       hspec::kStatusClear, st));
+  // no kernel before the attention's work list sets a status bit: the work list clears them
   if (hspec_status s = run_state(*mcfg, *mw, h_last, p.m.st, nullptr, st)) return s;
   HIP_TRY(hspec::launch_rmsnorm_planes(block_emb, !f32, norm1_w, M, mcfg->d_model, mcfg->eps, p.m.u_hi, p.m.u_lo, st));
   Planes u{p.m.u_hi, p.m.u_lo};
@@ -598,7 +609,7 @@ HSPEC_API hspec_status hspec_draft_step(const hspec_mamba_cfg* mcfg, const hspec
   HIP_TRY(hspec::launch_rmsnorm_planes(p.x1, 0, norm2_w, M, acfg->d_model, acfg->eps, p.at.xn_hi, p.at.xn_lo, st));
   Planes xn{p.at.xn_hi, p.at.xn_lo};
   return run_attn_core(*acfg, *aw, xn, k_cache, v_cache, page_table, ctx_lens, max_ctx_len, p.at, p.x1, 0, out, status,
-                       st);
+                       hspec::kStatusClear, st);
 }
 
 HSPEC_API size_t hspec_ssd_scan_workspace(int B, int T, int H, int P, int N, int G, hspec_dtype dtype) {
@@ -937,13 +948,11 @@ HSPEC_API hspec_status hspec_drafter_forward(const hspec_mamba_cfg* mcfg, const 
       x_bf16 = 0;
     }
     if (L.attn) {
-      // the work list (the same for every layer) and a fresh item queue for this sweep
-      HIP_TRY(hspec::launch_attention_plan(sweep_args(ac, p.at, page_table, ctx_lens, max_ctx_len, status), 0, st));
       HIP_TRY(hspec::launch_rmsnorm_planes(x, x_bf16, L.norm2_w, M, ac.d_model, ac.eps, p.at.xn_hi, p.at.xn_lo, st));
       Planes xn{p.at.xn_hi, p.at.xn_lo};
       y = dst();
       if (hspec_status s = run_attn_core(ac, *L.attn, xn, L.k_cache, L.v_cache, page_table, ctx_lens, max_ctx_len,
-                                         p.at, x, x_bf16, y, status, st))
+                                         p.at, x, x_bf16, y, status, 0, st))   // work list, fresh queue
         return s;
       x = y;
       x_bf16 = 0;

@@ -1,11 +1,11 @@
 // Block queries over one target layer's paged K/V cache, reused in place, plus the block's
 // own K/V (H-Spec Sec. 3.3.2): the KV sweep over the cache, split along the context, and the
-// reduction that adds the block keys and combines the splits.
+// reduction that combines the splits (and, in the precise mode, adds the block keys).
 //
 // Work unit = (request b, split s, KV head h).  Its query tile is the k*g rows of the block
 // positions j and the g query heads of the group, stored as columns c = j*g + i; each wave
 // owns 16 of those columns.  A persistent grid takes units from a device queue (the work list
-// puts full splits first, then the last splits by decreasing length).  Per unit, 32-key K/V
+// orders requests by decreasing split length).  Per unit, 32-key K/V
 // tiles of the cache stream into LDS by direct DMA in a 3-stage pipeline:
 //   * K tiles are read back as MFMA fragments, giving S^T = K Q^T with
 //     v_mfma_f32_16x16x32_bf16, so each lane holds 4 keys of one column;
@@ -17,9 +17,8 @@
 // writes its output directly.  With block_in_sweep off (HSPEC_ATTN_PRECISE_IO) every split
 // writes (unnormalised O, running max, running sum) and the reduction computes the block keys'
 // softmax terms in fp32 from the hi/lo planes of q, k and v: few keys with large weights, where
-// bf16 rounding does not average out over a stack of layers.  Either way the splits are combined
-// in a fixed order, so results are bitwise reproducible and independent of where pages live in
-// the pool.  Cache slots at or past ctx_len and pages the table does not
+// bf16 rounding does not average out over a stack of layers.  Either way the splits are combined in a fixed order, so results are bitwise
+// reproducible and independent of where pages live in the pool.  Cache slots at or past ctx_len and pages the table does not
 // reference are never read; page ids outside the pool raise a device status bit and read as
 // zeros.
 #include <climits>
@@ -27,6 +26,7 @@
 
 #include "common.h"
 #include "kernels.h"
+#include "worklist.h"
 
 #ifndef HSPEC_SWEEP_WPE
 #define HSPEC_SWEEP_WPE 2   // waves per SIMD the sweep's register budget is sized for
@@ -45,7 +45,6 @@ typedef short s16x8 __attribute__((ext_vector_type(8)));
 #define LDS_AS __attribute__((address_space(3)))
 #define GLB_AS __attribute__((address_space(1)))
 
-constexpr int MAX_SPLIT = 8192;                 // keys per split (host-enforced by the config check)
 constexpr int MIN_PAGE = 16;                    // smallest supported page size
 constexpr int MAX_PIDS = MAX_SPLIT / MIN_PAGE + 1;
 
@@ -73,42 +72,6 @@ struct Sweep {
   static_assert(KT % 32 == 0 && DMA >= 1 && KT * CPR % NT == 0, "tile shape");
   static_assert(ST >= 2 && ST <= 8 && VM < 64, "stages");
 };
-
-__device__ __forceinline__ int clamp_len(const AttnArgs& a, int b) {
-  int L = a.ctx_lens[b];
-  int cap = a.max_pages * a.ps;
-  if (cap > a.max_ctx_len) cap = a.max_ctx_len;
-  if (L < 0 || L > cap) {
-    set_status(a.status, ST_BAD_CTX_LEN);
-    L = L < 0 ? 0 : cap;
-  }
-  return L;
-}
-
-// First cache position a sweep reads for a request of length L.  Under a sliding window the
-// query at position L + j sees cache positions p >= L + j - window + 1, so no query of the
-// block sees p < L - window + 1; those positions are not read at all.
-__device__ __forceinline__ int swept_lo(const AttnArgs& a, int L) {
-  return a.window > 0 && L - a.window + 1 > 0 ? L - a.window + 1 : 0;
-}
-
-// Splits of one request: the swept range [swept_lo, L) cut into the fewest runs of at most
-// `split` positions (one split, with no cache keys, when the range is empty) ...
-__device__ __forceinline__ int n_splits(const AttnArgs& a, int L) {
-  const int n = L - swept_lo(a, L);
-  return n > 0 ? (n + a.split - 1) / a.split : 1;
-}
-
-// ... of near-equal length: every run but the last holds q = ceil(n / ns) positions rounded up
-// to a whole 32-key tile, the last one the rest.  q <= split (a multiple of 64), so
-// (ns - 1) q <= (ns - 1) split < n and the last run is never empty; no run is longer than
-// split, which bounds the page ids one split reads.
-__device__ __forceinline__ int split_len(const AttnArgs& a, int L) {
-  const int n = L - swept_lo(a, L);
-  if (n <= 0) return 0;
-  const int ns = (n + a.split - 1) / a.split;
-  return ((n + ns - 1) / ns + 31) & ~31;
-}
 
 // Element offset of (row, column d) in a swizzled K/V tile.  16-byte chunk c of row r lives at
 // chunk slot c ^ f(r).  For 256-byte rows f(r) = 2 (r mod 8) + (r / 8 mod 2): the 16 rows read
@@ -174,11 +137,10 @@ attn_sweep(AttnArgs a) {
   __syncthreads();
   const int item = s_item;
   if (item >= n_items) break;
-  const int2 unit_e = *reinterpret_cast<const int2*>(a.units + 2 * (item / a.Hkv));
+  const int4 unit_e = *reinterpret_cast<const int4*>(a.units + 4 * (item / a.Hkv));
   const int b = unit_e.x >> 16, sp = unit_e.x & 0xffff, h = item % a.Hkv;
   const int L = unit_e.y;   // validated by the work-list kernel
-  const int nsplit = n_splits(a, L);
-  const int qlen = split_len(a, L);
+  const int qlen = unit_e.z, nsplit = unit_e.w;
   const int k0 = swept_lo(a, L) + sp * qlen;
   const int k1 = min(L, k0 + qlen);
   const int kstart = k0;
@@ -464,93 +426,14 @@ attn_sweep(AttnArgs a) {
   }   // item loop
 }
 
-// Work list of the sweep: every (request, split) once, as (request << 16 | split, context
-// length), requests ordered by decreasing split length (all splits of a request together), so
-// that the persistent workgroups, taking items longest first, finish close together.
-// One workgroup of PLAN_THREADS.  Requests are ranked by split length (ties by index) and their
-// splits placed by a block-wide prefix sum over the ranks; beyond PLAN_RANK_MAX requests they
-// keep their own order.  Also resets the item queue and, as the first kernel of a call, its
-// status words.
-constexpr int PLAN_THREADS = 1024;
+// Work list of the sweep (build_worklist) as a kernel of its own: the first kernel of an
+// attention call that has no earlier kernel to carry it.
+constexpr int PLAN_THREADS = 256;
 constexpr int PLAN_RANK_MAX = 4096;
 
 __global__ void __launch_bounds__(PLAN_THREADS) attn_plan(AttnArgs a, int clear_words) {
-  __shared__ int s_key[PLAN_RANK_MAX];    // split length of request b
-  __shared__ int s_rank[PLAN_RANK_MAX];   // rank of request b
-  __shared__ int s_off[PLAN_RANK_MAX];    // splits of the request at rank r, then its first item
-  __shared__ int s_scan[PLAN_THREADS];
-  __shared__ int s_base;
-  const int tid = threadIdx.x;
-  if (tid < clear_words) a.status[tid] = 0;   // a call's first kernel clears its status words
-  if (tid == 0) s_base = 0;
-  __syncthreads();
-  const bool ranked = a.B <= PLAN_RANK_MAX;
-  if (ranked) {
-    for (int b = tid; b < a.B; b += PLAN_THREADS) s_key[b] = split_len(a, clamp_len(a, b));
-    __syncthreads();
-    for (int b = tid; b < a.B; b += PLAN_THREADS) {
-      const int key = s_key[b];
-      int rank = 0;
-      for (int o = 0; o < a.B; ++o) {
-        const int ko = s_key[o];
-        rank += (ko > key) || (ko == key && o < b);
-      }
-      s_rank[b] = rank;
-      s_off[rank] = n_splits(a, clamp_len(a, b));
-    }
-    __syncthreads();
-  }
-  // exclusive prefix sum of the split counts, in rank order (request order past PLAN_RANK_MAX),
-  // one block of PLAN_THREADS entries at a time
-  for (int r0 = 0; r0 < a.B; r0 += PLAN_THREADS) {
-    const int r = r0 + tid;
-    int cnt = 0, L = 0;
-    if (r < a.B) {
-      if (ranked) {
-        cnt = s_off[r];
-      } else {
-        L = clamp_len(a, r);
-        cnt = n_splits(a, L);
-      }
-    }
-    s_scan[tid] = cnt;
-    __syncthreads();
-    for (int o = 1; o < PLAN_THREADS; o <<= 1) {
-      const int v = tid >= o ? s_scan[tid - o] : 0;
-      __syncthreads();
-      s_scan[tid] += v;
-      __syncthreads();
-    }
-    const int first = s_base + s_scan[tid] - cnt;
-    if (r < a.B) {
-      if (ranked) {
-        s_off[r] = first;
-      } else {
-        for (int sp = 0; sp < cnt; ++sp) {
-          a.units[2 * (first + sp)] = (r << 16) | sp;
-          a.units[2 * (first + sp) + 1] = L;
-        }
-      }
-    }
-    __syncthreads();
-    if (tid == PLAN_THREADS - 1) s_base += s_scan[tid];
-    __syncthreads();
-  }
-  if (ranked) {
-    for (int b = tid; b < a.B; b += PLAN_THREADS) {
-      const int L = clamp_len(a, b);
-      const int ns = n_splits(a, L);
-      const int first = s_off[s_rank[b]];
-      for (int sp = 0; sp < ns; ++sp) {
-        a.units[2 * (first + sp)] = (b << 16) | sp;
-        a.units[2 * (first + sp) + 1] = L;
-      }
-    }
-  }
-  if (tid == 0) {
-    a.status[1] = s_base * a.Hkv;
-    a.status[2] = 0;
-  }
+  __shared__ WorklistLds<PLAN_RANK_MAX> lds;
+  build_worklist<PLAN_RANK_MAX>(a, clear_words, lds);
 }
 
 // Split reduction and block keys.  One workgroup per (request, KV head, 16 query columns);
@@ -573,6 +456,7 @@ __device__ __forceinline__ f32x4 ld4_planes(const bf16* hi, const bf16* lo, size
   return v;
 }
 
+
 // Split reduction when the sweep took the block keys: one thread per (column, 4 dims) and 2 per
 // thread; o = sum_s O_s 2^(m_s - m*) / sum_s l_s 2^(m_s - m*) in split order.  Requests with one
 // split were written by the sweep.
@@ -581,10 +465,7 @@ __global__ void __launch_bounds__(RED_THREADS) attn_merge(AttnArgs a) {
   const int cblocks = (R + RED_COLS - 1) / RED_COLS;
   const int bh = blockIdx.x / cblocks, c0 = (blockIdx.x % cblocks) * RED_COLS;
   const int b = bh / a.Hkv, h = bh % a.Hkv;
-  int L = a.ctx_lens[b];
-  const int cap = min(a.max_pages * a.ps, a.max_ctx_len);
-  L = L < 0 ? 0 : (L > cap ? cap : L);   // out-of-range lengths were flagged by the sweep
-  const int nsplit = n_splits(a, L);
+  const int nsplit = a.req[2 * b];   // splits of the request (the work-list kernel's choice)
   if (nsplit == 1) return;
   const size_t unit0 = ((size_t)b * a.Hkv + h) * a.max_splits;
   for (int it = threadIdx.x; it < RED_COLS * nq; it += RED_THREADS) {
@@ -654,10 +535,7 @@ __global__ void __launch_bounds__(RED_THREADS) attn_reduce(AttnArgs a) {
   const int cblocks = (R + RED_COLS - 1) / RED_COLS;
   const int bh = blockIdx.x / cblocks, c0 = (blockIdx.x % cblocks) * RED_COLS;
   const int b = bh / a.Hkv, h = bh % a.Hkv;
-  int L = a.ctx_lens[b];
-  const int cap = min(a.max_pages * a.ps, a.max_ctx_len);
-  L = L < 0 ? 0 : (L > cap ? cap : L);   // out-of-range lengths were flagged by the sweep
-  const int nsplit = n_splits(a, L);
+  const int nsplit = a.req[2 * b];   // splits of the request (the work-list kernel's choice)
   const size_t unit0 = ((size_t)b * a.Hkv + h) * a.max_splits;
   const int tid = threadIdx.x, ci = tid >> 4, ln = tid & 15;
   const bool live = c0 + ci < R;
@@ -807,41 +685,54 @@ __global__ void gather_slots_kernel(int B, int max_pages, int ps, int num_pages,
 #define HSPEC_SWEEP_KT 32   // keys per tile (at least; a multiple of 32)
 #endif
 
+// One compiled variant of the sweep: tile keys, pipeline depth and the kernel, from the head
+// dim, the waves per workgroup and the storage (LO: fp32 as hi/lo planes).
 template <int D, int QB, int NW, bool LO>
-hipError_t launch_sweep(const AttnArgs& a, hipStream_t s) {
-  constexpr int KT0 = 512 * NW / D > 32 ? 512 * NW / D : 32;  // every lane DMAs at least one chunk
-  constexpr int KT = KT0 > HSPEC_SWEEP_KT ? KT0 : HSPEC_SWEEP_KT;
-  constexpr int NDMA = 2 * (LO ? 2 : 1) * KT * (D / 8) / (64 * NW);
-  constexpr int ST_MAX = 2 + 63 / NDMA;                         // vmcnt holds at most 63
-  constexpr int ST = LO ? 2 : (HSPEC_SWEEP_ST < ST_MAX ? HSPEC_SWEEP_ST : ST_MAX);
-  auto kern = attn_sweep<D, QB, NW, KT, ST, LO>;
-  static int slots_of[64] = {};   // resident workgroups per device (persistent grid size)
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return e;
-  int& slots = slots_of[dev & 63];
-  if (slots == 0) {
-    int cus = 0, per_cu = 0;
-    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 64 * NW, 0);
-    if (e != hipSuccess) return e;
-    slots = cus * (per_cu > 0 ? per_cu : 1);
-  }
-  const long long items = (long long)a.B * a.max_splits * a.Hkv;
-  const int grid = (int)(items < slots ? items : slots);
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * NW), 0, s, a);
-  return hipGetLastError();
-}
+struct SweepVariant {
+  static constexpr int KT0 = 512 * NW / D > 32 ? 512 * NW / D : 32;  // every lane DMAs at least one chunk
+  static constexpr int KT = KT0 > HSPEC_SWEEP_KT ? KT0 : HSPEC_SWEEP_KT;
+  static constexpr int NDMA = 2 * (LO ? 2 : 1) * KT * (D / 8) / (64 * NW);
+  static constexpr int ST_MAX = 2 + 63 / NDMA;                       // vmcnt holds at most 63
+  static constexpr int ST = LO ? 2 : (HSPEC_SWEEP_ST < ST_MAX ? HSPEC_SWEEP_ST : ST_MAX);
+  static constexpr int THREADS = 64 * NW;
+  static constexpr auto kern = attn_sweep<D, QB, NW, KT, ST, LO>;
 
-template <int D, bool LO>
-hipError_t launch_sweep_nw(const AttnArgs& a, hipStream_t s) {
+  // Resident workgroups on the current device (the persistent grid), cached per device.
+  static hipError_t slots(int& out) {
+    static int slots_of[64] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    int& sl = slots_of[dev & 63];
+    if (sl == 0) {
+      int cus = 0, per_cu = 0;
+      e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+      if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, THREADS, 0);
+      if (e != hipSuccess) return e;
+      sl = cus * (per_cu > 0 ? per_cu : 1);
+    }
+    out = sl;
+    return hipSuccess;
+  }
+};
+
+// Calls f(SweepVariant<...>{}) for the variant the arguments select; hipErrorInvalidValue if none.
+// D: head dim; R: query rows per KV head (k g); lo: fp32 storage (the cache as hi/lo planes).
+template <class F>
+hipError_t with_sweep_variant(int D, int R, bool lo, F f) {
   constexpr int QB = HSPEC_SWEEP_QB;
-  const int R = a.T * (a.Hq / a.Hkv);
   const int nw = (R + 16 * QB - 1) / (16 * QB);
-  if (nw <= 1) return launch_sweep<D, QB, 1, LO>(a, s);
-  if (nw <= 2) return launch_sweep<D, QB, 2, LO>(a, s);
-  if (nw <= 4) return launch_sweep<D, QB, 4, LO>(a, s);
-  if (nw <= 8) return launch_sweep<D, QB, 8, LO>(a, s);
+  auto by_nw = [&](auto d, auto l) -> hipError_t {
+    constexpr int Dv = decltype(d)::value;
+    constexpr bool Lv = decltype(l)::value;
+    if (nw <= 1) return f(SweepVariant<Dv, QB, 1, Lv>{});
+    if (nw <= 2) return f(SweepVariant<Dv, QB, 2, Lv>{});
+    if (nw <= 4) return f(SweepVariant<Dv, QB, 4, Lv>{});
+    if (nw <= 8) return f(SweepVariant<Dv, QB, 8, Lv>{});
+    return hipErrorInvalidValue;
+  };
+  if (D == 128) return lo ? by_nw(Int<128>{}, std::true_type{}) : by_nw(Int<128>{}, std::false_type{});
+  if (D == 64) return lo ? by_nw(Int<64>{}, std::true_type{}) : by_nw(Int<64>{}, std::false_type{});
   return hipErrorInvalidValue;
 }
 
@@ -866,20 +757,41 @@ int attention_default_split(int B, int Hkv, int swept_len) {
   return (int)s;
 }
 
+int attention_sweep_grid(int D, int R, bool lo) {
+  int grid = 0;
+  const hipError_t e = with_sweep_variant(D, R, lo, [&](auto v) { return decltype(v)::slots(grid); });
+  return e == hipSuccess ? grid : 0;
+}
+
+int attention_min_auto_split(int host_split, int swept_len) {
+  // down to two thirds of the host's split size, and never more than 256 splits
+  long long s = ((long long)host_split * 2 / 3 + 63) / 64 * 64;
+  const long long min_for_256 = ((long long)swept_len + 255) / 256;
+  if (s < min_for_256) s = (min_for_256 + 63) / 64 * 64;
+  if (s < 64) s = 64;
+  return (int)(s < host_split ? s : host_split);
+}
+
 hipError_t launch_attention_plan(const AttnArgs& a, int clear_words, hipStream_t s) {
   hipLaunchKernelGGL(attn_plan, dim3(1), dim3(PLAN_THREADS), 0, s, a, clear_words);
   return hipGetLastError();
 }
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s, unsigned parts) {
-  const bool lo = a.kc_lo != nullptr;   // fp32 storage: the cache comes as hi/lo planes
   hipError_t e = hipSuccess;
   if (parts & ATTN_SWEEP) {
     if (!a.q_hi || !a.kc_hi || !a.vc_hi) return hipErrorInvalidValue;
     if (a.block_in_sweep ? (!a.kb_hi || !a.vb_hi) : (!a.part_o || !a.part_ml)) return hipErrorInvalidValue;
-    if (a.D == 128) e = lo ? launch_sweep_nw<128, true>(a, s) : launch_sweep_nw<128, false>(a, s);
-    else if (a.D == 64) e = lo ? launch_sweep_nw<64, true>(a, s) : launch_sweep_nw<64, false>(a, s);
-    else return hipErrorInvalidValue;
+    e = with_sweep_variant(a.D, a.T * (a.Hq / a.Hkv), a.kc_lo != nullptr, [&](auto v) -> hipError_t {
+      using V = decltype(v);
+      int slots = 0;
+      const hipError_t es = V::slots(slots);
+      if (es != hipSuccess) return es;
+      const long long items = (long long)a.B * a.max_splits * a.Hkv;
+      const int grid = (int)(items < slots ? items : slots);
+      hipLaunchKernelGGL(V::kern, dim3(grid), dim3(V::THREADS), 0, s, a);
+      return hipGetLastError();
+    });
     if (e != hipSuccess) return e;
   }
   if (parts & ATTN_REDUCE) {

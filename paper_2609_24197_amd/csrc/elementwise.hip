@@ -3,6 +3,7 @@
 // residual where the next contraction needs fp32-level accuracy).
 #include "common.h"
 #include "kernels.h"
+#include "worklist.h"
 
 namespace hspec {
 
@@ -372,11 +373,19 @@ __global__ void __launch_bounds__(256) gated_rmsnorm_kernel(const float* y, cons
 // first heads load.
 constexpr int QKR4_U = 4;
 
+template <bool PLAN>
 __global__ void __launch_bounds__(256) qk_norm_rope4_kernel(const float* qkv, const float* qw, const float* kw,
                                                             const int32_t* ctx_lens, int T, int Hq, int Hkv,
                                                             int D, float eps, double theta, bf16* q_hi,
                                                             bf16* q_lo, bf16* k_hi, bf16* k_lo, bf16* v_hi,
-                                                            bf16* v_lo) {
+                                                            bf16* v_lo, AttnArgs plan, int plan_clear) {
+  if constexpr (PLAN) {   // the last workgroup builds the KV sweep's work list
+    __shared__ WorklistLds<kWorklistFusedMax> wl;
+    if (blockIdx.x == gridDim.x - 1) {
+      build_worklist<kWorklistFusedMax>(plan, plan_clear, wl);
+      return;
+    }
+  }
   __shared__ float s_cs[256], s_sn[256];
   const int nh = Hq + 2 * Hkv;
   const int tok = blockIdx.x;
@@ -594,11 +603,18 @@ hipError_t launch_gated_rmsnorm(const float* y, const float* z, int z_ld, const 
 
 hipError_t launch_qk_norm_rope(const float* qkv, const float* qw, const float* kw, const int32_t* ctx_lens, int B,
                                int T, int Hq, int Hkv, int D, float eps, double theta, bf16* q_hi, bf16* q_lo,
-                               bf16* k_hi, bf16* k_lo, bf16* v_hi, bf16* v_lo, hipStream_t s) {
+                               bf16* k_hi, bf16* k_lo, bf16* v_hi, bf16* v_lo, hipStream_t s, const AttnArgs* plan,
+                               int plan_clear) {
   if (B * T <= 0) return hipSuccess;
   if (D < 8 || D % 8 || D > 512 || 64 % (D / 8)) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(qk_norm_rope4_kernel, dim3(B * T), dim3(256), 0, s, qkv, qw, kw, ctx_lens, T,
-                     Hq, Hkv, D, eps, theta, q_hi, q_lo, k_hi, k_lo, v_hi, v_lo);
+  if (plan) {
+    if (plan->B > kWorklistFusedMax) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(qk_norm_rope4_kernel<true>, dim3(B * T + 1), dim3(256), 0, s, qkv, qw, kw, ctx_lens, T,
+                       Hq, Hkv, D, eps, theta, q_hi, q_lo, k_hi, k_lo, v_hi, v_lo, *plan, plan_clear);
+  } else {
+    hipLaunchKernelGGL(qk_norm_rope4_kernel<false>, dim3(B * T), dim3(256), 0, s, qkv, qw, kw, ctx_lens, T,
+                       Hq, Hkv, D, eps, theta, q_hi, q_lo, k_hi, k_lo, v_hi, v_lo, AttnArgs{}, 0);
+  }
   return hipGetLastError();
 }
 

@@ -4,6 +4,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "hspec.h"
+
 namespace hspec {
 
 typedef __bf16 bf16;
@@ -50,8 +52,17 @@ struct AttnArgs {
   bf16* o_bf16 = nullptr;
   bf16* o_bf16_lo = nullptr;  // with o_bf16: the lo plane of o, or null
   int* status = nullptr;      // device status word; status[1] = work items, status[2] = queue (zero at launch)
-  int32_t* units = nullptr;   // [B * max_splits][2] work list (request << 16 | split, length)
+  int32_t* units = nullptr;   // [B * max_splits][4] work list (request << 16 | split, length, split length, splits)
+  int32_t* req = nullptr;     // [B][2] splits of each request and their length (written by the work list)
+  int grid = 0;               // persistent workgroups of the sweep (attention_sweep_grid)
+  int auto_split = 0;         // 1: the work list picks the split size in [min_split, split] from the lengths
+  int min_split = 0;
 };
+// Persistent workgroups the KV sweep runs with on the current device (head dim D, R = k g
+// query rows per KV head, lo: fp32 storage); 0 if the shape has no sweep variant.
+int attention_sweep_grid(int D, int R, bool lo);
+// Smallest split size the work-list kernel may choose under automatic splitting.
+int attention_min_auto_split(int host_split, int swept_len);
 // Work list of the sweep (reads only B, ctx_lens, split and the table sizes of a); clears
 // status[0, clear_words) first.  Must precede launch_attention on the stream.
 hipError_t launch_attention_plan(const AttnArgs& a, int clear_words, hipStream_t s);
@@ -60,6 +71,7 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s, unsigned parts = A
 size_t attention_partials_bytes(int B, int Hkv, int max_splits, int R, int D);
 constexpr int kStatusWords = 64;   // int32 words reserved at the start of every workspace
 constexpr int kStatusClear = 4;    // cleared at the start of every call: status bits, work items, queue
+constexpr int kWorklistFusedMax = 512;   // requests up to which the work list rides in the RoPE launch
 int attention_default_split(int B, int Hkv, int swept_len);
 // Longest run of cache positions the sweep reads for one request: max_ctx_len, or window - 1
 // under a sliding window (no query of the block sees an older position).
@@ -113,10 +125,13 @@ hipError_t launch_conv_split(const ConvArgs& a, hipStream_t s);
 hipError_t launch_gated_rmsnorm(const float* y, const float* z, int z_ld, const float* w, int rows,
                                 int n, int G, float eps, bf16* out_hi, bf16* out_lo, hipStream_t s);
 // q/k per-head RMSNorm + RoPE at position ctx_len + j; v copied.  qkv rows [Hq*D | Hkv*D | Hkv*D].
+// With `plan` (at most kWorklistFusedMax requests) one extra workgroup also builds the sweep's
+// work list for those attention arguments, clearing the first plan_clear status words, as
+// launch_attention_plan does.
 hipError_t launch_qk_norm_rope(const float* qkv, const float* qw, const float* kw, const int32_t* ctx_lens,
                                int B, int T, int Hq, int Hkv, int D, float eps, double theta,
                                bf16* q_hi, bf16* q_lo, bf16* k_hi, bf16* k_lo, bf16* v_hi, bf16* v_lo,
-                               hipStream_t s);
+                               hipStream_t s, const AttnArgs* plan = nullptr, int plan_clear = 0);
 // fp32 -> bf16 hi/lo planes (lo optional).
 hipError_t launch_split_planes(const float* x, size_t n, bf16* hi, bf16* lo, hipStream_t s);
 // SwiGLU: h = SiLU(gate) * up from rows [gate | up] (fp32, width 2 ff) -> bf16 planes [rows, ff].

@@ -143,6 +143,27 @@ def test_paged_attn_split_invariance():
         assert_close(o, base, f"split {s} vs whole context", max_abs=2e-3, rel_l2=3e-3)
 
 
+def test_paged_attn_workspace_reuse():
+    """Consecutive calls on one workspace with different queries, caches and tables: the split
+    partials a call combines inside the sweep are its own (stores and loads coherent across
+    the XCDs' caches), never a previous call's left in a cache."""
+    cfg = _small_attn_cfg(B=4, lengths="list:3000,2500,700,1900")
+    ws = None
+    for seed, split in ((11, 512), (12, 512), (13, 256), (14, 0)):
+        print(f"[paged_attn reuse] seed {seed} split {split}", flush=True)
+        c = cfg.replace(split_tokens=split)
+        x = I.make_attn_inputs(c, seed=seed, extra_pages=1)
+        d = dev(x)
+        maxL = int(max(x["ctx_lens"]))
+        need = hspec.paged_attn_workspace(c, x["page_table"].shape[1], x["num_pages"], maxL)
+        if ws is None or ws.numel() < need:
+            ws = hspec.workspace(max(need, 64 << 20))
+        o = empty((c.B, c.k, c.Hq, c.D))
+        hspec.paged_attn(c, d, o, ws, maxL)
+        assert hspec.read_status(ws) == 0
+        assert_close(host(o), _ref_attn(c, x), f"seed {seed}")
+
+
 def test_paged_attn_window_splits():
     """Under a sliding window the splits tile only the positions some query can see,
     starting at ctx_len - window + 1 (not page- or tile-aligned): lengths around the window,
