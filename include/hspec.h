@@ -329,6 +329,24 @@ hspec_status hspec_paged_attn(const hspec_attn_cfg* cfg, const void* q, const vo
 size_t hspec_paged_attn_workspace(const hspec_attn_cfg* cfg, int max_ctx_len);
 
 /*
+ * hspec_paged_attn for callers that cannot allocate device memory (code under graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): the same kernels, in the same order,
+ * with the same results, but no workspace argument.  The workspace is a fixed array of
+ * HSPEC_STATIC_WS_BYTES inside the library's device code object; each GPU the library runs on
+ * holds its own copy until the process ends.  A call whose hspec_paged_attn_workspace exceeds
+ * that size returns HSPEC_ERR_WORKSPACE before any launch.  All calls on one GPU share its
+ * array: calls that overlap on one GPU (different streams, or unordered threads) race and
+ * give undefined results.  status: a device int32 that receives the call's device status word
+ * (HSPEC_DEV_* bits), or NULL.  The call allocates nothing (no hipMalloc, no hipFree).
+ * Other arguments and errors as hspec_paged_attn.
+ */
+#define HSPEC_STATIC_WS_BYTES (64u << 20)
+hspec_status hspec_paged_attn_static(const hspec_attn_cfg* cfg, const void* q, const void* k_blk, const void* v_blk,
+                                     const void* k_cache, const void* v_cache, const int32_t* page_table,
+                                     const int32_t* ctx_lens, int max_ctx_len, float* o, int32_t* status,
+                                     void* stream);
+
+/*
  * hspec_paged_attn in separately launched phases, for timing one kernel at a time: the work
  * list (which also clears the workspace status words), the KV sweep (with any fp32 -> bf16
  * plane conversion of its inputs), and the cross-split reduction.  `phases` is an OR of the

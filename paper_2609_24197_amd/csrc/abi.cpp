@@ -1186,3 +1186,7 @@ HSPEC_API const char* hspec_status_string(hspec_status s) {
 }
 
 HSPEC_API const char* hspec_last_error(void) { return g_err; }
+
+namespace hspec {
+hspec_status api_fail(hspec_status s, const char* msg) { return fail(s, "%s", msg); }
+}  // namespace hspec

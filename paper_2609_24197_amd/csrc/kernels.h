@@ -166,4 +166,7 @@ hipError_t launch_head_clear(const HeadArgs& a, int status_words, hipStream_t s)
 // then the tokens.
 hipError_t launch_markov_head(const HeadArgs& a, hipStream_t s);
 
+// Host side of the ABI: records msg as this thread's last error (hspec_last_error) and returns s.
+hspec_status api_fail(hspec_status s, const char* msg);
+
 }  // namespace hspec

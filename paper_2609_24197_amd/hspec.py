@@ -87,6 +87,9 @@ EXPORTS = {
     "hspec_ssd_scan_workspace": (C.c_size_t, [C.c_int] * 7),
     "hspec_paged_attn": (C.c_int, [C.POINTER(AttnCfg)] + [C.c_void_p] * 7 + [C.c_int, C.c_void_p, C.c_void_p,
                                                                           C.c_size_t, C.c_void_p]),
+    "hspec_paged_attn_static": (C.c_int, [C.POINTER(AttnCfg), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                          C.c_void_p, C.c_void_p, C.c_void_p, C.c_int, C.c_void_p, C.c_void_p,
+                                          C.c_void_p]),
     "hspec_paged_attn_workspace": (C.c_size_t, [C.POINTER(AttnCfg), C.c_int]),
     "hspec_paged_attn_phase": (C.c_int, [C.POINTER(AttnCfg)] + [C.c_void_p] * 7 + [C.c_int, C.c_void_p, C.c_void_p,
                                                                                 C.c_size_t, C.c_uint, C.c_void_p]),
@@ -294,6 +297,17 @@ def paged_attn(cfg, X, o, ws, max_ctx_len, acfg: AttnCfg | None = None, phases: 
         _check(lib().hspec_paged_attn(*args, stream_ptr()))
     else:
         _check(lib().hspec_paged_attn_phase(*args, int(phases), stream_ptr()))
+
+
+STATIC_WS_BYTES = 64 << 20   # HSPEC_STATIC_WS_BYTES
+
+
+def paged_attn_static(cfg, X, o, max_ctx_len, status=None, acfg: AttnCfg | None = None):
+    """The attention core on the library's fixed device array (no workspace argument)."""
+    ac = acfg or attn_cfg(cfg, X["page_table"].shape[1], X["k_cache"].shape[0])
+    _check(lib().hspec_paged_attn_static(C.byref(ac), ptr(X["q"]), ptr(X["k_blk"]), ptr(X["v_blk"]),
+                                         ptr(X["k_cache"]), ptr(X["v_cache"]), ptr(X["page_table"]),
+                                         ptr(X["ctx_lens"]), int(max_ctx_len), ptr(o), ptr(status), stream_ptr()))
 
 
 def gather_slots(page_table, ctx_lens, page_size, num_pages, max_ctx_len, slots, status=None):

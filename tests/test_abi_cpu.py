@@ -105,6 +105,18 @@ def test_attention_validation():
     assert L.hspec_paged_attn(C.byref(c), FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, 8192, FAKE, ws, n, None) == 1
 
 
+def test_static_workspace_validation():
+    """The fixed-array attention refuses a null config and any attention whose workspace exceeds
+    its array, before touching the device."""
+    L = _lib()
+    assert L.hspec_paged_attn_static(None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 100, FAKE, None, None) == 1
+    c = hspec.attn_cfg(I.CONFIGS[5], 1024, 300000)
+    assert L.hspec_paged_attn_workspace(C.byref(c), 16384) > hspec.STATIC_WS_BYTES
+    assert L.hspec_paged_attn_static(C.byref(c), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 16384, FAKE, None,
+                                     None) == 5
+    assert b"HSPEC_STATIC_WS_BYTES" in L.hspec_last_error()
+
+
 def test_window_bounds_the_swept_context():
     """Under a sliding window the sweep's split buffers are sized by window - 1 positions,
     not by max_ctx_len."""
