@@ -296,7 +296,8 @@ def sweep_inputs(cfg, Xd, x, seed, torch):
 
 def counters(cfg, seed, torch):
     """One launch each of a 1 GiB device copy (to calibrate the byte counters), the state
-    projection and the KV sweep, for FETCH_SIZE / WRITE_SIZE collection under rocprofv3."""
+    projection and the attention core, then two whole drafting steps, for counter collection
+    under rocprofv3 (FETCH_SIZE / WRITE_SIZE, or SQ counters per kernel of the step)."""
     src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)
     torch.cuda.synchronize()
@@ -321,6 +322,23 @@ def counters(cfg, seed, torch):
     hspec.paged_attn(cfg, Ad, o, aws, int(x["ctx_lens"].max()))
     torch.cuda.synchronize()
     log("KV sweep: 1 launch")
+    del Ad, aws, o
+    W = I.make_weights(cfg, seed)
+    Wd = {k: hspec.to_device(v) for k, v in W.items()}
+    if cfg.dtype == "bf16":
+        Wd["W_dS_packed"] = hspec.pack_w_ds(Wd.pop("W_dS"), cfg.d_S, cfg.rank)
+    Xd["h_last"] = hspec.to_device(x["h_last"])
+    Xd["block_emb"] = hspec.to_device(x["block_emb"])
+    maxL = int(x["ctx_lens"].max())
+    ws = hspec.workspace(hspec.draft_step_workspace(cfg, x["page_table"].shape[1], x["num_pages"], maxL))
+    out = torch.empty((cfg.B, cfg.k, cfg.d_model), dtype=torch.float32, device="cuda")
+    for _ in range(2):
+        hspec.draft_step(cfg, Wd, Xd, out, ws, maxL)
+    torch.cuda.synchronize()
+    log("draft step: 2 launches")
+    del Wd, Xd, ws, out
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
 
 
 def main():
@@ -485,3 +503,9 @@ def main():
 
 if __name__ == "__main__":
     main()
+    # main's device tensors are released by now; leave nothing for exit-time teardown (which
+    # runs after a profiler's own finalisation when the program is profiled)
+    import torch as _t
+    if _t.cuda.is_available():
+        _t.cuda.synchronize()
+        _t.cuda.empty_cache()

@@ -163,6 +163,8 @@ hspec_status check_attn_cfg(const hspec_attn_cfg* c, int max_ctx_len) {
   const int split = c->split_tokens > 0 ? c->split_tokens : hspec::attention_default_split(c->B, c->Hkv, swept);
   if (swept > 0 && (swept + split - 1) / split > 256)
     return fail(HSPEC_ERR_UNSUPPORTED, "swept context / split_tokens gives more than 256 splits");
+  if ((long long)c->B * c->Hkv * (swept > 0 ? (swept + 63) / 64 : 1) > 0x7fffffffLL)
+    return fail(HSPEC_ERR_UNSUPPORTED, "B x Hkv x swept context is too large for the work list");
   if (split > 8192)   // the sweep holds one split's page ids in a fixed LDS array
     return fail(HSPEC_ERR_UNSUPPORTED, "swept context of %d keys needs splits above 8192 keys (at most 256 x 8192)",
                 swept);

@@ -379,16 +379,16 @@ __global__ void __launch_bounds__(256) qk_norm_rope4_kernel(const float* qkv, co
                                                             int D, float eps, double theta, bf16* q_hi,
                                                             bf16* q_lo, bf16* k_hi, bf16* k_lo, bf16* v_hi,
                                                             bf16* v_lo, AttnArgs plan, int plan_clear) {
-  if constexpr (PLAN) {   // the last workgroup builds the KV sweep's work list
+  if constexpr (PLAN) {   // the first workgroup (dispatched first) builds the KV sweep's work list
     __shared__ WorklistLds<kWorklistFusedMax> wl;
-    if (blockIdx.x == gridDim.x - 1) {
+    if (blockIdx.x == 0) {
       build_worklist<kWorklistFusedMax>(plan, plan_clear, wl);
       return;
     }
   }
   __shared__ float s_cs[256], s_sn[256];
   const int nh = Hq + 2 * Hkv;
-  const int tok = blockIdx.x;
+  const int tok = PLAN ? blockIdx.x - 1 : blockIdx.x;
   const int b = tok / T, j = tok % T;
   const int half = D / 2, lph = D / 8, hpw = 64 / lph;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;

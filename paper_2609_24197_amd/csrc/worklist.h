@@ -2,6 +2,8 @@
 // work-list kernel of the attention calls and by the q/k-norm + RoPE launch, which builds it in
 // one extra workgroup so that the list costs no launch of its own inside a drafting step.
 #pragma once
+#include <climits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -77,7 +79,7 @@ struct WorklistLds {
   int off[RANK_MAX];    // splits of the request at rank r, then its first item
   int wave[WL_THREADS / 64];
   int cnt[WL_NCAND];
-  int sum, max;
+  int sum, max, choice;
 };
 
 // Work list of the sweep: every (request, split) once, as (request << 16 | split, context
@@ -112,60 +114,69 @@ __device__ void build_worklist(const AttnArgs& a, int clear_words, WorklistLds<R
   const bool ranked = a.B <= RANK_MAX;
   const int cap = max(1, a.max_splits);
 
-  // candidate split sizes: the host's size down to min_split in WL_NCAND near-even steps (tiles)
+  // candidate split sizes: twice the host's size down to min_split in WL_NCAND near-even steps
   auto cand = [&](int c) {
     const int hi = min(MAX_SPLIT, 2 * a.split) / 32, lo = max(1, a.min_split / 32);
     return 32 * (hi - (hi - lo) * c / (WL_NCAND - 1));
   };
   int S = a.split;
-  if (a.auto_split && a.grid > 0) {
-    int cnt[WL_NCAND] = {}, sum = 0, mx = 0;
+  if (ranked) {
+    int sum = 0, mx = 0;
     for (int b = tid; b < a.B; b += WL_THREADS) {
       const int n = swept_n(a, clamp_len(a, b));
-      if (ranked) s_n[b] = n;
+      s_n[b] = n;
       sum += n;
       mx = max(mx, n);
-#pragma unroll
-      for (int c = 0; c < WL_NCAND; ++c) cnt[c] += plan_pieces(n, cand(c), cap);
     }
-    // wave sums first: one LDS atomic per wave and value (same-address atomics serialise)
+    if (a.auto_split && a.grid > 0) {
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-#pragma unroll
-      for (int c = 0; c < WL_NCAND; ++c) cnt[c] += __shfl_xor(cnt[c], o);
-      sum += __shfl_xor(sum, o);
-      mx = max(mx, __shfl_xor(mx, o));
-    }
-    if ((tid & 63) == 0) {
-#pragma unroll
-      for (int c = 0; c < WL_NCAND; ++c) atomicAdd(&s_cnt[c], cnt[c]);
-      atomicAdd(&s_sum, sum);
-      atomicMax(&s_max, mx);
-    }
-    __syncthreads();
-    const long long avg = (long long)s_sum * a.Hkv;   // positions of all items; per workgroup: / grid
-    int best = -1;
-    // one round: the largest size whose items fit the grid with the longest near the average
-    for (int c = 0; c < WL_NCAND && best < 0; ++c) {
-      const long long items = (long long)s_cnt[c] * a.Hkv;
-      const int longest = min(cand(c), s_max);
-      if (items <= a.grid && (long long)longest * a.grid * 16 <= avg * 17) best = c;
-    }
-    // else: closest below a whole number (>= 2) of rounds
-    if (best < 0) {
-      long long gap_best = LLONG_MAX;
-      for (int c = 0; c < WL_NCAND; ++c) {
-        const long long items = (long long)s_cnt[c] * a.Hkv;
-        if (items <= a.grid) continue;
-        const long long rounds = (items + a.grid - 1) / a.grid;
-        const long long gap = rounds * a.grid - items;   // idle slots of the last round
-        if (gap < gap_best) { gap_best = gap; best = c; }
+      for (int o = 32; o > 0; o >>= 1) {
+        sum += __shfl_xor(sum, o);
+        mx = max(mx, __shfl_xor(mx, o));
       }
+      if ((tid & 63) == 0) {
+        atomicAdd(&s_sum, sum);
+        atomicMax(&s_max, mx);
+      }
+      __syncthreads();
+      // splits at each candidate size: wave w takes candidates w, w + 4, ..., its lanes the
+      // requests (the divisions spread over the whole workgroup)
+      const int wv = tid >> 6, ln = tid & 63;
+      for (int c = wv; c < WL_NCAND; c += WL_THREADS / 64) {
+        const int Sc = cand(c);
+        int cnt = 0;
+        for (int b = ln; b < a.B; b += 64) cnt += plan_pieces(s_n[b], Sc, cap);
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o);
+        if (ln == 0) s_cnt[c] = cnt;
+      }
+      __syncthreads();
+      // Choice, one lane per candidate: the largest size (smallest c) whose items fit one round
+      // with the longest split within 1/16 of the average work per workgroup; else the size
+      // leaving the fewest idle slots in the last of two or more rounds (larger size on ties).
+      // (Item counts fit in 32 bits: the host bounds B x max_splits x Hkv.)
+      if (tid < 64) {
+        int key = INT_MAX;
+        if (tid < WL_NCAND) {
+          const long long avg = (long long)s_sum * a.Hkv;   // positions of all items; per workgroup: / grid
+          const int items = s_cnt[tid] * a.Hkv;
+          const int longest = min(cand(tid), s_max);
+          if (items <= a.grid) {
+            if ((long long)longest * a.grid * 16 <= avg * 17) key = tid;
+          } else {
+            const int rem = items % a.grid;
+            key = (1 << 24) + (rem ? a.grid - rem : 0) * 32 + tid;
+          }
+        }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) key = min(key, __shfl_xor(key, o));
+        if (tid == 0) lds.choice = key;
+      }
+      __syncthreads();
+      if (lds.choice != INT_MAX) S = cand(lds.choice & 31);
+    } else {
+      __syncthreads();
     }
-    if (best >= 0) S = cand(best);
-  } else if (ranked) {
-    for (int b = tid; b < a.B; b += WL_THREADS) s_n[b] = swept_n(a, clamp_len(a, b));
-    __syncthreads();
   }
   if (ranked) {
     // split length of each request, then its rank by split length (longest first)
@@ -174,6 +185,7 @@ __device__ void build_worklist(const AttnArgs& a, int clear_words, WorklistLds<R
     for (int b = tid; b < a.B; b += WL_THREADS) {
       const int key = s_off[b];
       int rank = 0;
+#pragma unroll 8
       for (int o = 0; o < a.B; ++o) {
         const int ko = s_off[o];
         rank += (ko > key) || (ko == key && o < b);
