@@ -193,6 +193,7 @@ struct StatePlan {
   GemmScratch gs;
   bf16 *F_hi = nullptr, *F_lo = nullptr;
   bf16 *S0_hi = nullptr, *S0_lo = nullptr;
+  _Float16* S0_h16 = nullptr;
 };
 
 void plan_state(Arena& ar, const hspec_mamba_cfg& c, bool s0_planes, StatePlan& p) {
@@ -204,8 +205,14 @@ void plan_state(Arena& ar, const hspec_mamba_cfg& c, bool s0_planes, StatePlan& 
   p.F_lo = ar.take<bf16>((size_t)c.B * c.r);
   p.gs = reserve_gemm(ar, c.dtype, {{c.B, c.r, c.d_h}, {c.B, (int)dS, c.r}});
   if (s0_planes) {
-    p.S0_hi = ar.take<bf16>((size_t)c.B * dS);
-    p.S0_lo = ar.take<bf16>((size_t)c.B * dS);
+    // S0 only feeds the scan: one fp16 plane (11 significant bits, half the bytes of hi/lo
+    // bf16 planes) where the state projection runs on the weight-streaming path, else hi/lo
+    if (!is_f32(c.dtype) && hspec::gemm_f16_out_ok(c.B, (int)dS, c.r)) {
+      p.S0_h16 = ar.take<_Float16>((size_t)c.B * dS);
+    } else {
+      p.S0_hi = ar.take<bf16>((size_t)c.B * dS);
+      p.S0_lo = ar.take<bf16>((size_t)c.B * dS);
+    }
   }
 }
 
@@ -229,7 +236,7 @@ hspec_status run_state(const hspec_mamba_cfg& c, const hspec_mamba_w& w, const v
   g2.W_hi = wds.hi; g2.W_lo = wds.lo; g2.ldw = c.r;
   g2.M = c.B; g2.N = dS; g2.K = c.r;
   g2.C = S0_f32; g2.ldc = dS;
-  g2.C_hi = p.S0_hi; g2.C_lo = p.S0_lo; g2.ldch = dS;
+  g2.C_hi = p.S0_hi; g2.C_lo = p.S0_lo; g2.C_h16 = p.S0_h16; g2.ldch = dS;
   g2.w_packed = (c.flags & HSPEC_W_DS_PACKED) ? 1 : 0;
   use_scratch(g2, p.gs);
   HIP_TRY(hspec::launch_gemm(g2, st));
@@ -303,7 +310,7 @@ hspec_status run_mamba_core(const hspec_mamba_cfg& c, const hspec_mamba_w& w, Pl
   hspec::ScanArgs sa;
   sa.x_hi = p.x_hi; sa.x_lo = p.x_lo; sa.dt = p.dt; sa.A = w.A_log; sa.A_is_log = 1;
   sa.B_hi = p.B_hi; sa.B_lo = p.B_lo; sa.C_hi = p.C_hi; sa.C_lo = p.C_lo; sa.Dskip = w.D;
-  sa.S0_hi = p.st.S0_hi; sa.S0_lo = p.st.S0_lo; sa.y = p.y; sa.S_final = S_final;
+  sa.S0_hi = p.st.S0_hi; sa.S0_lo = p.st.S0_lo; sa.S0_h16 = p.st.S0_h16; sa.y = p.y; sa.S_final = S_final;
   sa.B = c.B; sa.T = c.k; sa.H = c.H; sa.P = c.P; sa.N = c.N; sa.G = c.G; sa.chunk = c.chunk;
   sa.x_ld = di; sa.bc_ld = gn; sa.dt_ld = c.H;
   HIP_TRY(hspec::launch_ssd_scan(sa, st));

@@ -14,6 +14,8 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 
 constexpr int WAVE = 64;
 
@@ -43,6 +45,10 @@ __device__ __forceinline__ bf16x8 zero8() {
 // D[4(l/16)+i][l%16].
 __device__ __forceinline__ f32x4 mma16(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+// The same 16x16x32 product on fp16 operands (11 significant bits).
+__device__ __forceinline__ f32x4 mma16h(f16x8 a, f16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
 }
 // D += A(32x16) * B(16x32); lane l holds A[l%32][8(l/32)..+7], B[8(l/32)..+7][l%32],
 // D[8(i/4)+4(l/32)+i%4][l%32].

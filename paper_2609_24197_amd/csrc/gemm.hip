@@ -410,6 +410,8 @@ skinny_kernel(GemmArgs g, int kper, int nitems) {
         buf(g.C_hi ? g.C_hi + min(n0, g.N) : nullptr, !split && g.C_hi && cols ? (rows_span * g.ldch + cols) * 2 : 0);
     const __amdgpu_buffer_rsrc_t r_lo =
         buf(g.C_lo ? g.C_lo + min(n0, g.N) : nullptr, !split && g.C_lo && cols ? (rows_span * g.ldch + cols) * 2 : 0);
+    const __amdgpu_buffer_rsrc_t r_h16 =
+        buf(g.C_h16 ? g.C_h16 + min(n0, g.N) : nullptr, !split && g.C_h16 && cols ? (rows_span * g.ldch + cols) * 2 : 0);
     // residual R (RES: present and not split-K): one of the two loads reads, the other is empty
     const bool rf = RES && !g.r_bf16, rb = RES && g.r_bf16;
     [[maybe_unused]] const __amdgpu_buffer_rsrc_t r_rf =
@@ -448,6 +450,8 @@ skinny_kernel(GemmArgs g, int kper, int nitems) {
         __builtin_amdgcn_raw_buffer_store_b128(vb, r_c, ok ? (m * g.ldc + c4) * 4 : SK_OOB, 0, 16);
         __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2u32, h), r_hi, ok ? (m * g.ldch + c4) * 2 : SK_OOB, 0, 16);
         __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2u32, l), r_lo, ok ? (m * g.ldch + c4) * 2 : SK_OOB, 0, 16);
+        const f16x4 v16 = {(_Float16)v[0], (_Float16)v[1], (_Float16)v[2], (_Float16)v[3]};
+        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2u32, v16), r_h16, ok ? (m * g.ldch + c4) * 2 : SK_OOB, 0, 16);
       }
     }
   }
@@ -470,6 +474,7 @@ __global__ void __launch_bounds__(256) skinny_reduce(GemmArgs g, int nparts) {
       g.C_hi[(size_t)m * g.ldch + n] = h;
       if (g.C_lo) g.C_lo[(size_t)m * g.ldch + n] = f2bf(v - bf2f(h));
     }
+    if (g.C_h16) g.C_h16[(size_t)m * g.ldch + n] = (_Float16)v;
   }
 }
 
@@ -511,6 +516,9 @@ __global__ void __launch_bounds__(256) skinny_reduce4(GemmArgs g, int nparts) {
       *reinterpret_cast<bf16x4*>(g.C_hi + (size_t)m * g.ldch + n) = h;
       if (g.C_lo) *reinterpret_cast<bf16x4*>(g.C_lo + (size_t)m * g.ldch + n) = l;
     }
+    if (g.C_h16)
+      *reinterpret_cast<f16x4*>(g.C_h16 + (size_t)m * g.ldch + n) =
+          f16x4{(_Float16)v[0], (_Float16)v[1], (_Float16)v[2], (_Float16)v[3]};
   }
 }
 
@@ -573,7 +581,8 @@ hipError_t launch_skinny_t(const GemmArgs& g, const SkPlan& p, hipStream_t s) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.ksplit == 1) return e;
   const size_t total = (size_t)g.M * g.N;
-  const bool vec = g.N % 4 == 0 && (!g.C || g.ldc % 4 == 0) && (!g.R || g.ldr % 4 == 0) && (!g.C_hi || g.ldch % 4 == 0);
+  const bool vec = g.N % 4 == 0 && (!g.C || g.ldc % 4 == 0) && (!g.R || g.ldr % 4 == 0) &&
+                   (!(g.C_hi || g.C_h16) || g.ldch % 4 == 0);
   size_t blocks = ((vec ? total / 4 : total) + 255) / 256;
   if (blocks > 4096) blocks = 4096;
   if (vec) hipLaunchKernelGGL(skinny_reduce4, dim3((unsigned)blocks), dim3(256), 0, s, g, p.ksplit);
@@ -1249,6 +1258,10 @@ hipError_t launch_pack_w(const bf16* W, int N, int K, bf16* Wp, hipStream_t s) {
   return hipGetLastError();
 }
 
+bool gemm_f16_out_ok(int M, int N, int K) {
+  return skinny_plan(M, N, K, false, 256).use && N % 4 == 0;   // the weight-streaming conditions (any CU count)
+}
+
 size_t gemm_scratch_elems(int M, int N, int K, bool a_lo, bool w_lo) {
   (void)a_lo;
   if (M <= 0 || N <= 0 || K <= 0) return 0;
@@ -1284,7 +1297,8 @@ hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
     return hipSuccess;
   }
   SkPlan p = skinny_plan(g.M, g.N, g.K, g.W_lo != nullptr, device_cus());
-  if ((g.C && g.ldc % 4) || (g.C_hi && g.ldch % 4) || (g.R && g.ldr % 4)) p.use = false;   // 16-byte stores
+  if ((g.C && g.ldc % 4) || ((g.C_hi || g.C_h16) && g.ldch % 4) || (g.R && g.ldr % 4)) p.use = false;   // 16-byte stores
+  if (g.C_h16 && (!p.use || g.W2)) return hipErrorInvalidValue;   // only the weight-streaming path writes fp16
   if (g.w_packed && (g.N % 16 || g.K % BK || g.W_lo || g.R)) return hipErrorInvalidValue;   // packed W: no residual
   if (p.use) {
     if (p.ksplit > 1 && (!g.part || g.part_cap < (size_t)p.ksplit * g.M * g.N)) {

@@ -18,6 +18,7 @@ struct GemmArgs {
   float* C = nullptr; int ldc = 0;             // fp32 result (optional)
   const void* R = nullptr; int ldr = 0; int r_bf16 = 0;   // residual added (optional)
   bf16* C_hi = nullptr; bf16* C_lo = nullptr; int ldch = 0;  // bf16 planes of the result
+  _Float16* C_h16 = nullptr;   // fp16 copy of the result, leading dimension ldch (weight-streaming path only)
   float* part = nullptr; size_t part_cap = 0;  // split-K scratch (fp32 elements), optional
   int w_packed = 0;   // W_hi is in the fragment-major packed layout (launch_pack_w)
   // Optional row segments of W (bf16, not packed): rows [0, N1) come from W_hi, [N1, N1 + N2)
@@ -25,6 +26,9 @@ struct GemmArgs {
   const bf16* W2 = nullptr; const bf16* W3 = nullptr; int N1 = 0, N2 = 0;
 };
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
+// Whether launch_gemm takes an M x N x K product (bf16 W) on the weight-streaming path, the only
+// one that writes C_h16.
+bool gemm_f16_out_ok(int M, int N, int K);
 // fp32 elements of split-K scratch that launch_gemm uses for an M x N x K product when
 // given at least that much (0: the shape is never split).
 size_t gemm_scratch_elems(int M, int N, int K, bool a_lo, bool w_lo);
@@ -93,6 +97,7 @@ struct ScanArgs {
   const bf16 *C_hi = nullptr, *C_lo = nullptr;
   const float* Dskip = nullptr;                       // [H]
   const bf16 *S0_hi = nullptr, *S0_lo = nullptr;      // [B, H, P, N] or null
+  const _Float16* S0_h16 = nullptr;                    // [B, H, P, N] as one fp16 plane (instead of S0_hi/lo)
   float* y = nullptr;                                 // [B, T, H, P]
   float* S_final = nullptr;                           // [B, H, P, N] or null
   int B = 0, T = 0, H = 0, P = 0, N = 0, G = 0, chunk = 0;

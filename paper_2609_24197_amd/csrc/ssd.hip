@@ -11,7 +11,9 @@
 // the intra-chunk product is done in fp32 on the VALU.  The chunk-local cumulative sum of
 // dt*A is a 16-lane shuffle scan.  When the block fits one chunk and no final state is
 // requested (ssd_scan_one), the initial state is read straight from global memory into MFMA
-// fragments; otherwise (ssd_scan_kernel) the fp32 state lives in LDS between chunks.
+// fragments (as bf16 hi/lo planes, or as one fp16 plane multiplied with C rounded to fp16 on
+// v_mfma_f32_16x16x32_f16); otherwise (ssd_scan_kernel) the fp32 state lives in LDS between
+// chunks.
 #include "common.h"
 #include "kernels.h"
 
@@ -62,7 +64,9 @@ __global__ void __launch_bounds__(64) ssd_scan_kernel(ScanArgs a) {
   for (int p = 0; p < P; ++p) {
     for (int n = lane; n < N; n += 64) {
       float v = 0.f;
-      if (a.S0_hi) {
+      if (a.S0_h16) {
+        v = (float)a.S0_h16[s0_off + p * N + n];
+      } else if (a.S0_hi) {
         v = bf2f(a.S0_hi[s0_off + p * N + n]);
         if (a.S0_lo) v += bf2f(a.S0_lo[s0_off + p * N + n]);
       }
@@ -199,7 +203,7 @@ __global__ void __launch_bounds__(64) ssd_scan_kernel(ScanArgs a) {
 // ssd_scan_kernel<N, false>, with every global load of the wave (dt, the x tile, the B and C
 // fragments, all initial-state fragments) issued before the first is used, so that a wave
 // waits for memory once instead of once per state fragment.
-template <int N>
+template <int N, bool H16>
 __global__ void __launch_bounds__(64) ssd_scan_one(ScanArgs a) {
   constexpr int NS = (N + 31) / 32;
   __shared__ float xT[P * (QMAX + 1)];   // x^T tile, fp32, padded rows
@@ -232,17 +236,23 @@ __global__ void __launch_bounds__(64) ssd_scan_one(ScanArgs a) {
     bfr[ns] = ld8_or0(a.B_hi + tok_t + n, ok);
     bfl[ns] = a.B_lo ? ld8_or0(a.B_lo + tok_t + n, ok) : zero8();
   }
-  // initial state as B operand of C S^T: column p = 16 pb + l16, n = 32 ns + 8 g4 ..
-  bf16x8 sh[4][NS], sl[4][NS];
+  // initial state as B operand of C S^T: column p = 16 pb + l16, n = 32 ns + 8 g4 ..  (H16: one
+  // fp16 plane, multiplied with C rounded to fp16; otherwise bf16 hi/lo planes)
+  bf16x8 sh[4][H16 ? 1 : NS], sl[4][H16 ? 1 : NS];
+  f16x8 s16[4][H16 ? NS : 1];
 #pragma unroll
   for (int pb = 0; pb < 4; ++pb)
 #pragma unroll
     for (int ns = 0; ns < NS; ++ns) {
       const int n = 32 * ns + 8 * g4;
       const size_t off = s0_off + (size_t)(16 * pb + l16) * N + n;
-      const bool ok = a.S0_hi != nullptr && n < N;
-      sh[pb][ns] = ld8_or0(a.S0_hi + off, ok);
-      sl[pb][ns] = a.S0_lo != nullptr ? ld8_or0(a.S0_lo + off, ok) : zero8();
+      if constexpr (H16) {
+        s16[pb][ns] = n < N ? *reinterpret_cast<const f16x8*>(a.S0_h16 + off) : f16x8{};
+      } else {
+        const bool ok = a.S0_hi != nullptr && n < N;
+        sh[pb][ns] = ld8_or0(a.S0_hi + off, ok);
+        sl[pb][ns] = a.S0_lo != nullptr ? ld8_or0(a.S0_lo + off, ok) : zero8();
+      }
     }
   const float Ah = a.A_is_log ? -__expf(a.A[h]) : a.A[h], Dh = a.Dskip[h];
 
@@ -269,14 +279,28 @@ __global__ void __launch_bounds__(64) ssd_scan_one(ScanArgs a) {
   }
   // ---- state term C S^T: lane gets rows t = 4 g4 + i, column p = 16 pb + l16
   f32x4 ys[4];
+  if constexpr (H16) {
+    f16x8 c16[NS];   // C (hi + lo) rounded once to fp16
 #pragma unroll
-  for (int pb = 0; pb < 4; ++pb) {
-    ys[pb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int ns = 0; ns < NS; ++ns)
 #pragma unroll
-    for (int ns = 0; ns < NS; ++ns) {
-      ys[pb] = mma16(cf[ns], sh[pb][ns], ys[pb]);
-      if (a.C_lo) ys[pb] = mma16(cfl[ns], sh[pb][ns], ys[pb]);
-      if (a.S0_lo) ys[pb] = mma16(cf[ns], sl[pb][ns], ys[pb]);
+      for (int e = 0; e < 8; ++e) c16[ns][e] = (_Float16)(bf2f(cf[ns][e]) + bf2f(cfl[ns][e]));
+#pragma unroll
+    for (int pb = 0; pb < 4; ++pb) {
+      ys[pb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ns = 0; ns < NS; ++ns) ys[pb] = mma16h(c16[ns], s16[pb][ns], ys[pb]);
+    }
+  } else {
+#pragma unroll
+    for (int pb = 0; pb < 4; ++pb) {
+      ys[pb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ns = 0; ns < NS; ++ns) {
+        ys[pb] = mma16(cf[ns], sh[pb][ns], ys[pb]);
+        if (a.C_lo) ys[pb] = mma16(cfl[ns], sh[pb][ns], ys[pb]);
+        if (a.S0_lo) ys[pb] = mma16(cf[ns], sl[pb][ns], ys[pb]);
+      }
     }
   }
   // ---- decay-weighted mixing matrix M[t][s] = (C_t . B_s) exp(l_t - l_s) dt_s for s <= t
@@ -326,8 +350,8 @@ hipError_t launch_n(const ScanArgs& a, hipStream_t s) {
     auto kern = ssd_scan_kernel<N>;
     hipLaunchKernelGGL(kern, dim3(a.B * a.H), dim3(64), lds_multi, s, a);
   } else {
-    auto kern = ssd_scan_one<N>;
-    hipLaunchKernelGGL(kern, dim3(a.B * a.H), dim3(64), 0, s, a);
+    if (a.S0_h16) hipLaunchKernelGGL((ssd_scan_one<N, true>), dim3(a.B * a.H), dim3(64), 0, s, a);
+    else hipLaunchKernelGGL((ssd_scan_one<N, false>), dim3(a.B * a.H), dim3(64), 0, s, a);
   }
   return hipGetLastError();
 }
