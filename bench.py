@@ -355,6 +355,9 @@ def main():
                          "2048); default: the workload's own (full context)")
     ap.add_argument("--block-causal", action="store_true",
                     help="causal attention inside the drafted block instead of bidirectional")
+    ap.add_argument("--kv-heads", type=int, default=0,
+                    help="partial target-KV-head reuse: the drafter attends with this many of the "
+                         "target's KV heads (evenly spaced), keeping the GQA group size")
     ap.add_argument("--compare", action="store_true",
                     help="time the hybrid drafter against a block-diffusion drafter with KV injection "
                          "across concurrency and context length, print one JSON line and exit")
@@ -375,6 +378,12 @@ def main():
         cfg = cfg.replace(window=args.window)
     if args.block_causal:
         cfg = cfg.replace(block_causal=True)
+    if args.kv_heads:
+        n = args.kv_heads
+        if not 0 < n <= cfg.Hkv:
+            sys.exit(f"--kv-heads must be in 1..{cfg.Hkv}")
+        cfg = cfg.replace(Hkv=n, Hq=cfg.g * n, Hkv_target=cfg.Hkv,
+                          kv_heads=tuple(i * cfg.Hkv // n for i in range(n)))
     if args.counters:
         counters(cfg, args.seed, torch)
         return
@@ -488,6 +497,7 @@ def main():
                    "sum_ctx_tokens": int(L.sum()), "Hq": cfg.Hq, "Hkv": cfg.Hkv, "D": cfg.D,
                    "d_model": cfg.d_model, "mamba": f"H{cfg.H} P{cfg.P} N{cfg.N} G{cfg.G} chunk{cfg.chunk}",
                    "page_size": cfg.page_size, "window": cfg.window, "block_causal": cfg.block_causal,
+                   "kv_heads_reused": list(cfg.kv_map), "target_kv_heads": cfg.Hkv_cache,
                    "W_dS_layout": "packed" if cfg.dtype == "bf16" else "row-major",
                    "parallelism": "single GPU"},
         "roofline": roof,

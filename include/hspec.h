@@ -108,7 +108,7 @@ typedef struct {
  *   Hq query heads, Hkv KV heads (Hq % Hkv == 0, query head q reads KV head q / (Hq/Hkv)),
  *   D head dim (64 or 128), k * Hq/Hkv <= 128, B <= 32767, page_size a power of two >= 16.
  *   The target cache is two pools
- *   [num_pages, page_size, Hkv, D] (K stored after RoPE), addressed through page_table
+ *   [num_pages, page_size, Hkv, D] (K stored after RoPE; Hkv_cache heads per slot, below), addressed through page_table
  *   [B, max_pages] int32 and ctx_lens [B] int32: cache position i of request b lives in
  *   slot page_table[b, i / page_size] * page_size + i % page_size.  Block position j sits at
  *   RoPE position ctx_lens[b] + j.  window > 0 hides cache position p from the query at
@@ -121,6 +121,13 @@ typedef struct {
  *   0 = automatic.
  *   A setting outside these limits returns HSPEC_ERR_UNSUPPORTED.
  *   scale: softmax scale, 0 = 1/sqrt(D).  rope_theta: RoPE base (rotate-half pairing).
+ *   Partial target-KV-head reuse (Sec. 3.3.2 "KV dimension": reusing only a subset of the
+ *   target's KV heads, left to future work in Sec. 5): Hkv_cache is the number of KV heads per
+ *   slot of the target cache (0 = Hkv), and kv_heads (host array of Hkv entries, or NULL for
+ *   0 .. Hkv-1) names the cache head each of the drafter's Hkv KV heads reads; the drafter's
+ *   W_k, W_v and block K/V have Hkv heads, its queries Hq.  Hkv <= Hkv_cache <= 16 and every
+ *   entry in [0, Hkv_cache), else HSPEC_ERR_SHAPE / HSPEC_ERR_UNSUPPORTED.  The cache pools are
+ *   then [num_pages, page_size, Hkv_cache, D] and only the named heads are read.
  */
 typedef struct {
   int B, k, d_model, Hq, Hkv, D, page_size, max_pages, num_pages, window, split_tokens;
@@ -128,6 +135,8 @@ typedef struct {
   hspec_dtype dtype;
   float eps, scale;
   double rope_theta;
+  int Hkv_cache;
+  const int32_t* kv_heads;
 } hspec_attn_cfg;
 
 /*

@@ -290,7 +290,7 @@ def rope(x: np.ndarray, pos, theta: float) -> np.ndarray:
 
 def paged_attention(q, k_blk, v_blk, k_cache, v_cache, page_table, ctx_lens, *,
                     page_size: int, window: int = 0, block_causal: bool = False,
-                    scale: float | None = None, requests=None) -> np.ndarray:
+                    scale: float | None = None, requests=None, kv_heads=None) -> np.ndarray:
     """Block queries over the target's paged K/V (in place) plus the block's K/V.
 
     Sec. 3.3.2: the reused target KVs are the prefix context of the block;
@@ -298,8 +298,10 @@ def paged_attention(q, k_blk, v_blk, k_cache, v_cache, page_table, ctx_lens, *,
     cache keys i in [lo_j, L_b), lo_j = max(0, L_b + j - window + 1) when a
     sliding window is set, and block keys s in [0, k) (s <= j when
     ``block_causal``).  Query head hq reads KV head hq // (Hq / Hkv).
+    Partial target-KV-head reuse (Sec. 3.3.2 "KV dimension"; future work in Sec. 5): the
+    drafter's KV head h reads the target cache's head kv_heads[h] (default: head h).
     Naive softmax over the full score row (max subtracted).
-    q: [B, k, Hq, D]; k_blk, v_blk: [B, k, Hkv, D]; caches [pages, ps, Hkv, D].
+    q: [B, k, Hq, D]; k_blk, v_blk: [B, k, Hkv, D]; caches [pages, ps, Hkv_target, D].
     Returns o [B, k, Hq, D] (only rows of ``requests`` filled if given).
     """
     q, kb, vb = f64(q), f64(k_blk), f64(v_blk)
@@ -307,17 +309,20 @@ def paged_attention(q, k_blk, v_blk, k_cache, v_cache, page_table, ctx_lens, *,
     Hkv = kb.shape[2]
     g = Hq // Hkv
     scale = D ** -0.5 if scale is None else scale
-    kc = np.asarray(k_cache).reshape(-1, Hkv, D)
-    vc = np.asarray(v_cache).reshape(-1, Hkv, D)
+    Hc = np.asarray(k_cache).shape[-2]                              # KV heads of the target cache
+    kv_heads = list(range(Hkv)) if kv_heads is None or len(kv_heads) == 0 else list(kv_heads)
+    assert len(kv_heads) == Hkv and all(0 <= t < Hc for t in kv_heads)
+    kc = np.asarray(k_cache).reshape(-1, Hc, D)
+    vc = np.asarray(v_cache).reshape(-1, Hc, D)
     o = np.zeros((B, T, Hq, D))
     for b in (range(B) if requests is None else requests):
         L = int(ctx_lens[b])
         slots = gather_slots(page_table[b:b + 1], [L], page_size, L)[0]
-        Kc, Vc = f64(kc[slots]), f64(vc[slots])                     # [L, Hkv, D]
+        Kc, Vc = f64(kc[slots]), f64(vc[slots])                     # [L, Hc, D]
         for h in range(Hkv):
             heads = np.arange(h * g, (h + 1) * g)                   # the query heads of KV head h
-            Kh = np.ascontiguousarray(Kc[:, h, :])                  # [L, D]
-            Vh = np.ascontiguousarray(Vc[:, h, :])
+            Kh = np.ascontiguousarray(Kc[:, kv_heads[h], :])        # [L, D]: the target head it reuses
+            Vh = np.ascontiguousarray(Vc[:, kv_heads[h], :])
             for j in range(T):
                 pos = L + j
                 lo = max(0, pos - window + 1) if window > 0 else 0
@@ -352,7 +357,8 @@ def attention_layer(v, W, cache, cfg, return_parts: bool = False, requests=None)
     kb = rope(kb, pos, cfg.rope_theta)
     o = paged_attention(q, kb, vb, cache["k_cache"], cache["v_cache"], cache["page_table"],
                         cache["ctx_lens"], page_size=cfg.page_size, window=cfg.window,
-                        block_causal=cfg.block_causal, requests=requests)
+                        block_causal=cfg.block_causal, requests=requests,
+                        kv_heads=getattr(cfg, "kv_heads", None))
     out = o.reshape(Bsz, T, Hq * D) @ f64(W["W_o"]).T
     if return_parts:
         return out, dict(q=q, k_blk=kb, v_blk=vb, o=o)

@@ -138,6 +138,9 @@ hspec_status check_mamba(const hspec_mamba_cfg* c, const hspec_mamba_w* w, bool 
   return HSPEC_OK;
 }
 
+// KV heads per slot of the target cache.
+int cache_heads(const hspec_attn_cfg& c) { return c.Hkv_cache > 0 ? c.Hkv_cache : c.Hkv; }
+
 hspec_status check_attn_cfg(const hspec_attn_cfg* c, int max_ctx_len) {
   if (!c) return fail(HSPEC_ERR_NULL, "attention config is NULL");
   if (!dtype_ok(c->dtype)) return fail(HSPEC_ERR_DTYPE, "unknown dtype %d", (int)c->dtype);
@@ -150,6 +153,14 @@ hspec_status check_attn_cfg(const hspec_attn_cfg* c, int max_ctx_len) {
     return fail(HSPEC_ERR_UNSUPPORTED, "unknown attention flags 0x%x", c->flags);
   if (c->k * (c->Hq / c->Hkv) > 128)
     return fail(HSPEC_ERR_UNSUPPORTED, "k * Hq/Hkv must be <= 128, got %d", c->k * (c->Hq / c->Hkv));
+  if (c->Hkv_cache != 0 && (c->Hkv_cache < c->Hkv))
+    return fail(HSPEC_ERR_SHAPE, "Hkv_cache (%d) < Hkv (%d)", c->Hkv_cache, c->Hkv);
+  if (cache_heads(*c) > 16 && (c->kv_heads || c->Hkv_cache != 0))
+    return fail(HSPEC_ERR_UNSUPPORTED, "KV-head reuse supports at most 16 cache heads, got %d", cache_heads(*c));
+  if (c->kv_heads)
+    for (int i = 0; i < c->Hkv; ++i)
+      if (c->kv_heads[i] < 0 || c->kv_heads[i] >= cache_heads(*c))
+        return fail(HSPEC_ERR_SHAPE, "kv_heads[%d] = %d outside [0, %d)", i, c->kv_heads[i], cache_heads(*c));
   if (c->window < 0) return fail(HSPEC_ERR_SHAPE, "window < 0");
   if (c->window > 0 && c->k > c->window) return fail(HSPEC_ERR_SHAPE, "k > window");
   if (c->split_tokens < 0 || c->split_tokens % 64)
@@ -358,7 +369,7 @@ void plan_sweep(Arena& ar, const hspec_attn_cfg& c, int max_ctx_len, AttnPlan& p
     p.part_o = ar.take<float>(units * R * c.D);
     p.part_ml = ar.take<float>(units * R * 2);
   }
-  const size_t cache = (size_t)c.num_pages * c.page_size * c.Hkv * c.D;
+  const size_t cache = (size_t)c.num_pages * c.page_size * cache_heads(c) * c.D;
   p.kc = reserve_split(ar, c.dtype, cache);
   p.vc = reserve_split(ar, c.dtype, cache);
 }
@@ -400,6 +411,10 @@ hspec::AttnArgs sweep_args(const hspec_attn_cfg& c, const AttnPlan& p, const int
   hspec::AttnArgs a;
   a.page_table = pt; a.ctx_lens = lens;
   a.B = c.B; a.T = c.k; a.Hq = c.Hq; a.Hkv = c.Hkv; a.D = c.D; a.ps = c.page_size;
+  a.Hkv_cache = cache_heads(c);
+  a.kv_remap = c.kv_heads ? 1 : 0;   // (at most 16 cache heads then: checked)
+  a.kv_map = 0;
+  for (int h = 0; c.kv_heads && h < c.Hkv && h < 16; ++h) a.kv_map |= (unsigned long long)(c.kv_heads[h] & 15) << (4 * h);
   a.max_pages = c.max_pages; a.num_pages = c.num_pages; a.window = c.window;
   a.causal = (c.flags & HSPEC_BLOCK_CAUSAL) ? 1 : 0;
   a.block_in_sweep = (c.flags & HSPEC_ATTN_PRECISE_IO) ? 0 : 1;
@@ -1020,6 +1035,8 @@ HSPEC_API hspec_status hspec_kv_inject(const hspec_attn_cfg* cfg, int d_h, int n
                                        size_t ws_bytes, void* stream) {
   clear_err();
   if (hspec_status s = check_attn_cfg(cfg, 0)) return s;
+  if (cfg->kv_heads || (cfg->Hkv_cache != 0 && cfg->Hkv_cache != cfg->Hkv))
+    return fail(HSPEC_ERR_UNSUPPORTED, "KV injection writes the drafter's own caches: no KV-head subset");
   if (d_h <= 0 || n_layers < 1) return fail(HSPEC_ERR_SHAPE, "d_h and n_layers must be positive");
   if (d_h % 8) return fail(HSPEC_ERR_UNSUPPORTED, "d_h must be a multiple of 8");
   if (cfg->d_model <= 0 || cfg->d_model % 8) return fail(HSPEC_ERR_UNSUPPORTED, "d_model must be a positive multiple of 8");

@@ -139,6 +139,7 @@ attn_sweep(AttnArgs a) {
   if (item >= n_items) break;
   const int4 unit_e = *reinterpret_cast<const int4*>(a.units + 4 * (item / a.Hkv));
   const int b = unit_e.x >> 16, sp = unit_e.x & 0xffff, h = item % a.Hkv;
+  const int hc = a.kv_remap ? (int)((a.kv_map >> (4 * h)) & 15) : h;   // the cache head this KV head reads
   const int L = unit_e.y;   // validated by the work-list kernel
   const int qlen = unit_e.z, nsplit = unit_e.w;
   const int k0 = swept_lo(a, L) + sp * qlen;
@@ -202,7 +203,7 @@ attn_sweep(AttnArgs a) {
       if (cache) {
         key = key < k1 ? key : k0;
         const int slot_id = slot_in_page(pids[page_of(key, lps) - pg0], key, lps);
-        off = (size_t)slot_id * (a.Hkv * D) + (h * D + 8 * cl);
+        off = (size_t)slot_id * (a.Hkv_cache * D) + (hc * D + 8 * cl);
       } else {
         key = key < T ? key : 0;
         off = ((size_t)(b * T + key) * a.Hkv + h) * D + 8 * cl;

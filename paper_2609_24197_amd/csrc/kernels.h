@@ -48,6 +48,9 @@ struct AttnArgs {
   const int32_t* ctx_lens = nullptr;                  // [B]
   int B = 0, T = 0, Hq = 0, Hkv = 0, D = 0, ps = 0, max_pages = 0, num_pages = 0;
   int window = 0, causal = 0, max_ctx_len = 0, split = 0, max_splits = 0;
+  int Hkv_cache = 0;                  // KV heads per slot of the cache (>= Hkv)
+  int kv_remap = 0;                   // 1: drafter KV head h reads cache head kv_map[4h .. 4h+3], else h
+  unsigned long long kv_map = 0;
   int block_in_sweep = 1;     // 1: the sweep takes the block keys (bf16); 0: the reduction, in fp32
   float scale_log2 = 0.f;
   float* part_o = nullptr;    // [B*Hkv*max_splits, R, D]

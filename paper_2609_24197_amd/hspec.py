@@ -40,7 +40,7 @@ class AttnCfg(C.Structure):
     _fields_ = [(n, C.c_int) for n in ("B", "k", "d_model", "Hq", "Hkv", "D", "page_size", "max_pages",
                                         "num_pages", "window", "split_tokens")] + [
         ("flags", C.c_uint), ("dtype", C.c_int), ("eps", C.c_float), ("scale", C.c_float),
-        ("rope_theta", C.c_double)]
+        ("rope_theta", C.c_double), ("Hkv_cache", C.c_int), ("kv_heads", C.POINTER(C.c_int32))]
 
 
 class AttnW(C.Structure):
@@ -185,10 +185,14 @@ def mamba_cfg(cfg: I.StepConfig, W: dict | None = None) -> MambaCfg:
 
 
 def attn_cfg(cfg: I.StepConfig, max_pages: int, num_pages: int) -> AttnCfg:
-    return AttnCfg(cfg.B, cfg.k, cfg.d_model, cfg.Hq, cfg.Hkv, cfg.D, cfg.page_size, max_pages, num_pages,
-                   cfg.window, cfg.split_tokens,
-                   (BLOCK_CAUSAL if cfg.block_causal else 0) | (ATTN_PRECISE_IO if cfg.precise_io else 0), dtype_code(cfg),
-                   cfg.eps, 0.0, cfg.rope_theta)
+    c = AttnCfg(cfg.B, cfg.k, cfg.d_model, cfg.Hq, cfg.Hkv, cfg.D, cfg.page_size, max_pages, num_pages,
+                cfg.window, cfg.split_tokens,
+                (BLOCK_CAUSAL if cfg.block_causal else 0) | (ATTN_PRECISE_IO if cfg.precise_io else 0), dtype_code(cfg),
+                cfg.eps, 0.0, cfg.rope_theta, cfg.Hkv_target, None)
+    if cfg.kv_heads:   # partial target-KV-head reuse: the array lives as long as the config
+        c._kv_heads = (C.c_int32 * len(cfg.kv_heads))(*cfg.kv_heads)
+        c.kv_heads = C.cast(c._kv_heads, C.POINTER(C.c_int32))
+    return c
 
 
 def mamba_w(W: dict) -> MambaW:

@@ -48,7 +48,7 @@ class StepConfig:
     G: int            # B/C groups
     chunk: int        # SSD chunk length
     Hq: int           # query heads (= target's)
-    Hkv: int          # KV heads (= target's)
+    Hkv: int          # KV heads the drafter attends with (= target's, or a subset of them)
     D: int            # attention head dim
     lengths: str      # context-length recipe, see ``make_lengths``
     dtype: str = "bf16"   # storage dtype: "bf16" or "f32"
@@ -63,6 +63,8 @@ class StepConfig:
     ff: int = 0       # MLP hidden size of the full drafter, 0 = 3 * d_model
     r: int = 0        # fusion rank, 0 = d_model
     split_tokens: int = 0  # split-K size for the KV sweep, 0 = automatic
+    Hkv_target: int = 0    # KV heads per slot of the target cache, 0 = Hkv
+    kv_heads: tuple = ()   # target KV head read by each drafter KV head, () = 0 .. Hkv-1
 
     @property
     def d_h(self) -> int:
@@ -95,6 +97,14 @@ class StepConfig:
     @property
     def g(self) -> int:
         return self.Hq // self.Hkv
+
+    @property
+    def Hkv_cache(self) -> int:
+        return self.Hkv_target or self.Hkv
+
+    @property
+    def kv_map(self) -> tuple:
+        return tuple(self.kv_heads) if self.kv_heads else tuple(range(self.Hkv))
 
     def replace(self, **kw) -> "StepConfig":
         return dataclasses.replace(self, **kw)
@@ -252,8 +262,8 @@ def make_inputs(cfg: StepConfig, seed: int = 0, extra_pages: int = 0, pad_pages:
         "num_pages": num_pages,
         "h_last": normal("h_last", (cfg.B, cfg.d_h), 1.0, seed, cfg.dtype),
         "block_emb": normal("block_emb", (cfg.B, cfg.k, cfg.d_model), 1.0, seed, cfg.dtype),
-        "k_cache": normal("k_cache", (num_pages, cfg.page_size, cfg.Hkv, cfg.D), 1.0, seed, cfg.dtype),
-        "v_cache": normal("v_cache", (num_pages, cfg.page_size, cfg.Hkv, cfg.D), 1.0, seed, cfg.dtype),
+        "k_cache": normal("k_cache", (num_pages, cfg.page_size, cfg.Hkv_cache, cfg.D), 1.0, seed, cfg.dtype),
+        "v_cache": normal("v_cache", (num_pages, cfg.page_size, cfg.Hkv_cache, cfg.D), 1.0, seed, cfg.dtype),
     }
     return x
 

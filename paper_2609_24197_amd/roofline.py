@@ -25,7 +25,8 @@ def visible_ctx(cfg, L: int) -> int:
 def sweep_bytes(cfg, ctx_lens, elem_bytes: int = 2) -> int:
     """Algorithmic bytes of the target-KV attention (sweep and split reduction together).
 
-    Per visible context token: K and V rows of every KV head.  Per block position:
+    Per visible context token: K and V rows of every KV head the drafter reads (the reused
+    subset under partial target-KV-head reuse).  Per block position:
     its query heads, the block K/V, and the fp32 output row.  Split partials are not
     algorithmic bytes.
     """

@@ -142,6 +142,34 @@ def pin_page_permutation_invariance(O):
     assert np.array_equal(a, b)
 
 
+def pin_kv_head_subset(O):
+    """Partial target-KV-head reuse: reading heads `kv_heads` of a target cache equals reading
+    a cache that holds exactly those heads, in that order (brute-force slice); reading every
+    head in order is the plain path."""
+    r = rng0(33)
+    B, T, Hc, D, ps = 2, 3, 6, 8, 4
+    Ls = [9, 0]
+    Kd = [r.standard_normal((L, Hc, D)) for L in Ls]
+    Vd = [r.standard_normal((L, Hc, D)) for L in Ls]
+    kc, vc, table = _paged_from_dense(Kd, Vd, ps, r)
+    sel = [4, 1, 3]
+    g = 2
+    q = r.standard_normal((B, T, g * len(sel), D))
+    kb = r.standard_normal((B, T, len(sel), D))
+    vb = r.standard_normal((B, T, len(sel), D))
+    a = O.paged_attention(q, kb, vb, kc, vc, table, Ls, page_size=ps, kv_heads=sel)
+    kcs = np.ascontiguousarray(np.asarray(kc)[:, :, sel])
+    vcs = np.ascontiguousarray(np.asarray(vc)[:, :, sel])
+    b = O.paged_attention(q, kb, vb, kcs, vcs, table, Ls, page_size=ps)
+    assert np.allclose(a, b, rtol=1e-13, atol=1e-14)
+    q2 = r.standard_normal((B, T, g * Hc, D))
+    kb2 = r.standard_normal((B, T, Hc, D))
+    vb2 = r.standard_normal((B, T, Hc, D))
+    full = O.paged_attention(q2, kb2, vb2, kc, vc, table, Ls, page_size=ps)
+    same = O.paged_attention(q2, kb2, vb2, kc, vc, table, Ls, page_size=ps, kv_heads=list(range(Hc)))
+    assert np.array_equal(full, same)
+
+
 def pin_gather_slots(O):
     """P6: slots recover the logical order of a pool filled page by page; -1 past the length."""
     r = rng0(6)

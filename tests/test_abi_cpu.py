@@ -99,6 +99,11 @@ def test_attention_validation():
     assert call(_attn_cfg(max_pages=131073), maxL=2097153) == 4
     assert b"8192" in L.hspec_last_error()
     assert call(_attn_cfg(page_size=0)) == 2
+    # partial target-KV-head reuse: heads in range, cache heads >= Hkv, at most 16
+    sub = I.CONFIGS[3].replace(Hq=16, Hkv=4, Hkv_target=8, kv_heads=(0, 2, 9, 6))
+    assert call(hspec.attn_cfg(sub, 512, 20000)) == 2
+    assert call(hspec.attn_cfg(sub.replace(Hkv_target=3, kv_heads=()), 512, 20000)) == 2
+    assert call(hspec.attn_cfg(sub.replace(Hkv_target=32, kv_heads=(0, 8, 16, 24)), 512, 20000)) == 4
     assert call(_attn_cfg(dtype=9)) == 3
     assert call(_attn_cfg(), maxL=-1) == 2
     c = _attn_cfg()

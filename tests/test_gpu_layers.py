@@ -39,6 +39,9 @@ SMALL = {
     # hi/lo attention I/O, block keys in fp32 in the reduction (as in the whole drafter)
     "precise_io": I.StepConfig(name="s", B=3, k=16, d_model=512, H=8, P=64, N=128, G=1, chunk=16, Hq=32, Hkv=8,
                                D=128, lengths="list:300,0,77", precise_io=True),
+    # the drafter reuses 4 of the target's 8 KV heads (16 query heads)
+    "kv_subset": I.StepConfig(name="s", B=3, k=16, d_model=512, H=8, P=64, N=128, G=1, chunk=16, Hq=16, Hkv=4,
+                              D=128, lengths="list:300,0,77", Hkv_target=8, kv_heads=(0, 2, 4, 6)),
 }
 
 
@@ -158,3 +161,20 @@ def test_draft_step_full_config(num):
     worst = max(range(cfg.B), key=lambda b: float(np.max(np.abs(out[b] - ref[b]))))
     print(f"  worst request {worst} (length {int(L[worst])})", flush=True)
     assert_close(out, ref, f"config {num}")
+
+
+@pytest.mark.slow
+@pytest.mark.timeout(900)
+def test_draft_step_kv_subset_full():
+    """8b-serving-b64 with partial target-KV-head reuse: the drafter's 4 KV heads (16 query
+    heads) read heads 0, 2, 4, 6 of the target's 8-head cache; every request compared."""
+    cfg = I.CONFIGS[3].replace(Hq=16, Hkv=4, Hkv_target=8, kv_heads=(0, 2, 4, 6))
+    W = I.make_weights(cfg, 0)
+    x = I.make_inputs(cfg, 0)
+    Wd = dev(W)
+    Wd["W_dS_packed"] = hspec.pack_w_ds(Wd.pop("W_dS"), cfg.d_S, cfg.rank)
+    out, st = _draft(cfg, W, Wd, x)
+    assert st == 0
+    del Wd
+    ref = O.draft_step(W, x, cfg, progress=lambda s: print(f"  oracle: {s} done", flush=True))
+    assert_close(out, ref, "config 3, 4 of 8 KV heads")

@@ -92,7 +92,7 @@ def _run_attn(cfg, x, max_ctx_len=None, split=0):
 def _ref_attn(cfg, x):
     return O.paged_attention(x["q"], x["k_blk"], x["v_blk"], x["k_cache"], x["v_cache"], x["page_table"],
                              x["ctx_lens"], page_size=cfg.page_size, window=cfg.window,
-                             block_causal=cfg.block_causal)
+                             block_causal=cfg.block_causal, kv_heads=cfg.kv_heads)
 
 
 ATTN_CASES = {
@@ -111,6 +111,10 @@ ATTN_CASES = {
     "precise_empty_ctx": _small_attn_cfg(B=2, lengths="list:0,0", precise_io=True),
     "precise_d64_k7": _small_attn_cfg(Hq=4, Hkv=4, D=64, k=7, lengths="list:33,64,200", precise_io=True),
     "precise_f32": I.CONFIGS[1].replace(precise_io=True),
+    # partial target-KV-head reuse: 4 of the cache's 8 KV heads, in a shuffled order
+    "kv_subset": _small_attn_cfg(Hq=16, Hkv=4, Hkv_target=8, kv_heads=(6, 1, 3, 4), lengths="list:700,0,130"),
+    "kv_subset_precise": _small_attn_cfg(Hq=8, Hkv=2, Hkv_target=8, kv_heads=(7, 0), lengths="list:300,40,0",
+                                         precise_io=True),
 }
 
 

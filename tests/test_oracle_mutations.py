@@ -75,6 +75,7 @@ MUTATIONS = {
     "xBC_B_C_swapped": ("Bm = xBC[..., di:di + G * N].reshape(Bsz, T, G, N)\n    Cm = xBC[..., di + G * N:].reshape(Bsz, T, G, N)",
                         "Cm = xBC[..., di:di + G * N].reshape(Bsz, T, G, N)\n    Bm = xBC[..., di + G * N:].reshape(Bsz, T, G, N)"),
     "dt_before_xBC": ("dt = zxbcdt[..., 2 * di + 2 * G * N:]", "dt = zxbcdt[..., di:di + H]"),
+    "kv_subset_ignored": ("Kh = np.ascontiguousarray(Kc[:, kv_heads[h], :])", "Kh = np.ascontiguousarray(Kc[:, h, :])"),
     "chunk_decay_sign": ("decay = np.exp(lt[:, :, :, None] - lt[:, :, None, :])", "decay = np.exp(lt[:, :, None, :] - lt[:, :, :, None])"),
 }
 
