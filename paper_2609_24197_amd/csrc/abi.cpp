@@ -4,6 +4,7 @@
 
 #include <algorithm>
 #include <array>
+#include <climits>
 #include <cmath>
 #include <cstdarg>
 #include <initializer_list>
@@ -40,6 +41,13 @@ hspec_status fail(hspec_status s, const char* fmt, ...) {
 
 constexpr size_t ALIGN = 256;
 
+#ifdef HSPEC_HOST_SANITIZE
+}  // namespace
+// Host sanitizer build only: told every region cut from a caller's workspace.
+void hspec_host_carve(const void* p, size_t bytes);
+namespace {
+#endif
+
 // Bump allocator over the caller's workspace.  With base == nullptr it only measures.
 struct Arena {
   char* base = nullptr;
@@ -48,12 +56,16 @@ struct Arena {
   T* take(size_t count) {
     size_t o = (off + ALIGN - 1) / ALIGN * ALIGN;
     off = o + count * sizeof(T);
+#ifdef HSPEC_HOST_SANITIZE
+    if (base) hspec_host_carve(base + o, count * sizeof(T));
+#endif
     return base ? reinterpret_cast<T*>(base + o) : nullptr;
   }
   size_t size() const { return (off + ALIGN - 1) / ALIGN * ALIGN; }
 };
 
 bool is_f32(hspec_dtype d) { return d == HSPEC_F32; }
+long long ceil_div(long long a, long long b) { return (a + b - 1) / b; }
 bool dtype_ok(hspec_dtype d) { return d == HSPEC_BF16 || d == HSPEC_F32; }
 
 // A storage-dtype matrix as MFMA planes: bf16 storage is its own hi plane; fp32 storage is
@@ -169,16 +181,17 @@ hspec_status check_attn_cfg(const hspec_attn_cfg* c, int max_ctx_len) {
   if (c->B > 32767) return fail(HSPEC_ERR_UNSUPPORTED, "B must be <= 32767");
   if (c->page_size < 16 || (c->page_size & (c->page_size - 1)))
     return fail(HSPEC_ERR_UNSUPPORTED, "page_size must be a power of two >= 16, got %d", c->page_size);
-  if (c->split_tokens > 8192) return fail(HSPEC_ERR_UNSUPPORTED, "split_tokens must be <= 8192");
+  if (c->split_tokens > hspec::kMaxSplit)
+    return fail(HSPEC_ERR_UNSUPPORTED, "split_tokens must be <= %d", hspec::kMaxSplit);
   const int swept = hspec::attention_swept_len(max_ctx_len, c->window);
   const int split = c->split_tokens > 0 ? c->split_tokens : hspec::attention_default_split(c->B, c->Hkv, swept);
-  if (swept > 0 && (swept + split - 1) / split > 256)
+  if (swept > 0 && ceil_div(swept, split) > 256)
     return fail(HSPEC_ERR_UNSUPPORTED, "swept context / split_tokens gives more than 256 splits");
-  if ((long long)c->B * c->Hkv * (swept > 0 ? (swept + 63) / 64 : 1) > 0x7fffffffLL)
+  if ((long long)c->B * c->Hkv * (swept > 0 ? ceil_div(swept, 64) : 1) > 0x7fffffffLL)
     return fail(HSPEC_ERR_UNSUPPORTED, "B x Hkv x swept context is too large for the work list");
-  if (split > 8192)   // the sweep holds one split's page ids in a fixed LDS array
-    return fail(HSPEC_ERR_UNSUPPORTED, "swept context of %d keys needs splits above 8192 keys (at most 256 x 8192)",
-                swept);
+  if (split > hspec::kMaxSplit)   // the sweep holds one split's page ids in a fixed LDS array
+    return fail(HSPEC_ERR_UNSUPPORTED, "swept context of %d keys needs splits above %d keys (at most 256 x %d)",
+                swept, hspec::kMaxSplit, hspec::kMaxSplit);
   return HSPEC_OK;
 }
 
@@ -360,7 +373,9 @@ void plan_sweep(Arena& ar, const hspec_attn_cfg& c, int max_ctx_len, AttnPlan& p
   // attention_min_auto_split), so the buffers are sized for that many splits
   p.auto_split = c.split_tokens > 0 ? 0 : 1;
   p.min_split = p.auto_split ? hspec::attention_min_auto_split(p.split, swept) : p.split;
-  p.max_splits = swept > 0 ? (swept + p.min_split - 1) / p.min_split : 1;
+  // (a validated call has at most 256 splits; a query for any other config stays defined)
+  const long long ns = swept > 0 ? ceil_div(swept, p.min_split) : 1;
+  p.max_splits = (int)std::min<long long>(ns, INT_MAX);
   const int R = c.k * (c.Hq / c.Hkv);
   const size_t units = (size_t)c.B * c.Hkv * p.max_splits;
   p.units = ar.take<int32_t>((size_t)4 * c.B * p.max_splits);

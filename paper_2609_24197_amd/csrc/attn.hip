@@ -744,33 +744,10 @@ size_t attention_partials_bytes(int B, int Hkv, int max_splits, int R, int D) {
   return units * R * D * sizeof(float) + units * R * 2 * sizeof(float);
 }
 
-int attention_default_split(int B, int Hkv, int swept_len) {
-  // About 1024 (request, split, head) items of the longest requests: enough to fill every
-  // resident workgroup slot, few enough that split partials and unit start-up stay small.
-  long long want = ((long long)swept_len * B * Hkv + 1023) / 1024;
-  long long s = ((want + 63) / 64) * 64;
-  if (s < 256) s = 256;
-  long long cap = ((long long)(swept_len > 0 ? swept_len : 1) + 63) / 64 * 64;
-  if (s > cap) s = cap;
-  if (s > MAX_SPLIT) s = MAX_SPLIT;
-  const long long min_for_256 = ((long long)swept_len + 255) / 256;   // at most 256 splits
-  if (s < min_for_256) s = (min_for_256 + 63) / 64 * 64;
-  return (int)s;
-}
-
 int attention_sweep_grid(int D, int R, bool lo) {
   int grid = 0;
   const hipError_t e = with_sweep_variant(D, R, lo, [&](auto v) { return decltype(v)::slots(grid); });
   return e == hipSuccess ? grid : 0;
-}
-
-int attention_min_auto_split(int host_split, int swept_len) {
-  // down to two thirds of the host's split size, and never more than 256 splits
-  long long s = ((long long)host_split * 2 / 3 + 63) / 64 * 64;
-  const long long min_for_256 = ((long long)swept_len + 255) / 256;
-  if (s < min_for_256) s = (min_for_256 + 63) / 64 * 64;
-  if (s < 64) s = 64;
-  return (int)(s < host_split ? s : host_split);
 }
 
 hipError_t launch_attention_plan(const AttnArgs& a, int clear_words, hipStream_t s) {

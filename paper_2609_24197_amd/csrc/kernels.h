@@ -68,8 +68,6 @@ struct AttnArgs {
 // Persistent workgroups the KV sweep runs with on the current device (head dim D, R = k g
 // query rows per KV head, lo: fp32 storage); 0 if the shape has no sweep variant.
 int attention_sweep_grid(int D, int R, bool lo);
-// Smallest split size the work-list kernel may choose under automatic splitting.
-int attention_min_auto_split(int host_split, int swept_len);
 // Work list of the sweep (reads only B, ctx_lens, split and the table sizes of a); clears
 // status[0, clear_words) first.  Must precede launch_attention on the stream.
 hipError_t launch_attention_plan(const AttnArgs& a, int clear_words, hipStream_t s);
@@ -79,7 +77,31 @@ size_t attention_partials_bytes(int B, int Hkv, int max_splits, int R, int D);
 constexpr int kStatusWords = 64;   // int32 words reserved at the start of every workspace
 constexpr int kStatusClear = 4;    // cleared at the start of every call: status bits, work items, queue
 constexpr int kWorklistFusedMax = 512;   // requests up to which the work list rides in the RoPE launch
-int attention_default_split(int B, int Hkv, int swept_len);
+constexpr int kMaxSplit = 8192;          // cache keys per split (one split's page ids sit in LDS)
+// Split size (keys, multiple of 64) when the caller leaves it to the library: about 1024
+// (request, split, head) items over the longest requests, enough to fill every resident
+// workgroup slot, few enough that split partials and item start-up stay small; at most
+// kMaxSplit, and never more than 256 splits per request.
+inline int attention_default_split(int B, int Hkv, int swept_len) {
+  const long long want = ((long long)swept_len * B * Hkv + 1023) / 1024;
+  long long s = (want + 63) / 64 * 64;
+  if (s < 256) s = 256;
+  const long long cap = ((long long)(swept_len > 0 ? swept_len : 1) + 63) / 64 * 64;
+  if (s > cap) s = cap;
+  if (s > kMaxSplit) s = kMaxSplit;
+  const long long min_for_256 = ((long long)swept_len + 255) / 256;
+  if (s < min_for_256) s = (min_for_256 + 63) / 64 * 64;
+  return (int)s;
+}
+// Smallest split size the work-list kernel may choose under automatic splitting: two thirds
+// of the host's size, and never more than 256 splits.
+inline int attention_min_auto_split(int host_split, int swept_len) {
+  long long s = ((long long)host_split * 2 / 3 + 63) / 64 * 64;
+  const long long min_for_256 = ((long long)swept_len + 255) / 256;
+  if (s < min_for_256) s = (min_for_256 + 63) / 64 * 64;
+  if (s < 64) s = 64;
+  return (int)(s < host_split ? s : host_split);
+}
 // Longest run of cache positions the sweep reads for one request: max_ctx_len, or window - 1
 // under a sliding window (no query of the block sees an older position).
 inline int attention_swept_len(int max_ctx_len, int window) {

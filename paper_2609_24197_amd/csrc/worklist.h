@@ -9,7 +9,7 @@
 
 namespace hspec {
 
-constexpr int MAX_SPLIT = 8192;   // keys per split (host-enforced by the config check)
+constexpr int MAX_SPLIT = kMaxSplit;   // keys per split (host-enforced by the config check)
 constexpr int WL_THREADS = 256;   // threads of a workgroup that builds the list
 constexpr int WL_NCAND = 16;      // split sizes tried under automatic splitting
 
