@@ -77,7 +77,7 @@ enum { HSPEC_DEV_BAD_PAGE = 1, HSPEC_DEV_BAD_CTX_LEN = 2, HSPEC_DEV_BAD_TOKEN = 
  *   chunk = SSD chunk length (1..16), conv_w = causal conv width (1..8), eps of every RMSNorm.
  *   d_inner = H*P, d_S = H*P*N.  d_h, r, d_model must be multiples of 8.
  *   flags: HSPEC_W_DS_PACKED when hspec_mamba_w.W_dS points at the packed layout written by
- *   hspec_pack_w_ds (bf16 storage, r a multiple of 64), else 0.
+ *   hspec_pack_w_ds (bf16 storage, r a multiple of 64); HSPEC_MAMBA_PRECISE_IO (below).
  */
 typedef struct {
   int B, k, d_model, d_h, r, H, P, N, G, chunk, conv_w;
@@ -87,7 +87,14 @@ typedef struct {
 } hspec_mamba_cfg;
 
 /* hspec_mamba_cfg.flags */
-enum { HSPEC_W_DS_PACKED = 1u << 0 };
+enum {
+  HSPEC_W_DS_PACKED = 1u << 0,
+  HSPEC_MAMBA_PRECISE_IO = 1u << 1 /* with bf16 storage, the Mamba layer's normalised input enters
+                                      W_in, and its gated-norm output enters W_out, as bf16 hi/lo
+                                      planes (two products each) instead of one bf16 plane, as fp32
+                                      storage always does: for stacks of layers
+                                      (hspec_drafter_forward sets it) */
+};
 
 /*
  * Mamba weights.  Matrices are [out, in] row-major in the storage dtype:

@@ -133,7 +133,8 @@ hspec_status check_mamba(const hspec_mamba_cfg* c, const hspec_mamba_w* w, bool 
   if (c->N != 16 && c->N != 32 && c->N != 64 && c->N != 128)
     return fail(HSPEC_ERR_UNSUPPORTED, "N (d_state) must be 16, 32, 64 or 128, got %d", c->N);
   if (c->d_h % 8 || c->r % 8) return fail(HSPEC_ERR_UNSUPPORTED, "d_h and r must be multiples of 8");
-  if (c->flags & ~(unsigned)HSPEC_W_DS_PACKED) return fail(HSPEC_ERR_UNSUPPORTED, "unknown mamba flags 0x%x", c->flags);
+  if (c->flags & ~(unsigned)(HSPEC_W_DS_PACKED | HSPEC_MAMBA_PRECISE_IO))
+    return fail(HSPEC_ERR_UNSUPPORTED, "unknown mamba flags 0x%x", c->flags);
   if ((c->flags & HSPEC_W_DS_PACKED) && (is_f32(c->dtype) || c->r % 64))
     return fail(HSPEC_ERR_UNSUPPORTED, "a packed W_dS needs bf16 storage and r %% 64 == 0");
   if (!w->W_r || !w->W_dS) return fail(HSPEC_ERR_NULL, "W_r or W_dS is NULL");
@@ -279,14 +280,19 @@ struct MambaPlan {
   GemmScratch gs;
 };
 
+// Whether the Mamba projections take their activations as hi/lo planes (fp32 storage, or
+// HSPEC_MAMBA_PRECISE_IO) or as one bf16 plane.
+bool mamba_io_lo(const hspec_mamba_cfg& c) { return is_f32(c.dtype) || (c.flags & HSPEC_MAMBA_PRECISE_IO); }
+
 void plan_mamba(Arena& ar, const hspec_mamba_cfg& c, bool u_norm, MambaPlan& p) {
   plan_state(ar, c, true, p.st);
   const size_t M = (size_t)c.B * c.k;
   const size_t di = (size_t)c.H * c.P, gn = (size_t)c.G * c.N;
   const size_t dproj = 2 * di + 2 * gn + c.H;
+  const bool io_lo = mamba_io_lo(c);
   if (u_norm) {
     p.u_hi = ar.take<bf16>(M * c.d_model);
-    p.u_lo = ar.take<bf16>(M * c.d_model);
+    if (io_lo) p.u_lo = ar.take<bf16>(M * c.d_model);
   } else {
     p.u_in = reserve_split(ar, c.dtype, M * c.d_model);
   }
@@ -302,7 +308,7 @@ void plan_mamba(Arena& ar, const hspec_mamba_cfg& c, bool u_norm, MambaPlan& p) 
   p.dt = ar.take<float>(M * c.H);
   p.y = ar.take<float>(M * di);
   p.yn_hi = ar.take<bf16>(M * di);
-  p.yn_lo = ar.take<bf16>(M * di);
+  if (io_lo) p.yn_lo = ar.take<bf16>(M * di);
   p.gs = reserve_gemm(ar, c.dtype, {{(int)M, (int)dproj, c.d_model}, {(int)M, c.d_model, (int)di}});
 }
 
@@ -900,12 +906,14 @@ hspec_status run_mlp(const hspec_mamba_cfg& c, const hspec_layer_w& L, int ff, P
 HSPEC_API size_t hspec_drafter_forward_workspace(const hspec_mamba_cfg* mcfg, const hspec_attn_cfg* acfg, int ff,
                                                  int max_ctx_len) {
   if (!mcfg || !acfg || ff <= 0) return 0;
+  hspec_mamba_cfg mc = *mcfg;
+  mc.flags |= HSPEC_MAMBA_PRECISE_IO;
   hspec_attn_cfg ac = *acfg;
   ac.flags |= HSPEC_ATTN_PRECISE_IO;
   Arena ar;
   status_word(ar);
   ForwardPlan p;
-  plan_forward(ar, *mcfg, ac, ff, max_ctx_len < 0 ? 0 : max_ctx_len, p);
+  plan_forward(ar, mc, ac, ff, max_ctx_len < 0 ? 0 : max_ctx_len, p);
   return ar.size();
 }
 
@@ -950,9 +958,11 @@ HSPEC_API hspec_status hspec_drafter_forward(const hspec_mamba_cfg* mcfg, const 
   if (hspec_status s = check_ws(workspace, ws_bytes, hspec_drafter_forward_workspace(mcfg, acfg, ff, max_ctx_len)))
     return s;
   hipStream_t st = (hipStream_t)stream;
-  const hspec_mamba_cfg& mc = *mcfg;
+  // the layers' errors add up over the stack: activations enter every projection as hi/lo planes
+  hspec_mamba_cfg mc = *mcfg;
+  mc.flags |= HSPEC_MAMBA_PRECISE_IO;
   hspec_attn_cfg ac = *acfg;
-  ac.flags |= HSPEC_ATTN_PRECISE_IO;   // the layers' attention errors add up over the stack
+  ac.flags |= HSPEC_ATTN_PRECISE_IO;
   Arena ar{(char*)workspace};
   int* status = status_word(ar);
   ForwardPlan p;

@@ -21,6 +21,7 @@ BF16, F32 = 0, 1
 BLOCK_CAUSAL = 1
 ATTN_PRECISE_IO = 2
 W_DS_PACKED = 1
+MAMBA_PRECISE_IO = 2
 DEV_BAD_PAGE, DEV_BAD_CTX_LEN, DEV_BAD_TOKEN, DEV_NONFINITE = 1, 2, 4, 8
 STATUS = {0: "HSPEC_OK", 1: "HSPEC_ERR_NULL", 2: "HSPEC_ERR_SHAPE", 3: "HSPEC_ERR_DTYPE",
           4: "HSPEC_ERR_UNSUPPORTED", 5: "HSPEC_ERR_WORKSPACE", 6: "HSPEC_ERR_LAUNCH"}
@@ -178,8 +179,10 @@ def dtype_code(cfg: I.StepConfig) -> int:
 
 
 def mamba_cfg(cfg: I.StepConfig, W: dict | None = None) -> MambaCfg:
-    """The Mamba config; W_DS_PACKED is set when W carries "W_dS_packed" (see pack_w_ds)."""
+    """The Mamba config; W_DS_PACKED is set when W carries "W_dS_packed" (see pack_w_ds), and
+    MAMBA_PRECISE_IO with the config's precise_io."""
     flags = W_DS_PACKED if W is not None and W.get("W_dS_packed") is not None else 0
+    flags |= MAMBA_PRECISE_IO if cfg.precise_io else 0
     return MambaCfg(cfg.B, cfg.k, cfg.d_model, cfg.d_h, cfg.rank, cfg.H, cfg.P, cfg.N, cfg.G, cfg.chunk,
                     cfg.conv_w, flags, dtype_code(cfg), cfg.eps)
 

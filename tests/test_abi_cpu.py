@@ -253,7 +253,7 @@ def test_packed_w_ds_validation():
     def state(mc):
         return L.hspec_state_init(C.byref(mc), C.byref(mw), FAKE, S0, ws, n, None)
     mc = hspec.mamba_cfg(cfg)
-    mc.flags = 2
+    mc.flags = 4
     assert state(mc) == 4
     mc = hspec.mamba_cfg(cfg.replace(dtype="f32"))
     mc.flags = hspec.W_DS_PACKED
