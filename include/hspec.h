@@ -77,7 +77,8 @@ enum { HSPEC_DEV_BAD_PAGE = 1, HSPEC_DEV_BAD_CTX_LEN = 2, HSPEC_DEV_BAD_TOKEN = 
  *   chunk = SSD chunk length (1..16), conv_w = causal conv width (1..8), eps of every RMSNorm.
  *   d_inner = H*P, d_S = H*P*N.  d_h, r, d_model must be multiples of 8.
  *   flags: HSPEC_W_DS_PACKED when hspec_mamba_w.W_dS points at the packed layout written by
- *   hspec_pack_w_ds (bf16 storage, r a multiple of 64); HSPEC_MAMBA_PRECISE_IO (below).
+ *   hspec_pack_w_ds (bf16 storage, r a multiple of 64, d_h a multiple of 32);
+ *   HSPEC_MAMBA_PRECISE_IO (below).
  */
 typedef struct {
   int B, k, d_model, d_h, r, H, P, N, G, chunk, conv_w;
@@ -92,8 +93,9 @@ enum {
   HSPEC_MAMBA_PRECISE_IO = 1u << 1 /* with bf16 storage, the Mamba layer's normalised input enters
                                       W_in, and its gated-norm output enters W_out, as bf16 hi/lo
                                       planes (two products each) instead of one bf16 plane, as fp32
-                                      storage always does: for stacks of layers
-                                      (hspec_drafter_forward sets it) */
+                                      storage always does, and F = W_r h_last enters a packed W_dS
+                                      as fp16 hi/lo planes instead of one fp16 plane: for stacks of
+                                      layers (hspec_drafter_forward sets it) */
 };
 
 /*
@@ -296,7 +298,10 @@ size_t hspec_draft_head_workspace(const hspec_head_cfg* cfg);
  * step; this layout lets every wave read whole 1 KB blocks that are already MFMA operand
  * fragments.  Block (s, t) holds rows 16t..16t+15 and columns 32s..32s+31 of W_dS and
  * starts at byte ((s * d_S/16) + t) * 1024; inside it, the 8 consecutive columns
- * 32s + 8c .. +7 of row 16t + i are the 16 bytes at (i + 16c) * 16.
+ * 32s + 8c .. +7 of row 16t + i are the 16 bytes at (i + 16c) * 16.  Every element is the
+ * fp16 value of 256 x W_dS (exact for bf16 weights of magnitude 2^-25 .. 255; the projection
+ * divides the 256 back out), so that the projection runs as one fp16 product with F as one
+ * fp16 plane (hi/lo fp16 planes with HSPEC_MAMBA_PRECISE_IO).
  * W_dS [d_S, r] row-major bf16 in, W_packed (hspec_pack_w_ds_bytes bytes) out, both device
  * memory; d_S % 16 == 0 and r % 64 == 0, else HSPEC_ERR_UNSUPPORTED.  Asynchronous on stream.
  */

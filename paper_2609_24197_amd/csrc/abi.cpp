@@ -135,8 +135,8 @@ hspec_status check_mamba(const hspec_mamba_cfg* c, const hspec_mamba_w* w, bool 
   if (c->d_h % 8 || c->r % 8) return fail(HSPEC_ERR_UNSUPPORTED, "d_h and r must be multiples of 8");
   if (c->flags & ~(unsigned)(HSPEC_W_DS_PACKED | HSPEC_MAMBA_PRECISE_IO))
     return fail(HSPEC_ERR_UNSUPPORTED, "unknown mamba flags 0x%x", c->flags);
-  if ((c->flags & HSPEC_W_DS_PACKED) && (is_f32(c->dtype) || c->r % 64))
-    return fail(HSPEC_ERR_UNSUPPORTED, "a packed W_dS needs bf16 storage and r %% 64 == 0");
+  if ((c->flags & HSPEC_W_DS_PACKED) && (is_f32(c->dtype) || c->r % 64 || c->d_h % 32))
+    return fail(HSPEC_ERR_UNSUPPORTED, "a packed W_dS needs bf16 storage, r %% 64 == 0 and d_h %% 32 == 0");
   if (!w->W_r || !w->W_dS) return fail(HSPEC_ERR_NULL, "W_r or W_dS is NULL");
   if (!full) return HSPEC_OK;
   if (c->k <= 0 || c->d_model <= 0 || c->G <= 0 || c->chunk <= 0 || c->conv_w <= 0)
@@ -213,10 +213,16 @@ hspec_status check_ws(void* ws, size_t have, size_t need) {
 
 // ---------------------------------------------------------------------- layout + launch
 
+// F enters Proj_dS with the packed (fp16) W_dS as fp16 planes of F x 2^-kFScaleLog2, which
+// Proj_r writes directly: finite for |F| < 65504 x 64 (about 4e6), full fp16 precision down to
+// |F| = 2^-8, and an absolute error under 2^-19 below that.
+constexpr int kFScaleLog2 = 6;
+
 struct StatePlan {
   SplitSlot h, wr, wds;
   GemmScratch gs;
-  bf16 *F_hi = nullptr, *F_lo = nullptr;
+  bf16 *F_hi = nullptr, *F_lo = nullptr;        // bf16 planes of F (unpacked W_dS)
+  _Float16 *F_h16 = nullptr, *F_l16 = nullptr;  // fp16 planes of F (packed W_dS; l16 only precise)
   bf16 *S0_hi = nullptr, *S0_lo = nullptr;
   _Float16* S0_h16 = nullptr;
 };
@@ -226,8 +232,14 @@ void plan_state(Arena& ar, const hspec_mamba_cfg& c, bool s0_planes, StatePlan& 
   p.h = reserve_split(ar, c.dtype, (size_t)c.B * c.d_h);
   p.wr = reserve_split(ar, c.dtype, (size_t)c.r * c.d_h);
   p.wds = reserve_split(ar, c.dtype, dS * c.r);
-  p.F_hi = ar.take<bf16>((size_t)c.B * c.r);
-  p.F_lo = ar.take<bf16>((size_t)c.B * c.r);
+  if (c.flags & HSPEC_W_DS_PACKED) {
+    // one fp16 plane (11 significant bits), or hi/lo fp16 planes with HSPEC_MAMBA_PRECISE_IO
+    p.F_h16 = ar.take<_Float16>((size_t)c.B * c.r);
+    if (c.flags & HSPEC_MAMBA_PRECISE_IO) p.F_l16 = ar.take<_Float16>((size_t)c.B * c.r);
+  } else {
+    p.F_hi = ar.take<bf16>((size_t)c.B * c.r);
+    p.F_lo = ar.take<bf16>((size_t)c.B * c.r);
+  }
   p.gs = reserve_gemm(ar, c.dtype, {{c.B, c.r, c.d_h}, {c.B, (int)dS, c.r}});
   if (s0_planes) {
     // S0 only feeds the scan: one fp16 plane (11 significant bits, half the bytes of hi/lo
@@ -241,7 +253,8 @@ void plan_state(Arena& ar, const hspec_mamba_cfg& c, bool s0_planes, StatePlan& 
   }
 }
 
-// F = W_r h_last (bf16 planes), then S0 = W_dS F (fp32 and/or bf16 planes).
+// F = W_r h_last (bf16 planes, or fp16 planes for the packed W_dS), then S0 = W_dS F (fp32,
+// bf16 planes and/or one fp16 plane).
 hspec_status run_state(const hspec_mamba_cfg& c, const hspec_mamba_w& w, const void* h_last, const StatePlan& p,
                        float* S0_f32, hipStream_t st) {
   Planes h, wr, wds;
@@ -253,11 +266,18 @@ hspec_status run_state(const hspec_mamba_cfg& c, const hspec_mamba_w& w, const v
   g1.W_hi = wr.hi; g1.W_lo = wr.lo; g1.ldw = c.d_h;
   g1.M = c.B; g1.N = c.r; g1.K = c.d_h;
   g1.C_hi = p.F_hi; g1.C_lo = p.F_lo; g1.ldch = c.r;
+  g1.C_h16 = p.F_h16; g1.C_l16 = p.F_l16; g1.h16_scale = 1.f / (1 << kFScaleLog2);
   use_scratch(g1, p.gs);
   HIP_TRY(hspec::launch_gemm(g1, st));
   const int dS = c.H * c.P * c.N;
   hspec::GemmArgs g2;
   g2.A_hi = p.F_hi; g2.A_lo = p.F_lo; g2.lda = c.r;
+  if (p.F_h16) {   // fp16 product with the packed W_dS (x 2^kPackScaleLog2), F x 2^-kFScaleLog2
+    g2.A_hi = reinterpret_cast<const bf16*>(p.F_h16);
+    g2.A_lo = reinterpret_cast<const bf16*>(p.F_l16);
+    g2.f16 = 1;
+    g2.out_scale = (float)(1 << kFScaleLog2) / (float)(1 << hspec::kPackScaleLog2);
+  }
   g2.W_hi = wds.hi; g2.W_lo = wds.lo; g2.ldw = c.r;
   g2.M = c.B; g2.N = dS; g2.K = c.r;
   g2.C = S0_f32; g2.ldc = dS;
@@ -1209,7 +1229,7 @@ HSPEC_API hspec_status hspec_pack_w_ds(int d_S, int r, const void* W_dS, void* W
   if (d_S <= 0 || r <= 0) return fail(HSPEC_ERR_SHAPE, "non-positive W_dS dimension");
   if (d_S % 16 || r % 64) return fail(HSPEC_ERR_UNSUPPORTED, "packing needs d_S %% 16 == 0 and r %% 64 == 0");
   if (!W_dS || !W_packed) return fail(HSPEC_ERR_NULL, "W_dS or W_packed is NULL");
-  HIP_TRY(hspec::launch_pack_w(static_cast<const bf16*>(W_dS), d_S, r, static_cast<bf16*>(W_packed),
+  HIP_TRY(hspec::launch_pack_w(static_cast<const bf16*>(W_dS), d_S, r, static_cast<_Float16*>(W_packed),
                                (hipStream_t)stream));
   return HSPEC_OK;
 }

@@ -21,7 +21,11 @@
 // A weight read this way touches each 128-byte line in two halves a k-step apart, which caps
 // HBM efficiency; the packed layout (launch_pack_w) stores every 16x32 operand fragment as
 // one contiguous 1 KB block, k-step-major, so that the whole grid sweeps W in address order
-// with non-temporal loads.
+// with non-temporal loads.  The packed W holds fp16 values (scaled by a power of two so that
+// every bf16 weight converts exactly) and is multiplied with fp16 A planes by
+// v_mfma_f32_16x16x32_f16: one fp16 plane of an activation carries 11 significant bits where
+// a bf16 plane carries 8, so one product does what a bf16 hi/lo pair would otherwise be needed
+// for.  More than 128 rows run as 128-row launches, one after the other.
 #include <algorithm>
 #include <utility>
 
@@ -385,8 +389,14 @@ skinny_kernel(GemmArgs g, int kper, int nitems) {
         for (int t = 0; t < MT; ++t)
 #pragma unroll
           for (int j = 0; j < NTW; ++j) {
-            acc[t][j] = mma16(fa[t], wr[ks % SK_P][j], acc[t][j]);
-            if constexpr (ALO) acc[t][j] = mma16(fl[t], wr[ks % SK_P][j], acc[t][j]);
+            if constexpr (PK) {   // fp16 operands (the packed layout)
+              const f16x8 w16 = __builtin_bit_cast(f16x8, wr[ks % SK_P][j]);
+              acc[t][j] = mma16h(__builtin_bit_cast(f16x8, fa[t]), w16, acc[t][j]);
+              if constexpr (ALO) acc[t][j] = mma16h(__builtin_bit_cast(f16x8, fl[t]), w16, acc[t][j]);
+            } else {
+              acc[t][j] = mma16(fa[t], wr[ks % SK_P][j], acc[t][j]);
+              if constexpr (ALO) acc[t][j] = mma16(fl[t], wr[ks % SK_P][j], acc[t][j]);
+            }
           }
         load_w_next(wr[ks % SK_P]);
         __builtin_amdgcn_sched_barrier(0);   // keep each step's refill behind its own MFMAs
@@ -412,6 +422,9 @@ skinny_kernel(GemmArgs g, int kper, int nitems) {
         buf(g.C_lo ? g.C_lo + min(n0, g.N) : nullptr, !split && g.C_lo && cols ? (rows_span * g.ldch + cols) * 2 : 0);
     const __amdgpu_buffer_rsrc_t r_h16 =
         buf(g.C_h16 ? g.C_h16 + min(n0, g.N) : nullptr, !split && g.C_h16 && cols ? (rows_span * g.ldch + cols) * 2 : 0);
+    const __amdgpu_buffer_rsrc_t r_l16 =
+        buf(g.C_l16 ? g.C_l16 + min(n0, g.N) : nullptr, !split && g.C_l16 && cols ? (rows_span * g.ldch + cols) * 2 : 0);
+    const float osc = split ? 1.f : g.out_scale;   // split partials are scaled by the reduction
     // residual R (RES: present and not split-K): one of the two loads reads, the other is empty
     const bool rf = RES && !g.r_bf16, rb = RES && g.r_bf16;
     [[maybe_unused]] const __amdgpu_buffer_rsrc_t r_rf =
@@ -429,7 +442,7 @@ skinny_kernel(GemmArgs g, int kper, int nitems) {
         const int r = pass * RPP + lr;
         const int m = 16 * t + r;
         const bool ok = lane < LPR * RPP && m < g.M && c4 < cols;
-        f32x4 v = *reinterpret_cast<const f32x4*>(stg + r * S::PITCH + c4);
+        f32x4 v = *reinterpret_cast<const f32x4*>(stg + r * S::PITCH + c4) * osc;
         if constexpr (RES) {
           const int o4 = ok ? (m * g.ldr + c4) * 4 : SK_OOB;
           const int o2 = ok ? (m * g.ldr + c4) * 2 : SK_OOB;
@@ -450,8 +463,15 @@ skinny_kernel(GemmArgs g, int kper, int nitems) {
         __builtin_amdgcn_raw_buffer_store_b128(vb, r_c, ok ? (m * g.ldc + c4) * 4 : SK_OOB, 0, 16);
         __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2u32, h), r_hi, ok ? (m * g.ldch + c4) * 2 : SK_OOB, 0, 16);
         __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2u32, l), r_lo, ok ? (m * g.ldch + c4) * 2 : SK_OOB, 0, 16);
-        const f16x4 v16 = {(_Float16)v[0], (_Float16)v[1], (_Float16)v[2], (_Float16)v[3]};
+        f16x4 v16, l16;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float sv = v[e] * g.h16_scale;
+          v16[e] = (_Float16)sv;
+          l16[e] = (_Float16)(sv - (float)v16[e]);
+        }
         __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2u32, v16), r_h16, ok ? (m * g.ldch + c4) * 2 : SK_OOB, 0, 16);
+        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2u32, l16), r_l16, ok ? (m * g.ldch + c4) * 2 : SK_OOB, 0, 16);
       }
     }
   }
@@ -464,6 +484,7 @@ __global__ void __launch_bounds__(256) skinny_reduce(GemmArgs g, int nparts) {
     const int m = (int)(e / g.N), n = (int)(e % g.N);
     float v = 0.f;
     for (int p = 0; p < nparts; ++p) v += g.part[(size_t)p * total + e];
+    v *= g.out_scale;
     if (g.R) {
       v += g.r_bf16 ? bf2f(reinterpret_cast<const bf16*>(g.R)[(size_t)m * g.ldr + n])
                     : reinterpret_cast<const float*>(g.R)[(size_t)m * g.ldr + n];
@@ -474,7 +495,12 @@ __global__ void __launch_bounds__(256) skinny_reduce(GemmArgs g, int nparts) {
       g.C_hi[(size_t)m * g.ldch + n] = h;
       if (g.C_lo) g.C_lo[(size_t)m * g.ldch + n] = f2bf(v - bf2f(h));
     }
-    if (g.C_h16) g.C_h16[(size_t)m * g.ldch + n] = (_Float16)v;
+    if (g.C_h16) {
+      const float sv = v * g.h16_scale;
+      const _Float16 h = (_Float16)sv;
+      g.C_h16[(size_t)m * g.ldch + n] = h;
+      if (g.C_l16) g.C_l16[(size_t)m * g.ldch + n] = (_Float16)(sv - (float)h);
+    }
   }
 }
 
@@ -496,6 +522,7 @@ __global__ void __launch_bounds__(256) skinny_reduce4(GemmArgs g, int nparts) {
 #pragma unroll
       for (int k = 0; k < GROUP; ++k) v += part[k];   // absent parts add +0
     }
+    v *= g.out_scale;
     if (g.R) {
       if (g.r_bf16) {
         const bf16x4 r = *reinterpret_cast<const bf16x4*>(reinterpret_cast<const bf16*>(g.R) + (size_t)m * g.ldr + n);
@@ -516,9 +543,17 @@ __global__ void __launch_bounds__(256) skinny_reduce4(GemmArgs g, int nparts) {
       *reinterpret_cast<bf16x4*>(g.C_hi + (size_t)m * g.ldch + n) = h;
       if (g.C_lo) *reinterpret_cast<bf16x4*>(g.C_lo + (size_t)m * g.ldch + n) = l;
     }
-    if (g.C_h16)
-      *reinterpret_cast<f16x4*>(g.C_h16 + (size_t)m * g.ldch + n) =
-          f16x4{(_Float16)v[0], (_Float16)v[1], (_Float16)v[2], (_Float16)v[3]};
+    if (g.C_h16) {
+      f16x4 h, l;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float sv = v[i] * g.h16_scale;
+        h[i] = (_Float16)sv;
+        l[i] = (_Float16)(sv - (float)h[i]);
+      }
+      *reinterpret_cast<f16x4*>(g.C_h16 + (size_t)m * g.ldch + n) = h;
+      if (g.C_l16) *reinterpret_cast<f16x4*>(g.C_l16 + (size_t)m * g.ldch + n) = l;
+    }
   }
 }
 
@@ -727,11 +762,9 @@ __global__ void __launch_bounds__(256) gemm_dma_kernel(GemmArgs g) {
     const int u = (i * 4 + wave) * 64 + lane, row = u / C::CPRT;
     const int k = 8 * ((u % C::CPRT) ^ swz_key_t<KT>(row));
     const int n = n0 + min(row, rows_w - 1);
-    // packed W: 1 KB fragment (k-step k / 32, 16-row tile n / 16), piece (n % 16) + 16 (k % 32) / 8
-    w_off[i] = g.w_packed ? ((((size_t)(k >> 5) * (g.N >> 4) + (n >> 4)) * 64 + (n & 15) + 16 * ((k & 31) >> 3)) * 8)
-                          : (size_t)(n - wseg0) * g.ldw + k;
+    w_off[i] = (size_t)(n - wseg0) * g.ldw + k;
   }
-  const size_t w_step = g.w_packed ? (size_t)(KT / 32) * (g.N >> 4) * 512 : (size_t)KT;
+  const size_t w_step = (size_t)KT;
   auto issue = [&](int t, bf16* L, bf16* LW) {
     const size_t ka = (size_t)t * KT, kw = (size_t)t * w_step;
 #pragma unroll
@@ -1235,7 +1268,7 @@ hipError_t launch_cfg(const GemmArgs& g, hipStream_t s) {
   return launch_one<WM, WN, TM, TN, true, true>(g, s);
 }
 
-__global__ void __launch_bounds__(256) pack_w_kernel(const bf16* __restrict__ W, int N, int K, bf16* __restrict__ Wp) {
+__global__ void __launch_bounds__(256) pack_w_kernel(const bf16* __restrict__ W, int N, int K, _Float16* __restrict__ Wp) {
   // one 16-byte piece (row n, columns 8q..8q+7) per thread and iteration
   const int qr = K / 8, ntile = N / 16;
   const size_t total = (size_t)N * qr;
@@ -1243,13 +1276,23 @@ __global__ void __launch_bounds__(256) pack_w_kernel(const bf16* __restrict__ W,
     const int n = (int)(e / qr), q = (int)(e % qr);
     const int st = q / 4, c = q % 4, t = n / 16, i = n % 16;
     const size_t dst = (((size_t)st * ntile + t) * 64 + i + 16 * c) * 8;
-    *reinterpret_cast<bf16x8*>(Wp + dst) = ld8(W + (size_t)n * K + 8 * q);
+    const u32x4 w = *reinterpret_cast<const u32x4*>(W + (size_t)n * K + 8 * q);
+    f16x8 h;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      // fp32 of the bf16 with its exponent raised by kPackScaleLog2 (bit arithmetic, so the scale
+      // cannot be moved past the rounding to fp16; zeros and bf16 subnormals become +-0)
+      uint32_t b = ((w[e / 2] >> (16 * (e % 2))) & 0xffffu) << 16;
+      b = (b & 0x7f800000u) ? b + ((uint32_t)kPackScaleLog2 << 23) : (b & 0x80000000u);
+      h[e] = (_Float16)__uint_as_float(b);
+    }
+    *reinterpret_cast<f16x8*>(Wp + dst) = h;
   }
 }
 
 }  // namespace
 
-hipError_t launch_pack_w(const bf16* W, int N, int K, bf16* Wp, hipStream_t s) {
+hipError_t launch_pack_w(const bf16* W, int N, int K, _Float16* Wp, hipStream_t s) {
   if (N % 16 || K % SK_STEP || N <= 0 || K <= 0) return hipErrorInvalidValue;
   const size_t total = (size_t)N * (K / 8);
   size_t blocks = (total + 255) / 256;
@@ -1259,12 +1302,14 @@ hipError_t launch_pack_w(const bf16* W, int N, int K, bf16* Wp, hipStream_t s) {
 }
 
 bool gemm_f16_out_ok(int M, int N, int K) {
-  return skinny_plan(M, N, K, false, 256).use && N % 4 == 0;   // the weight-streaming conditions (any CU count)
+  // the weight-streaming conditions (any CU count), in launches of at most 128 rows
+  return M > 0 && skinny_plan(std::min(M, 128), N, K, false, 256).use && N % 4 == 0;
 }
 
 size_t gemm_scratch_elems(int M, int N, int K, bool a_lo, bool w_lo) {
   (void)a_lo;
   if (M <= 0 || N <= 0 || K <= 0) return 0;
+  // (past 128 rows the row-chunked weight-streaming launches run without a K split)
   const SkPlan p = skinny_plan(M, N, K, w_lo, device_cus());
   size_t n = p.use && p.ksplit > 1 ? (size_t)p.ksplit * M * N : 0;
   if (M >= HSPEC_BIG_MIN_M && !w_lo && K % GB_KT == 0) {
@@ -1276,6 +1321,26 @@ size_t gemm_scratch_elems(int M, int N, int K, bool a_lo, bool w_lo) {
 
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
+  if (g.f16 && !g.w_packed) return hipErrorInvalidValue;   // fp16 operands: the packed W only
+  // products with the packed (fp16) W and fp16 outputs run on the weight-streaming path, in
+  // launches of at most 128 rows
+  if ((g.w_packed || g.C_h16) && g.M > 128 && !g.W2) {
+    for (int m0 = 0; m0 < g.M; m0 += 128) {
+      GemmArgs h = g;
+      h.M = std::min(128, g.M - m0);
+      h.A_hi += (size_t)m0 * g.lda;
+      if (h.A_lo) h.A_lo += (size_t)m0 * g.lda;
+      if (h.C) h.C += (size_t)m0 * g.ldc;
+      if (h.C_hi) h.C_hi += (size_t)m0 * g.ldch;
+      if (h.C_lo) h.C_lo += (size_t)m0 * g.ldch;
+      if (h.C_h16) h.C_h16 += (size_t)m0 * g.ldch;
+      if (h.C_l16) h.C_l16 += (size_t)m0 * g.ldch;
+      if (h.R) h.R = h.r_bf16 ? (const void*)((const bf16*)h.R + (size_t)m0 * g.ldr)
+                              : (const void*)((const float*)h.R + (size_t)m0 * g.ldr);
+      if (hipError_t e = launch_gemm(h, s)) return e;
+    }
+    return hipSuccess;
+  }
   if (g.W2) {
     if (big_ok(g)) return launch_big(g, s);
     const bool dma = g.M > 64 && !g.W_lo && !g.w_packed && g.K % BK == 0 && g.N1 % 128 == 0 && g.N2 % 128 == 0;
@@ -1299,7 +1364,8 @@ hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
   SkPlan p = skinny_plan(g.M, g.N, g.K, g.W_lo != nullptr, device_cus());
   if ((g.C && g.ldc % 4) || ((g.C_hi || g.C_h16) && g.ldch % 4) || (g.R && g.ldr % 4)) p.use = false;   // 16-byte stores
   if (g.C_h16 && (!p.use || g.W2)) return hipErrorInvalidValue;   // only the weight-streaming path writes fp16
-  if (g.w_packed && (g.N % 16 || g.K % BK || g.W_lo || g.R)) return hipErrorInvalidValue;   // packed W: no residual
+  if (g.C_l16 && !g.C_h16) return hipErrorInvalidValue;
+  if (g.w_packed && (!p.use || g.N % 16 || g.K % BK || g.W_lo || g.R)) return hipErrorInvalidValue;   // packed W: no residual
   if (p.use) {
     if (p.ksplit > 1 && (!g.part || g.part_cap < (size_t)p.ksplit * g.M * g.N)) {
       p.ksplit = 1;

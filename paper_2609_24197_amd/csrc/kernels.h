@@ -18,9 +18,13 @@ struct GemmArgs {
   float* C = nullptr; int ldc = 0;             // fp32 result (optional)
   const void* R = nullptr; int ldr = 0; int r_bf16 = 0;   // residual added (optional)
   bf16* C_hi = nullptr; bf16* C_lo = nullptr; int ldch = 0;  // bf16 planes of the result
-  _Float16* C_h16 = nullptr;   // fp16 copy of the result, leading dimension ldch (weight-streaming path only)
+  _Float16* C_h16 = nullptr;   // fp16 copy of h16_scale x result, leading dimension ldch (weight-streaming path only)
+  _Float16* C_l16 = nullptr;   // with C_h16: the fp16 residual h16_scale x result - C_h16, or null
+  float h16_scale = 1.f;       // (a power of two)
+  float out_scale = 1.f;       // the product is multiplied by this (a power of two) before any output
+  int f16 = 0;                 // A planes and the packed W hold fp16 values (packed W only)
   float* part = nullptr; size_t part_cap = 0;  // split-K scratch (fp32 elements), optional
-  int w_packed = 0;   // W_hi is in the fragment-major packed layout (launch_pack_w)
+  int w_packed = 0;   // W_hi is in the fragment-major packed layout (launch_pack_w, fp16 W x 2^kPackScaleLog2)
   // Optional row segments of W (bf16, not packed): rows [0, N1) come from W_hi, [N1, N1 + N2)
   // from W2 and [N1 + N2, N) from W3, each with leading dimension ldw.
   const bf16* W2 = nullptr; const bf16* W3 = nullptr; int N1 = 0, N2 = 0;
@@ -34,8 +38,11 @@ bool gemm_f16_out_ok(int M, int N, int K);
 size_t gemm_scratch_elems(int M, int N, int K, bool a_lo, bool w_lo);
 // Rewrites a row-major bf16 W[N, K] (N % 16 == 0, K % 32 == 0) into the packed layout that
 // launch_gemm streams when w_packed is set: 1 KB blocks (k-step s, 16-row tile t) at
-// ((s * N/16) + t) * 1024 bytes, each one 16x32 MFMA operand fragment.
-hipError_t launch_pack_w(const bf16* W, int N, int K, bf16* Wp, hipStream_t s);
+// ((s * N/16) + t) * 1024 bytes, each one 16x32 MFMA operand fragment, holding the fp16 values of
+// W x 2^kPackScaleLog2 (exact for every bf16 W of magnitude 2^-25 .. 2^7).  The product with a
+// packed W is an fp16 product (f16 set, A as fp16 planes); out_scale takes the factor back.
+constexpr int kPackScaleLog2 = 8;
+hipError_t launch_pack_w(const bf16* W, int N, int K, _Float16* Wp, hipStream_t s);
 
 // Paged block attention (split-K sweep over the target cache + block keys, then reduce).
 struct AttnArgs {

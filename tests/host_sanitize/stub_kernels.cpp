@@ -167,19 +167,22 @@ hipError_t launch_gemm(const GemmArgs& g, hipStream_t) {
     if (g.ldc < g.N) die("ldc below N", g.C, 0);
     wr("C", g.C, strided(g.M, g.N, g.ldc) * F);
   }
+  if (g.f16 && !g.w_packed) die("fp16 operands without the packed W", nullptr, 0);
   if (g.C_hi || g.C_lo || g.C_h16) {
     if (g.ldch < g.N) die("ldch below N", g.C_hi, 0);
     wr_opt("C_hi", g.C_hi, strided(g.M, g.N, g.ldch) * BF);
     wr_opt("C_lo", g.C_lo, strided(g.M, g.N, g.ldch) * BF);
     if (g.C_h16 && !gemm_f16_out_ok(g.M, g.N, g.K)) return hipErrorInvalidValue;
     wr_opt("C_h16", g.C_h16, strided(g.M, g.N, g.ldch) * sizeof(_Float16));
+    if (g.C_l16 && !g.C_h16) die("C_l16 without C_h16", g.C_l16, 0);
+    wr_opt("C_l16", g.C_l16, strided(g.M, g.N, g.ldch) * sizeof(_Float16));
   }
   const size_t need = gemm_scratch_elems(g.M, g.N, g.K, g.A_lo != nullptr, g.W_lo != nullptr);
   if (need && g.part_cap >= need) wr("part", g.part, need * F);
   return hipSuccess;
 }
 
-hipError_t launch_pack_w(const bf16* W, int N, int K, bf16* Wp, hipStream_t) {
+hipError_t launch_pack_w(const bf16* W, int N, int K, _Float16* Wp, hipStream_t) {
   Scope s("launch_pack_w");
   rd("W", W, (size_t)N * K * BF);
   wr("Wp", Wp, (size_t)N * K * BF);

@@ -327,17 +327,25 @@ def test_ssd_scan_zero_input_zero_state():
 
 def _pack_host(W, r):
     """The packed W_dS layout as the header describes it: block (s, t) at ((s*T + t) * 1024)
-    bytes, row 16t+i, columns 32s+8c..+7 at (i + 16c) * 16 bytes inside the block."""
+    bytes, row 16t+i, columns 32s+8c..+7 at (i + 16c) * 16 bytes inside the block, each element
+    the fp16 value of 256 x W (bit patterns; numpy rounds to nearest even, as the device does)."""
     d_S = W.shape[0]
     T, S = d_S // 16, r // 32
-    blk = W.reshape(T, 16, S, 4, 8)              # [t, i, s, c, e]
+    w16 = (I.bf16_bits_to_f32(W).astype(np.float64) * 256.0).astype(np.float16).view(np.uint16)
+    blk = w16.reshape(T, 16, S, 4, 8)            # [t, i, s, c, e]
     return np.ascontiguousarray(blk.transpose(2, 0, 3, 1, 4)).reshape(-1)   # [s, t, c, i, e]
 
 
 @pytest.mark.parametrize("d_S,r", [(16, 64), (4096, 256), (2048, 192)])
 def test_pack_w_ds_layout(d_S, r):
-    """Packing is pure data movement: bit-exact against the host re-layout."""
+    """Packing is data movement and an exact fp16 conversion: bit-exact against the host
+    re-layout, over weights spanning 2^-25 .. 2^7 in magnitude."""
     W = I.normal("pack_W", (d_S, r), 1.0, 0, "bf16")
+    # a spread of exponents, both signs (bf16 bit patterns: sign, 8-bit exponent, 7-bit fraction)
+    e = np.random.default_rng(5).integers(127 - 25, 127 + 8, size=W.shape, dtype=np.int64)
+    fr = np.random.default_rng(6).integers(0, 128, size=W.shape, dtype=np.int64)
+    sg = np.random.default_rng(7).integers(0, 2, size=W.shape, dtype=np.int64)
+    W = ((sg << 15) | (e << 7) | fr).astype(np.uint16).view(W.dtype)
     d = dev(dict(W=W))
     packed = hspec.pack_w_ds(d["W"], d_S, r)
     got = packed.view(dtype=__import__("torch").int16).cpu().numpy().view(np.uint16)
