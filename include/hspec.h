@@ -299,9 +299,11 @@ size_t hspec_draft_head_workspace(const hspec_head_cfg* cfg);
  * fragments.  Block (s, t) holds rows 16t..16t+15 and columns 32s..32s+31 of W_dS and
  * starts at byte ((s * d_S/16) + t) * 1024; inside it, the 8 consecutive columns
  * 32s + 8c .. +7 of row 16t + i are the 16 bytes at (i + 16c) * 16.  Every element is the
- * fp16 value of 256 x W_dS (exact for bf16 weights of magnitude 2^-25 .. 255; the projection
- * divides the 256 back out), so that the projection runs as one fp16 product with F as one
- * fp16 plane (hi/lo fp16 planes with HSPEC_MAMBA_PRECISE_IO).
+ * fp16 value of 256 x W_dS (exact for bf16 weights of magnitude 2^-25 .. 255.875; smaller
+ * magnitudes round to fp16 subnormals in steps of 2^-32 of W_dS, bf16 subnormals become 0,
+ * larger magnitudes become +-inf and inf/NaN stay; the projection divides the 256 back out),
+ * so that the projection runs as one fp16 product with F as one fp16 plane (hi/lo fp16
+ * planes with HSPEC_MAMBA_PRECISE_IO).
  * W_dS [d_S, r] row-major bf16 in, W_packed (hspec_pack_w_ds_bytes bytes) out, both device
  * memory; d_S % 16 == 0 and r % 64 == 0, else HSPEC_ERR_UNSUPPORTED.  Asynchronous on stream.
  */

@@ -331,7 +331,8 @@ def _pack_host(W, r):
     the fp16 value of 256 x W (bit patterns; numpy rounds to nearest even, as the device does)."""
     d_S = W.shape[0]
     T, S = d_S // 16, r // 32
-    w16 = (I.bf16_bits_to_f32(W).astype(np.float64) * 256.0).astype(np.float16).view(np.uint16)
+    with np.errstate(over="ignore"):
+        w16 = (I.bf16_bits_to_f32(W).astype(np.float64) * 256.0).astype(np.float16).view(np.uint16)
     blk = w16.reshape(T, 16, S, 4, 8)            # [t, i, s, c, e]
     return np.ascontiguousarray(blk.transpose(2, 0, 3, 1, 4)).reshape(-1)   # [s, t, c, i, e]
 
@@ -339,12 +340,19 @@ def _pack_host(W, r):
 @pytest.mark.parametrize("d_S,r", [(16, 64), (4096, 256), (2048, 192)])
 def test_pack_w_ds_layout(d_S, r):
     """Packing is data movement and an exact fp16 conversion: bit-exact against the host
-    re-layout, over weights spanning 2^-25 .. 2^7 in magnitude."""
+    re-layout, over weights spanning 2^-25 .. 2^7 in magnitude, plus the ends of the range:
+    zeros and bf16 subnormals (to +-0), magnitudes below 2^-25 (rounded to fp16 subnormals),
+    above 255.875 up to the largest bf16 and infinities (to +-inf)."""
     W = I.normal("pack_W", (d_S, r), 1.0, 0, "bf16")
     # a spread of exponents, both signs (bf16 bit patterns: sign, 8-bit exponent, 7-bit fraction)
     e = np.random.default_rng(5).integers(127 - 25, 127 + 8, size=W.shape, dtype=np.int64)
     fr = np.random.default_rng(6).integers(0, 128, size=W.shape, dtype=np.int64)
     sg = np.random.default_rng(7).integers(0, 2, size=W.shape, dtype=np.int64)
+    # the first row: special exponents (0: zero or subnormal; 255 with fraction 0: inf)
+    special = np.array([0, 0, 127 - 40, 127 - 30, 127 - 26, 127 + 8, 127 + 15, 127 + 16, 127 + 120, 254, 255])
+    e[0, :special.size] = special
+    fr[0, 0] = 0
+    fr[0, special.size - 1] = 0
     W = ((sg << 15) | (e << 7) | fr).astype(np.uint16).view(W.dtype)
     d = dev(dict(W=W))
     packed = hspec.pack_w_ds(d["W"], d_S, r)
