@@ -296,8 +296,10 @@ size_t hspec_draft_head_workspace(const hspec_head_cfg* cfg);
  * Packed layout of W_dS for the state projection (Sec. 3.3.1, Proj_dS), written once when
  * the weights are loaded, never per step.  The projection streams W_dS from HBM once per
  * step; this layout lets every wave read whole 1 KB blocks that are already MFMA operand
- * fragments.  Block (s, t) holds rows 16t..16t+15 and columns 32s..32s+31 of W_dS and
- * starts at byte ((s * d_S/16) + t) * 1024; inside it, the 8 consecutive columns
+ * fragments, and every workgroup one contiguous run of blocks.  Block (s, t) holds rows
+ * 16t..16t+15 and columns 32s..32s+31 of W_dS; the 16-row tiles form groups of 32
+ * (g = t / 32, the last group holding gs = min(32, d_S/16 - 32g) tiles), and block (s, t)
+ * starts at byte (32 g (r/32) + s gs + t mod 32) * 1024; inside it, the 8 consecutive columns
  * 32s + 8c .. +7 of row 16t + i are the 16 bytes at (i + 16c) * 16.  Every element is the
  * fp16 value of 256 x W_dS (exact for bf16 weights of magnitude 2^-25 .. 255.875; smaller
  * magnitudes round to fp16 subnormals in steps of 2^-32 of W_dS, bf16 subnormals become 0,

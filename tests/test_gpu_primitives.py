@@ -326,18 +326,24 @@ def test_ssd_scan_zero_input_zero_state():
 # -------------------------------------------------------------------- state projection
 
 def _pack_host(W, r):
-    """The packed W_dS layout as the header describes it: block (s, t) at ((s*T + t) * 1024)
-    bytes, row 16t+i, columns 32s+8c..+7 at (i + 16c) * 16 bytes inside the block, each element
-    the fp16 value of 256 x W (bit patterns; numpy rounds to nearest even, as the device does)."""
+    """The packed W_dS layout as the header describes it: 16-row tiles in groups of 32 (the
+    last group holding what is left), block (s, t) at (32 g S + s gs + t mod 32) * 1024 bytes
+    for group g = t // 32 of gs tiles, row 16t+i, columns 32s+8c..+7 at (i + 16c) * 16 bytes
+    inside the block, each element the fp16 value of 256 x W (bit patterns; numpy rounds to
+    nearest even, as the device does)."""
     d_S = W.shape[0]
     T, S = d_S // 16, r // 32
     with np.errstate(over="ignore"):
         w16 = (I.bf16_bits_to_f32(W).astype(np.float64) * 256.0).astype(np.float16).view(np.uint16)
     blk = w16.reshape(T, 16, S, 4, 8)            # [t, i, s, c, e]
-    return np.ascontiguousarray(blk.transpose(2, 0, 3, 1, 4)).reshape(-1)   # [s, t, c, i, e]
+    out = []
+    for g0 in range(0, T, 32):                   # a group: its k-steps in order, each its tiles
+        grp = blk[g0:g0 + 32]                    # [gs, i, s, c, e]
+        out.append(np.ascontiguousarray(grp.transpose(2, 0, 3, 1, 4)).reshape(-1))   # [s, t, c, i, e]
+    return np.concatenate(out)
 
 
-@pytest.mark.parametrize("d_S,r", [(16, 64), (4096, 256), (2048, 192)])
+@pytest.mark.parametrize("d_S,r", [(16, 64), (4096, 256), (2048, 192), (640, 128), (1040, 64)])
 def test_pack_w_ds_layout(d_S, r):
     """Packing is data movement and an exact fp16 conversion: bit-exact against the host
     re-layout, over weights spanning 2^-25 .. 2^7 in magnitude, plus the ends of the range:
