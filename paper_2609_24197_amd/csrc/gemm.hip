@@ -585,15 +585,15 @@ struct SkPlan {
   int ntw = 4, ksplit = 1, kper = 0;
 };
 
-// Waves per workgroup: 128-row A chunks (hi and lo planes, double-buffered) leave LDS room for
-// the epilogue staging of 4 waves only.
-constexpr int sk_waves(int M) { return M > 64 ? 4 : SK_NW; }
+// Waves per workgroup: 128-row A chunks as hi and lo planes (double-buffered) leave LDS room
+// for the epilogue staging of 4 waves only; one plane leaves room for all 8.
+constexpr int sk_waves(int M, bool a_lo) { return M > 64 && a_lo ? 4 : SK_NW; }
 
-SkPlan skinny_plan(int M, int N, int K, bool w_lo, int cus) {
+SkPlan skinny_plan(int M, int N, int K, bool a_lo, bool w_lo, int cus) {
   SkPlan p;
   if (M > 128 || w_lo || K % SK_STEP != 0 || N % 4 != 0) return p;
   p.use = true;
-  const int nw = sk_waves(M);
+  const int nw = sk_waves(M, a_lo);
   const int want = 2 * cus;
   int tiles = (N + nw * 64 - 1) / (nw * 64);
   if (tiles < want) {
@@ -611,7 +611,7 @@ SkPlan skinny_plan(int M, int N, int K, bool w_lo, int cus) {
 
 template <int MT, int NTW, bool ALO, bool PK>
 hipError_t launch_skinny_t(const GemmArgs& g, const SkPlan& p, hipStream_t s) {
-  constexpr int NW = sk_waves(16 * MT);
+  constexpr int NW = sk_waves(16 * MT, ALO);
   using S = SkCfg<MT, NTW, NW, ALO>;
   // the residual is added by the reduction when K is split
   auto kern = (g.R && p.ksplit == 1 && !PK) ? skinny_kernel<MT, NTW, NW, ALO, PK, !PK>
@@ -1328,15 +1328,18 @@ hipError_t launch_pack_w(const bf16* W, int N, int K, _Float16* Wp, hipStream_t 
 
 bool gemm_f16_out_ok(int M, int N, int K) {
   // the weight-streaming conditions (any CU count), in launches of at most 128 rows
-  return M > 0 && skinny_plan(std::min(M, 128), N, K, false, 256).use && N % 4 == 0;
+  return M > 0 && skinny_plan(std::min(M, 128), N, K, false, false, 256).use && N % 4 == 0;
 }
 
 size_t gemm_scratch_elems(int M, int N, int K, bool a_lo, bool w_lo) {
-  (void)a_lo;
   if (M <= 0 || N <= 0 || K <= 0) return 0;
-  // (past 128 rows the row-chunked weight-streaming launches run without a K split)
-  const SkPlan p = skinny_plan(M, N, K, w_lo, device_cus());
-  size_t n = p.use && p.ksplit > 1 ? (size_t)p.ksplit * M * N : 0;
+  // (past 128 rows the row-chunked weight-streaming launches run without a K split); the
+  // plan for one A plane is covered too, since a caller sizing for hi/lo may pass one plane
+  size_t n = 0;
+  for (const bool lo : {a_lo, false}) {
+    const SkPlan p = skinny_plan(M, N, K, lo, w_lo, device_cus());
+    if (p.use && p.ksplit > 1) n = std::max(n, (size_t)p.ksplit * M * N);
+  }
   if (M >= HSPEC_BIG_MIN_M && !w_lo && K % GB_KT == 0) {
     n = std::max(n, big_scratch_elems(big_plan(M, N, K, false, device_cus())));
     n = std::max(n, big_scratch_elems(big_plan(M, N, K, true, device_cus())));
@@ -1386,7 +1389,7 @@ hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
     }
     return hipSuccess;
   }
-  SkPlan p = skinny_plan(g.M, g.N, g.K, g.W_lo != nullptr, device_cus());
+  SkPlan p = skinny_plan(g.M, g.N, g.K, g.A_lo != nullptr, g.W_lo != nullptr, device_cus());
   if ((g.C && g.ldc % 4) || ((g.C_hi || g.C_h16) && g.ldch % 4) || (g.R && g.ldr % 4)) p.use = false;   // 16-byte stores
   if (g.C_h16 && (!p.use || g.W2)) return hipErrorInvalidValue;   // only the weight-streaming path writes fp16
   if (g.C_l16 && !g.C_h16) return hipErrorInvalidValue;
