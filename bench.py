@@ -132,6 +132,28 @@ def head_figures(cfg, out, step, args, torch):
             "lm_head_frac_of_bf16_peak": round(flops / t_lm / 1e12 / RL.MFMA_BF16_PEAK_TFLOPS, 4)}
 
 
+def scan_figures(cfg, step, args, torch):
+    """The SSD scan launched alone at the step's shapes (B requests, k positions, H heads of
+    P x N), each call after one drafting step: the one-chunk kernel the step runs (S0 as bf16
+    hi/lo planes here) and the multi-chunk kernel, which carries the state across chunks and
+    writes S_final, at chunk = k and chunk = k/2."""
+    B, T, H, N, G = cfg.B, cfg.k, cfg.H, cfg.N, cfg.G
+    s = I.make_scan_inputs(B, T, H, cfg.P, N, G, seed=args.seed, dtype=cfg.dtype, s0=True)
+    d = {k: hspec.to_device(v) for k, v in s.items() if v is not None}
+    code = hspec.F32 if cfg.dtype == "f32" else hspec.BF16
+    ws = hspec.workspace(hspec.ssd_scan_workspace(B, T, H, cfg.P, N, G, code))
+    y = torch.empty((B, T, H, cfg.P), dtype=torch.float32, device="cuda")
+    Sf = torch.empty((B, H, cfg.P, N), dtype=torch.float32, device="cuda")
+    res = {}
+    for name, chunk, fin in (("one_chunk_us", T, False), ("with_final_state_us", T, True),
+                             ("two_chunks_with_final_state_us", max(1, T // 2), True)):
+        f = lambda: hspec.ssd_scan(B, T, H, cfg.P, N, G, chunk, code, d["x"], d["dt"], d["A"], d["Bm"],  # noqa: E731
+                                   d["Cm"], d["Dskip"], d["S0"], y, Sf if fin else None, ws)
+        res[name] = round(time_in_step(f, args.steps, args.warmup, step, torch) * 1e6, 2)
+    log(f"ssd scan alone: {res}")
+    return res
+
+
 def forward_figures(cfg, Wd, Xd, x, args, torch):
     """Timing of hspec_drafter_forward (3 x (Mamba, attention, MLP) + 1 x (Mamba, MLP), |M| = 5,
     MLP hidden 3 d_model) on the same batch: the step's packed W_dS (the same seeded values), a
@@ -347,7 +369,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=3)
-    ap.add_argument("--cpu-requests", type=int, default=8)
+    ap.add_argument("--cpu-requests", type=int, default=0,
+                    help="requests the CPU oracle drafts for cpu_baseline (default: the whole batch)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--window", type=int, default=None,
@@ -478,14 +501,16 @@ def main():
     # the draft head after the step (final norm, LM head over the pruned vocabulary, Markov
     # correction, greedy tokens) on the step's own output, and its LM-head GEMM alone
     head = head_figures(cfg, out, step, args, torch)
+    scan = scan_figures(cfg, step, args, torch)
     fwd = forward_figures(cfg, Wd, Xd, x, args, torch) if cfg.dtype == "bf16" else None
 
     cpu = None
     if not args.no_cpu_baseline:
         del Wd, Xd, ws, out
         torch.cuda.empty_cache()
-        log(f"cpu baseline: oracle on {args.cpu_requests} request(s) ...")
-        cpu = cpu_baseline(cfg, W, x, args.cpu_requests)
+        n_req = min(cfg.B, args.cpu_requests) if args.cpu_requests > 0 else cfg.B
+        log(f"cpu baseline: oracle on {n_req} request(s) ...")
+        cpu = cpu_baseline(cfg, W, x, n_req)
         log(f"cpu baseline: {cpu['value']:.2f} tok/s on {cpu['cores']} threads")
 
     rec = {
@@ -503,6 +528,7 @@ def main():
         "roofline": roof,
         "roofline_kv_sweep": roof_sweep,
         "cpu_baseline": cpu,
+        "ssd_scan": scan,
         "draft_head": dict(head, drafted_tok_s_with_head=round(cfg.B * cfg.k / (ms / 1e3 + head["avg_us"] / 1e6), 1)),
         "drafter_forward": None if fwd is None else dict(
             fwd, with_head_drafted_tok_s=round(cfg.B * cfg.k / (fwd["ms"] / 1e3 + head["avg_us"] / 1e6), 1)),

@@ -44,6 +44,29 @@ __device__ __forceinline__ void split8(const float* v, bf16x8& hi, bf16x8& lo) {
   }
 }
 
+// Intra-chunk term M x on v_mfma_f32_16x16x32_bf16: A = M (row t = lane % 16, k = s), B = x^T
+// (k = s, column p = 16 pb + lane % 16); k = 16..31 are zero.  Both fp32 tiles enter as bf16
+// hi/lo planes (three products).  Lane gets rows t = 4 (lane / 16) + i of column p, the layout
+// of the state term.  M is zero for s > t and outside the chunk, x^T for s outside it.
+__device__ __forceinline__ void mix_mfma(const float* Mm, const float* xT, int lane, f32x4 (&mx)[4]) {
+  const int g4 = lane >> 4, l16 = lane & 15;
+  float v[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = g4 < 2 ? Mm[l16 * (QMAX + 1) + 8 * g4 + e] : 0.f;
+  bf16x8 mh, ml;
+  split8(v, mh, ml);
+#pragma unroll
+  for (int pb = 0; pb < 4; ++pb) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = g4 < 2 ? xT[(16 * pb + l16) * (QMAX + 1) + 8 * g4 + e] : 0.f;
+    bf16x8 xh, xl;
+    split8(v, xh, xl);
+    mx[pb] = mma16(mh, xh, f32x4{0.f, 0.f, 0.f, 0.f});
+    mx[pb] = mma16(ml, xh, mx[pb]);
+    mx[pb] = mma16(mh, xl, mx[pb]);
+  }
+}
+
 template <int N>
 __global__ void __launch_bounds__(64) ssd_scan_kernel(ScanArgs a) {
   constexpr int NS = (N + 31) / 32;
@@ -61,52 +84,91 @@ __global__ void __launch_bounds__(64) ssd_scan_kernel(ScanArgs a) {
   const float Ah = a.A_is_log ? -__expf(a.A[h]) : a.A[h], Dh = a.Dskip[h];
   const size_t s0_off = ((size_t)b * H + h) * P * N;
 
-  for (int p = 0; p < P; ++p) {
-    for (int n = lane; n < N; n += 64) {
-      float v = 0.f;
-      if (a.S0_h16) {
-        v = (float)a.S0_h16[s0_off + p * N + n];
-      } else if (a.S0_hi) {
-        v = bf2f(a.S0_hi[s0_off + p * N + n]);
-        if (a.S0_lo) v += bf2f(a.S0_lo[s0_off + p * N + n]);
+  // S0 into LDS in 16-byte pieces (8 elements of a row), every load of a round issued before
+  // its first LDS write (two rounds at N = 128 to bound the registers)
+  {
+    constexpr int PR = N / 8, PER = P * PR / 64, RND = PER > 8 ? PER / 2 : PER;
+#pragma unroll
+    for (int r0 = 0; r0 < PER; r0 += RND) {
+      bf16x8 hv[RND], lv[RND];
+      f16x8 fv[RND];
+#pragma unroll
+      for (int j = 0; j < RND; ++j) {
+        const int q = (r0 + j) * 64 + lane, p = q / PR, n0 = (q % PR) * 8;
+        const size_t off = s0_off + (size_t)p * N + n0;
+        if (a.S0_h16) {
+          fv[j] = *reinterpret_cast<const f16x8*>(a.S0_h16 + off);
+        } else {
+          hv[j] = ld8_or0(a.S0_hi + off, a.S0_hi != nullptr);
+          lv[j] = ld8_or0(a.S0_lo + off, a.S0_lo != nullptr);
+        }
       }
-      S[p * (N + 1) + n] = v;
+#pragma unroll
+      for (int j = 0; j < RND; ++j) {
+        const int q = (r0 + j) * 64 + lane, p = q / PR, n0 = (q % PR) * 8;
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          S[p * (N + 1) + n0 + e] = a.S0_h16 ? (float)fv[j][e] : bf2f(hv[j][e]) + bf2f(lv[j][e]);
+      }
     }
   }
   __syncthreads();
 
+  // A chunk's global inputs (dt, the x tile, the C and B fragments) come into registers one
+  // chunk ahead: the next chunk's loads are in flight while this one is computed.
+  struct ChunkIn {
+    float dtv;
+    bf16x8 xh0, xh1, xl0, xl1;
+    bf16x8 cf[NS], cfl[NS], bfr[NS], bfl[NS];
+  };
+  auto load_chunk = [&](int c0, ChunkIn& r) {
+    const int Qc = max(0, min(a.chunk, T - c0));   // 0 past the last chunk: nothing is read
+    r.dtv = l16 < Qc ? a.dt[(size_t)(b * T + c0 + l16) * a.dt_ld + h] : 0.f;
+    // x tile: lane holds x[t = lane / 4][p = 16 (lane % 4) .. + 15], zero past the chunk
+    const int xt = lane >> 2, xp = 16 * (lane & 3);
+    const bool xok = xt < Qc;
+    const size_t xoff = (size_t)(b * T + c0 + xt) * a.x_ld + (size_t)h * P + xp;
+    r.xh0 = ld8_or0(a.x_hi + xoff, xok);
+    r.xh1 = ld8_or0(a.x_hi + xoff + 8, xok);
+    r.xl0 = a.x_lo ? ld8_or0(a.x_lo + xoff, xok) : zero8();
+    r.xl1 = a.x_lo ? ld8_or0(a.x_lo + xoff + 8, xok) : zero8();
+    // C (A operand, rows t) and B (B operand, columns s) fragments over n
+    const size_t tok_t = (size_t)(b * T + c0 + l16) * a.bc_ld + (size_t)grp * N;
+#pragma unroll
+    for (int ns = 0; ns < NS; ++ns) {
+      const int n = 32 * ns + 8 * g4;
+      const bool ok = l16 < Qc && n < N;
+      r.cf[ns] = ld8_or0(a.C_hi + tok_t + n, ok);
+      r.cfl[ns] = a.C_lo ? ld8_or0(a.C_lo + tok_t + n, ok) : zero8();
+      r.bfr[ns] = ld8_or0(a.B_hi + tok_t + n, ok);
+      r.bfl[ns] = a.B_lo ? ld8_or0(a.B_lo + tok_t + n, ok) : zero8();
+    }
+  };
+  ChunkIn nx;
+  load_chunk(0, nx);
+
   for (int c0 = 0; c0 < T; c0 += a.chunk) {
     const int Qc = min(a.chunk, T - c0);
-    // dt and the inclusive cumulative sum of dt*A over the chunk (lanes 0..15)
-    const float dtv = l16 < Qc ? a.dt[(size_t)(b * T + c0 + l16) * a.dt_ld + h] : 0.f;
+    const ChunkIn cur = nx;
+    load_chunk(c0 + a.chunk, nx);
+    const float dtv = cur.dtv;
+    // the inclusive cumulative sum of dt*A over the chunk (lanes 0..15)
     float cum = dtv * Ah;
 #pragma unroll
     for (int off = 1; off < 16; off <<= 1) {
       const float v = __shfl_up(cum, off, 16);
       if (l16 >= off) cum += v;
     }
-    // x^T tile in LDS: lane = head channel p
-    for (int s = 0; s < QMAX; ++s) {
-      float v = 0.f;
-      if (s < Qc) {
-        const size_t off = (size_t)(b * T + c0 + s) * a.x_ld + (size_t)h * P + lane;
-        v = bf2f(a.x_hi[off]);
-        if (a.x_lo) v += bf2f(a.x_lo[off]);
-      }
-      xT[lane * (QMAX + 1) + s] = v;
-    }
-    // C (A operand, rows t) and B (B operand, columns s) fragments over n
-    bf16x8 cf[NS], cfl[NS], bfr[NS], bfl[NS];
-    const size_t tok_t = (size_t)(b * T + c0 + l16) * a.bc_ld + (size_t)grp * N;
+    // x^T tile in LDS
+    {
+      const int xt = lane >> 2, xp = 16 * (lane & 3);
 #pragma unroll
-    for (int ns = 0; ns < NS; ++ns) {
-      const int n = 32 * ns + 8 * g4;
-      const bool ok = l16 < Qc && n < N;
-      cf[ns] = ld8_or0(a.C_hi + tok_t + n, ok);
-      cfl[ns] = a.C_lo ? ld8_or0(a.C_lo + tok_t + n, ok) : zero8();
-      bfr[ns] = ld8_or0(a.B_hi + tok_t + n, ok);
-      bfl[ns] = a.B_lo ? ld8_or0(a.B_lo + tok_t + n, ok) : zero8();
+      for (int e = 0; e < 8; ++e) {
+        xT[(xp + e) * (QMAX + 1) + xt] = bf2f(cur.xh0[e]) + bf2f(cur.xl0[e]);
+        xT[(xp + 8 + e) * (QMAX + 1) + xt] = bf2f(cur.xh1[e]) + bf2f(cur.xl1[e]);
+      }
     }
+    const bf16x8 *cf = cur.cf, *cfl = cur.cfl, *bfr = cur.bfr, *bfl = cur.bfl;
     // state term C S^T: lane gets rows t = 4 g4 + i, column p = 16 pb + l16
     f32x4 ys[4];
 #pragma unroll
@@ -144,58 +206,98 @@ __global__ void __launch_bounds__(64) ssd_scan_kernel(ScanArgs a) {
       const bool ok = l16 <= t && t < Qc;
       Mm[t * (QMAX + 1) + l16] = ok ? cb[i] * __expf(ell_t[i] - ell_s) * dt_s : 0.f;
     }
-    // B^T tile for the state update: Bt[n][s]
-    for (int s = 0; s < QMAX; ++s)
-      for (int n = lane; n < N; n += 64) {
-        float v = 0.f;
-        if (s < Qc) {
-          const size_t off = (size_t)(b * T + c0 + s) * a.bc_ld + (size_t)grp * N + n;
-          v = bf2f(a.B_hi[off]);
-          if (a.B_lo) v += bf2f(a.B_lo[off]);
-        }
-        Bt[n * (QMAX + 1) + s] = v;
+    // B^T tile for the state update, Bt[n][s], from the B fragments already in registers
+    // (token s = lane % 16, zero past the chunk)
+#pragma unroll
+    for (int ns = 0; ns < NS; ++ns)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int n = 32 * ns + 8 * g4 + e;
+        if (n < N) Bt[n * (QMAX + 1) + l16] = bf2f(bfr[ns][e]) + bf2f(bfl[ns][e]);
       }
     __syncthreads();
-    // y = exp(l_t) (C S^T) + M x + D x
+    // y = exp(l_t) (C S^T) + M x + D x, M x on MFMA
+    f32x4 mx[4];
+    mix_mfma(Mm, xT, lane, mx);
 #pragma unroll
     for (int pb = 0; pb < 4; ++pb) {
       const int p = 16 * pb + l16;
-      const float* xr = xT + p * (QMAX + 1);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int t = 4 * g4 + i;
         if (t >= Qc) continue;
-        const float* mr = Mm + t * (QMAX + 1);
-        float acc = __expf(ell_t[i]) * ys[pb][i] + Dh * xr[t];
-        for (int s = 0; s <= t; ++s) acc += mr[s] * xr[s];
+        const float acc = __expf(ell_t[i]) * ys[pb][i] + Dh * xT[p * (QMAX + 1) + t] + mx[pb][i];
         a.y[(size_t)(b * T + c0 + t) * H * P + (size_t)h * P + p] = acc;
       }
     }
     {
-      // S <- exp(l_end) S + sum_s exp(l_end - l_s) dt_s x_s (outer) B_s ; lane = row p
+      // S <- exp(l_end) S + (W X) B on v_mfma_f32_32x32x16_bf16: A = W X (row p, k = s) with
+      // W X [p][s] = exp(l_end - l_s) dt_s x_s[p], B = the B tile (k = s, column n), the
+      // accumulator the decayed state in the 32 x 32 block layout (lane holds rows
+      // 8 (i / 4) + 4 (lane / 32) + i % 4 of column lane % 32), read from and written back to
+      // LDS by the same lane.  fp32 operands as bf16 hi/lo planes (three products).
       const float ell_end = __shfl(cum, Qc - 1);
       const float dec = __expf(ell_end);
-      float wx[QMAX];
+      const int r32 = lane & 31, h2 = lane >> 5;
+      float wv[8];
 #pragma unroll
-      for (int s = 0; s < QMAX; ++s) {
-        const float w = __shfl(dtv, s) * __expf(ell_end - __shfl(cum, s));
-        wx[s] = s < Qc ? w * xT[lane * (QMAX + 1) + s] : 0.f;
+      for (int e = 0; e < 8; ++e) {
+        const int sx = 8 * h2 + e;
+        const float w = __shfl(dtv, sx) * __expf(ell_end - __shfl(cum, sx));
+        wv[e] = sx < Qc ? w : 0.f;
       }
-      float* Sr = S + lane * (N + 1);
-      for (int n = 0; n < N; ++n) {
-        const float* br = Bt + n * (QMAX + 1);
-        float acc = dec * Sr[n];
+      bf16x8 wh[2], wl[2];
 #pragma unroll
-        for (int s = 0; s < QMAX; ++s) acc += wx[s] * br[s];
-        Sr[n] = acc;
+      for (int pb = 0; pb < 2; ++pb) {
+        float v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = wv[e] * xT[(32 * pb + r32) * (QMAX + 1) + 8 * h2 + e];
+        split8(v, wh[pb], wl[pb]);
+      }
+#pragma unroll
+      for (int nb = 0; nb < (N + 31) / 32; ++nb) {
+        const int n = 32 * nb + r32;
+        const bool nok = n < N;
+        float v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = nok ? Bt[n * (QMAX + 1) + 8 * h2 + e] : 0.f;
+        bf16x8 bh, bl;
+        split8(v, bh, bl);
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb) {
+          f32x16 acc;
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int p = 32 * pb + 8 * (i / 4) + 4 * h2 + (i % 4);
+            acc[i] = nok ? dec * S[p * (N + 1) + n] : 0.f;
+          }
+          acc = mma32(wh[pb], bh, acc);
+          acc = mma32(wl[pb], bh, acc);
+          acc = mma32(wh[pb], bl, acc);
+          if (nok) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) S[(32 * pb + 8 * (i / 4) + 4 * h2 + (i % 4)) * (N + 1) + n] = acc[i];
+          }
+        }
       }
     }
     __syncthreads();
   }
 
   if (a.S_final) {
-    for (int p = 0; p < P; ++p)
-      for (int n = lane; n < N; n += 64) a.S_final[s0_off + p * N + n] = S[p * (N + 1) + n];
+    // 16-byte stores where the caller's buffer allows them
+    const bool vec = (reinterpret_cast<uintptr_t>(a.S_final) & 15) == 0;
+    for (int q = lane; q < P * N / 4; q += 64) {
+      const int p = q / (N / 4), n0 = (q % (N / 4)) * 4;
+      const float* sr = S + p * (N + 1) + n0;
+      float* dst = a.S_final + s0_off + (size_t)p * N + n0;
+      if (vec) {
+        *reinterpret_cast<f32x4*>(dst) = f32x4{sr[0], sr[1], sr[2], sr[3]};
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) dst[e] = sr[e];
+      }
+    }
   }
 }
 
@@ -315,28 +417,17 @@ __global__ void __launch_bounds__(64) ssd_scan_one(ScanArgs a) {
     Mm[t * (QMAX + 1) + l16] = ok ? cb[i] * __expf(ell_t[i] - ell_s) * dt_s : 0.f;
   }
   __syncthreads();
-  // ---- y = exp(l_t) (C S^T) + M x + D x.  The lane's four rows of M and, per p, the row of
-  // x^T are read into registers with independent LDS reads (every entry of both tiles is
-  // written above); terms with s > t are selected away, so the sum is the one over s <= t in
-  // order.
-  float mrow[4][QMAX];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int s2 = 0; s2 < QMAX; ++s2) mrow[i][s2] = Mm[(4 * g4 + i) * (QMAX + 1) + s2];
+  // ---- y = exp(l_t) (C S^T) + M x + D x, M x on MFMA (every entry of both tiles is written
+  // above: M is zero for s > t and past the block, x^T for s past it)
+  f32x4 mx[4];
+  mix_mfma(Mm, xT, lane, mx);
 #pragma unroll
   for (int pb = 0; pb < 4; ++pb) {
     const int p = 16 * pb + l16;
-    const float* xr = xT + p * (QMAX + 1);
-    float xv[QMAX];
-#pragma unroll
-    for (int s2 = 0; s2 < QMAX; ++s2) xv[s2] = xr[s2];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int t = 4 * g4 + i;
-      float acc = __expf(ell_t[i]) * ys[pb][i] + Dh * xr[t];
-#pragma unroll
-      for (int s2 = 0; s2 < QMAX; ++s2) acc += s2 <= t ? mrow[i][s2] * xv[s2] : 0.f;
+      const float acc = __expf(ell_t[i]) * ys[pb][i] + Dh * xT[p * (QMAX + 1) + t] + mx[pb][i];
       if (t < T) a.y[(size_t)(b * T + t) * H * P + (size_t)h * P + p] = acc;
     }
   }

@@ -288,6 +288,9 @@ SCAN_CASES = [
     (2, 16, 8, 128, 1, 16, "f32", True, False),
     (3, 7, 4, 64, 2, 8, "bf16", True, False),
     (1, 1, 2, 16, 1, 16, "f32", True, False),
+    # several chunks at N = 32 (state update in one 32-column block), and a ragged last chunk
+    (2, 24, 4, 32, 1, 8, "bf16", True, True),
+    (2, 13, 4, 128, 1, 5, "bf16", True, True),
 ]
 
 
