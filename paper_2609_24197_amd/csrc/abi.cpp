@@ -443,8 +443,9 @@ void plan_attn(Arena& ar, const hspec_attn_cfg& c, int max_ctx_len, bool x_norm,
   plan_sweep(ar, c, max_ctx_len, p);
   p.o_hi = ar.take<bf16>(M * c.Hq * c.D);
   if (io_lo) p.o_lo = ar.take<bf16>(M * c.Hq * c.D);
-  p.gs = reserve_gemm(ar, c.dtype, {{(int)M, c.Hq * c.D, c.d_model}, {(int)M, c.Hkv * c.D, c.d_model},
-                                    {(int)M, c.d_model, c.Hq * c.D}});
+  // the fused QKV product (one launch over the three weight segments) and the separate ones
+  p.gs = reserve_gemm(ar, c.dtype, {{(int)M, (c.Hq + 2 * c.Hkv) * c.D, c.d_model}, {(int)M, c.Hq * c.D, c.d_model},
+                                    {(int)M, c.Hkv * c.D, c.d_model}, {(int)M, c.d_model, c.Hq * c.D}});
 }
 
 hspec::AttnArgs sweep_args(const hspec_attn_cfg& c, const AttnPlan& p, const int32_t* pt, const int32_t* lens,
