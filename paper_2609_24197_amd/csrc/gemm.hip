@@ -432,6 +432,8 @@ skinny_kernel(GemmArgs g, int kper, int nitems) {
     const __amdgpu_buffer_rsrc_t r_l16 =
         buf(g.C_l16 ? g.C_l16 + min(n0, g.N) : nullptr, !split && g.C_l16 && cols ? (rows_span * g.ldch + cols) * 2 : 0);
     const float osc = split ? 1.f : g.out_scale;   // split partials are scaled by the reduction
+    // (packed products: exactly one of C_h16 and C, host-checked)
+    [[maybe_unused]] const bool h16_only = g.C_h16 != nullptr;
     // residual R (RES: present and not split-K): one of the two loads reads, the other is empty
     const bool rf = RES && !g.r_bf16, rb = RES && g.r_bf16;
     [[maybe_unused]] const __amdgpu_buffer_rsrc_t r_rf =
@@ -444,6 +446,41 @@ skinny_kernel(GemmArgs g, int kper, int nitems) {
       for (int j = 0; j < NTW; ++j)
 #pragma unroll
         for (int i = 0; i < 4; ++i) stg[(4 * (lane >> 4) + i) * S::PITCH + 16 * j + (lane & 15)] = acc[t][j][i];
+      if constexpr (PK) {
+        // The packed product writes one output: S0 as one fp16 plane (the step) or fp32 (the
+        // state-initialisation entry).  fp16: 8 consecutive columns per lane, one 16-byte store
+        // each (against 8-byte stores of 4 columns: 8b-serving-b64 step 2.061 -> 2.023 ms; the
+        // output's row layout made no difference).
+        if (h16_only) {
+          constexpr int L8 = S::BNW / 8, R8 = 64 / L8 < 16 ? 64 / L8 : 16;
+          const int lr8 = lane / L8, c8 = (lane % L8) * 8;
+#pragma unroll
+          for (int pass = 0; pass < 16 / R8; ++pass) {
+            const int r = pass * R8 + lr8;
+            const int m = 16 * t + r;
+            const bool ok = lane < L8 * R8 && m < g.M && c8 < cols;
+            const f32x4 v0 = *reinterpret_cast<const f32x4*>(stg + r * S::PITCH + c8) * osc;
+            const f32x4 v1 = *reinterpret_cast<const f32x4*>(stg + r * S::PITCH + c8 + 4) * osc;
+            f16x8 h8;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              h8[e] = (_Float16)(v0[e] * g.h16_scale);
+              h8[4 + e] = (_Float16)(v1[e] * g.h16_scale);
+            }
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, h8), r_h16, ok ? (m * g.ldch + c8) * 2 : SK_OOB, 0, 16);
+          }
+        } else {
+#pragma unroll
+          for (int pass = 0; pass < 16 / RPP; ++pass) {
+            const int r = pass * RPP + lr;
+            const int m = 16 * t + r;
+            const bool ok = lane < LPR * RPP && m < g.M && c4 < cols;
+            const f32x4 v = *reinterpret_cast<const f32x4*>(stg + r * S::PITCH + c4) * osc;
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r_c, ok ? (m * g.ldc + c4) * 4 : SK_OOB, 0, 16);
+          }
+        }
+        continue;
+      }
 #pragma unroll
       for (int pass = 0; pass < 16 / RPP; ++pass) {
         const int r = pass * RPP + lr;
@@ -578,8 +615,10 @@ int device_cus() {
 
 constexpr int SK_NW = HSPEC_SK_NW;
 
-// Launch shape of the weight-streaming path: wide N uses 4 column tiles per wave; narrow N
-// uses 1 and splits K until the grid covers the chip once (measured on 64 x 4096 x 4096 with
+// Launch shape of the weight-streaming path: wide N uses 4 column tiles per wave (2 at 65..128
+// rows with one A plane, where 4 tiles of 128 rows would not leave room for the W prefetch in
+// the 256 registers of two waves per SIMD); narrow N uses 1 and splits K until the grid covers
+// the chip once (measured on 64 x 4096 x 4096 with
 // the weights out of cache, reduction included: 29.6 us at one workgroup per CU, 33.0 us at
 // two, 41.2 us at four).
 struct SkPlan {
@@ -597,7 +636,9 @@ SkPlan skinny_plan(int M, int N, int K, bool a_lo, bool w_lo, int cus) {
   p.use = true;
   const int nw = sk_waves(M, a_lo);
   const int want = cus;
-  int tiles = (N + nw * 64 - 1) / (nw * 64);
+  const int wide = M > 64 && !a_lo ? 2 : 4;
+  int tiles = (N + nw * 16 * wide - 1) / (nw * 16 * wide);
+  p.ntw = wide;
   if (tiles < want) {
     p.ntw = 1;
     tiles = (N + nw * 16 - 1) / (nw * 16);
@@ -636,6 +677,9 @@ hipError_t launch_skinny_t(const GemmArgs& g, const SkPlan& p, hipStream_t s) {
 
 template <int MT, bool ALO>
 hipError_t launch_skinny_m(const GemmArgs& g, const SkPlan& p, hipStream_t s) {
+  if constexpr (MT == 8 && !ALO) {
+    if (p.ntw == 2) return g.w_packed ? launch_skinny_t<MT, 2, ALO, true>(g, p, s) : launch_skinny_t<MT, 2, ALO, false>(g, p, s);
+  }
   if (g.w_packed) return p.ntw == 4 ? launch_skinny_t<MT, 4, ALO, true>(g, p, s) : launch_skinny_t<MT, 1, ALO, true>(g, p, s);
   return p.ntw == 4 ? launch_skinny_t<MT, 4, ALO, false>(g, p, s) : launch_skinny_t<MT, 1, ALO, false>(g, p, s);
 }
@@ -1396,6 +1440,9 @@ hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
   if (g.C_h16 && (!p.use || g.W2)) return hipErrorInvalidValue;   // only the weight-streaming path writes fp16
   if (g.C_l16 && !g.C_h16) return hipErrorInvalidValue;
   if (g.w_packed && (!p.use || g.N % 16 || g.K % BK || g.W_lo || g.R)) return hipErrorInvalidValue;   // packed W: no residual
+  // packed W: one output, fp32 C or one fp16 plane (16-byte rows), not both, no bf16 planes
+  if (g.w_packed && ((g.C != nullptr) == (g.C_h16 != nullptr) || g.C_hi || g.C_lo || g.C_l16 || (g.C_h16 && g.ldch % 8)))
+    return hipErrorInvalidValue;
   if (p.use) {
     if (p.ksplit > 1 && (!g.part || g.part_cap < (size_t)p.ksplit * g.M * g.N)) {
       p.ksplit = 1;
