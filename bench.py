@@ -44,15 +44,16 @@ def kernel_hash(files) -> str:
     return h.hexdigest()[:16]
 
 
-def traffic_for(name: str, src_hash: str):
-    """HBM bytes per launch from committed rocprofv3 counter runs, if taken on this source."""
+def traffic_for(name: str, src_hash: str, workload: str):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if taken on this source and
+    on this workload (else None)."""
     p = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(p):
         return None
     with open(p) as f:
         t = json.load(f)
     e = t.get(name)
-    if not e or e.get("source_hash") != src_hash:
+    if not e or e.get("source_hash") != src_hash or e.get("workload") != workload:
         return None
     return e.get("bytes_per_launch")
 
@@ -480,13 +481,13 @@ def main():
     h_sweep = kernel_hash(["attn.hip"])
     roof = {"bound": "hbm", "achieved": round(b_state / t_state / 1e9, 1), "peak": RL.HBM_PEAK_GBS,
             "unit": "GB/s", "frac": round(b_state / t_state / 1e9 / RL.HBM_PEAK_GBS, 4),
-            "traffic": traffic_for("state_proj", h_state), "kernel": "state projection (Proj_r + Proj_dS GEMMs)",
+            "traffic": traffic_for("state_proj", h_state, cfg.name), "kernel": "state projection (Proj_r + Proj_dS GEMMs)",
             "algorithmic_bytes": int(b_state), "avg_launch_us": round(t_state * 1e6, 2)}
     # headline: the attention core on the step's path (split-K sweep + cross-split reduction;
     # the work list rides in the step's q/k-norm + RoPE launch); the sweep alone is a sub-field
     roof_sweep = {"bound": "hbm", "achieved": round(b_sweep / t_core / 1e9, 1), "peak": RL.HBM_PEAK_GBS,
                   "unit": "GB/s", "frac": round(b_sweep / t_core / 1e9 / RL.HBM_PEAK_GBS, 4),
-                  "traffic": traffic_for("kv_sweep", h_sweep),
+                  "traffic": traffic_for("kv_sweep", h_sweep, cfg.name),
                   "kernel": "target-KV attention core: split-K sweep + cross-split reduction",
                   "algorithmic_bytes": int(b_sweep), "avg_us": round(t_core * 1e6, 2),
                   "reduction_us": round(t_red * 1e6, 2),
