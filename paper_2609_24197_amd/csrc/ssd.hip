@@ -433,6 +433,147 @@ __global__ void __launch_bounds__(64) ssd_scan_one(ScanArgs a) {
   }
 }
 
+// The drafting step's case (one chunk, no final state, S0 as one fp16 plane) with HW waves per
+// workgroup, one per head, for HW heads of one request that read the same B and C.  Each wave
+// loads only its own head's S0, dt and x, so it holds a third fewer registers than
+// ssd_scan_one and more waves stay resident; wave w loads the w-th (mod HW) 32-wide slices of
+// C and B, rounds its C slice to fp16 into LDS and leaves its part of C B^T there, and every
+// wave adds the parts in slice order.  The arithmetic is ssd_scan_one<N, true>'s: C S0^T as
+// sum over slices of fp16 products, C B^T from the hi/lo planes, the rest unchanged.
+constexpr int SCAN_HW = 4;
+template <int N>
+__global__ void __launch_bounds__(64 * SCAN_HW) __attribute__((amdgpu_waves_per_eu(4))) ssd_scan_grp(ScanArgs a) {
+  constexpr int NS = (N + 31) / 32;
+  constexpr int CP = N + 8;   // fp16 C row pitch (16 bytes of padding)
+  __shared__ float xT_all[SCAN_HW][P * (QMAX + 1)];
+  __shared__ float Mm_all[SCAN_HW][QMAX * (QMAX + 1)];
+  __shared__ __align__(16) _Float16 c16s[QMAX * CP];   // C rounded to fp16, rows t
+  __shared__ f32x4 cbp[NS][64];                         // parts of C B^T, one per slice
+
+  const int H = a.H, T = a.T, G = a.G;
+  // (the wave index made visibly uniform: the head's A, D and offsets become scalar values)
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, g4 = lane >> 4, l16 = lane & 15;
+  const int hpb = H / SCAN_HW;                          // workgroups per request
+  const int b = blockIdx.x / hpb, h = (blockIdx.x % hpb) * SCAN_HW + wave;
+  const int grp = h / (H / G);                          // the same for the workgroup's heads
+  const size_t s0_off = ((size_t)b * H + h) * P * N;
+  float* xT = xT_all[wave];
+  float* Mm = Mm_all[wave];
+
+  // ---- loads, in order of use: dt and x of this head, this wave's slices of C and B, S0.
+  // Lanes past the block read token 0 (no branch around a load, whose merged value would
+  // have to arrive before the next load is issued) and drop the value where it is used.
+  const bool tok_ok = l16 < T;
+  const float dt_raw = a.dt[(size_t)(b * T + (tok_ok ? l16 : 0)) * a.dt_ld + h];
+  const int xt = lane >> 2, xp = 16 * (lane & 3);
+  const bool xok = xt < T;
+  const size_t xoff = (size_t)(b * T + (xok ? xt : 0)) * a.x_ld + (size_t)h * P + xp;
+  const bf16x8 xh0 = ld8(a.x_hi + xoff), xh1 = ld8(a.x_hi + xoff + 8);
+  // (lo planes: the hi plane is read in their place when there is none, and dropped)
+  const bf16* x_lo = a.x_lo ? a.x_lo : a.x_hi;
+  const bf16x8 xl0 = ld8(x_lo + xoff), xl1 = ld8(x_lo + xoff + 8);
+  const size_t tok_t = (size_t)(b * T + (tok_ok ? l16 : 0)) * a.bc_ld + (size_t)grp * N;
+  constexpr int NSW = (NS + SCAN_HW - 1) / SCAN_HW;    // slices per wave
+  bf16x8 cf[NSW], cfl[NSW], bfr[NSW], bfl[NSW];
+#pragma unroll
+  for (int kk = 0; kk < NSW; ++kk) {
+    const int ns = wave + SCAN_HW * kk;
+    const int n = 32 * ns + 8 * g4;
+    const int nc = ns < NS && n < N ? n : 0;   // (in range; the value is dropped below)
+    cf[kk] = ld8(a.C_hi + tok_t + nc);
+    cfl[kk] = ld8((a.C_lo ? a.C_lo : a.C_hi) + tok_t + nc);
+    bfr[kk] = ld8(a.B_hi + tok_t + nc);
+    bfl[kk] = ld8((a.B_lo ? a.B_lo : a.B_hi) + tok_t + nc);
+  }
+  f16x8 s16[4][NS];
+#pragma unroll
+  for (int pb = 0; pb < 4; ++pb)
+#pragma unroll
+    for (int ns = 0; ns < NS; ++ns) {
+      const int n = 32 * ns + 8 * g4;
+      s16[pb][ns] = n < N ? *reinterpret_cast<const f16x8*>(a.S0_h16 + s0_off + (size_t)(16 * pb + l16) * N + n)
+                          : f16x8{};
+    }
+  const float Ah = a.A_is_log ? -__expf(a.A[h]) : a.A[h], Dh = a.Dskip[h];
+
+  // ---- this wave's C slices (fp16, rows t = l16) and parts of C B^T into LDS
+#pragma unroll
+  for (int kk = 0; kk < NSW; ++kk) {
+    const int ns = wave + SCAN_HW * kk;
+    if (ns < NS) {   // (uniform: ns depends on the wave only)
+      // the C and B rows of tokens past the block, and columns past N, are zero
+      const bool ok = tok_ok && 32 * ns + 8 * g4 < N;
+      const bf16x8 cv = ok ? cf[kk] : zero8(), cvl = ok && a.C_lo ? cfl[kk] : zero8();
+      const bf16x8 bv = ok ? bfr[kk] : zero8(), bvl = ok && a.B_lo ? bfl[kk] : zero8();
+      f32x4 part = {0.f, 0.f, 0.f, 0.f};
+      part = mma16(cv, bv, part);
+      if (a.C_lo) part = mma16(cvl, bv, part);
+      if (a.B_lo) part = mma16(cv, bvl, part);
+      cbp[ns][lane] = part;
+      f16x8 c;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) c[e] = (_Float16)(bf2f(cv[e]) + bf2f(cvl[e]));
+      if (32 * ns + 8 * g4 < N) *reinterpret_cast<f16x8*>(c16s + l16 * CP + 32 * ns + 8 * g4) = c;
+    }
+  }
+  // ---- inclusive cumulative sum of dt*A over the chunk (lanes 0..15)
+  const float dtv = tok_ok ? dt_raw : 0.f;
+  float cum = dtv * Ah;
+#pragma unroll
+  for (int off = 1; off < 16; off <<= 1) {
+    const float v = __shfl_up(cum, off, 16);
+    if (l16 >= off) cum += v;
+  }
+  // ---- x^T tile of this head in LDS (zero past the block)
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    xT[(xp + e) * (QMAX + 1) + xt] = xok ? bf2f(xh0[e]) + (a.x_lo ? bf2f(xl0[e]) : 0.f) : 0.f;
+    xT[(xp + 8 + e) * (QMAX + 1) + xt] = xok ? bf2f(xh1[e]) + (a.x_lo ? bf2f(xl1[e]) : 0.f) : 0.f;
+  }
+  __syncthreads();   // C slices and parts of C B^T from every wave
+  // ---- C B^T: lane gets rows t = 4 g4 + i, column s = l16 (parts added in slice order)
+  f32x4 cb = cbp[0][lane];
+#pragma unroll
+  for (int ns = 1; ns < NS; ++ns) cb += cbp[ns][lane];
+  // ---- state term C S^T: lane gets rows t = 4 g4 + i, column p = 16 pb + l16
+  f32x4 ys[4];
+#pragma unroll
+  for (int pb = 0; pb < 4; ++pb) ys[pb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ns = 0; ns < NS; ++ns) {
+    const int n = 32 * ns + 8 * g4;   // (columns past N, N = 16: zero, as S0 is there)
+    const f16x8 c = n < N ? *reinterpret_cast<const f16x8*>(c16s + l16 * CP + n) : f16x8{};
+#pragma unroll
+    for (int pb = 0; pb < 4; ++pb) ys[pb] = mma16h(c, s16[pb][ns], ys[pb]);
+  }
+  // ---- decay-weighted mixing matrix M[t][s] = (C_t . B_s) exp(l_t - l_s) dt_s for s <= t
+  const float ell_s = __shfl(cum, l16);
+  const float dt_s = __shfl(dtv, l16);
+  float ell_t[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int t = 4 * g4 + i;
+    ell_t[i] = __shfl(cum, t);
+    const bool ok = l16 <= t && t < T;
+    Mm[t * (QMAX + 1) + l16] = ok ? cb[i] * __expf(ell_t[i] - ell_s) * dt_s : 0.f;
+  }
+  __syncthreads();   // (each wave reads only its own tiles; one barrier for the LDS writes)
+  // ---- y = exp(l_t) (C S^T) + M x + D x
+  f32x4 mx[4];
+  mix_mfma(Mm, xT, lane, mx);
+#pragma unroll
+  for (int pb = 0; pb < 4; ++pb) {
+    const int p = 16 * pb + l16;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int t = 4 * g4 + i;
+      const float acc = __expf(ell_t[i]) * ys[pb][i] + Dh * xT[p * (QMAX + 1) + t] + mx[pb][i];
+      if (t < T) a.y[(size_t)(b * T + t) * H * P + (size_t)h * P + p] = acc;
+    }
+  }
+}
+
 template <int N>
 hipError_t launch_n(const ScanArgs& a, hipStream_t s) {
   const bool multi = a.S_final != nullptr || a.T > a.chunk;
@@ -441,7 +582,10 @@ hipError_t launch_n(const ScanArgs& a, hipStream_t s) {
     auto kern = ssd_scan_kernel<N>;
     hipLaunchKernelGGL(kern, dim3(a.B * a.H), dim3(64), lds_multi, s, a);
   } else {
-    if (a.S0_h16) hipLaunchKernelGGL((ssd_scan_one<N, true>), dim3(a.B * a.H), dim3(64), 0, s, a);
+    // heads in groups of SCAN_HW that share B and C: one workgroup per group of heads
+    const bool grouped = a.S0_h16 && a.H % SCAN_HW == 0 && (a.H / a.G) % SCAN_HW == 0;
+    if (grouped) hipLaunchKernelGGL(ssd_scan_grp<N>, dim3(a.B * (a.H / SCAN_HW)), dim3(64 * SCAN_HW), 0, s, a);
+    else if (a.S0_h16) hipLaunchKernelGGL((ssd_scan_one<N, true>), dim3(a.B * a.H), dim3(64), 0, s, a);
     else hipLaunchKernelGGL((ssd_scan_one<N, false>), dim3(a.B * a.H), dim3(64), 0, s, a);
   }
   return hipGetLastError();
