@@ -39,6 +39,12 @@ SMALL = {
     # hi/lo attention I/O, block keys in fp32 in the reduction (as in the whole drafter)
     "precise_io": I.StepConfig(name="s", B=3, k=16, d_model=512, H=8, P=64, N=128, G=1, chunk=16, Hq=32, Hkv=8,
                                D=128, lengths="list:300,0,77", precise_io=True),
+    # the drafting step's grouped scan (4 heads of a request per workgroup) over several B/C
+    # groups: N = 64 with 2 groups of 4 heads, N = 32 with 4 groups of 4 heads
+    "grp_n64_g2": I.StepConfig(name="s", B=3, k=16, d_model=512, H=8, P=64, N=64, G=2, chunk=16, Hq=32, Hkv=8,
+                               D=128, lengths="list:300,0,77"),
+    "grp_n32_g4": I.StepConfig(name="s", B=2, k=16, d_model=256, H=16, P=64, N=32, G=4, chunk=16, Hq=8, Hkv=2,
+                               D=128, lengths="list:120,40"),
     # the drafter reuses 4 of the target's 8 KV heads (16 query heads)
     "kv_subset": I.StepConfig(name="s", B=3, k=16, d_model=512, H=8, P=64, N=128, G=1, chunk=16, Hq=16, Hkv=4,
                               D=128, lengths="list:300,0,77", Hkv_target=8, kv_heads=(0, 2, 4, 6)),
