@@ -12,8 +12,10 @@
 // dt*A is a 16-lane shuffle scan.  When the block fits one chunk and no final state is
 // requested (ssd_scan_one), the initial state is read straight from global memory into MFMA
 // fragments (as bf16 hi/lo planes, or as one fp16 plane multiplied with C rounded to fp16 on
-// v_mfma_f32_16x16x32_f16); otherwise (ssd_scan_kernel) the fp32 state lives in LDS between
-// chunks.
+// v_mfma_f32_16x16x32_f16); with the fp16 plane and heads in groups of 4 that share B and C
+// (the drafting step), ssd_scan_grp runs those 4 heads in one workgroup, one wave each, and
+// shares the C and C B^T work through LDS; otherwise (ssd_scan_kernel) the fp32 state lives
+// in LDS between chunks.
 #include "common.h"
 #include "kernels.h"
 
