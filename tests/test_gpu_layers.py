@@ -171,6 +171,26 @@ def test_draft_step_full_config(num):
 
 @pytest.mark.slow
 @pytest.mark.timeout(900)
+@pytest.mark.parametrize("causal", [False, True])
+def test_draft_step_window_full(causal):
+    """8b-serving-b64 under the sliding window of 2048 (Sec. 3.3.2 attention masks), with and
+    without the block-causal mask: the swept range starts at L - 2047, so requests shorter than
+    the window, longer ones (split at their visible range) and the window edge inside a block
+    are all in the batch; every request compared."""
+    cfg = I.CONFIGS[3].replace(window=2048, block_causal=causal)
+    W = I.make_weights(cfg, 0)
+    x = I.make_inputs(cfg, 0)
+    Wd = dev(W)
+    Wd["W_dS_packed"] = hspec.pack_w_ds(Wd.pop("W_dS"), cfg.d_S, cfg.rank)
+    out, st = _draft(cfg, W, Wd, x)
+    assert st == 0
+    del Wd
+    ref = O.draft_step(W, x, cfg, progress=lambda s: print(f"  oracle: {s} done", flush=True))
+    assert_close(out, ref, f"config 3, window 2048, block-causal {causal}")
+
+
+@pytest.mark.slow
+@pytest.mark.timeout(900)
 def test_draft_step_kv_subset_full():
     """8b-serving-b64 with partial target-KV-head reuse: the drafter's 4 KV heads (16 query
     heads) read heads 0, 2, 4, 6 of the target's 8-head cache; every request compared."""
