@@ -465,7 +465,7 @@ def main():
     t_state = time_in_step(state, args.steps, args.warmup, step, torch)
     b_state = RL.state_proj_bytes(cfg, 2, 4) + cfg.rank * cfg.d_h * 2
 
-    # the target-KV sweep (the spec bar), same cache, table and lengths: the sweep kernel
+    # the target-KV sweep and its split reduction, same cache, table and lengths: the sweep kernel
     # alone, and the whole attention core (work list + sweep + split reduction)
     Ad, aws, o = sweep_inputs(cfg, Xd, x, args.seed, torch)
     t_plan, t_sweep, t_red = time_attention(cfg, Ad, o, aws, maxL, args.steps, args.warmup, step, torch)
