@@ -45,6 +45,10 @@ SMALL = {
                                D=128, lengths="list:300,0,77"),
     "grp_n32_g4": I.StepConfig(name="s", B=2, k=16, d_model=256, H=16, P=64, N=32, G=4, chunk=16, Hq=8, Hkv=2,
                                D=128, lengths="list:120,40"),
+    # the grouped scan with a block shorter than its 16-token tile (lanes past the block read
+    # token 0 and drop it)
+    "grp_k5": I.StepConfig(name="s", B=2, k=5, d_model=256, H=8, P=64, N=64, G=2, chunk=8, Hq=8, Hkv=2,
+                           D=128, lengths="list:50,300"),
     # the drafter reuses 4 of the target's 8 KV heads (16 query heads)
     "kv_subset": I.StepConfig(name="s", B=3, k=16, d_model=512, H=8, P=64, N=128, G=1, chunk=16, Hq=16, Hkv=4,
                               D=128, lengths="list:300,0,77", Hkv_target=8, kv_heads=(0, 2, 4, 6)),
