@@ -4,7 +4,9 @@
 // KV-head subsets, packed W_dS, batches past the fused work-list limit and empty contexts, each
 // with a workspace of exactly the queried size; then rejected calls (short or misaligned
 // workspace, NULL pointers, bad sizes), which must return their error code and enqueue
-// nothing; then the workspace queries at serving sizes and at the limits of every size.
+// nothing; then the workspace queries at serving sizes and at the limits of every size; then
+// 300 seeded random configurations (a sixth of them outside the documented shapes), each call
+// accepted with every extent in bounds or refused with nothing enqueued.
 // Prints one line per case; exits non-zero on the first failed expectation.
 #include <climits>
 #include <cstdint>
@@ -471,6 +473,147 @@ void run_queries() {
 
 }  // namespace
 
+// ------------------------------------------------------------ seeded random configurations
+
+// Configurations drawn from a fixed seed over the shapes the ABI documents (and some it refuses).
+// Every call is either accepted, with every extent a kernel would touch inside the caller's
+// buffers and inside its workspace region (the stand-ins abort otherwise), or rejected with a
+// message and nothing enqueued.
+struct Lcg {
+  unsigned long long s;
+  int operator()(int n) {
+    s = s * 6364136223846793005ull + 1442695040888963407ull;
+    return (int)((s >> 33) % (unsigned long long)n);
+  }
+  template <size_t K>
+  int pick(const int (&v)[K]) { return v[(*this)((int)K)]; }
+};
+
+int g_rand_ok = 0, g_rand_rejected = 0;
+
+void accepted_or_refused(const char* what, hspec_status got, long launches_before) {
+  ++g_cases;
+  if (got == HSPEC_OK) {
+    if (hspec_last_error()[0] != 0) {
+      std::fprintf(stderr, "FAIL %s: success left the message '%s'\n", what, hspec_last_error());
+      std::exit(1);
+    }
+    ++g_rand_ok;
+    return;
+  }
+  if (hspec_last_error()[0] == 0) {
+    std::fprintf(stderr, "FAIL %s: error %d without a message\n", what, (int)got);
+    std::exit(1);
+  }
+  if (stub_launches() != launches_before) {
+    std::fprintf(stderr, "FAIL %s: a refused call launched %ld kernels\n", what, stub_launches() - launches_before);
+    std::exit(1);
+  }
+  ++g_rand_rejected;
+}
+
+// Workspace of exactly the queried size, or (when the query gives none) a small one the call
+// must refuse.
+void* random_ws(Pool& pool, size_t n) { return pool.get(n > 0 ? n : 256); }
+
+void run_random_calls(int count) {
+  Lcg r{0x2609241970ull};
+  static const int Bs[] = {1, 2, 3, 5, 8}, ks[] = {1, 3, 5, 8, 16}, dms[] = {64, 128, 256, 320};
+  static const int Hs[] = {1, 2, 4, 5, 8, 12, 16}, Ns[] = {16, 32, 64, 128}, Ds[] = {64, 128};
+  static const int Hkvs[] = {1, 2, 4, 8}, gs[] = {1, 2, 4, 8}, wins[] = {0, 0, 16, 64};
+  static const int splits[] = {0, 0, 64, 128}, pages[] = {1, 2, 8, 20}, dhs[] = {128, 256}, rs[] = {64, 128};
+  for (int i = 0; i < count; ++i) {
+    char what[160];
+    const hspec_dtype dt = r(6) ? HSPEC_BF16 : HSPEC_F32;
+    const int B = r.pick(Bs), k = r.pick(ks), d_model = r.pick(dms);
+    hspec_mamba_cfg mc = mamba_cfg(dt, B, k, d_model, r.pick(Ns));
+    mc.H = r.pick(Hs);
+    int G = 1 << r(3);
+    while (mc.H % G) G >>= 1;
+    mc.G = G;
+    mc.chunk = 1 + r(16);
+    mc.conv_w = r(4) ? 4 : 2 + r(5);
+    mc.d_h = r.pick(dhs);
+    mc.r = r.pick(rs);
+    if (dt == HSPEC_BF16 && r(2)) mc.flags |= HSPEC_W_DS_PACKED;
+    const int Hkv = r.pick(Hkvs), g = r.pick(gs);
+    hspec_attn_cfg ac = attn_cfg(dt, B, k, d_model, Hkv * g, Hkv, r.pick(Ds));
+    ac.window = r.pick(wins);
+    ac.flags = (r(3) == 0 ? HSPEC_BLOCK_CAUSAL : 0u) | (r(4) == 0 ? HSPEC_ATTN_PRECISE_IO : 0u);
+    ac.split_tokens = r.pick(splits);
+    ac.max_pages = r.pick(pages);
+    ac.num_pages = ac.max_pages * B + 3 * r(2);
+    // about one draw in six leaves the documented shapes in one respect, which must be refused
+    // before anything is enqueued
+    switch (r(6) == 0 ? 1 + r(6) : 0) {
+      case 1: mc.N = 48; break;
+      case 2: ac.page_size = 8; break;
+      case 3: ac.D = 96; break;
+      case 4: ac.k = mc.k = 16; ac.Hq = ac.Hkv * 16; break;
+      case 5: mc.chunk = 17; break;
+      case 6: ac.d_model = mc.d_model = d_model + 4; break;
+      default: break;
+    }
+    const int max_ctx = r(ac.max_pages * ac.page_size + 1);
+    std::printf("     random %d: %s B=%d k=%d d=%d H=%d N=%d G=%d chunk=%d conv=%d packed=%d Hq=%d Hkv=%d D=%d "
+                "win=%d flags=%u split=%d pages=%d max_ctx=%d\n",
+                i, dt == HSPEC_BF16 ? "bf16" : "f32", B, mc.k, mc.d_model, mc.H, mc.N, mc.G, mc.chunk, mc.conv_w,
+                (mc.flags & HSPEC_W_DS_PACKED) ? 1 : 0, ac.Hq, ac.Hkv, ac.D, ac.window, ac.flags, ac.split_tokens,
+                ac.max_pages, max_ctx);
+
+    Pool pool;
+    MambaW m = make_mamba(pool, mc);
+    if (mc.flags & HSPEC_W_DS_PACKED) {
+      const int dS = mc.H * mc.P * mc.N;
+      const size_t pb = hspec_pack_w_ds_bytes(dS, mc.r);
+      void* packed = pool.get(pb > 0 ? pb : 256);
+      const long before = stub_launches();
+      std::snprintf(what, sizeof what, "random %d: pack_w_ds", i);
+      const hspec_status st = hspec_pack_w_ds(dS, mc.r, m.w.W_dS, packed, nullptr);
+      accepted_or_refused(what, st, before);
+      if (st == HSPEC_OK) m.w.W_dS = packed;
+      else mc.flags &= ~HSPEC_W_DS_PACKED;
+    }
+    const hspec_attn_w aw = make_attn(pool, ac);
+    const Paged pg = make_paged(pool, ac);
+    const size_t s = esz(dt), M = (size_t)B * mc.k, dm = (size_t)mc.d_model;
+    const float* n1 = (const float*)pool.get(dm * 4);
+    const float* n2 = (const float*)pool.get(dm * 4);
+    void* h = pool.get((size_t)B * mc.d_h * s);
+    void* e = pool.get(M * dm * s);
+    float* out = (float*)pool.get(M * dm * 4);
+    {
+      const size_t n = hspec_draft_step_workspace(&mc, &ac, max_ctx);
+      void* ws = random_ws(pool, n);
+      const long before = stub_launches();
+      std::snprintf(what, sizeof what, "random %d: draft_step", i);
+      accepted_or_refused(what, hspec_draft_step(&mc, &m.w, n1, &ac, &aw, n2, h, e, pg.kc, pg.vc, pg.pt, pg.lens,
+                                                 max_ctx, out, ws, n > 0 ? n : 256, nullptr),
+                          before);
+    }
+    {
+      const size_t n = hspec_mamba_block_scan_workspace(&mc);
+      void* ws = random_ws(pool, n);
+      float* S = (float*)pool.get((size_t)B * mc.H * mc.P * mc.N * 4);
+      const long before = stub_launches();
+      std::snprintf(what, sizeof what, "random %d: mamba_block_scan", i);
+      accepted_or_refused(what, hspec_mamba_block_scan(&mc, &m.w, h, e, out, r(2) ? S : nullptr, ws, n > 0 ? n : 256,
+                                                       nullptr),
+                          before);
+    }
+    {
+      const size_t n = hspec_target_kv_block_attn_workspace(&ac, max_ctx);
+      void* ws = random_ws(pool, n);
+      const long before = stub_launches();
+      std::snprintf(what, sizeof what, "random %d: target_kv_block_attn", i);
+      accepted_or_refused(what, hspec_target_kv_block_attn(&ac, &aw, e, pg.kc, pg.vc, pg.pt, pg.lens, max_ctx, out, ws,
+                                                           n > 0 ? n : 256, nullptr),
+                          before);
+    }
+  }
+  std::printf("ok   random configurations: %d calls accepted, %d refused\n", g_rand_ok, g_rand_rejected);
+}
+
 int main() {
   const hspec_dtype dts[2] = {HSPEC_BF16, HSPEC_F32};
   for (hspec_dtype dt : dts) {
@@ -517,6 +660,7 @@ int main() {
   }
   run_head_calls();
   run_queries();
+  run_random_calls(300);
   std::printf("host sanitizer driver: %d cases passed\n", g_cases);
   return 0;
 }
