@@ -127,17 +127,33 @@ attn_sweep(AttnArgs a) {
   const int g = a.Hq / a.Hkv, T = a.T, R = T * g;
   const int n_items = min(a.status[1], a.B * a.max_splits * a.Hkv);   // work-list length, capped at its array
 
-  // Persistent workgroups pull (request, split, KV head) items, longest splits first.  The
-  // next item is claimed while the last round of the current one is multiplied.
-  int next = -1;   // thread 0: item claimed ahead
+  // The work list's entries (one per (request, split)) are copied to LDS when they fit, so
+  // that an item's start waits on no memory round trip for its entry.  Otherwise thread 0
+  // copies each claimed item's entry to s_units[0]; either way the entry is read from LDS.
+  constexpr int UNITS_LDS = NW >= 4 ? 512 : 1;
+  __shared__ int4 s_units[UNITS_LDS];
+  const int n_units = (n_items + a.Hkv - 1) / a.Hkv;
+  const bool units_lds = NW >= 4 && n_units <= UNITS_LDS;
+  if (units_lds)
+    for (int u = tid; u < n_units; u += C::NT) s_units[u] = reinterpret_cast<const int4*>(a.units)[u];
+
+  // Persistent workgroups pull (request, split, KV head) items, longest splits first.  A
+  // workgroup's first item is its own index; later ones come from the queue counter, offset by
+  // the grid.  The next item is claimed while the last round of the current one is multiplied.
+  // thread 0: queue ticket claimed ahead (item = grid + ticket), INT_MIN for none
+  int next = (int)blockIdx.x - (int)gridDim.x;
   for (;;) {
   __syncthreads();                    // the previous item is finished by every wave
-  if (tid == 0) s_item = next >= 0 ? next : atomicAdd(a.status + 2, 1);
-  next = -1;
+  if (tid == 0) {
+    const int it = (int)gridDim.x + (next != INT_MIN ? next : atomicAdd(a.status + 2, 1));
+    s_item = it;
+    if (!units_lds && it < n_items) s_units[0] = reinterpret_cast<const int4*>(a.units)[it / a.Hkv];
+  }
+  next = INT_MIN;
   __syncthreads();
   const int item = s_item;
   if (item >= n_items) break;
-  const int4 unit_e = *reinterpret_cast<const int4*>(a.units + 4 * (item / a.Hkv));
+  const int4 unit_e = s_units[units_lds ? item / a.Hkv : 0];
   const int b = unit_e.x >> 16, sp = unit_e.x & 0xffff, h = item % a.Hkv;
   const int hc = a.kv_remap ? (int)((a.kv_map >> (4 * h)) & 15) : h;   // the cache head this KV head reads
   const int L = unit_e.y;   // validated by the work-list kernel
@@ -384,7 +400,8 @@ attn_sweep(AttnArgs a) {
     ((I < ntiles ? issue(I, stage(Int<I>{})) : void()), ...);
   }(std::make_integer_sequence<int, ST - 1>{});
   for (int t0 = 0; t0 < ntiles; t0 += ST) {
-    if (tid == 0 && t0 + ST >= ntiles) next = (int)atomicInc(reinterpret_cast<unsigned*>(a.status + 2), 0xffffffffu);
+    if (tid == 0 && t0 + ST >= ntiles)
+      next = (int)atomicInc(reinterpret_cast<unsigned*>(a.status + 2), 0xffffffffu);
     round(t0, std::make_integer_sequence<int, ST>{});
   }
 
