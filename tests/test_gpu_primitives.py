@@ -147,6 +147,20 @@ def test_paged_attn_split_invariance():
         assert_close(o, base, f"split {s} vs whole context", max_abs=2e-3, rel_l2=3e-3)
 
 
+def test_paged_attn_many_work_units():
+    """More (request, split) entries than the sweep keeps in LDS (512): the sweep then reads each
+    claimed item's entry from the work list in memory.  Ragged lengths, 64-key splits."""
+    lens = [1100 - 13 * i for i in range(40)]
+    split = 64
+    assert sum(-(-L // split) for L in lens) > 512
+    cfg = _small_attn_cfg(B=len(lens), lengths="list:" + ",".join(map(str, lens)))
+    print(f"[paged_attn] many work units {cfg}", flush=True)
+    x = I.make_attn_inputs(cfg, seed=5)
+    o, st = _run_attn(cfg, x, split=split)
+    assert st == 0
+    assert_close(o, _ref_attn(cfg, x), "many work units")
+
+
 def test_paged_attn_workspace_reuse():
     """Consecutive calls on one workspace with different queries, caches and tables: the split
     partials a call combines inside the sweep are its own (stores and loads coherent across
