@@ -475,63 +475,97 @@ __device__ __forceinline__ f32x4 ld4_planes(const bf16* hi, const bf16* lo, size
 }
 
 
-// Split reduction when the sweep took the block keys: one thread per (column, 4 dims) and 2 per
-// thread; o = sum_s O_s 2^(m_s - m*) / sum_s l_s 2^(m_s - m*) in split order.  Requests with one
-// split were written by the sweep.
+// Split reduction when the sweep took the block keys: one thread per (column, 4 dims), PER of
+// them per thread; o = sum_s O_s 2^(m_s - m*) / sum_s l_s 2^(m_s - m*) in split order.  Every
+// load of a thread is issued before its first store (the stores could alias the partials as
+// far as the compiler knows, so a loop over the PER outputs would serialise them).  Requests
+// with one split were written by the sweep.
+template <int D>
 __global__ void __launch_bounds__(RED_THREADS) attn_merge(AttnArgs a) {
-  const int g = a.Hq / a.Hkv, T = a.T, R = T * g, D = a.D, nq = D / 4;
+  constexpr int nq = D / 4, PER = RED_COLS * nq / RED_THREADS;
+  static_assert(PER >= 1 && RED_COLS * nq % RED_THREADS == 0, "merge shape");
+  const int g = a.Hq / a.Hkv, T = a.T, R = T * g;
   const int cblocks = (R + RED_COLS - 1) / RED_COLS;
   const int bh = blockIdx.x / cblocks, c0 = (blockIdx.x % cblocks) * RED_COLS;
   const int b = bh / a.Hkv, h = bh % a.Hkv;
   const int nsplit = a.req[2 * b];   // splits of the request (the work-list kernel's choice)
   if (nsplit == 1) return;
   const size_t unit0 = ((size_t)b * a.Hkv + h) * a.max_splits;
-  for (int it = threadIdx.x; it < RED_COLS * nq; it += RED_THREADS) {
-    const int c = c0 + it / nq, d4 = (it % nq) * 4;
-    if (c >= R) continue;
-    float m[RED_NS], l[RED_NS];
-    f32x4 o[RED_NS];
-    auto fetch = [&](int s0) {
+  int cc[PER], d4[PER];
+  bool ok[PER];
+#pragma unroll
+  for (int p = 0; p < PER; ++p) {
+    const int it = threadIdx.x + p * RED_THREADS;
+    ok[p] = c0 + it / nq < R;
+    cc[p] = ok[p] ? c0 + it / nq : c0;   // c0 < R: a valid column for the masked lanes
+    d4[p] = (it % nq) * 4;
+  }
+  float m[PER][RED_NS], l[PER][RED_NS];
+  f32x4 o[PER][RED_NS];
+  auto fetch = [&](int s0) {
+#pragma unroll
+    for (int p = 0; p < PER; ++p)
 #pragma unroll
       for (int i = 0; i < RED_NS; ++i) {
-        const bool in = s0 + i < nsplit;
-        const size_t u = (unit0 + s0 + (in ? i : 0)) * R + c;
-        m[i] = in ? a.part_ml[u * 2] : -INFINITY;
-        l[i] = in ? a.part_ml[u * 2 + 1] : 0.f;
-        o[i] = in ? *reinterpret_cast<const f32x4*>(a.part_o + u * D + d4) : f32x4{0.f, 0.f, 0.f, 0.f};
+        // unconditional loads from a valid unit, dropped where unused: a branch around a load
+        // would make the merged value wait before the next load goes out
+        const bool in = ok[p] && s0 + i < nsplit;
+        const size_t u = (unit0 + s0 + (s0 + i < nsplit ? i : 0)) * R + cc[p];
+        const float2 ml = *reinterpret_cast<const float2*>(a.part_ml + u * 2);
+        const f32x4 ov = *reinterpret_cast<const f32x4*>(a.part_o + u * D + d4[p]);
+        m[p][i] = in ? ml.x : -INFINITY;
+        l[p][i] = in ? ml.y : 0.f;
+        o[p][i] = in ? ov : f32x4{0.f, 0.f, 0.f, 0.f};
       }
-    };
-    float mstar = -INFINITY;
-    if (nsplit <= RED_NS) {
-      fetch(0);
+  };
+  float mstar[PER];
 #pragma unroll
-      for (int i = 0; i < RED_NS; ++i) mstar = fmaxf(mstar, m[i]);
-    } else {
-      for (int sp = 0; sp < nsplit; ++sp) mstar = fmaxf(mstar, a.part_ml[((unit0 + sp) * R + c) * 2]);
-    }
-    const float m_use = mstar == -INFINITY ? 0.f : mstar;
-    float lsum = 0.f;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int s0 = 0; s0 < nsplit; s0 += RED_NS) {
-      if (nsplit > RED_NS) fetch(s0);
+  for (int p = 0; p < PER; ++p) mstar[p] = -INFINITY;
+  if (nsplit <= RED_NS) {
+    fetch(0);
+#pragma unroll
+    for (int p = 0; p < PER; ++p)
+#pragma unroll
+      for (int i = 0; i < RED_NS; ++i) mstar[p] = fmaxf(mstar[p], m[p][i]);
+  } else {
+    for (int sp = 0; sp < nsplit; ++sp)
+#pragma unroll
+      for (int p = 0; p < PER; ++p) mstar[p] = fmaxf(mstar[p], a.part_ml[((unit0 + sp) * R + cc[p]) * 2]);
+  }
+  float lsum[PER];
+  f32x4 acc[PER];
+#pragma unroll
+  for (int p = 0; p < PER; ++p) {
+    lsum[p] = 0.f;
+    acc[p] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  for (int s0 = 0; s0 < nsplit; s0 += RED_NS) {
+    if (nsplit > RED_NS) fetch(s0);
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const float m_use = mstar[p] == -INFINITY ? 0.f : mstar[p];
 #pragma unroll
       for (int i = 0; i < RED_NS; ++i) {
-        const float e = exp2f(m[i] - m_use);
-        lsum += l[i] * e;
-        acc += o[i] * e;
+        const float e = exp2f(m[p][i] - m_use);
+        lsum[p] += l[p][i] * e;
+        acc[p] += o[p][i] * e;
       }
     }
-    acc *= 1.f / lsum;
-    const int j = c / g, hq = h * g + c % g;
-    const size_t off = ((size_t)(b * T + j) * a.Hq + hq) * D + d4;
-    if (a.o_f32) *reinterpret_cast<f32x4*>(a.o_f32 + off) = acc;
+  }
+#pragma unroll
+  for (int p = 0; p < PER; ++p) {
+    if (!ok[p]) continue;
+    const f32x4 v = acc[p] * (1.f / lsum[p]);
+    const int j = cc[p] / g, hq = h * g + cc[p] % g;
+    const size_t off = ((size_t)(b * T + j) * a.Hq + hq) * D + d4[p];
+    if (a.o_f32) *reinterpret_cast<f32x4*>(a.o_f32 + off) = v;
     if (a.o_bf16) {
-      bf16x4 hv = {f2bf(acc[0]), f2bf(acc[1]), f2bf(acc[2]), f2bf(acc[3])};
+      bf16x4 hv = {f2bf(v[0]), f2bf(v[1]), f2bf(v[2]), f2bf(v[3])};
       *reinterpret_cast<bf16x4*>(a.o_bf16 + off) = hv;
       if (a.o_bf16_lo) {
         bf16x4 lv;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) lv[e] = f2bf(acc[e] - bf2f(hv[e]));
+        for (int e = 0; e < 4; ++e) lv[e] = f2bf(v[e] - bf2f(hv[e]));
         *reinterpret_cast<bf16x4*>(a.o_bf16_lo + off) = lv;
       }
     }
@@ -795,7 +829,8 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s, unsigned parts) {
     if (a.block_in_sweep) {
       if (a.max_splits > 1) {
         if (!a.part_o || !a.part_ml) return hipErrorInvalidValue;
-        hipLaunchKernelGGL(attn_merge, dim3(a.B * a.Hkv * cblocks), dim3(RED_THREADS), 0, s, a);
+        if (a.D == 128) hipLaunchKernelGGL(attn_merge<128>, dim3(a.B * a.Hkv * cblocks), dim3(RED_THREADS), 0, s, a);
+        else hipLaunchKernelGGL(attn_merge<64>, dim3(a.B * a.Hkv * cblocks), dim3(RED_THREADS), 0, s, a);
       }
       return hipGetLastError();
     }
