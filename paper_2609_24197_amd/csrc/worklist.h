@@ -11,7 +11,7 @@ namespace hspec {
 
 constexpr int MAX_SPLIT = kMaxSplit;   // keys per split (host-enforced by the config check)
 constexpr int WL_THREADS = 256;   // threads of a workgroup that builds the list
-constexpr int WL_NCAND = 16;      // split sizes tried under automatic splitting
+constexpr int WL_NCAND = 64;      // split sizes tried under automatic splitting (one lane each)
 
 __device__ __forceinline__ int clamp_len(const AttnArgs& a, int b) {
   int L = a.ctx_lens[b];
@@ -165,7 +165,7 @@ __device__ void build_worklist(const AttnArgs& a, int clear_words, WorklistLds<R
             if ((long long)longest * a.grid * 16 <= avg * 17) key = tid;
           } else {
             const int rem = items % a.grid;
-            key = (1 << 24) + (rem ? a.grid - rem : 0) * 32 + tid;
+            key = (1 << 24) + (rem ? a.grid - rem : 0) * WL_NCAND + tid;
           }
         }
 #pragma unroll
@@ -173,7 +173,7 @@ __device__ void build_worklist(const AttnArgs& a, int clear_words, WorklistLds<R
         if (tid == 0) lds.choice = key;
       }
       __syncthreads();
-      if (lds.choice != INT_MAX) S = cand(lds.choice & 31);
+      if (lds.choice != INT_MAX) S = cand(lds.choice & (WL_NCAND - 1));
     } else {
       __syncthreads();
     }
