@@ -783,6 +783,14 @@ hipError_t with_sweep_variant(int D, int R, bool lo, F f) {
     if (nw <= 8) return f(SweepVariant<Dv, QB, 8, Lv>{});
     return hipErrorInvalidValue;
   };
+  // 65..128 rows with one storage plane: two 16-column blocks per wave, so that four waves
+  // cover the rows and two workgroups share a CU (one workgroup of eight waves stalls the
+  // whole CU at each tile barrier)
+  if (!lo && QB == 1 && R > 64 && R <= 128) {
+    if (D == 128) return f(SweepVariant<128, 2, 4, false>{});
+    if (D == 64) return f(SweepVariant<64, 2, 4, false>{});
+    return hipErrorInvalidValue;
+  }
   if (D == 128) return lo ? by_nw(Int<128>{}, std::true_type{}) : by_nw(Int<128>{}, std::false_type{});
   if (D == 64) return lo ? by_nw(Int<64>{}, std::true_type{}) : by_nw(Int<64>{}, std::false_type{});
   return hipErrorInvalidValue;
