@@ -12,6 +12,7 @@ namespace hspec {
 constexpr int MAX_SPLIT = kMaxSplit;   // keys per split (host-enforced by the config check)
 constexpr int WL_THREADS = 256;   // threads of a workgroup that builds the list
 constexpr int WL_NCAND = 64;      // split sizes tried under automatic splitting (one lane each)
+static_assert(WL_NCAND <= 64 && (WL_NCAND & (WL_NCAND - 1)) == 0, "one lane of a wave per candidate size");
 
 __device__ __forceinline__ int clamp_len(const AttnArgs& a, int b) {
   int L = a.ctx_lens[b];
@@ -43,10 +44,21 @@ __device__ __forceinline__ int split_len_for(int n, int ns) {
   return n > 0 ? ((n + ns - 1) / ns + 31) & ~31 : 0;
 }
 
-// Splits of a request of n swept positions when splits may hold up to S positions.
+// ceil(n / s) for 0 <= n < 2^24 and s >= 1: a float estimate, then corrected to the exact
+// value (the estimate is off by at most one; an integer division costs several times more,
+// and the split-size choice takes one per candidate size and request).
+__device__ __forceinline__ int ceil_div_est(int n, int s) {
+  int q = (int)((float)n * __builtin_amdgcn_rcpf((float)s));
+  while (q * s < n) ++q;
+  while (q > 0 && (q - 1) * s >= n) --q;
+  return q;
+}
+
+// Splits of a request of n swept positions when splits may hold up to S positions (n is at
+// most 256 x MAX_SPLIT: host-enforced).
 __device__ __forceinline__ int plan_pieces(int n, int S, int cap) {
   if (n <= 0) return 1;
-  const int ns = max((n + S - 1) / S, (n + MAX_SPLIT - 1) / MAX_SPLIT);
+  const int ns = max(ceil_div_est(n, S), (n + MAX_SPLIT - 1) / MAX_SPLIT);
   return max(1, min(ns, cap));
 }
 
@@ -139,16 +151,14 @@ __device__ void build_worklist(const AttnArgs& a, int clear_words, WorklistLds<R
         atomicMax(&s_max, mx);
       }
       __syncthreads();
-      // splits at each candidate size: wave w takes candidates w, w + 4, ..., its lanes the
-      // requests (the divisions spread over the whole workgroup)
+      // splits at each candidate size: lane l of every wave counts candidate l over the
+      // requests b = w, w + 4, ... of its wave w; the four partial counts meet in LDS
       const int wv = tid >> 6, ln = tid & 63;
-      for (int c = wv; c < WL_NCAND; c += WL_THREADS / 64) {
-        const int Sc = cand(c);
+      if (ln < WL_NCAND) {
+        const int Sc = cand(ln);
         int cnt = 0;
-        for (int b = ln; b < a.B; b += 64) cnt += plan_pieces(s_n[b], Sc, cap);
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o);
-        if (ln == 0) s_cnt[c] = cnt;
+        for (int b = wv; b < a.B; b += WL_THREADS / 64) cnt += plan_pieces(s_n[b], Sc, cap);
+        atomicAdd(&s_cnt[ln], cnt);
       }
       __syncthreads();
       // Choice, one lane per candidate: the largest size (smallest c) whose items fit one round
